@@ -1,0 +1,547 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test checks the oracle (fp64 / int64) against something the paper or the
+mathematics fixes independently: the table definition written as loops, Eq. 1
+written as loops, the paper's own four-corner + bilinear route (Eq. 2-3) on a
+table built here, a library correlation for integer boxes, a supersampled
+integral, closed forms (identity box, constant image), the adjoint identity,
+and finite differences for every gradient.  The mutation tests at the end plant
+plausible mistakes in the oracle and check that some pin catches each one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1906_11367_amd import workloads as wlmod
+
+
+def _real_boxes(rng, C, B, cmax, rmin, rmax):
+    bx = np.empty((C, B, 4), dtype=np.float32)
+    bx[..., :2] = rng.uniform(-cmax, cmax, size=(C, B, 2))
+    bx[..., 2:] = rng.uniform(rmin, rmax, size=(C, B, 2))
+    return bx
+
+
+def _int_boxes(rng, C, B, smax, span):
+    bx = np.empty((C, B, 4), dtype=np.float32)
+    for ax in range(2):
+        s = rng.integers(1, smax + 1, size=(C, B))
+        lo = rng.integers(-span - s + 1, span + 1)
+        bx[..., ax] = lo + (s - 1) / 2.0
+        bx[..., 2 + ax] = s / 2.0
+    return bx
+
+
+# --------------------------------------------------------------------------
+# Summed-area table: definition before Eq. 2 (exclusive form)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("kind", ["int", "float"])
+def test_sat_matches_definition_loops(kind):
+    rng = np.random.default_rng(11)
+    x = (rng.integers(-9, 10, size=(2, 5, 7)) if kind == "int"
+         else rng.standard_normal((2, 5, 7)))
+    s = O.sat_exclusive(x)
+    assert s.shape == (2, 6, 8)
+    for m in range(2):
+        for u in range(6):
+            for v in range(8):
+                want = 0
+                for i in range(u):
+                    for j in range(v):
+                        want += x[m, i, j]
+                if kind == "int":
+                    assert s[m, u, v] == want
+                else:
+                    assert abs(s[m, u, v] - want) <= 1e-12 * (1 + abs(want))
+
+
+# --------------------------------------------------------------------------
+# Forward box filter
+# --------------------------------------------------------------------------
+def test_forward_equals_eq1_loops_integer():
+    """Eq. 1 literally (integer corners, integer data): exact int64 equality."""
+    rng = np.random.default_rng(1)
+    x = rng.integers(-8, 9, size=(2, 3, 9, 7)).astype(np.int32)
+    bx = _int_boxes(rng, 3, 4, smax=9, span=5)
+    got = O.box_forward(x, bx)
+    assert got.dtype == np.int64
+    np.testing.assert_array_equal(got, O.naive_box_forward_eq1(x, bx))
+
+
+def test_forward_equals_tiny_workload_eq1():
+    """The tiny integer workload's own box generator at reduced size."""
+    wl = wlmod.WORKLOADS[1].scaled(C=2, H=12, W=10)
+    d = wlmod.make_inputs(wl)
+    np.testing.assert_array_equal(O.box_forward(d["x"], d["boxes"]),
+                                  O.naive_box_forward_eq1(d["x"], d["boxes"]))
+
+
+def _four_corner_bilinear(x, bx):
+    """The paper's route, written independently of the oracle: exclusive SAT
+    by nested loops over a running sum, sample each corner with Eq. 3
+    (bilinear weights from alpha = frac, indices clamped to the table), and
+    combine the four corners with Eq. 2's signs."""
+    N, C, H, W = x.shape
+    B = bx.shape[1]
+    out = np.zeros((N, C * B, H, W))
+    for n in range(N):
+        for c in range(C):
+            S = np.zeros((H + 1, W + 1))
+            for u in range(1, H + 1):
+                run = 0.0
+                for v in range(1, W + 1):
+                    run += float(x[n, c, u - 1, v - 1])
+                    S[u, v] = S[u - 1, v] + run
+
+            def samp(yy, xx):
+                fy, fx = np.floor(yy), np.floor(xx)
+                be, al = yy - fy, xx - fx
+                iy0 = int(min(max(fy, 0), H)); iy1 = int(min(max(fy + 1, 0), H))
+                ix0 = int(min(max(fx, 0), W)); ix1 = int(min(max(fx + 1, 0), W))
+                return ((1 - al) * (1 - be) * S[iy0, ix0] + al * (1 - be) * S[iy0, ix1]
+                        + (1 - al) * be * S[iy1, ix0] + al * be * S[iy1, ix1])
+
+            for b in range(B):
+                cx, cy, rx, ry = [float(v) for v in bx[c, b]]
+                for yy in range(H):
+                    for xx in range(W):
+                        xl = xx + 0.5 + cx - rx
+                        xh1 = xx + 0.5 + cx + rx
+                        yl = yy + 0.5 + cy - ry
+                        yh1 = yy + 0.5 + cy + ry
+                        out[n, c * B + b, yy, xx] = (samp(yh1, xh1) + samp(yl, xl)
+                                                     - samp(yh1, xl) - samp(yl, xh1))
+    return out
+
+
+def test_forward_equals_sat_four_corner_bilinear():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((2, 2, 11, 9)).astype(np.float32)
+    bx = _real_boxes(rng, 2, 3, cmax=6.0, rmin=0.3, rmax=7.0)
+    got = O.box_forward(x, bx)
+    want = _four_corner_bilinear(x, bx)
+    assert np.max(np.abs(got - want)) <= 1e-11 * (1 + np.max(np.abs(want)))
+
+
+def test_forward_identity_box_exact():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((2, 3, 8, 6)).astype(np.float32)
+    bx = np.zeros((3, 1, 4), dtype=np.float32)
+    bx[..., 2:] = 0.5
+    np.testing.assert_array_equal(O.box_forward(x, bx), x.astype(np.float64))
+    xi = rng.integers(-5, 6, size=(1, 3, 8, 6)).astype(np.int32)
+    np.testing.assert_array_equal(O.box_forward(xi, bx), xi.astype(np.int64))
+
+
+def test_forward_constant_image_is_area():
+    H, W = 20, 24
+    x = np.ones((1, 1, H, W), dtype=np.float32)
+    bx = np.array([[[0.25, -0.5, 1.25, 1.625], [1.0, 2.0, 3.0, 2.5]]], dtype=np.float32)
+    o = O.box_forward(x, bx)
+    for b in range(2):
+        cx, cy, rx, ry = bx[0, b]
+        m = int(np.ceil(abs(cx) + rx + 1)), int(np.ceil(abs(cy) + ry + 1))
+        interior = o[0, b, m[1]:H - m[1], m[0]:W - m[0]]
+        assert interior.size > 0
+        np.testing.assert_array_equal(interior, np.float64(2 * rx) * np.float64(2 * ry))
+
+
+def test_forward_supersampled_integral():
+    """Edges on a 1/8-pixel grid: refine every pixel into 8x8 sub-pixels of
+    value I/64; the box is then an integer box on the fine grid, summed by
+    brute force.  Exact up to fp64 rounding."""
+    rng = np.random.default_rng(4)
+    H, W, s = 7, 6, 8
+    x = rng.standard_normal((1, 1, H, W)).astype(np.float32)
+    bx = np.empty((1, 3, 4), dtype=np.float32)
+    bx[..., :2] = rng.integers(-12, 13, size=(1, 3, 2)) / 4.0
+    bx[..., 2:] = rng.integers(1, 14, size=(1, 3, 2)) / 8.0  # edges on 1/8 grid
+    got = O.box_forward(x, bx)
+    fine = np.kron(x[0, 0].astype(np.float64), np.ones((s, s))) / (s * s)
+    a, b, c, d = O.box_edges(bx)
+    for k in range(3):
+        for yy in range(H):
+            for xx in range(W):
+                x0, x1 = int(round((xx + a[0, k]) * s)), int(round((xx + b[0, k]) * s))
+                y0, y1 = int(round((yy + c[0, k]) * s)), int(round((yy + d[0, k]) * s))
+                tot = 0.0
+                for i in range(max(y0, 0), min(y1, H * s)):
+                    for j in range(max(x0, 0), min(x1, W * s)):
+                        tot += fine[i, j]
+                assert abs(got[0, k, yy, xx] - tot) <= 1e-12 * (1 + abs(tot))
+
+
+def test_forward_integer_box_equals_library_correlation():
+    """Integer corners reduce to a plain correlation with an all-ones kernel:
+    torch's CPU conv2d in fp64 on a zero-padded map."""
+    rng = np.random.default_rng(5)
+    H, W = 13, 11
+    x = rng.standard_normal((2, 1, H, W))
+    bx = _int_boxes(rng, 1, 5, smax=9, span=6)
+    got = O.box_forward(x, bx)
+    a, b, c, d = O.box_edges(bx)
+    M = 24
+    xp = torch.nn.functional.pad(torch.from_numpy(x), (M, M, M, M))
+    for k in range(5):
+        hh, ww = int(d[0, k] - c[0, k]), int(b[0, k] - a[0, k])
+        ker = torch.ones((1, 1, hh, ww), dtype=torch.float64)
+        full = torch.nn.functional.conv2d(xp, ker).numpy()
+        r0, s0 = int(c[0, k]) + M, int(a[0, k]) + M
+        want = full[:, 0, r0:r0 + H, s0:s0 + W]
+        np.testing.assert_allclose(got[:, k], want, rtol=0, atol=1e-12)
+
+
+def test_forward_naive_overlap_loop_matches():
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((1, 2, 6, 5))
+    bx = _real_boxes(rng, 2, 2, cmax=3.0, rmin=0.2, rmax=4.0)
+    np.testing.assert_allclose(O.box_forward(x, bx), O.naive_box_forward_overlap(x, bx),
+                               rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Input gradient: adjoint of the forward map
+# --------------------------------------------------------------------------
+def test_input_grad_adjoint_and_mirrored_box():
+    rng = np.random.default_rng(7)
+    N, C, B, H, W = 2, 3, 4, 10, 8
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = _real_boxes(rng, C, B, cmax=5.0, rmin=0.2, rmax=6.0)
+    dx = O.box_backward_input(g, bx, H, W)
+    lhs = np.sum(O.box_forward(x, bx) * g)
+    rhs = np.sum(x * dx)
+    assert abs(lhs - rhs) <= 1e-12 * (1 + abs(lhs))
+    # Adjoint = the mirrored box (centre offset negated) applied to dO, summed
+    # over the boxes of each channel.
+    want = np.zeros((N, C, H, W))
+    mb = O.mirrored_boxes(bx)
+    for c in range(C):
+        for b in range(B):
+            want[:, c] += O.box_forward(g[:, c * B + b][:, None], mb[c:c + 1, b:b + 1])[:, 0]
+    np.testing.assert_allclose(dx, want, rtol=0, atol=1e-11)
+
+
+def test_input_grad_finite_difference():
+    rng = np.random.default_rng(8)
+    N, C, B, H, W = 1, 2, 2, 7, 6
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = _real_boxes(rng, C, B, cmax=3.0, rmin=0.3, rmax=3.5)
+    dx = O.box_backward_input(g, bx, H, W)
+    for (c, i, j) in [(0, 0, 0), (1, 3, 2), (0, 6, 5), (1, 2, 5)]:
+        e = np.zeros_like(x)
+        e[0, c, i, j] = 1.0
+        fd = np.sum(O.box_forward(x + e, bx) * g) - np.sum(O.box_forward(x, bx) * g)
+        assert abs(fd - dx[0, c, i, j]) <= 1e-10 * (1 + abs(fd))
+
+
+# --------------------------------------------------------------------------
+# Box-parameter gradient: Eq. 4 and the text after it
+# --------------------------------------------------------------------------
+def _boxes_away_from_kinks(rng, C, B, cmax, rmin, rmax, margin=0.05):
+    """Real boxes whose four edges all sit at least `margin` from an integer,
+    so a small one-sided step stays inside one linear piece."""
+    out = np.empty((C, B, 4), dtype=np.float32)
+    for c in range(C):
+        for b in range(B):
+            while True:
+                p = np.array([rng.uniform(-cmax, cmax), rng.uniform(-cmax, cmax),
+                              rng.uniform(rmin, rmax), rng.uniform(rmin, rmax)],
+                             dtype=np.float32)
+                e = np.array(O.box_edges(p[None])).ravel()
+                f = e - np.floor(e)
+                if np.all((f > margin) & (f < 1 - margin)):
+                    out[c, b] = p
+                    break
+    return out
+
+
+def test_param_grad_finite_difference_exact():
+    """L = <G, O(theta)> is linear in each parameter while no edge crosses a
+    pixel boundary, so a one-sided difference is exact up to rounding."""
+    rng = np.random.default_rng(9)
+    N, C, B, H, W = 2, 2, 3, 12, 10
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = _boxes_away_from_kinks(rng, C, B, 4.0, 0.4, 6.0)
+    grad = O.box_backward_params(x, g, bx)
+    L0 = np.sum(O.box_forward(x, bx) * g)
+    for c in range(C):
+        for b in range(B):
+            for k in range(4):
+                p = bx.copy()
+                p[c, b, k] = np.float32(p[c, b, k] + np.float32(0.01))
+                h = float(p[c, b, k]) - float(bx[c, b, k])
+                fd = (np.sum(O.box_forward(x, p) * g) - L0) / h
+                assert abs(fd - grad[c, b, k]) <= 1e-8 * (1 + abs(fd)), (c, b, k, fd, grad[c, b, k])
+
+
+def test_param_grad_edges_clipped_at_border():
+    """Boxes hanging over the image border: the gradient of the part outside
+    is zero (zero padding); finite differences still agree."""
+    rng = np.random.default_rng(10)
+    N, C, B, H, W = 1, 1, 4, 8, 9
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = _boxes_away_from_kinks(rng, C, B, 9.0, 3.0, 9.0)
+    grad = O.box_backward_params(x, g, bx)
+    L0 = np.sum(O.box_forward(x, bx) * g)
+    for b in range(B):
+        for k in range(4):
+            p = bx.copy()
+            p[0, b, k] = np.float32(p[0, b, k] - np.float32(0.01))
+            h = float(p[0, b, k]) - float(bx[0, b, k])
+            fd = (np.sum(O.box_forward(x, p) * g) - L0) / h
+            assert abs(fd - grad[0, b, k]) <= 1e-8 * (1 + abs(fd))
+
+
+def test_param_grad_constant_image_closed_form():
+    """I = 1, box inside the image: O = (2 rx)(2 ry), so dO/drx = 2 * height,
+    dO/dry = 2 * width, dO/dcx = dO/dcy = 0 at that pixel."""
+    H, W = 16, 16
+    x = np.ones((1, 1, H, W))
+    bx = np.array([[[0.3, -0.7, 2.2, 3.4]]], dtype=np.float32)
+    g = np.zeros((1, 1, H, W))
+    g[0, 0, 8, 8] = 1.0
+    gr = O.box_backward_params(x, g, bx)[0, 0]
+    rx, ry = float(bx[0, 0, 2]), float(bx[0, 0, 3])
+    np.testing.assert_allclose(gr, [0.0, 0.0, 2 * (2 * ry), 2 * (2 * rx)], atol=1e-12)
+
+
+def test_param_grad_right_derivative_at_integer_edge():
+    """At an edge exactly on a pixel boundary the oracle uses each edge's right
+    derivative.  Moving the centre right moves both x edges right, so the
+    cx-gradient equals a forward difference in cx (and generally differs from
+    the backward difference)."""
+    H, W = 9, 9
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((1, 1, H, W))
+    g = rng.standard_normal((1, 1, H, W))
+    bx = np.array([[[0.0, 0.0, 1.5, 1.5]]], dtype=np.float32)  # integer corners
+    grad = O.box_backward_params(x, g, bx)[0, 0]
+    L0 = np.sum(O.box_forward(x, bx) * g)
+    for k in (0, 1):
+        p = bx.copy(); p[0, 0, k] += np.float32(0.125)
+        fd_right = (np.sum(O.box_forward(x, p) * g) - L0) / 0.125
+        assert abs(fd_right - grad[k]) <= 1e-10 * (1 + abs(fd_right))
+        p = bx.copy(); p[0, 0, k] -= np.float32(0.125)
+        fd_left = (L0 - np.sum(O.box_forward(x, p) * g)) / 0.125
+        assert abs(fd_left - grad[k]) > 1e-6
+
+
+# --------------------------------------------------------------------------
+# 1x1 mix
+# --------------------------------------------------------------------------
+def test_bf16_round_matches_torch():
+    rng = np.random.default_rng(13)
+    v = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * np.float32(3.0),
+        np.array([0.0, -0.0, 1.0, 1.00390625, 1.01171875, 1.0078125, 65504.0, 3e38,
+                  1e-40, -1e-40, np.inf, -np.inf], dtype=np.float32),
+        # exact ties: mantissa low half = 0x8000
+        (np.arange(64, dtype=np.uint32) << 16 | 0x3F808000).view(np.float32),
+    ]).astype(np.float32)
+    want = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.bf16_round(v)
+    np.testing.assert_array_equal(got, want)
+    assert np.isnan(O.bf16_round(np.array([np.nan], dtype=np.float32))[0])
+
+
+def test_mix_forward_integer_loops():
+    rng = np.random.default_rng(14)
+    w = rng.integers(-2, 3, size=(3, 5)).astype(np.int32)
+    o = rng.integers(-50, 51, size=(2, 5, 2, 3)).astype(np.int64)
+    z = O.mix_forward(w, o, compute="i32")
+    for n in range(2):
+        for m in range(3):
+            for i in range(2):
+                for j in range(3):
+                    assert z[n, m, i, j] == sum(int(w[m, k]) * int(o[n, k, i, j]) for k in range(5))
+
+
+def test_mix_backward_adjoint_and_weight_loops():
+    rng = np.random.default_rng(15)
+    N, M, K, H, W = 2, 4, 6, 3, 5
+    w = rng.standard_normal((M, K)).astype(np.float32)
+    o = rng.standard_normal((N, K, H, W)).astype(np.float32)
+    gz = rng.standard_normal((N, M, H, W)).astype(np.float32)
+    for comp in ("f32", "bf16"):
+        lhs = np.sum(O.mix_forward(w, o, compute=comp) * O.bf16_round(gz) if comp == "bf16"
+                     else O.mix_forward(w, o, compute=comp) * gz)
+        ob = O.bf16_round(o) if comp == "bf16" else o.astype(np.float64)
+        rhs = np.sum(ob * O.mix_backward_data(w, gz, compute=comp))
+        assert abs(lhs - rhs) <= 1e-10 * (1 + abs(lhs))
+        dw = O.mix_backward_weight(gz, o, compute=comp)
+        gb = O.bf16_round(gz) if comp == "bf16" else gz.astype(np.float64)
+        for m in range(M):
+            for k in range(K):
+                s = 0.0
+                for n in range(N):
+                    for p in range(H * W):
+                        s += gb[n, m].ravel()[p] * ob[n, k].ravel()[p]
+                assert abs(dw[m, k] - s) <= 1e-10 * (1 + abs(s))
+
+
+def test_relu_mask_in_backward():
+    rng = np.random.default_rng(16)
+    w = rng.standard_normal((3, 4))
+    z = rng.standard_normal((1, 3, 2, 2))
+    gz = rng.standard_normal((1, 3, 2, 2))
+    got = O.mix_backward_data(w, gz, relu_out=np.maximum(z, 0))
+    want = O.mix_backward_data(w, gz * (z > 0))
+    np.testing.assert_allclose(got, want, atol=0)
+
+
+# --------------------------------------------------------------------------
+# Whole stacked layers: scalar-loss finite differences (fp64, 'f32' operands)
+# --------------------------------------------------------------------------
+def test_stack_two_layers_finite_differences():
+    rng = np.random.default_rng(17)
+    N, C, B, H, W, M = 1, 2, 2, 8, 7, 2
+    x = np.abs(rng.standard_normal((N, C, H, W)))
+    layers = [(_boxes_away_from_kinks(rng, C, B, 3.0, 0.4, 4.0),
+               rng.standard_normal((M, C * B)) / 2.0) for _ in range(2)]
+    G = rng.standard_normal((N, M, H, W))
+
+    def loss(xx, lys):
+        return float(np.sum(O.stack_forward(xx, lys)[-1][2] * G))
+
+    cache = O.stack_forward(x, layers)
+    dx, grads = O.stack_backward(cache, layers, G)
+    L0 = loss(x, layers)
+    # the relu kinks: the step must not flip any sign
+    zs = np.concatenate([c[2].ravel() for c in cache])
+    assert np.min(np.abs(zs[zs != 0])) > 1e-6
+    h = 1e-7
+    for (c, i, j) in [(0, 1, 1), (1, 4, 5)]:
+        e = np.zeros_like(x); e[0, c, i, j] = h
+        fd = (loss(x + e, layers) - L0) / h
+        assert abs(fd - dx[0, c, i, j]) <= 1e-5 * (1 + abs(fd))
+    for li in range(2):
+        for (m, k) in [(0, 1), (1, 3)]:
+            lys = [(b_, w_.copy()) for b_, w_ in layers]
+            lys[li][1][m, k] += h
+            fd = (loss(x, lys) - L0) / h
+            assert abs(fd - grads[li][1][m, k]) <= 1e-5 * (1 + abs(fd))
+        for (c, b, k) in [(0, 1, 0), (1, 0, 3)]:
+            lys = [(b_.copy(), w_) for b_, w_ in layers]
+            lys[li][0][c, b, k] = np.float32(lys[li][0][c, b, k] + np.float32(0.01))
+            hh = float(lys[li][0][c, b, k]) - float(layers[li][0][c, b, k])
+            fd = (loss(x, lys) - L0) / hh
+            # relu can switch sign over a finite step; the step is small and
+            # the data smooth enough that this case stays linear
+            assert abs(fd - grads[li][0][c, b, k]) <= 1e-4 * (1 + abs(fd))
+
+
+# --------------------------------------------------------------------------
+# Comparison metric
+# --------------------------------------------------------------------------
+def test_rel_errors_metric():
+    r = np.array([1.0, -2.0, 0.0, 3.0])
+    pw, nw = O.rel_errors(r, r)
+    assert pw == 0 and nw == 0
+    pw, _ = O.rel_errors(r + np.array([0, 0, 1e-3, 0]), r)
+    rms = np.sqrt(np.mean(r * r))
+    assert abs(pw - 1e-3 / rms) < 1e-12
+
+
+# --------------------------------------------------------------------------
+# Planted mistakes: each plausible bug in the oracle must break some pin.
+# --------------------------------------------------------------------------
+import oracle.boxconv_oracle as _OM  # noqa: E402
+
+
+def _mut_edges_sign(boxes):
+    p = np.asarray(boxes, dtype=np.float32).astype(np.float64)
+    cx, cy, rx, ry = p[..., 0], p[..., 1], p[..., 2], p[..., 3]
+    return 0.5 - cx - rx, 0.5 - cx + rx, 0.5 + cy - ry, 0.5 + cy + ry
+
+
+def _mut_edges_corner_origin(boxes):
+    p = np.asarray(boxes, dtype=np.float32).astype(np.float64)
+    cx, cy, rx, ry = p[..., 0], p[..., 1], p[..., 2], p[..., 3]
+    return cx - rx, cx + rx, cy - ry, cy + ry
+
+
+def _mut_overlap_no_padding(n, lo, hi):
+    # wraps around instead of treating outside pixels as zero
+    m = _ORIG["overlap_matrix"](3 * n, lo + n, hi + n)[n:2 * n]
+    return m[:, :n] + m[:, n:2 * n] + m[:, 2 * n:]
+
+
+def _mut_mirror_x_only(boxes):
+    m = np.array(boxes, dtype=np.float32, copy=True)
+    m[..., 0] = -m[..., 0]
+    return m
+
+
+def _mut_edge_selector_ceil(n, edge):
+    return _ORIG["_edge_selector"](n, edge + 1.0)
+
+
+def _mut_param_sign(x, grad_y, boxes):
+    e = _OM.box_param_grad_from_edges(x, grad_y, boxes)
+    ga, gb, gc, gd = e[..., 0], e[..., 1], e[..., 2], e[..., 3]
+    return np.stack([ga + gb, gc + gd, ga - gb, gd - gc], axis=-1)
+
+
+def _mut_bf16_truncate(v):
+    f = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
+    u = (f.view(np.uint32) >> np.uint32(16)) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+def _mut_backward_input_no_transpose(grad_y, boxes, H, W):
+    g = np.asarray(grad_y, dtype=np.float64)
+    C, B = boxes.shape[0], boxes.shape[1]
+    N = g.shape[0]
+    g = g.reshape(N, C, B, H, W)
+    a, b, c, d = _OM.box_edges(boxes)
+    out = np.zeros((N, C, H, W))
+    for ci in range(C):
+        for bi in range(B):
+            wx = _OM.overlap_matrix(W, a[ci, bi], b[ci, bi])
+            wy = _OM.overlap_matrix(H, c[ci, bi], d[ci, bi])
+            out[:, ci] += wy @ g[:, ci, bi] @ wx.T
+    return out
+
+
+_ORIG = {k: getattr(_OM, k) for k in ("overlap_matrix", "_edge_selector")}
+
+_MUTATIONS = {
+    "edges_sign": ("box_edges", _mut_edges_sign),
+    "edges_corner_origin": ("box_edges", _mut_edges_corner_origin),
+    "overlap_wraps": ("overlap_matrix", _mut_overlap_no_padding),
+    "mirror_x_only": ("mirrored_boxes", _mut_mirror_x_only),
+    "edge_selector_ceil": ("_edge_selector", _mut_edge_selector_ceil),
+    "param_sign": ("box_backward_params", _mut_param_sign),
+    "bf16_truncate": ("bf16_round", _mut_bf16_truncate),
+    "bwd_input_no_transpose": ("box_backward_input", _mut_backward_input_no_transpose),
+}
+
+_PINS = [
+    test_forward_equals_eq1_loops_integer, test_forward_equals_sat_four_corner_bilinear,
+    test_forward_identity_box_exact, test_forward_supersampled_integral,
+    test_forward_integer_box_equals_library_correlation,
+    test_input_grad_adjoint_and_mirrored_box, test_input_grad_finite_difference,
+    test_param_grad_finite_difference_exact, test_param_grad_edges_clipped_at_border,
+    test_param_grad_constant_image_closed_form, test_bf16_round_matches_torch,
+]
+
+
+@pytest.mark.parametrize("name", sorted(_MUTATIONS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, fn = _MUTATIONS[name]
+    monkeypatch.setattr(_OM, attr, fn)
+    import oracle
+    if hasattr(oracle, attr):
+        monkeypatch.setattr(oracle, attr, fn)
+    caught = []
+    for pin in _PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin caught mutation {name}"
