@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the SAT box-convolution layer on one MI355X.
+
+One step = one pass of the whole layer over one batch: box filter forward
+(table + four-corner bilinear lookups), 1x1 mix forward (MFMA), mix backward
+to the weights and to the filtered maps, and the box filter backward (input
+and box-parameter gradients).  Inputs are seeded synthetic arrays shaped like
+pose-estimation feature maps, already resident in HBM when timing starts.
+
+Prints ONE JSON line.  `value` is filtered-map elements (pixel*box, summed over
+layers) per second of the whole step, in Gpix*box/s.  `roofline` reports the
+dominant library call, timed with HIP events on the stream it runs on;
+`cpu_baseline` times the CPU oracle on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "box-conv fwd+bwd Gpix·box/s; SAT/box HBM GB/s and 1×1 MFMA util vs peak"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+DEFAULT_WORKLOAD = 3
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", type=int, default=DEFAULT_WORKLOAD, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget-s", type=float, default=20.0,
+                   help="rough CPU time the oracle sample may take")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 256 MiB device-to-device copy 5 times (reference for the "
+                        "FETCH_SIZE / WRITE_SIZE counters) and exit")
+    return p.parse_args()
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1906_11367_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def call_cost(label, wl, o_bytes):
+    """Algorithmic bytes and FLOPs of one launch of a library call (one layer).
+
+    box_conv_fwd : read x (4 B/pixel) + write O (o_bytes per pixel*box)
+    box_conv_bwd : read x + read dO (4 B/pixel*box) + write dx (4 B/pixel)
+    mix_*        : 2*N*M*K*P FLOPs (one GEMM)
+    """
+    px = wl.N * wl.C * wl.H * wl.W
+    pb = px * wl.B
+    if label == "box_conv_fwd":
+        return {"bound": "hbm", "bytes": 4 * px + o_bytes * pb}
+    if label == "box_conv_bwd":
+        return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 4 * px}
+    flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * wl.H * wl.W
+    return {"bound": "mfma", "flops": flops}
+
+
+def load_traffic(label, wl_key, src_hash):
+    """HBM bytes per launch measured with rocprofv3 counters, if a committed
+    summary for this call and workload exists and the sources have not
+    changed since it was taken; else None."""
+    path = os.path.join(ROOT, "profiles", f"{label}_{wl_key}_counters.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            d = json.load(f)
+        if d.get("source_hash") != src_hash:
+            return None
+        return float(d["hbm_bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def cpu_baseline(wl, d, budget_s):
+    """Times the CPU oracle (fwd + bwd of the layer) on a sample of images.
+
+    The sample keeps every channel and box of the workload and takes the
+    first n images (n chosen from a one-image probe to fit the budget)."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = None
+
+    def run(n):
+        x = d["x"][:n]
+        g = d["grad"][:n] if d["grad"] is not None else None
+        if wl.layers > 1:
+            layers = d["layers"][:1]   # one layer of the stack per sample image
+            cache = O.stack_forward(x, layers, compute=wl.mix_dtype, apply_relu=wl.relu)
+            O.stack_backward(cache, layers, g, compute=wl.mix_dtype, apply_relu=wl.relu)
+            return n * wl.C * wl.B * wl.H * wl.W
+        o = O.box_forward(x, d["boxes"])
+        if wl.mix_out is None:
+            if g is not None:
+                O.box_backward_input(g, d["boxes"], wl.H, wl.W)
+                O.box_backward_params(x, g, d["boxes"])
+            return n * wl.C * wl.B * wl.H * wl.W
+        O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
+        if g is not None:
+            O.mix_backward_weight(g, o, compute=wl.mix_dtype)
+            do = O.mix_backward_data(d["w"], g, compute=wl.mix_dtype)
+            O.box_backward_input(do, d["boxes"], wl.H, wl.W)
+            O.box_backward_params(x, do, d["boxes"])
+        return n * wl.C * wl.B * wl.H * wl.W
+
+    t0 = time.perf_counter()
+    pb = run(1)
+    t1 = time.perf_counter() - t0
+    n = int(max(1, min(wl.N, budget_s / max(t1, 1e-3))))
+    if n > 1:
+        t0 = time.perf_counter()
+        pb = run(n)
+        t1 = time.perf_counter() - t0
+    return {"value": pb / t1 / 1e9, "unit": "Gpix·box/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of {wl.N} images, all {wl.C} channels x {wl.B} boxes, one layer, "
+                      f"fwd+bwd, fp64 NumPy, {t1:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the layer's multi-GPU sharding is a design note only)", file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_per_launch": src.numel() * 4, "launches": 5}), flush=True)
+        return 0
+
+    from paper_1906_11367_amd import boxconv as bc
+    from paper_1906_11367_amd import workloads as wlmod
+    from paper_1906_11367_amd.layer import Stack
+
+    bc.load_library()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = wlmod.WORKLOADS[args.workload]
+    print(f"[bench] workload {wl.key}: generating inputs", file=sys.stderr, flush=True)
+    d = wlmod.make_inputs(wl)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    x = dev(d["x"])
+    params = [(dev(b), dev(w) if w is not None else None) for b, w in d["layers"]]
+    grad = dev(d["grad"]) if d["grad"] is not None else None
+    x_dt = torch.int32 if wl.x_kind == "int8range" else torch.float32
+    flags = bc.BC_FLAG_MEAN_OFFSET if wl.mean_offset else 0
+    st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, wl.mix_dtype, wl.relu, x_dt, flags,
+               wl.backward)
+    stream = torch.cuda.current_stream()
+    timing = {"on": False, "events": []}
+
+    def tap(label):
+        if timing["on"]:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            timing["events"].append((label, e))
+
+    def step():
+        if timing["on"]:
+            tap("start")
+        inputs, out = st.forward(x, params, tap)
+        if wl.backward:
+            st.backward(inputs, params, grad, tap)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: plain steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # second timed pass with an event after every library call
+    timing["on"] = True
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per = {}
+    evs = timing["events"]
+    for (l0, a), (l1, b) in zip(evs[:-1], evs[1:]):
+        if l1 == "start":
+            continue
+        per.setdefault(l1, []).append(a.elapsed_time(b))
+    o_bytes = 2 if (wl.mix_out is not None and wl.mix_dtype == "bf16") else 4
+    src_hash = source_hash()
+    calls = {}
+    for label, ts in per.items():
+        avg_ms = sum(ts) / len(ts)
+        c = call_cost(label, wl, o_bytes)
+        ent = {"avg_us": round(avg_ms * 1e3, 2), "launches": len(ts) // args.steps, "bound": c["bound"],
+               "share": round(sum(ts) / args.steps / ms, 3)}
+        if c["bound"] == "hbm":
+            ent["algo_bytes"] = c["bytes"]
+            ent["achieved"] = c["bytes"] / (avg_ms * 1e-3) / 1e9
+            ent["peak"] = HBM_PEAK_GBS
+            ent["unit"] = "GB/s"
+        else:
+            ent["algo_flops"] = c["flops"]
+            ent["achieved"] = c["flops"] / (avg_ms * 1e-3) / 1e12
+            ent["peak"] = MFMA_PEAK_TFLOPS["bf16" if wl.mix_dtype == "bf16" else "f32"]
+            ent["unit"] = "TFLOP/s"
+        ent["frac"] = ent["achieved"] / ent["peak"]
+        ent["achieved"] = round(ent["achieved"], 2)
+        ent["frac"] = round(ent["frac"], 4)
+        calls[label] = ent
+    dom = max(calls, key=lambda k: calls[k]["avg_us"] * calls[k]["launches"])
+    dc = calls[dom]
+    traffic = load_traffic(dom, wl.key, src_hash)
+    roofline = {"bound": dc["bound"], "achieved": dc["achieved"], "peak": dc["peak"], "unit": dc["unit"],
+                "frac": dc["frac"], "traffic": traffic, "kernel": dom, "avg_us": dc["avg_us"],
+                "per_launch": ("algo_bytes=%d" % dc["algo_bytes"]) if dc["bound"] == "hbm"
+                else ("algo_flops=%d" % dc["algo_flops"])}
+
+    pix_box = wl.pixel_box * wl.layers
+    value = pix_box / (ms * 1e-3) / 1e9
+    box_ms = sum(calls[k]["avg_us"] * calls[k]["launches"] for k in calls if k.startswith("box")) / 1e3
+    line = {
+        "metric": METRIC, "value": round(value, 3), "unit": "Gpix·box/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if x_dt == torch.float32 else "i32",
+        "data": "synthetic",
+        "config": {"workload": wl.key, "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "B": wl.B,
+                   "mix": None if wl.mix_out is None else f"{wl.C * wl.B}->{wl.mix_out} {wl.mix_dtype}",
+                   "layers": wl.layers, "relu": wl.relu, "mean_offset": wl.mean_offset,
+                   "parallelism": "single GPU"},
+        "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
+        "roofline": roofline,
+        "calls": calls,
+        "source_hash": src_hash,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,197 @@
+/*
+ * boxconv.h -- C ABI of the MI355X (gfx950) summed-area-table box-convolution
+ * layer: Zhang, Halber, Rusinkiewicz, "Accelerating Large-Kernel Convolution
+ * Using Summed-Area Tables".
+ *
+ * The layer (Section 3.1 and 3.2 of the paper):
+ *   1. per input channel, an exclusive summed-area table of the H x W map;
+ *   2. B boxes per channel applied depthwise: each output pixel reads the
+ *      table at the box's four corners (Eq. 2), a corner at a sub-pixel
+ *      position by bilinear interpolation of the table (Eq. 3), whatever the
+ *      box size;
+ *   3. a 1x1 convolution mixing the C*B filtered maps;
+ *   and their gradients: to the input, to the box parameters (Eq. 4) and to
+ *   the 1x1 weights.
+ *
+ * Conventions common to every entry point
+ *   - Tensors are dense, row-major, NCHW.  Every pointer argument that names a
+ *     tensor is a DEVICE pointer, 16-byte aligned; otherwise BC_ERR_ALIGN.
+ *   - Box parameters are device fp32 [C][B][4] = (cx, cy, rx, ry) in pixels:
+ *     (cx, cy) offsets the box centre from the output pixel's centre, rx, ry
+ *     are its half-width and half-height (the paper's four variables: the x,y
+ *     location and the size).  For output pixel (x, y), whose cell is
+ *     [x, x+1) x [y, y+1), the box covers [x + a, x + b) x [y + c, y + d),
+ *     a = 1/2 + cx - rx, b = 1/2 + cx + rx, c = 1/2 + cy - ry,
+ *     d = 1/2 + cy + ry; the paper's integer corners are x_l = a, x_h = b - 1,
+ *     y_l = c, y_h = d - 1.  cx = cy = 0, rx = ry = 1/2 is the identity.
+ *     rx, ry >= 0 is the caller's precondition (not checked: the values live
+ *     on the device).
+ *   - Output channel of box b on input channel c is c*B + b.  Stride 1,
+ *     output size = input size, pixels outside the map are zero.
+ *   - The caller owns every buffer and keeps it alive until the stream has
+ *     finished the call.  The library allocates nothing and keeps no pointer
+ *     after returning.  Workspaces are caller-provided device memory of at
+ *     least bc_*_workspace_bytes() bytes; their contents on entry are ignored.
+ *   - Every call is asynchronous on `stream` (0 = the null stream).  Argument
+ *     errors return before anything is launched.  A failed launch returns
+ *     BC_ERR_HIP.  Faults during execution surface at the caller's sync.
+ *   - Outputs are overwritten (pointwise_mix with accumulate = 1 excepted).
+ */
+#ifndef BOXCONV_H
+#define BOXCONV_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BC_OK = 0,
+  BC_ERR_NULL = 1,        /* a required pointer is NULL */
+  BC_ERR_SHAPE = 2,       /* a size is non-positive, too large, or inconsistent */
+  BC_ERR_DTYPE = 3,       /* unsupported dtype or dtype combination */
+  BC_ERR_ALIGN = 4,       /* a tensor pointer is not 16-byte aligned */
+  BC_ERR_WORKSPACE = 5,   /* workspace missing or smaller than required */
+  BC_ERR_HIP = 6,         /* the HIP runtime reported an error at launch */
+  BC_ERR_UNSUPPORTED = 7  /* valid request this build does not implement */
+} bc_status;
+
+typedef enum { BC_I32 = 0, BC_F32 = 1, BC_BF16 = 2 } bc_dtype;
+
+typedef enum {
+  BC_MIX_FWD = 0,         /* out[n] = w * in[n]                          */
+  BC_MIX_BWD_DATA = 1,    /* out[n] = w^T * grad[n]                      */
+  BC_MIX_BWD_WEIGHT = 2   /* out    = sum_n grad[n] * in[n]^T            */
+} bc_mix_mode;
+
+/* Flags of box_conv_fwd / box_conv_bwd. */
+#define BC_FLAG_MEAN_OFFSET 1u   /* fp32 only: build the table of (map - mean of
+                                    the map) and add mean * (clipped box area)
+                                    back analytically; limits cancellation in
+                                    large tables. */
+#define BC_FLAG_FORCE_HBM 2u     /* use the HBM-table path even when a map's table
+                                    fits in LDS (both paths compute the same). */
+
+/* ------------------------------------------------------------------------
+ * box_prep -- the per-box precomputation of Section 3.1 (after Eq. 4): since
+ * integer shifts leave the corner fractions unchanged, each box is reduced
+ * once to integer tap offsets and bilinear weights.
+ *
+ * boxes : device fp32 [C][B][4] (cx, cy, rx, ry).
+ * table : device, 2*C*B records of 16 32-bit words.  Record r < C*B is box r
+ *         (r = c*B + b); record C*B + r is its mirror (centre offset negated:
+ *         the box whose correlation is the transpose of box r's).  Words:
+ *           0..3  int32  floor(a), floor(b), floor(c), floor(d), each clamped
+ *                        to [-2^20, 2^20]; edges evaluated in fp64;
+ *           4..7  fp32   x weights of columns floor(a), floor(a)+1, floor(b),
+ *                        floor(b)+1: alpha_a - 1, -alpha_a, 1 - alpha_b,
+ *                        alpha_b (alpha = edge - floor(edge), in fp64, then
+ *                        rounded once to fp32);
+ *           8..11 fp32   y weights, same for c, d;
+ *          12..15        zero.
+ *         The 16 tap weights of the paper are the products of an x and a y
+ *         weight.  The other entry points compute this internally; it is
+ *         exported for inspection and testing.
+ * ---------------------------------------------------------------------- */
+bc_status box_prep(const float* boxes, int C, int B, void* table, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * sat_build -- the summed-area table (Section 3.1, before Eq. 2), exclusive
+ * form: sat[m][u][v] = sum_{i<u, j<v} x[m][i][j] for u in [0,H], v in [0,W]
+ * (row 0 and column 0 are zero; rows/columns 1.. are the paper's inclusive
+ * table).  m ranges over the N*C maps.
+ *
+ * x      : device [N*C][H][W], dtype dt (BC_I32 or BC_F32).
+ * sat    : device [N*C][H+1][W+1], same dtype as x.  int32 arithmetic wraps
+ *          if |x| * H * W >= 2^31 (the caller's precondition).
+ * mean   : NULL, or (BC_F32 only) device fp32 [N*C]: the call then writes
+ *          each map's mean there and tabulates (x - mean) instead of x.
+ * Limits : 1 <= W <= 1024.
+ * ---------------------------------------------------------------------- */
+bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
+                    int N, int C, int H, int W, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * box_conv_fwd -- depthwise box filter by four bilinear table lookups per box
+ * (Section 3.1, Eq. 2-3; Section 3.2):
+ *   y[n][c*B+b][v][u] = integral of the zero-padded map x[n][c] over the box
+ *   [u+a, u+b) x [v+c, v+d) of box (c, b).
+ *
+ * x      : device [N][C][H][W], x_dt = BC_I32 or BC_F32.
+ * y      : device [N][C*B][H][W]; y_dt = BC_I32 iff x_dt = BC_I32, else
+ *          BC_F32 or BC_BF16 (the fp32 result rounded to nearest even).
+ * BC_I32 : corners are floored (fractions ignored) and the sum is exact int32
+ *          arithmetic -- callers pass integer corners (half-integer cx - rx).
+ * flags  : BC_FLAG_MEAN_OFFSET (BC_F32), BC_FLAG_FORCE_HBM.
+ * ws     : >= bc_box_workspace_bytes(0, ...) bytes (0 when the map's table fits
+ *          in LDS and BC_FLAG_FORCE_HBM is not set).
+ * ---------------------------------------------------------------------- */
+bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
+                       int N, int C, int H, int W, int B,
+                       void* y, bc_dtype y_dt, unsigned flags,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * box_conv_bwd -- gradients of L = <grad_y, y> (fp32):
+ *   grad_x[n][c] = sum_b (box (c,b))^T grad_y[n][c*B+b]: the transposed box
+ *     sum, evaluated as the mirrored box (centre offset negated) read from the
+ *     summed-area table of each upstream-gradient map.
+ *   grad_boxes[c][b] = d L / d(cx, cy, rx, ry): each edge's derivative is the
+ *     integral of x along that edge (Eq. 4 differenced between the box's two
+ *     corners on that edge), read from the table of x; at an edge lying
+ *     exactly on a pixel boundary the right derivative is taken.
+ *
+ * x          : device fp32 [N][C][H][W]     (the forward input)
+ * grad_y     : device fp32 [N][C*B][H][W]
+ * grad_x     : device fp32 [N][C][H][W] or NULL (skip)
+ * grad_boxes : device fp32 [C][B][4] or NULL (skip); summed over n with a
+ *              fixed-order (deterministic) reduction.
+ * ws         : >= bc_box_workspace_bytes(1, ...) bytes.
+ * ---------------------------------------------------------------------- */
+bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
+                       int N, int C, int H, int W, int B,
+                       float* grad_x, float* grad_boxes, unsigned flags,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * pointwise_mix -- the 1x1 convolution over the C*B filtered maps
+ * (Section 1, Section 3.2), per image n with P = H*W pixels, on MFMA:
+ *   BC_MIX_FWD        : a = w [M][K], b = in [N][K][P]   -> out [N][M][P]
+ *   BC_MIX_BWD_DATA   : a = w [M][K], b = grad [N][M][P] -> out [N][K][P]
+ *   BC_MIX_BWD_WEIGHT : a = grad [N][M][P], b = in [N][K][P] -> out [M][K]
+ * compute_dt : BC_F32  (fp32 operands and accumulation; exact for integer
+ *                       data while every partial sum stays below 2^24),
+ *              BC_BF16 (operands rounded to bf16, nearest even, on load;
+ *                       fp32 accumulation).
+ * a_dt, b_dt : dtype of the stored operands: BC_F32, BC_BF16 (bf16 storage,
+ *              compute_dt must be BC_BF16) or BC_I32 (compute_dt BC_F32,
+ *              values converted exactly while |v| < 2^24).
+ * out_dt     : BC_F32, or BC_I32 when both operands are BC_I32.
+ * relu       : FWD: out = max(out, 0).  BWD_DATA / BWD_WEIGHT: the incoming
+ *              gradient is multiplied by (aux > 0), aux = the forward output
+ *              [N][M][P] fp32 (required then).
+ * accumulate : BWD_WEIGHT only: 1 = out += result.
+ * ws         : >= bc_mix_workspace_bytes(mode, ...) bytes.
+ * ---------------------------------------------------------------------- */
+bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt,
+                        const void* b, bc_dtype b_dt, void* out, bc_dtype out_dt,
+                        int N, int M, int K, int P, bc_dtype compute_dt,
+                        int relu, const float* aux, int accumulate,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd. */
+size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags);
+size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt);
+
+/* Human-readable status; never NULL. */
+const char* bc_status_string(bc_status s);
+
+/* ABI version of this library (incremented on incompatible changes). */
+int bc_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BOXCONV_H */

@@ -1,0 +1,158 @@
+"""Thin ctypes binding of libboxconv.so (C ABI: include/boxconv.h).
+
+Argument marshalling only: tensors are passed as device pointers together with
+torch's current HIP stream; every step of the layer runs in the library's
+kernels.  The library is required: if it is not built, or a GPU is not
+present, the calls raise -- there is no fallback implementation.
+
+Entry points (same names as the C ABI): box_prep, sat_build, box_conv_fwd,
+box_conv_bwd, pointwise_mix, plus the workspace-size queries.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libboxconv.so")
+
+BC_I32, BC_F32, BC_BF16 = 0, 1, 2
+BC_MIX_FWD, BC_MIX_BWD_DATA, BC_MIX_BWD_WEIGHT = 0, 1, 2
+BC_FLAG_MEAN_OFFSET, BC_FLAG_FORCE_HBM = 1, 2
+STATUS = {0: "BC_OK", 1: "BC_ERR_NULL", 2: "BC_ERR_SHAPE", 3: "BC_ERR_DTYPE", 4: "BC_ERR_ALIGN",
+          5: "BC_ERR_WORKSPACE", 6: "BC_ERR_HIP", 7: "BC_ERR_UNSUPPORTED"}
+
+# Exported symbols and their C signatures (kept in step with boxconv.h).
+_vp, _i, _u, _sz, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint, ctypes.c_size_t, ctypes.c_float
+SIGNATURES = {
+    "box_prep": (_i, [_vp, _i, _i, _vp, _vp]),
+    "sat_build": (_i, [_vp, _i, _vp, _vp, _i, _i, _i, _i, _vp]),
+    "box_conv_fwd": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
+    "box_conv_bwd": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
+    "pointwise_mix": (_i, [_i, _vp, _i, _vp, _i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
+    "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
+    "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
+    "bc_status_string": (ctypes.c_char_p, [_i]),
+    "bc_abi_version": (_i, []),
+}
+
+_lib = None
+
+
+class BoxConvError(RuntimeError):
+    pass
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libboxconv.so (no GPU needed to load it)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise BoxConvError(f"{path} is not built: run `python -m paper_1906_11367_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        msg = load_library().bc_status_string(status).decode()
+        raise BoxConvError(f"{what}: {STATUS.get(status, status)} ({msg})")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise BoxConvError("tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise BoxConvError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.int32:
+        return BC_I32
+    if t.dtype == torch.float32:
+        return BC_F32
+    if t.dtype == torch.bfloat16:
+        return BC_BF16
+    raise BoxConvError(f"unsupported dtype {t.dtype}")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor | None:
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def box_workspace_bytes(op: int, N, C, H, W, B, flags=0) -> int:
+    return int(load_library().bc_box_workspace_bytes(op, N, C, H, W, B, flags))
+
+
+def mix_workspace_bytes(mode: int, N, M, K, P, compute_dt) -> int:
+    return int(load_library().bc_mix_workspace_bytes(mode, N, M, K, P, compute_dt))
+
+
+def box_prep(boxes: torch.Tensor, table: torch.Tensor):
+    """table: int32 tensor of 2*C*B*16 words (see boxconv.h)."""
+    C, B = boxes.shape[0], boxes.shape[1]
+    _check(load_library().box_prep(_ptr(boxes), C, B, _ptr(table), _stream()), "box_prep")
+    return table
+
+
+def sat_build(x: torch.Tensor, sat: torch.Tensor, mean: torch.Tensor | None = None):
+    """x [N, C, H, W] int32/fp32 -> sat [N, C, H+1, W+1] (exclusive table)."""
+    N, C, H, W = x.shape
+    _check(load_library().sat_build(_ptr(x), dtype_code(x), _ptr(sat), _ptr(mean), N, C, H, W, _stream()),
+           "sat_build")
+    return sat
+
+
+def box_conv_fwd(x: torch.Tensor, boxes: torch.Tensor, y: torch.Tensor, flags: int = 0,
+                 ws: torch.Tensor | None = None):
+    """x [N, C, H, W], boxes [C, B, 4] fp32 -> y [N, C*B, H, W] (int32, fp32 or bf16)."""
+    N, C, H, W = x.shape
+    B = boxes.shape[1]
+    if ws is None:
+        ws = _workspace(box_workspace_bytes(0, N, C, H, W, B, flags), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().box_conv_fwd(_ptr(x), dtype_code(x), _ptr(boxes), N, C, H, W, B, _ptr(y),
+                                       dtype_code(y), flags, _ptr(ws), nbytes, _stream()), "box_conv_fwd")
+    return y
+
+
+def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, grad_x: torch.Tensor | None,
+                 grad_boxes: torch.Tensor | None, flags: int = 0, ws: torch.Tensor | None = None):
+    N, C, H, W = x.shape
+    B = boxes.shape[1]
+    if ws is None:
+        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().box_conv_bwd(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, _ptr(grad_x),
+                                       _ptr(grad_boxes), flags, _ptr(ws), nbytes, _stream()), "box_conv_bwd")
+    return grad_x, grad_boxes
+
+
+def pointwise_mix(mode: int, a: torch.Tensor, b: torch.Tensor, out: torch.Tensor, N: int, M: int, K: int,
+                  P: int, compute_dt: int, relu: int = 0, aux: torch.Tensor | None = None,
+                  accumulate: int = 0, ws: torch.Tensor | None = None):
+    if ws is None:
+        ws = _workspace(mix_workspace_bytes(mode, N, M, K, P, compute_dt), a.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().pointwise_mix(mode, _ptr(a), dtype_code(a), _ptr(b), dtype_code(b), _ptr(out),
+                                        dtype_code(out), N, M, K, P, compute_dt, relu, _ptr(aux), accumulate,
+                                        _ptr(ws), nbytes, _stream()), "pointwise_mix")
+    return out

@@ -1,0 +1,214 @@
+// C-ABI front end: argument validation, path selection, workspace layout and
+// launches.  Every check runs on the host before anything is enqueued.
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/boxconv.h"
+#include "bc_internal.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;           // workspace sub-buffer alignment
+constexpr size_t kLdsBudget = 64 * 1024; // LDS per block for the table paths
+constexpr long kMaxDim = 1 << 16;
+
+inline size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool dims_ok(long N, long C, long H, long W, long B) {
+  if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || B <= 0) return false;
+  if (N > kMaxDim || C > kMaxDim || H > kMaxDim || W > kMaxDim || B > kMaxDim) return false;
+  // plane and grid indices stay within int range
+  if ((long)H * W > (1L << 30)) return false;
+  if (N * C * B > (1L << 30)) return false;
+  return true;
+}
+
+size_t table_elems(int H, int W) { return (size_t)(H + 1) * (W + 1); }
+
+bool fwd_lds_fits(int H, int W) {
+  return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget;
+}
+bool bwd_lds_fits(int N, int C, int H, int W) {
+  return (size_t)2 * (H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(N, C, H, W) > 0;
+}
+
+struct FwdWs { size_t sat, means, total; };
+FwdWs fwd_ws(int N, int C, int H, int W) {
+  FwdWs w;
+  w.sat = 0;
+  w.means = align_up((size_t)N * C * table_elems(H, W) * 4);
+  w.total = w.means + align_up((size_t)N * C * 4);
+  return w;
+}
+
+struct BwdWs { size_t sat_x, means, sat_g, partials, total; int P; };
+BwdWs bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+  BwdWs w{};
+  if (!hbm) {
+    w.P = N;
+    w.partials = 0;
+    w.total = align_up((size_t)N * C * B * 4 * 4);
+    return w;
+  }
+  const int nblk = bc::box_bwd_gather_blocks(H, W);
+  w.P = N * nblk;
+  w.sat_x = 0;
+  w.means = align_up((size_t)N * C * table_elems(H, W) * 4);
+  w.sat_g = w.means + align_up((size_t)N * C * 4);
+  w.partials = w.sat_g + align_up((size_t)N * C * B * table_elems(H, W) * 4);
+  w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
+  return w;
+}
+
+bc_status hip_status(hipError_t e) { return e == hipSuccess ? BC_OK : BC_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int bc_abi_version(void) { return 1; }
+
+const char* bc_status_string(bc_status s) {
+  switch (s) {
+    case BC_OK: return "ok";
+    case BC_ERR_NULL: return "a required pointer is NULL";
+    case BC_ERR_SHAPE: return "invalid or unsupported shape";
+    case BC_ERR_DTYPE: return "unsupported dtype or dtype combination";
+    case BC_ERR_ALIGN: return "a tensor pointer is not 16-byte aligned";
+    case BC_ERR_WORKSPACE: return "workspace missing or too small";
+    case BC_ERR_HIP: return "HIP runtime error at launch";
+    case BC_ERR_UNSUPPORTED: return "unsupported request";
+  }
+  return "unknown status";
+}
+
+bc_status box_prep(const float* boxes, int C, int B, void* table, hipStream_t stream) {
+  if (!boxes || !table) return BC_ERR_NULL;
+  if (C <= 0 || B <= 0 || (long)C * B > (1L << 28)) return BC_ERR_SHAPE;
+  if (!aligned16(boxes) || !aligned16(table)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_box_prep(boxes, C, B, table, stream));
+}
+
+bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean, int N, int C, int H, int W,
+                    hipStream_t stream) {
+  if (!x || !sat) return BC_ERR_NULL;
+  if (!dims_ok(N, C, H, W, 1) || W > 1024) return BC_ERR_SHAPE;
+  if (dt != BC_I32 && dt != BC_F32) return BC_ERR_DTYPE;
+  if (mean && dt != BC_F32) return BC_ERR_DTYPE;
+  if (!aligned16(x) || !aligned16(sat) || (mean && !aligned16(mean))) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_sat_build(x, dt == BC_I32, sat, mean, N * C, H, W, stream));
+}
+
+size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags) {
+  if (!dims_ok(N, C, H, W, B)) return 0;
+  if (op == 0) {
+    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
+    return hbm ? fwd_ws(N, C, H, W).total : 0;
+  }
+  if (op == 1) {
+    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(N, C, H, W);
+    return bwd_ws(N, C, H, W, B, hbm).total;
+  }
+  return 0;
+}
+
+bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
+                       void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!x || !boxes || !y) return BC_ERR_NULL;
+  if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM)) return BC_ERR_UNSUPPORTED;
+  const bool is_int = x_dt == BC_I32;
+  if (x_dt != BC_I32 && x_dt != BC_F32) return BC_ERR_DTYPE;
+  if (is_int ? (y_dt != BC_I32) : (y_dt != BC_F32 && y_dt != BC_BF16)) return BC_ERR_DTYPE;
+  if (is_int && (flags & BC_FLAG_MEAN_OFFSET)) return BC_ERR_DTYPE;
+  if (!aligned16(x) || !aligned16(boxes) || !aligned16(y)) return BC_ERR_ALIGN;
+  const int out_kind = y_dt == BC_BF16 ? 2 : (is_int ? 0 : 1);
+  const bool offset = (flags & BC_FLAG_MEAN_OFFSET) != 0;
+  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
+  if (!hbm) return hip_status(bc::launch_box_fwd_lds(x, is_int, boxes, y, out_kind, N, C, H, W, B, offset, stream));
+  if (W > 1024) return BC_ERR_SHAPE;
+  const FwdWs L = fwd_ws(N, C, H, W);
+  if (!ws) return BC_ERR_WORKSPACE;
+  if (ws_bytes < L.total) return BC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BC_ERR_ALIGN;
+  char* base = static_cast<char*>(ws);
+  float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
+  hipError_t e = bc::launch_sat_build(x, is_int, base + L.sat, means, N * C, H, W, stream);
+  if (e != hipSuccess) return BC_ERR_HIP;
+  return hip_status(bc::launch_box_fwd_gather(base + L.sat, is_int, means, boxes, y, out_kind, N, C, H, W, B, stream));
+}
+
+bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,
+                       float* grad_x, float* grad_boxes, unsigned flags, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  if (!x || !boxes || !grad_y) return BC_ERR_NULL;
+  if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM)) return BC_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(boxes) || !aligned16(grad_y) || (grad_x && !aligned16(grad_x)) ||
+      (grad_boxes && !aligned16(grad_boxes)))
+    return BC_ERR_ALIGN;
+  if (!grad_x && !grad_boxes) return BC_OK;
+  const bool offset = (flags & BC_FLAG_MEAN_OFFSET) != 0;
+  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(N, C, H, W);
+  if (hbm && W > 1024) return BC_ERR_SHAPE;
+  const BwdWs L = bwd_ws(N, C, H, W, B, hbm);
+  if (!ws) return BC_ERR_WORKSPACE;
+  if (ws_bytes < L.total) return BC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BC_ERR_ALIGN;
+  char* base = static_cast<char*>(ws);
+  float* partials = reinterpret_cast<float*>(base + L.partials);
+  hipError_t e;
+  if (!hbm) {
+    e = bc::launch_box_bwd_lds(x, boxes, grad_y, grad_x, partials, N, C, H, W, B, offset, stream);
+  } else {
+    float* sat_x = reinterpret_cast<float*>(base + L.sat_x);
+    float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
+    float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
+    e = bc::launch_sat_build(x, false, sat_x, means, N * C, H, W, stream);
+    if (e == hipSuccess) e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
+    if (e == hipSuccess)
+      e = bc::launch_box_bwd_gather(sat_x, means, sat_g, boxes, grad_y, grad_x, partials, N, C, H, W, B, stream);
+  }
+  if (e != hipSuccess) return BC_ERR_HIP;
+  if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);
+  return hip_status(e);
+}
+
+size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt) {
+  if (N <= 0 || M <= 0 || K <= 0 || P <= 0) return 0;
+  return bc::mix_workspace_bytes((int)mode, N, M, K, P, (int)compute_dt);
+}
+
+bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt, const void* b, bc_dtype b_dt, void* out,
+                        bc_dtype out_dt, int N, int M, int K, int P, bc_dtype compute_dt, int relu, const float* aux,
+                        int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!a || !b || !out) return BC_ERR_NULL;
+  if (mode != BC_MIX_FWD && mode != BC_MIX_BWD_DATA && mode != BC_MIX_BWD_WEIGHT) return BC_ERR_UNSUPPORTED;
+  if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || N > kMaxDim || M > kMaxDim || K > kMaxDim) return BC_ERR_SHAPE;
+  if ((long)K * P > (1L << 30) || (long)M * P > (1L << 30) || (long)M * K > (1L << 30)) return BC_ERR_SHAPE;
+  if (compute_dt != BC_F32 && compute_dt != BC_BF16) return BC_ERR_DTYPE;
+  for (bc_dtype d : {a_dt, b_dt}) {
+    if (d != BC_I32 && d != BC_F32 && d != BC_BF16) return BC_ERR_DTYPE;
+    if (d == BC_BF16 && compute_dt != BC_BF16) return BC_ERR_DTYPE;
+    if (d == BC_I32 && compute_dt != BC_F32) return BC_ERR_DTYPE;
+  }
+  const bool ints = a_dt == BC_I32 && b_dt == BC_I32;
+  if ((a_dt == BC_I32) != (b_dt == BC_I32)) return BC_ERR_DTYPE;
+  if (out_dt == BC_I32 ? (!ints || mode == BC_MIX_BWD_WEIGHT) : out_dt != BC_F32) return BC_ERR_DTYPE;
+  if (ints && (relu || mode != BC_MIX_FWD)) return BC_ERR_DTYPE;
+  if (relu && mode != BC_MIX_FWD && !aux) return BC_ERR_NULL;
+  if (accumulate && mode != BC_MIX_BWD_WEIGHT) return BC_ERR_UNSUPPORTED;
+  if (!aligned16(a) || !aligned16(b) || !aligned16(out) || (aux && !aligned16(aux))) return BC_ERR_ALIGN;
+  const size_t need = bc::mix_workspace_bytes((int)mode, N, M, K, P, (int)compute_dt);
+  if (need > 0) {
+    if (!ws) return BC_ERR_WORKSPACE;
+    if (ws_bytes < need) return BC_ERR_WORKSPACE;
+    if (!aligned16(ws)) return BC_ERR_ALIGN;
+  }
+  return hip_status(bc::launch_mix((int)mode, a, (int)a_dt, b, (int)b_dt, out, (int)out_dt, N, M, K, P,
+                                   (int)compute_dt, relu, mode == BC_MIX_FWD ? nullptr : aux, accumulate, ws,
+                                   ws_bytes, stream));
+}
+
+}  // extern "C"

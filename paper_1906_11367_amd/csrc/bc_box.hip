@@ -1,0 +1,658 @@
+// Box filter kernels: per-box precomputation, summed-area tables, forward
+// evaluation and backward (input and box-parameter gradients).  gfx950, wave64.
+#include "bc_common.hpp"
+#include "bc_internal.hpp"
+
+namespace bc {
+
+// ---------------------------------------------------------------------------
+// Helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lds_pitch_dev(int W) { return ((W + 1) & 1) ? (W + 1) : (W + 2); }
+
+template <typename T> __device__ __forceinline__ Taps<T> taps_for(const float* p, int limx, int limy);
+template <> __device__ __forceinline__ Taps<float> taps_for<float>(const float* p, int limx, int limy) {
+  return make_taps_f32(p, false, limx, limy);
+}
+template <> __device__ __forceinline__ Taps<int> taps_for<int>(const float* p, int limx, int limy) {
+  return make_taps_i32(p, limx, limy);
+}
+
+template <typename OutT, typename T> __device__ __forceinline__ OutT convert_out(T v);
+template <> __device__ __forceinline__ float convert_out<float, float>(float v) { return v; }
+template <> __device__ __forceinline__ int convert_out<int, int>(int v) { return v; }
+template <> __device__ __forceinline__ uint16_t convert_out<uint16_t, float>(float v) { return f32_to_bf16_rne(v); }
+
+// Grid-to-work mapping that keeps consecutive logical blocks on one XCD.
+// Blocks are dispatched to the 8 XCDs round-robin by block index; logical
+// block L = xcd * (grid/8) + slot gives each XCD one contiguous range of
+// logical blocks, so all blocks reading one map's table share that XCD's L2.
+// The grid is padded to a multiple of 8; logical ids >= total exit.
+__device__ __forceinline__ int xcd_remap(int bid, int grid) {
+  const int per = grid >> 3;
+  return (bid & 7) * per + (bid >> 3);
+}
+inline int pad8(int n) { return (n + 7) & ~7; }
+
+// Mean of one map, fp32, fixed summation order for a given block size.
+__device__ float block_mean(const float* __restrict__ src, int n, float* red) {
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) s += src[i];
+  s = wave_sum(s);
+  const int wave = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = s;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w = 0; w < nw; ++w) tot += red[w];
+  __syncthreads();
+  return tot / (float)n;
+}
+
+// Sum of 4 values over the block; result valid in thread 0 (fixed order).
+__device__ void block_sum4(float* v, float* red) {
+  const int wave = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) v[k] = wave_sum(v[k]);
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) red[wave * 4 + k] = v[k];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 0; k < 4; ++k) {
+      float t = 0.f;
+      for (int w = 0; w < nw; ++w) t += red[w * 4 + k];
+      v[k] = t;
+    }
+  }
+  __syncthreads();
+}
+
+// Exclusive table of one H x W map in LDS, S[u * pitch + v].  First pass:
+// lanes own columns and run down them reading the map straight from global
+// memory (coalesced along the row); second pass: lanes own rows and run along
+// them (odd pitch: conflict-free).  With `sub`, mu is subtracted first.
+template <typename T>
+__device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch,
+                                float mu, bool sub) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int u = tid; u <= H; u += nt) S[u * pitch] = (T)0;
+  for (int v = tid; v <= W; v += nt) S[v] = (T)0;
+  for (int v = tid; v < W; v += nt) {
+    T run = (T)0;
+    const T* col = src + v;
+#pragma unroll 8
+    for (int i = 0; i < H; ++i) {
+      T val = col[(size_t)i * W];
+      if (sub) val = (T)((float)val - mu);
+      run += val;
+      S[(i + 1) * pitch + v + 1] = run;
+    }
+  }
+  __syncthreads();
+  for (int u = tid + 1; u <= H; u += nt) {
+    T* row = S + u * pitch;
+    T run = (T)0;
+#pragma unroll 8
+    for (int v = 1; v <= W; ++v) {
+      run += row[v];
+      row[v] = run;
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Walks with compile-time segment length (registers indexed statically)
+// ---------------------------------------------------------------------------
+
+// Forward walk: emit(s, y, o) for s in [0, SEG) with y = y0 + s < y1.
+template <int SEG, typename T, bool kOffset, typename Src, typename Emit>
+__device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H, int W, int x0,
+                                         int y0, int y1, float mu, Emit emit) {
+  int ca[kQ + 1], cb[kQ + 1];
+  column_indices(tp, x0, W, ca, cb);
+  T uc[kQ], ud[kQ];
+  table_row(S, clampi(y0 + tp.oy[0], 0, H), ca, cb, tp, uc);
+  table_row(S, clampi(y0 + tp.oy[2], 0, H), ca, cb, tp, ud);
+  float ex[kQ];
+  if (kOffset) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+      ex[q] = (float)tp.wx[0] * (float)ca[q] + (float)tp.wx[1] * (float)ca[q + 1] +
+              (float)tp.wx[2] * (float)cb[q] + (float)tp.wx[3] * (float)cb[q + 1];
+  }
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    const int y = y0 + s;
+    if (y < y1) {
+      T uc1[kQ], ud1[kQ];
+      table_row(S, clampi(y + tp.oy[1], 0, H), ca, cb, tp, uc1);
+      table_row(S, clampi(y + tp.oy[3], 0, H), ca, cb, tp, ud1);
+      T o[kQ];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q)
+        o[q] = tp.wy[0] * uc[q] + tp.wy[1] * uc1[q] + tp.wy[2] * ud[q] + tp.wy[3] * ud1[q];
+      if (kOffset) {
+        const float ey = (float)tp.wy[0] * (float)clampi(y + tp.oy[0], 0, H) +
+                         (float)tp.wy[1] * (float)clampi(y + tp.oy[1], 0, H) +
+                         (float)tp.wy[2] * (float)clampi(y + tp.oy[2], 0, H) +
+                         (float)tp.wy[3] * (float)clampi(y + tp.oy[3], 0, H);
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
+      }
+      emit(s, y, o);
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
+    }
+  }
+}
+
+// Box-parameter gradient walk over one item: accumulates
+//   acc[0..3] += sum_{y,x} g(y,x) * dO(y,x)/d(a, b, c, d).
+// dO/da = -sum_r wy[r] * (S(u_r, x+fa+1) - S(u_r, x+fa)): minus the integral
+// of the edge column floor(x+a) between the box's y edges (Eq. 4 along x,
+// differenced between the two y corners); dO/db likewise at floor(x+b), with
+// a plus sign; dO/dc = -(U(fc+1) - U(fc)), dO/dd = U(fd+1) - U(fd) with U the
+// x-interpolated table rows (Eq. 4 along y).  With an offset table the
+// analytic derivative of mu * (clipped area) is added.
+template <int SEG, bool kOffset, typename Src>
+__device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0,
+                                          int y0, int y1, float mu, const float* __restrict__ g,
+                                          float* acc) {
+  int ca[kQ + 1], cb[kQ + 1];
+  column_indices(tp, x0, W, ca, cb);
+  float Uc[kQ], DAc[kQ], DBc[kQ], Ud[kQ], DAd[kQ], DBd[kQ];
+  table_row_grad(S, clampi(y0 + tp.oy[0], 0, H), ca, cb, tp, Uc, DAc, DBc);
+  table_row_grad(S, clampi(y0 + tp.oy[2], 0, H), ca, cb, tp, Ud, DAd, DBd);
+  float ex[kQ], dxa[kQ], dxb[kQ];
+  if (kOffset) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      ex[q] = tp.wx[0] * (float)ca[q] + tp.wx[1] * (float)ca[q + 1] + tp.wx[2] * (float)cb[q] +
+              tp.wx[3] * (float)cb[q + 1];
+      dxa[q] = (float)(ca[q + 1] - ca[q]);
+      dxb[q] = (float)(cb[q + 1] - cb[q]);
+    }
+  }
+  float ga = 0.f, gb = 0.f, gc = 0.f, gd = 0.f;
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    const int y = y0 + s;
+    if (y < y1) {
+      float Uc1[kQ], DAc1[kQ], DBc1[kQ], Ud1[kQ], DAd1[kQ], DBd1[kQ];
+      const int r0 = clampi(y + tp.oy[0], 0, H), r1 = clampi(y + tp.oy[1], 0, H);
+      const int r2 = clampi(y + tp.oy[2], 0, H), r3 = clampi(y + tp.oy[3], 0, H);
+      table_row_grad(S, r1, ca, cb, tp, Uc1, DAc1, DBc1);
+      table_row_grad(S, r3, ca, cb, tp, Ud1, DAd1, DBd1);
+      float ey = 0.f, dyc = 0.f, dyd = 0.f;
+      if (kOffset) {
+        ey = tp.wy[0] * (float)r0 + tp.wy[1] * (float)r1 + tp.wy[2] * (float)r2 + tp.wy[3] * (float)r3;
+        dyc = (float)(r1 - r0);
+        dyd = (float)(r3 - r2);
+      }
+      const float* grow = g + (size_t)y * W + x0;
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        if (x0 + q < W) {
+          const float gv = grow[q];
+          float oa = -(tp.wy[0] * DAc[q] + tp.wy[1] * DAc1[q] + tp.wy[2] * DAd[q] + tp.wy[3] * DAd1[q]);
+          float ob = tp.wy[0] * DBc[q] + tp.wy[1] * DBc1[q] + tp.wy[2] * DBd[q] + tp.wy[3] * DBd1[q];
+          float oc = Uc[q] - Uc1[q];
+          float od = Ud1[q] - Ud[q];
+          if (kOffset) {
+            oa -= mu * (ey * dxa[q]);
+            ob += mu * (ey * dxb[q]);
+            oc -= mu * (ex[q] * dyc);
+            od += mu * (ex[q] * dyd);
+          }
+          ga += gv * oa;
+          gb += gv * ob;
+          gc += gv * oc;
+          gd += gv * od;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        Uc[q] = Uc1[q]; DAc[q] = DAc1[q]; DBc[q] = DBc1[q];
+        Ud[q] = Ud1[q]; DAd[q] = DAd1[q]; DBd[q] = DBd1[q];
+      }
+    }
+  }
+  acc[0] += ga; acc[1] += gb; acc[2] += gc; acc[3] += gd;
+}
+
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+__global__ void k_box_prep(const float* __restrict__ boxes, int CB, int* __restrict__ table) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 2 * CB) return;
+  const bool mirror = i >= CB;
+  const Taps<float> t = make_taps_f32(boxes + (size_t)(mirror ? i - CB : i) * 4, mirror, 1 << 20, 1 << 20);
+  int* r = table + (size_t)i * 16;
+  float* f = reinterpret_cast<float*>(r);
+  r[0] = t.ox[0]; r[1] = t.ox[2]; r[2] = t.oy[0]; r[3] = t.oy[2];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { f[4 + k] = t.wx[k]; f[8 + k] = t.wy[k]; r[12 + k] = 0; }
+}
+
+// Standalone table in HBM, one block per map.  The map is processed in strips
+// of kStrip rows staged in LDS: each wave scans whole rows (every lane holds a
+// run of consecutive elements, scanned serially, then a wave-level scan of
+// the lane totals), then lanes own columns and carry the column sums down the
+// strip, writing finished table rows coalesced.
+constexpr int kStrip = 16;
+constexpr int kSatMaxK = 16;  // elements per lane in a row scan: W <= 1024
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* __restrict__ sat,
+                                                   float* __restrict__ mean, int H, int W) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);
+  __shared__ float red[16];
+  const int map = blockIdx.x;
+  const T* src = x + (size_t)map * H * W;
+  T* dst = sat + (size_t)map * (H + 1) * (W + 1);
+  float mu = 0.f;
+  const bool sub = mean != nullptr;
+  if (sub) {
+    mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
+    if (threadIdx.x == 0) mean[map] = mu;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int K = (W + 63) >> 6;
+  for (int v = tid; v <= W; v += blockDim.x) dst[v] = (T)0;
+  T carry[kSatMaxK / 4];
+#pragma unroll
+  for (int j = 0; j < kSatMaxK / 4; ++j) carry[j] = (T)0;
+  for (int r0 = 0; r0 < H; r0 += kStrip) {
+    const int rows = min(kStrip, H - r0);
+    for (int rr = wave; rr < rows; rr += nw) {
+      const T* row = src + (size_t)(r0 + rr) * W;
+      T v[kSatMaxK];
+      T run = (T)0;
+#pragma unroll
+      for (int k = 0; k < kSatMaxK; ++k) {
+        if (k < K) {
+          const int idx = lane * K + k;
+          T val = idx < W ? row[idx] : (T)0;
+          if (sub && idx < W) val = (T)((float)val - mu);
+          run += val;
+          v[k] = run;
+        }
+      }
+      const T excl = wave_incl_scan(run, lane) - run;
+#pragma unroll
+      for (int k = 0; k < kSatMaxK; ++k) {
+        const int idx = lane * K + k;
+        if (k < K && idx < W) tile[rr * W + idx] = v[k] + excl;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSatMaxK / 4; ++j) {
+      const int v = tid + j * 256;
+      if (v < W) {
+        T cs = carry[j];
+        for (int rr = 0; rr < rows; ++rr) {
+          cs += tile[rr * W + v];
+          dst[(size_t)(r0 + rr + 1) * (W + 1) + v + 1] = cs;
+        }
+        carry[j] = cs;
+      }
+    }
+    if (tid < rows) dst[(size_t)(r0 + tid + 1) * (W + 1)] = (T)0;
+    __syncthreads();
+  }
+}
+
+// Forward, table in LDS: one block per (map, group of boxes).  The block
+// builds the map's table once and evaluates every box of its group; item
+// `it` is (box, row segment, 3-column chunk), chunk fastest so that adjacent
+// lanes write adjacent columns.
+template <typename T, typename OutT, int SEG, bool kOffset>
+__global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const float* __restrict__ boxes,
+                                                     OutT* __restrict__ y, int C, int H, int W, int B, int bpg) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  T* S = reinterpret_cast<T*>(smem_raw);
+  __shared__ float red[16];
+  const int pitch = lds_pitch_dev(W);
+  const int ngrp = (B + bpg - 1) / bpg;
+  const int map = blockIdx.x / ngrp, grp = blockIdx.x - map * ngrp;
+  const int c = map % C;
+  const T* src = x + (size_t)map * H * W;
+  float mu = 0.f;
+  if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
+  build_table_lds(src, S, H, W, pitch, mu, kOffset);
+  const int b0 = grp * bpg, nb = min(bpg, B - b0);
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
+  const LdsTable<T> tab{S, pitch};
+  for (int it = threadIdx.x; it < nb * per_box; it += blockDim.x) {
+    const int bl = it / per_box, r = it - bl * per_box;
+    const int seg = r / nch, ch = r - seg * nch;
+    const int b = b0 + bl;
+    const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
+    OutT* out = y + ((size_t)map * B + b) * H * W;
+    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+    box_walk<SEG, T, kOffset>(tab, tp, H, W, x0, y0, y1, mu, [&](int, int yy, const T* o) {
+      OutT* row = out + (size_t)yy * W + x0;
+#pragma unroll
+      for (int q = 0; q < kQ; ++q)
+        if (x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
+    });
+  }
+}
+
+// Forward, table in HBM: one block per (map, box, block of 256 items), mapped
+// so that one map's blocks run on one XCD.
+template <typename T, typename OutT, int SEG, bool kOffset>
+__global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sat, const float* __restrict__ means,
+                                                        const float* __restrict__ boxes, OutT* __restrict__ y,
+                                                        int C, int H, int W, int B, int nblk, int total) {
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= total) return;
+  const int blk = L % nblk, mb = L / nblk;
+  const int b = mb % B, map = mb / B, c = map % C;
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = blk * 256 + threadIdx.x;
+  if (it >= nch * nseg) return;
+  const int seg = it / nch, ch = it - seg * nch;
+  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1};
+  const float mu = kOffset ? means[map] : 0.f;
+  const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
+  OutT* out = y + ((size_t)map * B + b) * H * W;
+  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+  box_walk<SEG, T, kOffset>(tab, tp, H, W, x0, y0, y1, mu, [&](int, int yy, const T* o) {
+    OutT* row = out + (size_t)yy * W + x0;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+      if (x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
+  });
+}
+
+// Backward, tables in LDS: one block per map (n, c); items (row segment,
+// chunk), one per thread.  For each box b: the table of grad_y[n][c*B+b] is
+// built in LDS; the thread accumulates the box-parameter gradient from the
+// table of x and the input gradient from the mirrored box on the gradient's
+// table (in registers, summed over b); the block reduces the 4 edge
+// gradients of box b into partials[n][c*B+b][4].
+template <int SEG, bool kOffset>
+__global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const float* __restrict__ boxes,
+                                                     const float* __restrict__ gy, float* __restrict__ gx,
+                                                     float* __restrict__ partials, int C, int H, int W, int B) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int pitch = lds_pitch_dev(W);
+  float* SI = reinterpret_cast<float*>(smem_raw);
+  float* SG = SI + (H + 1) * pitch;
+  __shared__ float red[64];
+  const int map = blockIdx.x, c = map % C;
+  const float* xs = x + (size_t)map * H * W;
+  float mu = 0.f;
+  if (kOffset) mu = block_mean(xs, H * W, red);
+  build_table_lds(xs, SI, H, W, pitch, mu, kOffset);
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = threadIdx.x;
+  const bool active = it < nch * nseg;
+  const int seg = it / nch, ch = it - seg * nch;
+  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+  float acc[SEG][kQ];
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  const LdsTable<float> ti{SI, pitch}, tg{SG, pitch};
+  for (int b = 0; b < B; ++b) {
+    const float* gp = gy + ((size_t)map * B + b) * H * W;
+    __syncthreads();
+    build_table_lds(gp, SG, H, W, pitch, 0.f, false);
+    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+      const float* p = boxes + (size_t)(c * B + b) * 4;
+      const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
+      const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
+      grad_walk<SEG, kOffset>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+      box_walk<SEG, float, false>(tg, tm, H, W, x0, y0, y1, 0.f, [&](int s, int, const float* o) {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
+      });
+    }
+    block_sum4(g4, red);
+    if (threadIdx.x == 0) {
+      float* pp = partials + ((size_t)map * B + b) * 4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) pp[k] = g4[k];
+    }
+  }
+  if (active && gx != nullptr) {
+    float* out = gx + (size_t)map * H * W;
+#pragma unroll
+    for (int s = 0; s < SEG; ++s) {
+      const int yy = y0 + s;
+      if (yy < y1) {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q)
+          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = acc[s][q];
+      }
+    }
+  }
+}
+
+// Backward, tables in HBM (built beforehand: table of x, one table per
+// gradient map).  One block per (map, block of 256 items); loops over boxes.
+// partials: [n * nblk + blk][c*B+b][4].
+template <int SEG, bool kOffset>
+__global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict__ sat_x, const float* __restrict__ means,
+                                                        const float* __restrict__ sat_g, const float* __restrict__ boxes,
+                                                        const float* __restrict__ gy, float* __restrict__ gx,
+                                                        float* __restrict__ partials, int C, int H, int W, int B,
+                                                        int nblk, int total) {
+  __shared__ float red[64];
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= total) return;
+  const int blk = L % nblk, map = L / nblk;
+  const int n = map / C, c = map - n * C;
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = blk * 256 + threadIdx.x;
+  const bool active = it < nch * nseg;
+  const int seg = it / nch, ch = it - seg * nch;
+  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+  const size_t tsz = (size_t)(H + 1) * (W + 1);
+  const GlobalTable<float> ti{sat_x + (size_t)map * tsz, W + 1};
+  const float mu = kOffset ? means[map] : 0.f;
+  float acc[SEG][kQ];
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  for (int b = 0; b < B; ++b) {
+    const float* gp = gy + ((size_t)map * B + b) * H * W;
+    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1};
+    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+      const float* p = boxes + (size_t)(c * B + b) * 4;
+      const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
+      const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
+      grad_walk<SEG, kOffset>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+      box_walk<SEG, float, false>(tg, tm, H, W, x0, y0, y1, 0.f, [&](int s, int, const float* o) {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
+      });
+    }
+    block_sum4(g4, red);
+    if (threadIdx.x == 0) {
+      float* pp = partials + (((size_t)n * nblk + blk) * C * B + (size_t)c * B + b) * 4;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) pp[k] = g4[k];
+    }
+  }
+  if (active && gx != nullptr) {
+    float* out = gx + (size_t)map * H * W;
+#pragma unroll
+    for (int s = 0; s < SEG; ++s) {
+      const int yy = y0 + s;
+      if (yy < y1) {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q)
+          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = acc[s][q];
+      }
+    }
+  }
+}
+
+// Second stage of the box-parameter gradient: fixed-order sum of the partial
+// edge gradients, then the change of variables a = 1/2+cx-rx, b = 1/2+cx+rx,
+// c = 1/2+cy-ry, d = 1/2+cy+ry:  dcx = ga+gb, dcy = gc+gd, drx = gb-ga,
+// dry = gd-gc.
+__global__ void k_box_grad_reduce(const float* __restrict__ partials, int P, int CB, float* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= CB) return;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < P; ++p) {
+    const float* pp = partials + ((size_t)p * CB + i) * 4;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] += pp[k];
+  }
+  float* o = out + (size_t)i * 4;
+  o[0] = s[0] + s[1];
+  o[1] = s[2] + s[3];
+  o[2] = s[1] - s[0];
+  o[3] = s[3] - s[2];
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+static hipError_t last_error() { return hipGetLastError(); }
+
+hipError_t launch_box_prep(const float* boxes, int C, int B, void* table, hipStream_t s) {
+  const int n = 2 * C * B;
+  hipLaunchKernelGGL(k_box_prep, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, (int*)table);
+  return last_error();
+}
+
+hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W,
+                            hipStream_t s) {
+  const size_t shm = (size_t)kStrip * W * 4;
+  if (is_int)
+    hipLaunchKernelGGL(k_sat_build<int>, dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat, (float*)nullptr, H, W);
+  else
+    hipLaunchKernelGGL(k_sat_build<float>, dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat, mean, H, W);
+  return last_error();
+}
+
+template <typename T, typename OutT, bool kOffset>
+static void fwd_lds_t(const void* x, const float* boxes, void* y, int N, int C, int H, int W, int B, hipStream_t s) {
+  constexpr int SEG = 16;
+  const int per_box = n_chunks(W) * n_segs(H, SEG);
+  int bpg = 256 / per_box;
+  if (bpg < 1) bpg = 1;
+  if (bpg > B) bpg = B;
+  // keep enough blocks in flight to fill the chip
+  while (bpg > 1 && (long)N * C * ((B + bpg - 1) / bpg) < 2048) bpg = (bpg + 1) / 2;
+  const int ngrp = (B + bpg - 1) / bpg;
+  int threads = bpg * per_box;
+  threads = ((threads + 63) / 64) * 64;
+  if (threads > 256) threads = 256;
+  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
+  hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset>), dim3(N * C * ngrp), dim3(threads), shm, s,
+                     (const T*)x, boxes, (OutT*)y, C, H, W, B, bpg);
+}
+
+hipError_t launch_box_fwd_lds(const void* x, bool is_int, const float* boxes, void* y, int out_kind, int N, int C,
+                              int H, int W, int B, bool offset, hipStream_t s) {
+  if (is_int) {
+    fwd_lds_t<int, int, false>(x, boxes, y, N, C, H, W, B, s);
+  } else if (out_kind == 2) {
+    if (offset) fwd_lds_t<float, uint16_t, true>(x, boxes, y, N, C, H, W, B, s);
+    else fwd_lds_t<float, uint16_t, false>(x, boxes, y, N, C, H, W, B, s);
+  } else {
+    if (offset) fwd_lds_t<float, float, true>(x, boxes, y, N, C, H, W, B, s);
+    else fwd_lds_t<float, float, false>(x, boxes, y, N, C, H, W, B, s);
+  }
+  return last_error();
+}
+
+template <typename T, typename OutT, bool kOffset>
+static void fwd_gather_t(const void* sat, const float* means, const float* boxes, void* y, int N, int C, int H,
+                         int W, int B, hipStream_t s) {
+  constexpr int SEG = 16;
+  const int items = n_chunks(W) * n_segs(H, SEG);
+  const int nblk = (items + 255) / 256;
+  const int total = N * C * B * nblk;
+  hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset>), dim3(pad8(total)), dim3(256), 0, s,
+                     (const T*)sat, means, boxes, (OutT*)y, C, H, W, B, nblk, total);
+}
+
+hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const float* boxes, void* y,
+                                 int out_kind, int N, int C, int H, int W, int B, hipStream_t s) {
+  const bool offset = means != nullptr;
+  if (is_int) {
+    fwd_gather_t<int, int, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+  } else if (out_kind == 2) {
+    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, boxes, y, N, C, H, W, B, s);
+    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+  } else {
+    if (offset) fwd_gather_t<float, float, true>(sat, means, boxes, y, N, C, H, W, B, s);
+    else fwd_gather_t<float, float, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+  }
+  return last_error();
+}
+
+template <int SEG, bool kOffset>
+static void bwd_lds_t(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N, int C,
+                      int H, int W, int B, hipStream_t s) {
+  const int items = n_chunks(W) * n_segs(H, SEG);
+  const int threads = ((items + 63) / 64) * 64;
+  const size_t shm = (size_t)2 * (H + 1) * lds_pitch(W) * sizeof(float);
+  hipLaunchKernelGGL((k_box_bwd_lds<SEG, kOffset>), dim3(N * C), dim3(threads), shm, s, x, boxes, gy, gx, partials, C,
+                     H, W, B);
+}
+
+// Segment length of the LDS backward: the longest that still gives >= 4096
+// waves (16 per CU), and whose item count fits one 256-thread block.
+int box_bwd_lds_seg(int N, int C, int H, int W) {
+  const int segs[3] = {16, 8, 4};
+  int pick = 0;
+  for (int i = 0; i < 3; ++i) {
+    const int items = n_chunks(W) * n_segs(H, segs[i]);
+    if (items > 256) break;
+    pick = segs[i];
+    const long waves = (long)N * C * ((items + 63) / 64);
+    if (waves >= 4096) break;
+  }
+  return pick;
+}
+
+hipError_t launch_box_bwd_lds(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N,
+                              int C, int H, int W, int B, bool offset, hipStream_t s) {
+  const int seg = box_bwd_lds_seg(N, C, H, W);
+  if (seg == 0) return hipErrorInvalidValue;
+  if (seg == 16) { if (offset) bwd_lds_t<16, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<16, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
+  else if (seg == 8) { if (offset) bwd_lds_t<8, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<8, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
+  else { if (offset) bwd_lds_t<4, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<4, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
+  return last_error();
+}
+
+int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, 16) + 255) / 256; }
+
+hipError_t launch_box_bwd_gather(const float* sat_x, const float* means, const float* sat_g, const float* boxes,
+                                 const float* gy, float* gx, float* partials, int N, int C, int H, int W, int B,
+                                 hipStream_t s) {
+  const int nblk = box_bwd_gather_blocks(H, W);
+  const int total = N * C * nblk;
+  if (means != nullptr)
+    hipLaunchKernelGGL((k_box_bwd_gather<16, true>), dim3(pad8(total)), dim3(256), 0, s, sat_x, means, sat_g, boxes,
+                       gy, gx, partials, C, H, W, B, nblk, total);
+  else
+    hipLaunchKernelGGL((k_box_bwd_gather<16, false>), dim3(pad8(total)), dim3(256), 0, s, sat_x, means, sat_g, boxes,
+                       gy, gx, partials, C, H, W, B, nblk, total);
+  return last_error();
+}
+
+hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes, hipStream_t s) {
+  hipLaunchKernelGGL(k_box_grad_reduce, dim3((CB + 255) / 256), dim3(256), 0, s, partials, P, CB, grad_boxes);
+  return last_error();
+}
+
+}  // namespace bc

@@ -1,0 +1,50 @@
+// Host-side launcher declarations shared by the C-ABI front end (bc_api.cpp)
+// and the kernel translation units.  Not part of the public interface.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bc {
+
+// Row pitch (elements) of a table kept in LDS: W+1 rounded up to odd, so
+// lanes walking down different rows of one column hit distinct banks.
+inline int lds_pitch(int W) { return ((W + 1) & 1) ? (W + 1) : (W + 2); }
+
+// Items of the sliding-window walk: kQ-column chunks x seg-row segments.
+inline int n_chunks(int W) { return (W + 2) / 3; }
+inline int n_segs(int H, int seg) { return (H + seg - 1) / seg; }
+
+hipError_t launch_box_prep(const float* boxes, int C, int B, void* table, hipStream_t s);
+
+hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean,
+                            int maps, int H, int W, hipStream_t s);
+
+// Forward, table in LDS.  out_kind: 0 = same type as x, 1 = fp32, 2 = bf16.
+hipError_t launch_box_fwd_lds(const void* x, bool is_int, const float* boxes, void* y, int out_kind,
+                              int N, int C, int H, int W, int B, bool offset, hipStream_t s);
+// Forward, table read from HBM (built beforehand by sat_build into `sat`).
+hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const float* boxes,
+                                 void* y, int out_kind, int N, int C, int H, int W, int B,
+                                 hipStream_t s);
+
+// Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
+hipError_t launch_box_bwd_lds(const float* x, const float* boxes, const float* gy, float* gx,
+                              float* partials, int N, int C, int H, int W, int B, bool offset,
+                              hipStream_t s);
+int box_bwd_gather_blocks(int H, int W);
+// Segment length the LDS backward uses for this shape; 0 = does not fit.
+int box_bwd_lds_seg(int N, int C, int H, int W);
+hipError_t launch_box_bwd_gather(const float* sat_x, const float* means, const float* sat_g,
+                                 const float* boxes, const float* gy, float* gx, float* partials,
+                                 int N, int C, int H, int W, int B, hipStream_t s);
+hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
+                                  hipStream_t s);
+
+// 1x1 mix GEMMs.
+hipError_t launch_mix(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out,
+                      int out_dt, int N, int M, int K, int P, int compute_dt, int relu,
+                      const float* aux, int accumulate, void* ws, size_t ws_bytes, hipStream_t s);
+size_t mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt);
+
+}  // namespace bc

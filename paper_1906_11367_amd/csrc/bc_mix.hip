@@ -1,0 +1,476 @@
+// 1x1 mix over the C*B filtered maps (Section 1 and 3.2 of the paper: the
+// depthwise box filters are followed by a 1x1 convolution), as MFMA GEMMs on
+// gfx950.  Per image n with P = H*W pixels:
+//   FWD        out[n] (M x P) = w (M x K)   * in[n] (K x P)
+//   BWD_DATA   out[n] (K x P) = w^T (K x M) * grad[n] (M x P)
+//   BWD_WEIGHT out   (M x K) = sum_n grad[n] (M x P) * in[n]^T (P x K)
+// One kernel template covers the three: C(i, j) = sum_l A(i, l) * B(l, j)
+// with A and B either contiguous along the reduction index l ("KC") or along
+// their row/column index.  Tiles are staged through LDS in l-contiguous
+// layout (transposed on the way in where needed) and fed to
+// v_mfma_f32_32x32x16_bf16 (bf16 operands) or v_mfma_f32_32x32x2_f32.
+#include "bc_common.hpp"
+#include "bc_internal.hpp"
+#include <type_traits>
+
+namespace bc {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 128, kBN = 128;
+constexpr int kMixThreads = 256;  // 4 waves in a 2 x 2 arrangement of 64 x 64 sub-tiles
+
+// Storage dtype codes follow bc_dtype: 0 = int32, 1 = fp32, 2 = bf16.
+template <int DT> struct StoreBytes { static constexpr int v = DT == 2 ? 2 : 4; };
+
+// Raw storage bits of one element.
+template <int DT>
+__device__ __forceinline__ uint32_t ld_bits(const char* base, size_t idx) {
+  if constexpr (DT == 2) return reinterpret_cast<const uint16_t*>(base)[idx];
+  else return reinterpret_cast<const uint32_t*>(base)[idx];
+}
+
+// N consecutive elements as raw bits (one 32-bit word per element; bf16 in
+// the low half).  `vec` = in range and aligned for one wide load.
+template <int DT, int N>
+__device__ __forceinline__ void ld_run(const char* base, size_t idx, bool vec, int avail, uint32_t* w) {
+  if (vec) {
+    if constexpr (DT == 2) {
+      static_assert(N == 4 || N == 8, "bf16 runs are 4 or 8 long");
+      if constexpr (N == 8) {
+        const uint4 q = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + idx);
+        const uint32_t p[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) { w[2 * k] = p[k] & 0xffffu; w[2 * k + 1] = p[k] >> 16; }
+      } else {
+        const uint2 q = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(base) + idx);
+        w[0] = q.x & 0xffffu; w[1] = q.x >> 16; w[2] = q.y & 0xffffu; w[3] = q.y >> 16;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < N; k += 4) {
+        const uint4 q = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(base) + idx + k);
+        w[k] = q.x; w[k + 1] = q.y; w[k + 2] = q.z; w[k + 3] = q.w;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = k < avail ? ld_bits<DT>(base, idx + k) : 0u;
+  }
+}
+
+// Storage bits -> fp32 value.
+template <int DT>
+__device__ __forceinline__ float bits_to_f32(uint32_t b) {
+  if constexpr (DT == 0) return (float)(int)b;
+  else if constexpr (DT == 1) return __uint_as_float(b);
+  else return __uint_as_float(b << 16);
+}
+
+// Storage bits (+ optional mask bits) -> bf16 code of the compute operand.
+template <int DT, bool MASK>
+__device__ __forceinline__ uint32_t to_bf16(uint32_t b, uint32_t m) {
+  uint32_t h;
+  if constexpr (DT == 2) h = b;
+  else h = f32_to_bf16_rne(bits_to_f32<DT>(b));
+  if constexpr (MASK) h = (__uint_as_float(m) > 0.f) ? h : 0u;
+  return h;
+}
+
+template <int DT, bool MASK>
+__device__ __forceinline__ float to_f32(uint32_t b, uint32_t m) {
+  float f = bits_to_f32<DT>(b);
+  if constexpr (MASK) f = (__uint_as_float(m) > 0.f) ? f : 0.f;
+  return f;
+}
+
+// One GEMM operand X(r, l): rows r in [0, rows), reduction index l in
+// [0, depth).  KC: element (r, l) at p[r * ld + l] (l contiguous); otherwise
+// at p[l * ld + r] (r contiguous).  Optional fp32 mask with the same indexing:
+// elements whose mask is not > 0 read as zero (ReLU derivative).
+//
+// A block stages rows [r0, r0 + 128) x l in [l0, l0 + BK) into an LDS tile
+// T[128][PITCH] in the compute type with l contiguous (what the MFMA operand
+// registers hold).  The stager splits loading (global -> registers, issued a
+// whole K-step ahead) from storing (registers -> LDS), so the loads of the
+// next tile are in flight while the current one feeds the MFMAs.
+//   KC:     a unit is UL consecutive l of one row        (NU = 4 per thread)
+//   not KC: a unit is UL consecutive l x 4 consecutive r (1 per thread); the
+//           4 x UL block is transposed in registers so every LDS write is
+//           16 contiguous bytes of one row.
+template <bool BF16, int DT, bool KC, bool MASK>
+struct Stager {
+  static constexpr int BK = BF16 ? 64 : 32;
+  static constexpr int PITCH = BF16 ? BK + 8 : BK + 1;  // elements; bf16 rows are 16-byte aligned
+  static constexpr int UL = BF16 ? 8 : 4;               // l per unit
+  static constexpr int NU = KC ? (kBM * BK / UL) / kMixThreads : 1;
+  static constexpr int NV = KC ? NU * UL : 4 * UL;      // elements held per thread
+  using E = typename std::conditional<BF16, uint16_t, float>::type;
+
+  const char* p;
+  const float* mask;
+  long ld;
+  int rows, depth;
+  bool vec_ok;
+  uint32_t v[NV];
+  uint32_t m[MASK ? NV : 1];
+
+  // Whole tile in range and aligned: the block takes the unguarded path
+  // (the condition is uniform, so no lane diverges and the wide loads stay in
+  // flight until store() consumes them).
+  __device__ __forceinline__ void load(int r0, int l0) {
+    if (vec_ok && r0 + kBM <= rows && l0 + BK <= depth) load_tile<true>(r0, l0);
+    else load_tile<false>(r0, l0);
+  }
+
+  template <bool kFull>
+  __device__ __forceinline__ void load_tile(int r0, int l0) {
+    const int tid = threadIdx.x;
+    if constexpr (KC) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int unit = tid + u * kMixThreads;
+        const int r = r0 + unit / (BK / UL), l = l0 + (unit % (BK / UL)) * UL;
+        if constexpr (kFull) {
+          const size_t idx = (size_t)r * ld + l;
+          ld_run<DT, UL>(p, idx, true, UL, v + u * UL);
+          if constexpr (MASK) ld_run<1, UL>(reinterpret_cast<const char*>(mask), idx, true, UL, m + u * UL);
+        } else {
+          const bool in = r < rows;
+          const int avail = in ? min(UL, max(0, depth - l)) : 0;
+          const size_t idx = (size_t)(in ? r : 0) * ld + (avail > 0 ? l : 0);
+          ld_run<DT, UL>(p, idx, false, avail, v + u * UL);
+          if constexpr (MASK) ld_run<1, UL>(reinterpret_cast<const char*>(mask), idx, false, avail, m + u * UL);
+        }
+      }
+    } else {
+      const int r = r0 + (tid % (kBM / 4)) * 4, lb = l0 + (tid / (kBM / 4)) * UL;
+      const int ravail = max(0, min(4, rows - r));
+#pragma unroll
+      for (int e = 0; e < UL; ++e) {
+        const int l = lb + e;
+        if constexpr (kFull) {
+          const size_t idx = (size_t)l * ld + r;
+          ld_run<DT, 4>(p, idx, true, 4, v + e * 4);
+          if constexpr (MASK) ld_run<1, 4>(reinterpret_cast<const char*>(mask), idx, true, 4, m + e * 4);
+        } else {
+          const int avail = l < depth ? ravail : 0;
+          const size_t idx = (size_t)(avail > 0 ? l : 0) * ld + (avail > 0 ? r : 0);
+          ld_run<DT, 4>(p, idx, false, avail, v + e * 4);
+          if constexpr (MASK) ld_run<1, 4>(reinterpret_cast<const char*>(mask), idx, false, avail, m + e * 4);
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ uint32_t mk(int i) const { return MASK ? m[i] : 0u; }
+
+  __device__ __forceinline__ void store(E* T) const {
+    const int tid = threadIdx.x;
+    if constexpr (KC) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int unit = tid + u * kMixThreads;
+        E* dst = T + (unit / (BK / UL)) * PITCH + (unit % (BK / UL)) * UL;
+        const uint32_t* src = v + u * UL;
+        if constexpr (BF16) {
+          uint4 q;
+          q.x = to_bf16<DT, MASK>(src[0], mk(u * UL + 0)) | (to_bf16<DT, MASK>(src[1], mk(u * UL + 1)) << 16);
+          q.y = to_bf16<DT, MASK>(src[2], mk(u * UL + 2)) | (to_bf16<DT, MASK>(src[3], mk(u * UL + 3)) << 16);
+          q.z = to_bf16<DT, MASK>(src[4], mk(u * UL + 4)) | (to_bf16<DT, MASK>(src[5], mk(u * UL + 5)) << 16);
+          q.w = to_bf16<DT, MASK>(src[6], mk(u * UL + 6)) | (to_bf16<DT, MASK>(src[7], mk(u * UL + 7)) << 16);
+          *reinterpret_cast<uint4*>(dst) = q;
+        } else {
+#pragma unroll
+          for (int k = 0; k < UL; ++k) dst[k] = to_f32<DT, MASK>(src[k], mk(u * UL + k));
+        }
+      }
+    } else {
+      const int r = (tid % (kBM / 4)) * 4, lb = (tid / (kBM / 4)) * UL;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        E* dst = T + (r + i) * PITCH + lb;
+        if constexpr (BF16) {
+          uint4 q;
+          q.x = to_bf16<DT, MASK>(v[0 * 4 + i], mk(0 * 4 + i)) | (to_bf16<DT, MASK>(v[1 * 4 + i], mk(1 * 4 + i)) << 16);
+          q.y = to_bf16<DT, MASK>(v[2 * 4 + i], mk(2 * 4 + i)) | (to_bf16<DT, MASK>(v[3 * 4 + i], mk(3 * 4 + i)) << 16);
+          q.z = to_bf16<DT, MASK>(v[4 * 4 + i], mk(4 * 4 + i)) | (to_bf16<DT, MASK>(v[5 * 4 + i], mk(5 * 4 + i)) << 16);
+          q.w = to_bf16<DT, MASK>(v[6 * 4 + i], mk(6 * 4 + i)) | (to_bf16<DT, MASK>(v[7 * 4 + i], mk(7 * 4 + i)) << 16);
+          *reinterpret_cast<uint4*>(dst) = q;
+        } else {
+#pragma unroll
+          for (int e = 0; e < UL; ++e) dst[e] = to_f32<DT, MASK>(v[e * 4 + i], mk(e * 4 + i));
+        }
+      }
+    }
+  }
+};
+
+// Stores the 2 x 2 accumulator tiles of one wave.  OK: 0 = fp32, 1 = int32
+// (exact integer values), 3 = fp32 accumulate, 4 = fp32 with ReLU.  `full`
+// (block-uniform) skips the bounds checks.
+template <int OK>
+__device__ __forceinline__ void epilogue(const f32x16_t (&acc)[2][2], char* cbase, int ib, int jb, int rows,
+                                         int cols, long ldc, bool full) {
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = ib + x * 32 + 8 * (r >> 2) + (r & 3);
+        const int j = jb + y * 32;
+        if (full || (i < rows && j < cols)) {
+          const float v = acc[x][y][r];
+          const size_t o = (size_t)i * ldc + j;
+          if constexpr (OK == 1) reinterpret_cast<int*>(cbase)[o] = (int)v;
+          else if constexpr (OK == 3) reinterpret_cast<float*>(cbase)[o] += v;
+          else if constexpr (OK == 4) reinterpret_cast<float*>(cbase)[o] = fmaxf(v, 0.f);
+          else reinterpret_cast<float*>(cbase)[o] = v;
+        }
+      }
+}
+
+// out-kind: 0 = store fp32 (relu optional), 1 = store int32 (exact integers),
+// 2 = store fp32 partial (BWD_WEIGHT split), 3 = fp32 with accumulate.
+template <bool BF16, int ADT, bool AKC, bool AMASK, int BDT, bool BKC, bool BMASK>
+__global__ __launch_bounds__(kMixThreads) void k_mix_gemm(
+    const void* __restrict__ a, const void* __restrict__ b, const float* __restrict__ aux, void* __restrict__ out,
+    int rows, int cols, int depth, long lda, long ldb, long ldc, long a_bs, long b_bs, long c_bs,
+    int mt, int nt, int zt, int nsplit_p, int pchunk, int out_kind, int relu) {
+  using SA = Stager<BF16, ADT, AKC, AMASK>;
+  using SB = Stager<BF16, BDT, BKC, BMASK>;
+  constexpr int BK = SA::BK, PITCH = SA::PITCH;
+  using E = typename SA::E;
+  __shared__ __align__(16) E As[kBM * PITCH];
+  __shared__ __align__(16) E Bs[kBN * PITCH];
+
+  // logical tile id: XCD-contiguous, row tiles fastest (blocks sharing one B
+  // tile run together on one XCD)
+  const int total = mt * nt * zt;
+  const int per = gridDim.x >> 3;
+  const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (L >= total) return;
+  const int tm = L % mt, tn = (L / mt) % nt, z = L / (mt * nt);
+
+  // batch item and reduction range of this block
+  int n = z, l_begin = 0, l_end = depth;
+  if (nsplit_p > 0) {  // BWD_WEIGHT: z = n * nsplit_p + sp
+    n = z / nsplit_p;
+    const int sp = z - n * nsplit_p;
+    l_begin = sp * pchunk;
+    l_end = min(depth, l_begin + pchunk);
+  }
+  SA sa;
+  sa.p = reinterpret_cast<const char*>(a) + (size_t)n * a_bs * StoreBytes<ADT>::v;
+  sa.mask = AMASK ? aux + (size_t)n * a_bs : nullptr;
+  sa.ld = lda; sa.rows = rows; sa.depth = depth;
+  sa.vec_ok = (lda & 7) == 0 && ((uintptr_t)sa.p & 15) == 0 && (!AMASK || ((uintptr_t)sa.mask & 15) == 0);
+  SB sb;
+  sb.p = reinterpret_cast<const char*>(b) + (size_t)n * b_bs * StoreBytes<BDT>::v;
+  sb.mask = BMASK ? aux + (size_t)n * b_bs : nullptr;
+  sb.ld = ldb; sb.rows = cols; sb.depth = depth;
+  sb.vec_ok = (ldb & 7) == 0 && ((uintptr_t)sb.p & 15) == 0 && (!BMASK || ((uintptr_t)sb.mask & 15) == 0);
+
+  const int i0 = tm * kBM, j0 = tn * kBN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.f;
+
+  if (l_begin < l_end) {
+    sa.load(i0, l_begin);
+    sb.load(j0, l_begin);
+    sa.store(As);
+    sb.store(Bs);
+    __syncthreads();
+  }
+  for (int l0 = l_begin; l0 < l_end; l0 += BK) {
+    const bool more = l0 + BK < l_end;
+    if (more) {  // next tile's loads in flight during this tile's MFMAs
+      sa.load(i0, l0 + BK);
+      sb.load(j0, l0 + BK);
+    }
+    if constexpr (BF16) {
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 16) {
+        bf16x8_t af[2], bfr[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          af[t] = *reinterpret_cast<const bf16x8_t*>(As + (wm * 64 + t * 32 + (lane & 31)) * PITCH + kk + 8 * (lane >> 5));
+          bfr[t] = *reinterpret_cast<const bf16x8_t*>(Bs + (wn * 64 + t * 32 + (lane & 31)) * PITCH + kk + 8 * (lane >> 5));
+        }
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int y = 0; y < 2; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[x], bfr[y], acc[x][y], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < BK; kk += 2) {
+        float af[2], bfr[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          af[t] = As[(wm * 64 + t * 32 + (lane & 31)) * PITCH + kk + (lane >> 5)];
+          bfr[t] = Bs[(wn * 64 + t * 32 + (lane & 31)) * PITCH + kk + (lane >> 5)];
+        }
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int y = 0; y < 2; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[x], bfr[y], acc[x][y], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+    if (more) {
+      sa.store(As);
+      sb.store(Bs);
+      __syncthreads();
+    }
+  }
+
+  // Epilogue.  Accumulator element r of lane t in a 32 x 32 tile is
+  // C[8 * (r / 4) + 4 * (t / 32) + r % 4][t % 32].
+  char* cbase = reinterpret_cast<char*>(out) + (size_t)z * c_bs * 4;
+  const bool full = i0 + kBM <= rows && j0 + kBN <= cols;
+  const int ib = i0 + wm * 64 + 4 * (lane >> 5), jb = j0 + wn * 64 + (lane & 31);
+  switch (out_kind) {
+    case 1: epilogue<1>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    case 3: epilogue<3>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    default:
+      if (relu) epilogue<4>(acc, cbase, ib, jb, rows, cols, ldc, full);
+      else epilogue<0>(acc, cbase, ib, jb, rows, cols, ldc, full);
+  }
+}
+
+// Fixed-order sum of split-K partials: out = (accumulate ? out : 0) + sum_s part[s].
+__global__ void k_mix_reduce(const float* __restrict__ part, int S, size_t n, float* __restrict__ out, int accumulate) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = accumulate ? out[i] : 0.f;
+  for (int k = 0; k < S; ++k) s += part[(size_t)k * n + i];
+  out[i] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+struct WeightSplit { int sp, chunk, S; };
+
+static WeightSplit weight_split(int N, int M, int K, int P, bool bf16) {
+  const int BK = bf16 ? 64 : 32;
+  const int tiles = ((M + kBM - 1) / kBM) * ((K + kBN - 1) / kBN);
+  const int max_sp = (P + BK - 1) / BK;
+  int sp = (512 + tiles * N - 1) / (tiles * N);
+  if (sp < 1) sp = 1;
+  if (sp > max_sp) sp = max_sp;
+  int chunk = (P + sp - 1) / sp;
+  chunk = ((chunk + BK - 1) / BK) * BK;
+  sp = (P + chunk - 1) / chunk;
+  return {sp, chunk, N * sp};
+}
+
+size_t mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt) {
+  if (mode != 2) return 0;
+  const WeightSplit ws = weight_split(N, M, K, P, compute_dt == 2);
+  return ws.S > 1 ? (size_t)ws.S * M * K * sizeof(float) : 0;
+}
+
+template <bool BF16, int ADT, bool AKC, bool AMASK, int BDT, bool BKC, bool BMASK>
+static void gemm_launch(const void* a, const void* b, const float* aux, void* out, int rows, int cols, int depth,
+                        long lda, long ldb, long ldc, long a_bs, long b_bs, long c_bs, int zt, int nsplit_p,
+                        int pchunk, int out_kind, int relu, hipStream_t s) {
+  const int mt = (rows + kBM - 1) / kBM, nt = (cols + kBN - 1) / kBN;
+  const int total = mt * nt * zt;
+  const int grid = (total + 7) & ~7;
+  hipLaunchKernelGGL((k_mix_gemm<BF16, ADT, AKC, AMASK, BDT, BKC, BMASK>), dim3(grid), dim3(kMixThreads), 0, s,
+                     a, b, aux, out, rows, cols, depth, lda, ldb, ldc, a_bs, b_bs, c_bs, mt, nt, zt, nsplit_p,
+                     pchunk, out_kind, relu);
+}
+
+// Stored operand dtypes instantiated per compute type: bf16 compute reads
+// fp32 or bf16 storage; fp32 compute reads int32 or fp32 storage.
+template <bool BF16, typename F>
+static void with_dt(int dt, F&& f) {
+  if constexpr (BF16) {
+    if (dt == 2) f(std::integral_constant<int, 2>{});
+    else f(std::integral_constant<int, 1>{});
+  } else {
+    if (dt == 0) f(std::integral_constant<int, 0>{});
+    else f(std::integral_constant<int, 1>{});
+  }
+}
+
+template <bool BF16>
+static hipError_t launch_mix_t(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out, int out_dt,
+                               int N, int M, int K, int P, int relu, const float* aux, int accumulate, void* ws,
+                               hipStream_t s) {
+  const int out_kind_plain = out_dt == 0 ? 1 : 0;
+  if (mode == 0) {
+    // C = out[n] (M x P): A = w (row-major M x K), B(l=k, j=p) = in[n][k][p]
+    with_dt<BF16>(a_dt, [&](auto ad) {
+      with_dt<BF16>(b_dt, [&](auto bd) {
+        gemm_launch<BF16, decltype(ad)::value, true, false, decltype(bd)::value, false, false>(
+            a, b, nullptr, out, M, P, K, K, P, P, 0, (long)K * P, (long)M * P, N, 0, 0, out_kind_plain, relu, s);
+      });
+    });
+    return hipGetLastError();
+  }
+  if (mode == 1) {
+    // C = out[n] (K x P): A(i=k, l=m) = w[m][k] (k contiguous), B(l=m, j=p) = grad[n][m][p]
+    with_dt<BF16>(a_dt, [&](auto ad) {
+      with_dt<BF16>(b_dt, [&](auto bd) {
+        if (relu)
+          gemm_launch<BF16, decltype(ad)::value, false, false, decltype(bd)::value, false, true>(
+              a, b, aux, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, out_kind_plain, 0, s);
+        else
+          gemm_launch<BF16, decltype(ad)::value, false, false, decltype(bd)::value, false, false>(
+              a, b, nullptr, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, out_kind_plain, 0, s);
+      });
+    });
+    return hipGetLastError();
+  }
+  // C = out (M x K): A(i=m, l=p) = grad[n][m][p], B(l=p, j=k) = in[n][k][p]; both p-contiguous.
+  // The reduction over (n, p) is split over images and p-chunks into fp32
+  // partials, summed in a fixed order by k_mix_reduce.
+  const WeightSplit sp = weight_split(N, M, K, P, BF16);
+  const bool direct = sp.S == 1;
+  void* dst = direct ? out : ws;
+  const int ok = direct ? (accumulate ? 3 : 0) : 2;
+  with_dt<BF16>(a_dt, [&](auto ad) {
+    with_dt<BF16>(b_dt, [&](auto bd) {
+      if (relu)
+        gemm_launch<BF16, decltype(ad)::value, true, true, decltype(bd)::value, true, false>(
+            a, b, aux, dst, M, K, P, P, P, K, (long)M * P, (long)K * P, direct ? 0 : (long)M * K, sp.S, sp.sp,
+            sp.chunk, ok, 0, s);
+      else
+        gemm_launch<BF16, decltype(ad)::value, true, false, decltype(bd)::value, true, false>(
+            a, b, nullptr, dst, M, K, P, P, P, K, (long)M * P, (long)K * P, direct ? 0 : (long)M * K, sp.S, sp.sp,
+            sp.chunk, ok, 0, s);
+    });
+  });
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || direct) return e;
+  const size_t n = (size_t)M * K;
+  hipLaunchKernelGGL(k_mix_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const float*)ws, sp.S, n,
+                     (float*)out, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_mix(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out, int out_dt, int N,
+                      int M, int K, int P, int compute_dt, int relu, const float* aux, int accumulate, void* ws,
+                      size_t ws_bytes, hipStream_t s) {
+  (void)ws_bytes;
+  if (compute_dt == 2)
+    return launch_mix_t<true>(mode, a, a_dt, b, b_dt, out, out_dt, N, M, K, P, relu, aux, accumulate, ws, s);
+  return launch_mix_t<false>(mode, a, a_dt, b, b_dt, out, out_dt, N, M, K, P, relu, aux, accumulate, ws, s);
+}
+
+}  // namespace bc

@@ -1,0 +1,136 @@
+"""One box-convolution layer and a stack of them, composed from the C-ABI calls.
+
+Forward:  O = box_conv_fwd(x)            (bf16 copy when the mix runs in bf16)
+          Z = pointwise_mix(FWD, w, O)   (+ ReLU when configured)
+Backward: dW = pointwise_mix(BWD_WEIGHT, dZ, O)
+          dO = pointwise_mix(BWD_DATA, w, dZ)
+          dx, dboxes = box_conv_bwd(x, dO)
+All buffers and workspaces are allocated once per plan (torch is used for
+device memory only); every arithmetic step runs in libboxconv's kernels.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import torch
+
+from . import boxconv as bc
+
+
+@dataclasses.dataclass
+class LayerPlan:
+    N: int
+    C: int
+    H: int
+    W: int
+    B: int
+    M: int | None          # mix output channels; None = box filter only
+    x_dtype: torch.dtype   # int32 or float32
+    mix_dtype: str         # 'i32' | 'f32' | 'bf16'
+    relu: bool = False
+    flags: int = 0
+    with_backward: bool = True
+    device: str = "cuda"
+
+    def __post_init__(self):
+        dev = torch.device(self.device)
+        N, C, H, W, B = self.N, self.C, self.H, self.W, self.B
+        K = C * B
+        P = H * W
+        self.K, self.P = K, P
+        integer = self.x_dtype == torch.int32
+        if integer:
+            o_dt = torch.int32
+        elif self.M is not None and self.mix_dtype == "bf16":
+            o_dt = torch.bfloat16
+        else:
+            o_dt = torch.float32
+        self.o = torch.empty((N, K, H, W), dtype=o_dt, device=dev)
+        self.compute = bc.BC_BF16 if self.mix_dtype == "bf16" else bc.BC_F32
+        self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
+        if self.M is not None:
+            self.z = torch.empty((N, self.M, H, W), dtype=torch.int32 if integer else torch.float32, device=dev)
+        if self.with_backward:
+            self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
+            self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
+            self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
+            if self.M is not None:
+                self.do = torch.empty((N, K, H, W), dtype=torch.float32, device=dev)
+                self.dw = torch.empty((self.M, K), dtype=torch.float32, device=dev)
+                self.ws_mixw = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, N, self.M, K, P,
+                                                          self.compute), dev)
+
+    def forward(self, x: torch.Tensor, boxes: torch.Tensor, w: torch.Tensor | None, tap=None):
+        """tap(label), if given, is called after each library call (the benchmark
+        records a stream event there)."""
+        tap = tap or _no_tap
+        bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd)
+        tap("box_conv_fwd")
+        if self.M is None:
+            return self.o
+        bc.pointwise_mix(bc.BC_MIX_FWD, w, self.o, self.z, self.N, self.M, self.K, self.P, self.compute,
+                         relu=int(self.relu))
+        tap("mix_fwd")
+        return self.z
+
+    def backward(self, x: torch.Tensor, boxes: torch.Tensor, w: torch.Tensor | None, grad_out: torch.Tensor,
+                 tap=None):
+        """grad_out: dL/dZ (or dL/dO without a mix).  Returns (dx, dboxes, dw)."""
+        tap = tap or _no_tap
+        if self.M is None:
+            do = grad_out
+            dw = None
+        else:
+            aux = self.z if self.relu else None
+            bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, grad_out, self.o, self.dw, self.N, self.M, self.K, self.P,
+                             self.compute, relu=int(self.relu), aux=aux, ws=self.ws_mixw)
+            tap("mix_bwd_weight")
+            bc.pointwise_mix(bc.BC_MIX_BWD_DATA, w, grad_out, self.do, self.N, self.M, self.K, self.P,
+                             self.compute, relu=int(self.relu), aux=aux)
+            tap("mix_bwd_data")
+            do = self.do
+            dw = self.dw
+        bc.box_conv_bwd(x, boxes, do, self.dx, self.dboxes, self.flags, self.ws_bwd)
+        tap("box_conv_bwd")
+        return self.dx, self.dboxes, dw
+
+
+def _no_tap(label):
+    return None
+
+
+def _ws(nbytes: int, dev):
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=dev)
+
+
+class Stack:
+    """`layers` box-conv layers in sequence; layer l's mix output feeds layer l+1."""
+
+    def __init__(self, N, C, H, W, B, M, layers, mix_dtype, relu, x_dtype=torch.float32, flags=0,
+                 backward=True, device="cuda"):
+        if layers > 1 and M != C:
+            raise ValueError("stacked layers need M == C")
+        self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device)
+                      for _ in range(layers)]
+
+    def forward(self, x, params, tap=None):
+        """params: list of (boxes, w) device tensors.  Returns the inputs of every
+        layer (for the backward) and the last output."""
+        inputs = []
+        cur = x
+        for plan, (boxes, w) in zip(self.plans, params):
+            inputs.append(cur)
+            cur = plan.forward(cur, boxes, w, tap)
+        return inputs, cur
+
+    def backward(self, inputs, params, grad_out, tap=None):
+        grads = [None] * len(self.plans)
+        g = grad_out
+        for li in range(len(self.plans) - 1, -1, -1):
+            boxes, w = params[li]
+            dx, dboxes, dw = self.plans[li].backward(inputs[li], boxes, w, g, tap)
+            grads[li] = (dboxes, dw)
+            g = dx
+        return g, grads

@@ -1,0 +1,140 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry point
+that include/boxconv.h declares, and rejects bad arguments before launching
+anything (no kernel runs in these tests, so they need no GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1906_11367_amd import boxconv as bc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "boxconv.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(bc.LIB_PATH), reason="libboxconv.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(",
+                       text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_four_entry_points():
+    names = declared_functions()
+    for n in ("sat_build", "box_conv_fwd", "box_conv_bwd", "pointwise_mix", "box_prep",
+              "bc_box_workspace_bytes", "bc_mix_workspace_bytes", "bc_status_string", "bc_abi_version"):
+        assert n in names, n
+
+
+def test_library_exports_every_declared_symbol():
+    lib = bc.load_library()
+    for n in declared_functions():
+        assert hasattr(lib, n), f"missing export {n}"
+        assert n in bc.SIGNATURES, f"binding lacks a signature for {n}"
+
+
+def test_status_strings_and_version():
+    lib = bc.load_library()
+    assert lib.bc_abi_version() == 1
+    for s in range(8):
+        assert lib.bc_status_string(s)
+    assert lib.bc_status_string(99) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x100000)        # never dereferenced: every call below fails validation
+FAKE_MISALIGNED = ctypes.c_void_p(0x100004)
+
+
+def test_fwd_argument_errors():
+    lib = bc.load_library()
+    ok = (FAKE, bc.BC_F32, FAKE, 2, 3, 8, 8, 4, FAKE, bc.BC_F32, 0, None, 0, None)
+    assert lib.box_conv_fwd(None, *ok[1:]) == 1
+    a = list(ok); a[2] = None
+    assert lib.box_conv_fwd(*a) == 1
+    for idx in (3, 4, 5, 6, 7):
+        a = list(ok); a[idx] = 0
+        assert lib.box_conv_fwd(*a) == 2
+    a = list(ok); a[1] = bc.BC_BF16
+    assert lib.box_conv_fwd(*a) == 3
+    a = list(ok); a[1] = bc.BC_I32          # int input needs int output
+    assert lib.box_conv_fwd(*a) == 3
+    a = list(ok); a[1] = bc.BC_I32; a[9] = bc.BC_I32; a[10] = bc.BC_FLAG_MEAN_OFFSET
+    assert lib.box_conv_fwd(*a) == 3
+    a = list(ok); a[0] = FAKE_MISALIGNED
+    assert lib.box_conv_fwd(*a) == 4
+    a = list(ok); a[10] = 1 << 7
+    assert lib.box_conv_fwd(*a) == 7
+    # a map whose table does not fit LDS needs a workspace
+    a = list(ok); a[5] = 300; a[6] = 300
+    assert lib.box_conv_fwd(*a) == 5
+    a[11] = FAKE; a[12] = 16
+    assert lib.box_conv_fwd(*a) == 5
+    a = list(ok); a[10] = bc.BC_FLAG_FORCE_HBM
+    assert lib.box_conv_fwd(*a) == 5
+
+
+def test_bwd_argument_errors():
+    lib = bc.load_library()
+    ok = [FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, FAKE, FAKE, 0, None, 0, None]
+    assert lib.box_conv_bwd(*([None] + ok[1:])) == 1
+    a = list(ok); a[7] = -1
+    assert lib.box_conv_bwd(*a) == 2
+    assert lib.box_conv_bwd(*ok) == 5      # workspace required (gradient partials)
+    a = list(ok); a[11] = FAKE; a[12] = 1
+    assert lib.box_conv_bwd(*a) == 5
+    a = list(ok); a[8] = FAKE_MISALIGNED
+    assert lib.box_conv_bwd(*a) == 4
+    a = list(ok); a[8] = None; a[9] = None  # nothing requested: no-op
+    assert lib.box_conv_bwd(*a) == 0
+
+
+def test_mix_argument_errors():
+    lib = bc.load_library()
+    ok = [bc.BC_MIX_FWD, FAKE, bc.BC_F32, FAKE, bc.BC_F32, FAKE, bc.BC_F32, 2, 64, 512, 3072, bc.BC_F32,
+          0, None, 0, None, 0, None]
+    a = list(ok); a[1] = None
+    assert lib.pointwise_mix(*a) == 1
+    a = list(ok); a[0] = 9
+    assert lib.pointwise_mix(*a) == 7
+    a = list(ok); a[8] = 0
+    assert lib.pointwise_mix(*a) == 2
+    a = list(ok); a[2] = bc.BC_BF16           # bf16 storage needs bf16 compute
+    assert lib.pointwise_mix(*a) == 3
+    a = list(ok); a[2] = bc.BC_I32            # mixed int / float operands
+    assert lib.pointwise_mix(*a) == 3
+    a = list(ok); a[0] = bc.BC_MIX_BWD_DATA; a[12] = 1   # relu without aux
+    assert lib.pointwise_mix(*a) == 1
+    a = list(ok); a[14] = 1                   # accumulate is BWD_WEIGHT only
+    assert lib.pointwise_mix(*a) == 7
+    a = list(ok); a[5] = FAKE_MISALIGNED
+    assert lib.pointwise_mix(*a) == 4
+    a = list(ok); a[0] = bc.BC_MIX_BWD_WEIGHT  # split-K partials need a workspace
+    assert lib.pointwise_mix(*a) == 5
+
+
+def test_sat_and_prep_argument_errors():
+    lib = bc.load_library()
+    assert lib.sat_build(FAKE, bc.BC_F32, FAKE, None, 1, 1, 8, 2000, None) == 2   # W > 1024
+    assert lib.sat_build(FAKE, bc.BC_BF16, FAKE, None, 1, 1, 8, 8, None) == 3
+    assert lib.sat_build(FAKE, bc.BC_I32, FAKE, FAKE, 1, 1, 8, 8, None) == 3      # mean needs fp32
+    assert lib.sat_build(None, bc.BC_F32, FAKE, None, 1, 1, 8, 8, None) == 1
+    assert lib.box_prep(FAKE, 0, 4, FAKE, None) == 2
+    assert lib.box_prep(FAKE_MISALIGNED, 2, 4, FAKE, None) == 4
+
+
+def test_workspace_queries():
+    lib = bc.load_library()
+    # 64x48 maps: tables fit LDS -> forward needs none; backward needs partials
+    assert lib.bc_box_workspace_bytes(0, 32, 256, 64, 48, 4, 0) == 0
+    assert lib.bc_box_workspace_bytes(1, 32, 256, 64, 48, 4, 0) >= 32 * 256 * 4 * 16
+    # forced HBM path and 256x256 maps need tables in the workspace
+    big = lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, 0)
+    assert big >= 4 * 128 * 257 * 257 * 4
+    assert lib.bc_box_workspace_bytes(0, 2, 3, 8, 8, 4, bc.BC_FLAG_FORCE_HBM) >= 2 * 3 * 81 * 4
+    assert lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0) >= 4 * 128 * 8 * 257 * 257 * 4
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_FWD, 32, 256, 1024, 3072, bc.BC_BF16) == 0
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, 32, 256, 1024, 3072, bc.BC_BF16) > 0

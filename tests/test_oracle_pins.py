@@ -124,6 +124,36 @@ def test_forward_equals_sat_four_corner_bilinear():
     assert np.max(np.abs(got - want)) <= 1e-11 * (1 + np.max(np.abs(want)))
 
 
+def test_box_taps_reproduce_forward_on_exact_table():
+    """The precomputed taps (floors + separable weights) evaluated on the
+    exact table with clamped indices give the oracle's forward result."""
+    rng = np.random.default_rng(20)
+    N, C, B, H, W = 1, 2, 3, 9, 8
+    x = rng.standard_normal((N, C, H, W))
+    bx = _real_boxes(rng, C, B, cmax=5.0, rmin=0.2, rmax=6.0)
+    fl, wx, wy = O.box_taps(bx)
+    S = O.sat_exclusive(x)
+    want = O.box_forward(x, bx)
+    for c in range(C):
+        for b in range(B):
+            fa, fb, fc, fd = fl[c, b]
+            ox = [fa, fa + 1, fb, fb + 1]
+            oy = [fc, fc + 1, fd, fd + 1]
+            for yy in range(H):
+                for xx in range(W):
+                    v = 0.0
+                    for r in range(4):
+                        for k in range(4):
+                            u = min(max(yy + oy[r], 0), H)
+                            t = min(max(xx + ox[k], 0), W)
+                            v += float(wy[c, b, r]) * float(wx[c, b, k]) * S[0, c, u, t]
+                    assert abs(v - want[0, c * B + b, yy, xx]) <= 1e-5 * (1 + abs(v))
+    # mirror = negated centre offset
+    flm, _, _ = O.box_taps(bx, mirror=True)
+    a, b_, c_, d = O.box_edges(O.mirrored_boxes(bx))
+    np.testing.assert_array_equal(flm[..., 0], np.floor(a))
+
+
 def test_forward_identity_box_exact():
     rng = np.random.default_rng(3)
     x = rng.standard_normal((2, 3, 8, 6)).astype(np.float32)
