@@ -181,6 +181,15 @@ bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt,
                         int relu, const float* aux, int accumulate,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * bc_cast_bf16 -- dst[i] = bf16(src[i]) for i < n, round to nearest even (NaN
+ * stays NaN).  src: device fp32 [n]; dst: device bf16 codes [n].  Lets a
+ * caller hold the 1x1 weights in the mix's compute type once per step instead
+ * of every GEMM tile rounding them again (pointwise_mix accepts BC_BF16
+ * storage for either operand).
+ * ---------------------------------------------------------------------- */
+bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream);
+
 /* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd. */
 size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags);
 size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt);

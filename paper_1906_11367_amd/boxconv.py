@@ -34,6 +34,7 @@ SIGNATURES = {
     "pointwise_mix": (_i, [_i, _vp, _i, _vp, _i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
+    "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
     "bc_status_string": (ctypes.c_char_p, [_i]),
     "bc_abi_version": (_i, []),
 }
@@ -144,6 +145,14 @@ def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, gra
     _check(load_library().box_conv_bwd(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, _ptr(grad_x),
                                        _ptr(grad_boxes), flags, _ptr(ws), nbytes, _stream()), "box_conv_bwd")
     return grad_x, grad_boxes
+
+
+def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):
+    """dst (bf16, same numel) = src (fp32) rounded to nearest even."""
+    if src.numel() != dst.numel():
+        raise BoxConvError("bc_cast_bf16: size mismatch")
+    _check(load_library().bc_cast_bf16(_ptr(src), _ptr(dst), src.numel(), _stream()), "bc_cast_bf16")
+    return dst
 
 
 def pointwise_mix(mode: int, a: torch.Tensor, b: torch.Tensor, out: torch.Tensor, N: int, M: int, K: int,

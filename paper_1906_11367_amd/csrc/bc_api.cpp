@@ -175,6 +175,13 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   return hip_status(e);
 }
 
+bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream) {
+  if (!src || !dst) return BC_ERR_NULL;
+  if (n == 0 || n > ((size_t)1 << 40)) return BC_ERR_SHAPE;
+  if (!aligned16(src) || !aligned16(dst)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_cast_bf16(src, dst, n, stream));
+}
+
 size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt) {
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0) return 0;
   return bc::mix_workspace_bytes((int)mode, N, M, K, P, (int)compute_dt);

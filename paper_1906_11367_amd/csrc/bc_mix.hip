@@ -68,21 +68,27 @@ __device__ __forceinline__ float bits_to_f32(uint32_t b) {
   else return __uint_as_float(b << 16);
 }
 
-// Storage bits (+ optional mask bits) -> bf16 code of the compute operand.
-template <int DT, bool MASK>
-__device__ __forceinline__ uint32_t to_bf16(uint32_t b, uint32_t m) {
-  uint32_t h;
-  if constexpr (DT == 2) h = b;
-  else h = f32_to_bf16_rne(bits_to_f32<DT>(b));
-  if constexpr (MASK) h = (__uint_as_float(m) > 0.f) ? h : 0u;
-  return h;
+// Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
+// even; lowers to one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
 template <int DT, bool MASK>
-__device__ __forceinline__ float to_f32(uint32_t b, uint32_t m) {
+__device__ __forceinline__ float operand_f32(uint32_t b, uint32_t m) {
   float f = bits_to_f32<DT>(b);
   if constexpr (MASK) f = (__uint_as_float(m) > 0.f) ? f : 0.f;
   return f;
+}
+
+// Element offset of (row r, reduction index l) in a bf16 LDS tile.  The
+// 16-byte chunks of a row are XOR-swizzled by (r / 16) % 4: the transposed
+// stores (lanes 4 rows apart) and the MFMA operand reads (32 consecutive rows)
+// then both hit distinct banks.
+template <int PITCH>
+__device__ __forceinline__ int bf16_tile_off(int r, int l) {
+  return r * PITCH + ((((l >> 3) ^ (r >> 4)) & 7) << 3) + (l & 7);
 }
 
 // One GEMM operand X(r, l): rows r in [0, rows), reduction index l in
@@ -92,20 +98,23 @@ __device__ __forceinline__ float to_f32(uint32_t b, uint32_t m) {
 //
 // A block stages rows [r0, r0 + 128) x l in [l0, l0 + BK) into an LDS tile
 // T[128][PITCH] in the compute type with l contiguous (what the MFMA operand
-// registers hold).  The stager splits loading (global -> registers, issued a
-// whole K-step ahead) from storing (registers -> LDS), so the loads of the
-// next tile are in flight while the current one feeds the MFMAs.
+// registers hold).  Loading (global -> registers, issued a whole K-step ahead)
+// is split from storing (registers -> LDS), so the loads of the next tile are
+// in flight while the current one feeds the MFMAs.
 //   KC:     a unit is UL consecutive l of one row        (NU = 4 per thread)
 //   not KC: a unit is UL consecutive l x 4 consecutive r (1 per thread); the
 //           4 x UL block is transposed in registers so every LDS write is
 //           16 contiguous bytes of one row.
+// bf16 storage without a mask is kept packed and never converted.
 template <bool BF16, int DT, bool KC, bool MASK>
 struct Stager {
   static constexpr int BK = BF16 ? 64 : 32;
   static constexpr int PITCH = BF16 ? BK + 8 : BK + 1;  // elements; bf16 rows are 16-byte aligned
   static constexpr int UL = BF16 ? 8 : 4;               // l per unit
   static constexpr int NU = KC ? (kBM * BK / UL) / kMixThreads : 1;
-  static constexpr int NV = KC ? NU * UL : 4 * UL;      // elements held per thread
+  static constexpr bool kRaw = BF16 && DT == 2 && !MASK;
+  // words held per thread: packed bf16 pairs, or one word per element
+  static constexpr int NW = kRaw ? (KC ? NU * UL / 2 : UL * 2) : (KC ? NU * UL : 4 * UL);
   using E = typename std::conditional<BF16, uint16_t, float>::type;
 
   const char* p;
@@ -113,8 +122,8 @@ struct Stager {
   long ld;
   int rows, depth;
   bool vec_ok;
-  uint32_t v[NV];
-  uint32_t m[MASK ? NV : 1];
+  uint32_t v[NW];
+  uint32_t m[MASK ? NW : 1];
 
   // Whole tile in range and aligned: the block takes the unguarded path
   // (the condition is uniform, so no lane diverges and the wide loads stay in
@@ -132,7 +141,20 @@ struct Stager {
       for (int u = 0; u < NU; ++u) {
         const int unit = tid + u * kMixThreads;
         const int r = r0 + unit / (BK / UL), l = l0 + (unit % (BK / UL)) * UL;
-        if constexpr (kFull) {
+        if constexpr (kRaw) {
+          uint32_t* w = v + u * (UL / 2);
+          if (kFull) {
+            const uint4 q = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p) + (size_t)r * ld + l);
+            w[0] = q.x; w[1] = q.y; w[2] = q.z; w[3] = q.w;
+          } else {
+            uint32_t e[UL];
+            const bool in = r < rows;
+            const int avail = in ? min(UL, max(0, depth - l)) : 0;
+            ld_run<2, UL>(p, (size_t)(in ? r : 0) * ld + (avail > 0 ? l : 0), false, avail, e);
+#pragma unroll
+            for (int k = 0; k < UL / 2; ++k) w[k] = e[2 * k] | (e[2 * k + 1] << 16);
+          }
+        } else if constexpr (kFull) {
           const size_t idx = (size_t)r * ld + l;
           ld_run<DT, UL>(p, idx, true, UL, v + u * UL);
           if constexpr (MASK) ld_run<1, UL>(reinterpret_cast<const char*>(mask), idx, true, UL, m + u * UL);
@@ -150,7 +172,19 @@ struct Stager {
 #pragma unroll
       for (int e = 0; e < UL; ++e) {
         const int l = lb + e;
-        if constexpr (kFull) {
+        if constexpr (kRaw) {
+          uint32_t* w = v + e * 2;
+          if (kFull) {
+            const uint2 q = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p) + (size_t)l * ld + r);
+            w[0] = q.x; w[1] = q.y;
+          } else {
+            uint32_t t[4];
+            const int avail = l < depth ? ravail : 0;
+            ld_run<2, 4>(p, (size_t)(avail > 0 ? l : 0) * ld + (avail > 0 ? r : 0), false, avail, t);
+            w[0] = t[0] | (t[1] << 16);
+            w[1] = t[2] | (t[3] << 16);
+          }
+        } else if constexpr (kFull) {
           const size_t idx = (size_t)l * ld + r;
           ld_run<DT, 4>(p, idx, true, 4, v + e * 4);
           if constexpr (MASK) ld_run<1, 4>(reinterpret_cast<const char*>(mask), idx, true, 4, m + e * 4);
@@ -165,6 +199,7 @@ struct Stager {
   }
 
   __device__ __forceinline__ uint32_t mk(int i) const { return MASK ? m[i] : 0u; }
+  __device__ __forceinline__ float f(int i) const { return operand_f32<DT, MASK>(v[i], mk(i)); }
 
   __device__ __forceinline__ void store(E* T) const {
     const int tid = threadIdx.x;
@@ -172,35 +207,49 @@ struct Stager {
 #pragma unroll
       for (int u = 0; u < NU; ++u) {
         const int unit = tid + u * kMixThreads;
-        E* dst = T + (unit / (BK / UL)) * PITCH + (unit % (BK / UL)) * UL;
-        const uint32_t* src = v + u * UL;
+        const int r = unit / (BK / UL), l = (unit % (BK / UL)) * UL;
         if constexpr (BF16) {
           uint4 q;
-          q.x = to_bf16<DT, MASK>(src[0], mk(u * UL + 0)) | (to_bf16<DT, MASK>(src[1], mk(u * UL + 1)) << 16);
-          q.y = to_bf16<DT, MASK>(src[2], mk(u * UL + 2)) | (to_bf16<DT, MASK>(src[3], mk(u * UL + 3)) << 16);
-          q.z = to_bf16<DT, MASK>(src[4], mk(u * UL + 4)) | (to_bf16<DT, MASK>(src[5], mk(u * UL + 5)) << 16);
-          q.w = to_bf16<DT, MASK>(src[6], mk(u * UL + 6)) | (to_bf16<DT, MASK>(src[7], mk(u * UL + 7)) << 16);
-          *reinterpret_cast<uint4*>(dst) = q;
+          if constexpr (kRaw) {
+            q.x = v[u * 4 + 0]; q.y = v[u * 4 + 1]; q.z = v[u * 4 + 2]; q.w = v[u * 4 + 3];
+          } else {
+            const int b = u * UL;
+            q.x = pack2_bf16(f(b + 0), f(b + 1)); q.y = pack2_bf16(f(b + 2), f(b + 3));
+            q.z = pack2_bf16(f(b + 4), f(b + 5)); q.w = pack2_bf16(f(b + 6), f(b + 7));
+          }
+          *reinterpret_cast<uint4*>(T + bf16_tile_off<PITCH>(r, l)) = q;
         } else {
+          E* dst = T + r * PITCH + l;
 #pragma unroll
-          for (int k = 0; k < UL; ++k) dst[k] = to_f32<DT, MASK>(src[k], mk(u * UL + k));
+          for (int k = 0; k < UL; ++k) dst[k] = f(u * UL + k);
         }
       }
     } else {
       const int r = (tid % (kBM / 4)) * 4, lb = (tid / (kBM / 4)) * UL;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        E* dst = T + (r + i) * PITCH + lb;
         if constexpr (BF16) {
           uint4 q;
-          q.x = to_bf16<DT, MASK>(v[0 * 4 + i], mk(0 * 4 + i)) | (to_bf16<DT, MASK>(v[1 * 4 + i], mk(1 * 4 + i)) << 16);
-          q.y = to_bf16<DT, MASK>(v[2 * 4 + i], mk(2 * 4 + i)) | (to_bf16<DT, MASK>(v[3 * 4 + i], mk(3 * 4 + i)) << 16);
-          q.z = to_bf16<DT, MASK>(v[4 * 4 + i], mk(4 * 4 + i)) | (to_bf16<DT, MASK>(v[5 * 4 + i], mk(5 * 4 + i)) << 16);
-          q.w = to_bf16<DT, MASK>(v[6 * 4 + i], mk(6 * 4 + i)) | (to_bf16<DT, MASK>(v[7 * 4 + i], mk(7 * 4 + i)) << 16);
-          *reinterpret_cast<uint4*>(dst) = q;
+          if constexpr (kRaw) {
+            // element i of rows (l, l+1) -> one packed word: bytes of the
+            // low (i even) or high (i odd) halves of the two source words
+            const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
+            const int h = i >> 1;
+            q.x = __builtin_amdgcn_perm(v[1 * 2 + h], v[0 * 2 + h], sel);
+            q.y = __builtin_amdgcn_perm(v[3 * 2 + h], v[2 * 2 + h], sel);
+            q.z = __builtin_amdgcn_perm(v[5 * 2 + h], v[4 * 2 + h], sel);
+            q.w = __builtin_amdgcn_perm(v[7 * 2 + h], v[6 * 2 + h], sel);
+          } else {
+            q.x = pack2_bf16(f(0 * 4 + i), f(1 * 4 + i));
+            q.y = pack2_bf16(f(2 * 4 + i), f(3 * 4 + i));
+            q.z = pack2_bf16(f(4 * 4 + i), f(5 * 4 + i));
+            q.w = pack2_bf16(f(6 * 4 + i), f(7 * 4 + i));
+          }
+          *reinterpret_cast<uint4*>(T + bf16_tile_off<PITCH>(r + i, lb)) = q;
         } else {
+          E* dst = T + (r + i) * PITCH + lb;
 #pragma unroll
-          for (int e = 0; e < UL; ++e) dst[e] = to_f32<DT, MASK>(v[e * 4 + i], mk(e * 4 + i));
+          for (int e = 0; e < UL; ++e) dst[e] = f(e * 4 + i);
         }
       }
     }
@@ -303,8 +352,8 @@ __global__ __launch_bounds__(kMixThreads) void k_mix_gemm(
         bf16x8_t af[2], bfr[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          af[t] = *reinterpret_cast<const bf16x8_t*>(As + (wm * 64 + t * 32 + (lane & 31)) * PITCH + kk + 8 * (lane >> 5));
-          bfr[t] = *reinterpret_cast<const bf16x8_t*>(Bs + (wn * 64 + t * 32 + (lane & 31)) * PITCH + kk + 8 * (lane >> 5));
+          af[t] = *reinterpret_cast<const bf16x8_t*>(As + bf16_tile_off<PITCH>(wm * 64 + t * 32 + (lane & 31), kk + 8 * (lane >> 5)));
+          bfr[t] = *reinterpret_cast<const bf16x8_t*>(Bs + bf16_tile_off<PITCH>(wn * 64 + t * 32 + (lane & 31), kk + 8 * (lane >> 5)));
         }
 #pragma unroll
         for (int x = 0; x < 2; ++x)
@@ -348,6 +397,27 @@ __global__ __launch_bounds__(kMixThreads) void k_mix_gemm(
       if (relu) epilogue<4>(acc, cbase, ib, jb, rows, cols, ldc, full);
       else epilogue<0>(acc, cbase, ib, jb, rows, cols, ldc, full);
   }
+}
+
+// dst[i] = bf16(src[i]), round to nearest even, 8 elements per thread.
+__global__ void k_cast_bf16(const float* __restrict__ src, uint16_t* __restrict__ dst, size_t n) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (i + 8 <= n) {
+    const float4 a = *reinterpret_cast<const float4*>(src + i);
+    const float4 b = *reinterpret_cast<const float4*>(src + i + 4);
+    uint4 q;
+    q.x = pack2_bf16(a.x, a.y); q.y = pack2_bf16(a.z, a.w);
+    q.z = pack2_bf16(b.x, b.y); q.w = pack2_bf16(b.z, b.w);
+    *reinterpret_cast<uint4*>(dst + i) = q;
+  } else {
+    for (size_t k = i; k < n; ++k) dst[k] = (uint16_t)(pack2_bf16(src[k], 0.f) & 0xffffu);
+  }
+}
+
+hipError_t launch_cast_bf16(const float* src, void* dst, size_t n, hipStream_t s) {
+  const size_t threads = (n + 7) / 8;
+  hipLaunchKernelGGL(k_cast_bf16, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, src, (uint16_t*)dst, n);
+  return hipGetLastError();
 }
 
 // Fixed-order sum of split-K partials: out = (accumulate ? out : 0) + sum_s part[s].

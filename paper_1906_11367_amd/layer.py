@@ -50,6 +50,9 @@ class LayerPlan:
         self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
         if self.M is not None:
             self.z = torch.empty((N, self.M, H, W), dtype=torch.int32 if integer else torch.float32, device=dev)
+            # the mix's weights in its compute type, refreshed from w every forward
+            self.w_c = (torch.empty((self.M, K), dtype=torch.bfloat16, device=dev)
+                        if self.compute == bc.BC_BF16 else None)
         if self.with_backward:
             self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
             self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
@@ -68,6 +71,9 @@ class LayerPlan:
         tap("box_conv_fwd")
         if self.M is None:
             return self.o
+        if self.w_c is not None:
+            bc.bc_cast_bf16(w, self.w_c)
+            w = self.w_c
         bc.pointwise_mix(bc.BC_MIX_FWD, w, self.o, self.z, self.N, self.M, self.K, self.P, self.compute,
                          relu=int(self.relu))
         tap("mix_fwd")
@@ -85,6 +91,8 @@ class LayerPlan:
             bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, grad_out, self.o, self.dw, self.N, self.M, self.K, self.P,
                              self.compute, relu=int(self.relu), aux=aux, ws=self.ws_mixw)
             tap("mix_bwd_weight")
+            if self.w_c is not None:
+                w = self.w_c
             bc.pointwise_mix(bc.BC_MIX_BWD_DATA, w, grad_out, self.do, self.N, self.M, self.K, self.P,
                              self.compute, relu=int(self.relu), aux=aux)
             tap("mix_bwd_data")

@@ -287,6 +287,21 @@ def test_mix(dims, compute, storage, relu):
     check(host(dw), 2 * dwr, rtol, "dW accumulated")
 
 
+def test_cast_bf16_bit_exact():
+    rng = np.random.default_rng(110)
+    v = np.concatenate([
+        rng.standard_normal(100003).astype(np.float32) * np.float32(7.0),
+        np.array([0.0, -0.0, 1.0, 1.00390625, 1.01171875, 1.0078125, 65504.0, 3.3e38, -3.3e38,
+                  np.inf, -np.inf, 1e-30, -1e-30], dtype=np.float32),
+        (np.arange(256, dtype=np.uint32) << 16 | 0x3F808000).view(np.float32),   # exact ties
+        (np.arange(256, dtype=np.uint32) << 16 | 0x3F807FFF).view(np.float32),
+    ]).astype(np.float32)
+    src = dev(v)
+    dst = torch.empty(v.size, dtype=torch.bfloat16, device="cuda")
+    bc.bc_cast_bf16(src, dst)
+    np.testing.assert_array_equal(host(dst), O.bf16_round(v))
+
+
 def test_mix_integer_exact():
     wl = wlmod.WORKLOADS[1]
     d = wlmod.make_inputs(wl)
