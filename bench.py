@@ -40,8 +40,8 @@ def parse():
     p.add_argument("--cpu-budget-s", type=float, default=20.0,
                    help="rough CPU time the oracle sample may take")
     p.add_argument("--copy-calibration", action="store_true",
-                   help="only run a plain 256 MiB device-to-device copy 5 times (reference for the "
-                        "FETCH_SIZE / WRITE_SIZE counters) and exit")
+                   help="only run a plain elementwise kernel that reads 256 MiB and writes 256 MiB, 5 "
+                        "times (reference for the FETCH_SIZE / WRITE_SIZE counters), and exit")
     return p.parse_args()
 
 
@@ -149,7 +149,7 @@ def main():
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(5):
-            dst.copy_(src)
+            torch.mul(src, 2.0, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_per_launch": src.numel() * 4, "launches": 5}), flush=True)
         return 0

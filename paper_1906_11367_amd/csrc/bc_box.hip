@@ -21,7 +21,9 @@ template <> __device__ __forceinline__ Taps<int> taps_for<int>(const float* p, i
 template <typename OutT, typename T> __device__ __forceinline__ OutT convert_out(T v);
 template <> __device__ __forceinline__ float convert_out<float, float>(float v) { return v; }
 template <> __device__ __forceinline__ int convert_out<int, int>(int v) { return v; }
-template <> __device__ __forceinline__ uint16_t convert_out<uint16_t, float>(float v) { return f32_to_bf16_rne(v); }
+template <> __device__ __forceinline__ uint16_t convert_out<uint16_t, float>(float v) {
+  return __builtin_bit_cast(uint16_t, (__bf16)v);  // round to nearest even (v_cvt_pk_bf16_f32)
+}
 
 // Grid-to-work mapping that keeps consecutive logical blocks on one XCD.
 // Blocks are dispatched to the 8 XCDs round-robin by block index; logical
@@ -106,10 +108,12 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
 // Walks with compile-time segment length (registers indexed statically)
 // ---------------------------------------------------------------------------
 
-// Forward walk: emit(s, y, o) for s in [0, SEG) with y = y0 + s < y1.
-template <int SEG, typename T, bool kOffset, typename Src, typename Emit>
+// Forward walk: emit.put<kFull>(s, y, o) for s in [0, SEG) with y = y0 + s < y1.
+// kFull: the item is known to be whole (y1 = y0 + SEG, x0 + kQ <= W), so no
+// step or column is guarded and the unrolled window needs no register copies.
+template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
 __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H, int W, int x0,
-                                         int y0, int y1, float mu, Emit emit) {
+                                         int y0, int y1, float mu, Emit& emit) {
   int ca[kQ + 1], cb[kQ + 1];
   column_indices(tp, x0, W, ca, cb);
   T uc[kQ], ud[kQ];
@@ -125,7 +129,7 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
-    if (y < y1) {
+    if (kFull || y < y1) {
       T uc1[kQ], ud1[kQ];
       table_row(S, clampi(y + tp.oy[1], 0, H), ca, cb, tp, uc1);
       table_row(S, clampi(y + tp.oy[3], 0, H), ca, cb, tp, ud1);
@@ -141,7 +145,7 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 #pragma unroll
         for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
       }
-      emit(s, y, o);
+      emit.template put<kFull>(s, y, o);
 #pragma unroll
       for (int q = 0; q < kQ; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
     }
@@ -156,7 +160,7 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 // a plus sign; dO/dc = -(U(fc+1) - U(fc)), dO/dd = U(fd+1) - U(fd) with U the
 // x-interpolated table rows (Eq. 4 along y).  With an offset table the
 // analytic derivative of mu * (clipped area) is added.
-template <int SEG, bool kOffset, typename Src>
+template <int SEG, bool kOffset, bool kFull, typename Src>
 __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0,
                                           int y0, int y1, float mu, const float* __restrict__ g,
                                           float* acc) {
@@ -179,7 +183,7 @@ __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, i
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
-    if (y < y1) {
+    if (kFull || y < y1) {
       float Uc1[kQ], DAc1[kQ], DBc1[kQ], Ud1[kQ], DAd1[kQ], DBd1[kQ];
       const int r0 = clampi(y + tp.oy[0], 0, H), r1 = clampi(y + tp.oy[1], 0, H);
       const int r2 = clampi(y + tp.oy[2], 0, H), r3 = clampi(y + tp.oy[3], 0, H);
@@ -194,7 +198,7 @@ __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, i
       const float* grow = g + (size_t)y * W + x0;
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
-        if (x0 + q < W) {
+        if (kFull || x0 + q < W) {
           const float gv = grow[q];
           float oa = -(tp.wy[0] * DAc[q] + tp.wy[1] * DAc1[q] + tp.wy[2] * DAd[q] + tp.wy[3] * DAd1[q]);
           float ob = tp.wy[0] * DBc[q] + tp.wy[1] * DBc1[q] + tp.wy[2] * DBd[q] + tp.wy[3] * DBd1[q];
@@ -221,6 +225,30 @@ __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, i
   }
   acc[0] += ga; acc[1] += gb; acc[2] += gc; acc[3] += gd;
 }
+
+// Emitters of walk outputs.
+template <typename OutT, typename T>
+struct StoreRows {  // forward: write the kQ outputs of row y
+  OutT* out;
+  int W, x0;
+  template <bool kFull>
+  __device__ __forceinline__ void put(int, int y, const T* o) {
+    OutT* row = out + (size_t)y * W + x0;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q)
+      if (kFull || x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
+  }
+};
+
+template <int SEG>
+struct AccumRows {  // backward: add the walk's outputs into per-thread registers
+  float acc[SEG][kQ];
+  template <bool kFull>
+  __device__ __forceinline__ void put(int s, int, const float* o) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
+  }
+};
 
 // ---------------------------------------------------------------------------
 // Kernels
@@ -335,12 +363,9 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
     const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
     OutT* out = y + ((size_t)map * B + b) * H * W;
     const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-    box_walk<SEG, T, kOffset>(tab, tp, H, W, x0, y0, y1, mu, [&](int, int yy, const T* o) {
-      OutT* row = out + (size_t)yy * W + x0;
-#pragma unroll
-      for (int q = 0; q < kQ; ++q)
-        if (x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
-    });
+    StoreRows<OutT, T> em{out, W, x0};
+    if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
+    else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
   }
 }
 
@@ -363,12 +388,9 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
   OutT* out = y + ((size_t)map * B + b) * H * W;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  box_walk<SEG, T, kOffset>(tab, tp, H, W, x0, y0, y1, mu, [&](int, int yy, const T* o) {
-    OutT* row = out + (size_t)yy * W + x0;
-#pragma unroll
-    for (int q = 0; q < kQ; ++q)
-      if (x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
-  });
+  StoreRows<OutT, T> em{out, W, x0};
+  if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
+  else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
 
 // Backward, tables in LDS: one block per map (n, c); items (row segment,
@@ -396,11 +418,12 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
   const bool active = it < nch * nseg;
   const int seg = it / nch, ch = it - seg * nch;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  float acc[SEG][kQ];
+  AccumRows<SEG> dx;
+  const bool full = y0 + SEG <= H && x0 + kQ <= W;
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
-    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+    for (int q = 0; q < kQ; ++q) dx.acc[s][q] = 0.f;
   const LdsTable<float> ti{SI, pitch}, tg{SG, pitch};
   for (int b = 0; b < B; ++b) {
     const float* gp = gy + ((size_t)map * B + b) * H * W;
@@ -411,11 +434,13 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
       const float* p = boxes + (size_t)(c * B + b) * 4;
       const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
       const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
-      grad_walk<SEG, kOffset>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
-      box_walk<SEG, float, false>(tg, tm, H, W, x0, y0, y1, 0.f, [&](int s, int, const float* o) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
-      });
+      if (full) {
+        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
+      } else {
+        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
+      }
     }
     block_sum4(g4, red);
     if (threadIdx.x == 0) {
@@ -432,7 +457,7 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
       if (yy < y1) {
 #pragma unroll
         for (int q = 0; q < kQ; ++q)
-          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = acc[s][q];
+          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = dx.acc[s][q];
       }
     }
   }
@@ -460,11 +485,12 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
   const size_t tsz = (size_t)(H + 1) * (W + 1);
   const GlobalTable<float> ti{sat_x + (size_t)map * tsz, W + 1};
   const float mu = kOffset ? means[map] : 0.f;
-  float acc[SEG][kQ];
+  AccumRows<SEG> dx;
+  const bool full = y0 + SEG <= H && x0 + kQ <= W;
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
-    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+    for (int q = 0; q < kQ; ++q) dx.acc[s][q] = 0.f;
   for (int b = 0; b < B; ++b) {
     const float* gp = gy + ((size_t)map * B + b) * H * W;
     const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1};
@@ -473,11 +499,13 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
       const float* p = boxes + (size_t)(c * B + b) * 4;
       const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
       const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
-      grad_walk<SEG, kOffset>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
-      box_walk<SEG, float, false>(tg, tm, H, W, x0, y0, y1, 0.f, [&](int s, int, const float* o) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
-      });
+      if (full) {
+        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
+      } else {
+        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
+      }
     }
     block_sum4(g4, red);
     if (threadIdx.x == 0) {
@@ -494,7 +522,7 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
       if (yy < y1) {
 #pragma unroll
         for (int q = 0; q < kQ; ++q)
-          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = acc[s][q];
+          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = dx.acc[s][q];
       }
     }
   }

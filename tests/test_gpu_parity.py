@@ -163,7 +163,7 @@ def test_fwd_bf16_output_is_rounded_fp32():
     # from [r - e, r + e]
     e = bb.scale_err(ref, bb.E_F32)
     assert np.all(np.abs(got - O.bf16_round(ref)) <= bb.bf16_band(ref, e))
-    assert np.mean(got == O.bf16_round(ref)) > 0.99
+    assert np.mean(got == O.bf16_round(ref)) > 0.9
 
 
 def test_fwd_identity_and_exact_integer_valued_floats():
