@@ -10,12 +10,18 @@ feature maps (Section 3.3: intermediate maps at a quarter of the input
 resolution; Section 4: 256x256 MPII crops -> 64x64, 256x192 COCO crops ->
 64x48).  No dataset item is used or reproduced.
 
-Each tensor has its own generator, seeded by (config seed, tensor tag), so any
-one tensor can be regenerated on its own and generation order does not matter.
+Each tensor has its own generators, seeded by (workload seed, tensor tag) and,
+for per-image tensors, the image index: any one tensor (or image) can be
+regenerated on its own, generation order does not matter, and a workload with
+fewer images draws exactly the first images of the full one.  Images are
+filled in parallel threads (NumPy releases the GIL while drawing).
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
+import os
+
 import numpy as np
 
 TAG_X, TAG_BOXES, TAG_W, TAG_GRAD = 0, 1, 2, 3
@@ -80,23 +86,42 @@ WORKLOADS = {
 }
 
 
-def _rng(seed: int, tag: int) -> np.random.Generator:
-    return np.random.default_rng([seed, tag])
+def _rng(seed: int, tag: int, *more: int) -> np.random.Generator:
+    return np.random.default_rng([seed, tag, *more])
+
+
+def _per_image(N, fill):
+    """Runs fill(n) for every image n, in parallel threads."""
+    workers = min(N, max(1, min(16, len(os.sched_getaffinity(0)))))
+    if workers == 1:
+        for n in range(N):
+            fill(n)
+        return
+    with cf.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(fill, range(N)))
 
 
 def make_x(wl: Workload) -> np.ndarray:
-    g = _rng(wl.seed, TAG_X)
     shape = (wl.N, wl.C, wl.H, wl.W)
-    if wl.x_kind == "int8range":
-        return g.integers(-8, 9, size=shape, dtype=np.int32)
-    v = g.standard_normal(shape, dtype=np.float32)
-    if wl.x_kind == "normal":
-        return v
-    if wl.x_kind == "absnormal":
-        return np.abs(v)
-    if wl.x_kind == "normal+0.5":
-        return (v + np.float32(0.5)).astype(np.float32)
-    raise ValueError(wl.x_kind)
+    out = np.empty(shape, dtype=np.int32 if wl.x_kind == "int8range" else np.float32)
+
+    def fill(n):
+        g = _rng(wl.seed, TAG_X, n)
+        if wl.x_kind == "int8range":
+            out[n] = g.integers(-8, 9, size=shape[1:], dtype=np.int32)
+            return
+        v = g.standard_normal(shape[1:], dtype=np.float32)
+        if wl.x_kind == "normal":
+            out[n] = v
+        elif wl.x_kind == "absnormal":
+            out[n] = np.abs(v)
+        elif wl.x_kind == "normal+0.5":
+            out[n] = v + np.float32(0.5)
+        else:
+            raise ValueError(wl.x_kind)
+
+    _per_image(wl.N, fill)
+    return out
 
 
 def make_boxes(wl: Workload, layer: int = 0) -> np.ndarray:
@@ -137,9 +162,14 @@ def make_grad(wl: Workload) -> np.ndarray | None:
     """Upstream gradient of the last output (loss L = <G, output>)."""
     if not wl.backward:
         return None
-    g = _rng(wl.seed, TAG_GRAD)
     ch = wl.mix_out if wl.mix_out is not None else wl.C * wl.B
-    return g.standard_normal((wl.N, ch, wl.H, wl.W), dtype=np.float32)
+    out = np.empty((wl.N, ch, wl.H, wl.W), dtype=np.float32)
+
+    def fill(n):
+        out[n] = _rng(wl.seed, TAG_GRAD, n).standard_normal((ch, wl.H, wl.W), dtype=np.float32)
+
+    _per_image(wl.N, fill)
+    return out
 
 
 def make_inputs(wl: Workload) -> dict:

@@ -1,0 +1,164 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py
+times (LayerPlan / Stack over the whole batch), checked on outputs the oracle
+can compute one image, one map or one box at a time.
+
+* fp32 layer: the whole step, every output (the oracle finishes in seconds).
+* pose layer (bf16 mix): images 0 and N-1 for O, Z, dO, dx; box-parameter and
+  weight gradients for sampled boxes / mix inputs summed over every image.
+* large maps (256x256, mean-offset table): sampled maps of O and dx, sampled
+  boxes' parameter gradients over every image.
+* 6-layer stack: image 0's output and input gradient (normwise).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1906_11367_amd import boxconv as bc
+from paper_1906_11367_amd import workloads as wlmod
+from paper_1906_11367_amd.layer import LayerPlan, Stack
+
+import bf16_bounds as bb  # noqa: E402
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+RTOL_F32 = 1e-4
+RTOL_BF16 = 1e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy()
+
+
+def check(got, ref, rtol, what):
+    pw, nw = O.rel_errors(got, ref)
+    say(f"  {what}: pointwise {pw:.3e}  normwise {nw:.3e}  (rtol {rtol})")
+    assert pw <= rtol, f"{what}: {pw} > {rtol}"
+
+
+def check_bounded(got, ref, bound, rtol, what):
+    excess, plain, bnd = bb.bounded_error(got, ref, bound)
+    say(f"  {what}: beyond-bound {excess:.3e}  plain {plain:.3e}  max bound {bnd:.3e}")
+    assert excess <= rtol, f"{what}: {excess} > {rtol}"
+
+
+def run_layer(wl, d):
+    x_dt = torch.int32 if wl.x_kind == "int8range" else torch.float32
+    flags = bc.BC_FLAG_MEAN_OFFSET if wl.mean_offset else 0
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, x_dt, wl.mix_dtype, wl.relu, flags, wl.backward)
+    xd, bd = dev(d["x"]), dev(d["boxes"])
+    wd = dev(d["w"]) if wl.mix_out is not None else None
+    out = plan.forward(xd, bd, wd)
+    grads = plan.backward(xd, bd, wd, dev(d["grad"])) if wl.backward else None
+    torch.cuda.synchronize()
+    return plan, out, grads
+
+
+def test_fp32_layer_full_size_every_output():
+    wl = wlmod.WORKLOADS[2]
+    d = wlmod.make_inputs(wl)
+    say(f"{wl.key} full size")
+    plan, z, (dx, db, dw) = run_layer(wl, d)
+    o = O.box_forward(d["x"], d["boxes"])
+    check(host(plan.o), o, RTOL_F32, "O")
+    check(host(z), O.mix_forward(d["w"], o, compute="f32"), RTOL_F32, "Z")
+    do = O.mix_backward_data(d["w"], d["grad"], compute="f32")
+    check(host(plan.do), do, RTOL_F32, "dO")
+    check(host(dw), O.mix_backward_weight(d["grad"], o, compute="f32"), RTOL_F32, "dW")
+    check(host(dx), O.box_backward_input(do, d["boxes"], wl.H, wl.W), RTOL_F32, "dx")
+    check(host(db), O.box_backward_params(d["x"], do, d["boxes"]), RTOL_F32, "dboxes")
+
+
+def test_pose_layer_full_size_sampled():
+    wl = wlmod.WORKLOADS[3]
+    d = wlmod.make_inputs(wl)
+    say(f"{wl.key} full size")
+    plan, z, (dx, db, dw) = run_layer(wl, d)
+    B, K = wl.B, wl.C * wl.B
+    for n in (0, wl.N - 1):
+        fw = bb.layer_forward(d["x"][n:n + 1].astype(np.float64), d["boxes"], d["w"], relu=False)
+        check_bounded(host(plan.o[n:n + 1]), O.bf16_round(fw["o"]), fw["D"], RTOL_BF16, f"O[{n}] (bf16)")
+        check_bounded(host(z[n:n + 1]), fw["z"], fw["ez"], RTOL_BF16, f"Z[{n}]")
+        bw = bb.layer_backward(fw, d["boxes"], d["w"], d["grad"][n:n + 1].astype(np.float64))
+        check(host(plan.do[n:n + 1]), bw["do"], RTOL_BF16, f"dO[{n}]")
+        check(host(dx[n:n + 1]), bw["dx"], RTOL_BF16, f"dx[{n}]")
+    # gradients summed over all images, for sampled boxes (c, b) = mix input k = c*B + b
+    rng = np.random.default_rng(7)
+    ks = sorted(rng.choice(K, size=12, replace=False).tolist())
+    wb = O.bf16_round(d["w"])
+    gb = O.bf16_round(d["grad"]).reshape(wl.N, wl.mix_out, -1)
+    dw_got = host(dw)
+    db_got = host(db)
+    for k in ks:
+        c, b = divmod(k, B)
+        bx = d["boxes"][c:c + 1, b:b + 1]
+        o_k = O.box_forward(d["x"][:, c:c + 1], bx)[:, 0]                      # [N, H, W]
+        D_k = bb.bf16_band(o_k, bb.scale_err(o_k, bb.E_F32))
+        ob = O.bf16_round(o_k).reshape(wl.N, -1)
+        dw_ref = np.einsum("nmp,np->m", gb, ob)
+        dw_bnd = np.einsum("nmp,np->m", np.abs(gb), D_k.reshape(wl.N, -1))
+        check_bounded(dw_got[:, k], dw_ref, dw_bnd, RTOL_BF16, f"dW[:, {k}]")
+        do_k = np.einsum("m,nmp->np", wb[:, k], gb).reshape(wl.N, 1, wl.H, wl.W)
+        db_ref = O.box_backward_params(d["x"][:, c:c + 1], do_k, bx)[0, 0]
+        pw = np.abs(db_got[c, b] - db_ref) / (np.abs(db_ref) + np.sqrt(np.mean(db_ref ** 2)))
+        say(f"  dboxes[{c},{b}]: {pw.max():.3e}")
+        assert pw.max() <= RTOL_BF16
+
+
+# The large-map workload builds its tables from (map - mean): bar 1e-4.  The
+# plain fp32 table is the reported comparison: its edge integrals are
+# differences of table values ~ 3e4 (0.5-mean maps of 65536 pixels), so the
+# box-parameter gradient carries ~1e-4 of cancellation; bar 2e-4 there.
+@pytest.mark.parametrize("offset,rtol_params", [(True, 1e-4), (False, 2e-4)])
+def test_large_maps_full_size_sampled(offset, rtol_params):
+    wl = wlmod.WORKLOADS[4].scaled(mean_offset=offset)
+    d = wlmod.make_inputs(wl)
+    say(f"{wl.key} full size, mean offset {offset}")
+    plan, o, (dx, db, _) = run_layer(wl, d)
+    B = wl.B
+    for (n, c) in [(0, 0), (wl.N - 1, wl.C - 1), (1, 77)]:
+        o_ref = O.box_forward(d["x"][n:n + 1, c:c + 1], d["boxes"][c:c + 1])
+        check(host(o[n:n + 1, c * B:(c + 1) * B]), o_ref, RTOL_F32, f"O[{n}, c={c}]")
+        dx_ref = O.box_backward_input(d["grad"][n:n + 1, c * B:(c + 1) * B], d["boxes"][c:c + 1], wl.H, wl.W)
+        check(host(dx[n:n + 1, c:c + 1]), dx_ref, RTOL_F32, f"dx[{n}, c={c}]")
+    db_got = host(db)
+    for (c, b) in [(0, 0), (5, 7), (wl.C - 1, 3)]:
+        k = c * B + b
+        ref = O.box_backward_params(d["x"][:, c:c + 1], d["grad"][:, k:k + 1], d["boxes"][c:c + 1, b:b + 1])[0, 0]
+        pw = np.abs(db_got[c, b] - ref) / (np.abs(ref) + np.sqrt(np.mean(ref ** 2)))
+        say(f"  dboxes[{c},{b}]: {pw.max():.3e}")
+        assert pw.max() <= rtol_params
+
+
+def test_stack6_full_size_image0():
+    wl = wlmod.WORKLOADS[5]
+    d = wlmod.make_inputs(wl)
+    say(f"{wl.key} full size")
+    st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, "bf16", True)
+    params = [(dev(b), dev(w)) for b, w in d["layers"]]
+    inputs, out = st.forward(dev(d["x"]), params)
+    dx, grads = st.backward(inputs, params, dev(d["grad"]))
+    torch.cuda.synchronize()
+    cache = O.stack_forward(d["x"][:1], d["layers"], compute="bf16", apply_relu=True)
+    dxr, _ = O.stack_backward(cache, d["layers"], d["grad"][:1], compute="bf16", apply_relu=True)
+    # end-to-end sanity bar, scaled with depth: ReLU decisions that the two
+    # sides may legitimately take differently compound through the layers
+    # (the elementwise parity of every layer is tested on oracle inputs)
+    bar = 5e-3 * wl.layers
+    for name, got, ref in [("Z_last[0]", out[:1], cache[-1][2]), ("dx[0]", dx[:1], dxr)]:
+        pw, nw = O.rel_errors(host(got), ref)
+        say(f"  {name}: normwise {nw:.3e}  pointwise {pw:.3e}  (bar {bar})")
+        assert nw <= bar
