@@ -70,25 +70,66 @@ __device__ void block_sum4(float* v, float* red) {
   __syncthreads();
 }
 
-// Exclusive table of one H x W map in LDS, S[u * pitch + v].  First pass:
-// lanes own columns and run down them reading the map straight from global
-// memory (coalesced along the row); second pass: lanes own rows and run along
-// them (odd pitch: conflict-free).  With `sub`, mu is subtracted first.
+// 16-byte vector of the map element type.
+template <typename T> struct Vec4;
+template <> struct Vec4<float> { using type = float4; };
+template <> struct Vec4<int> { using type = int4; };
+
+// Exclusive table of one H x W map in LDS, S[u * pitch + v].  The map is first
+// copied into the table's interior with every thread issuing 16-byte loads in
+// batches (the loads of a batch are all in flight together; out-of-range
+// slots re-read the last vector and are not stored, so no lane branches around
+// a load), optionally also into a plain copy P[i * pitch + j].  Then a column
+// pass (lanes own columns) and a row pass (lanes own rows; odd pitch: no bank
+// conflicts) in LDS.  With `sub`, mu is subtracted from the tabulated values.
 template <typename T>
 __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch,
-                                float mu, bool sub) {
+                                float mu, bool sub, T* P = nullptr) {
+  using V = typename Vec4<T>::type;
+  constexpr int kBatch = 8;
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int u = tid; u <= H; u += nt) S[u * pitch] = (T)0;
   for (int v = tid; v <= W; v += nt) S[v] = (T)0;
-  for (int v = tid; v < W; v += nt) {
+  const int n = H * W;
+  if ((W & 3) == 0 && ((uintptr_t)src & 15) == 0) {
+    const int n4 = n >> 2;
+    const V* s4 = reinterpret_cast<const V*>(src);
+    for (int base = 0; base < n4; base += nt * kBatch) {
+      V q[kBatch];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) q[b] = s4[min(base + b * nt + tid, n4 - 1)];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        const int k = base + b * nt + tid;
+        if (k < n4) {
+          const int e = k << 2, i = e / W, j = e - i * W;
+          T* d = S + (i + 1) * pitch + j + 1;
+          const T w4[4] = {(T)q[b].x, (T)q[b].y, (T)q[b].z, (T)q[b].w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) d[t] = sub ? (T)((float)w4[t] - mu) : w4[t];
+          if (P) {
+            T* pp = P + i * pitch + j;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) pp[t] = w4[t];
+          }
+        }
+      }
+    }
+  } else {
+    for (int k = tid; k < n; k += nt) {
+      const int i = k / W, j = k - i * W;
+      const T v = src[k];
+      S[(i + 1) * pitch + j + 1] = sub ? (T)((float)v - mu) : v;
+      if (P) P[i * pitch + j] = v;
+    }
+  }
+  __syncthreads();
+  for (int v = tid + 1; v <= W; v += nt) {
     T run = (T)0;
-    const T* col = src + v;
 #pragma unroll 8
-    for (int i = 0; i < H; ++i) {
-      T val = col[(size_t)i * W];
-      if (sub) val = (T)((float)val - mu);
-      run += val;
-      S[(i + 1) * pitch + v + 1] = run;
+    for (int u = 1; u <= H; ++u) {
+      run += S[u * pitch + v];
+      S[u * pitch + v] = run;
     }
   }
   __syncthreads();
@@ -163,7 +204,7 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 template <int SEG, bool kOffset, bool kFull, typename Src>
 __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0,
                                           int y0, int y1, float mu, const float* __restrict__ g,
-                                          float* acc) {
+                                          int gpitch, float* acc) {
   int ca[kQ + 1], cb[kQ + 1];
   column_indices(tp, x0, W, ca, cb);
   float Uc[kQ], DAc[kQ], DBc[kQ], Ud[kQ], DAd[kQ], DBd[kQ];
@@ -195,7 +236,7 @@ __device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, i
         dyc = (float)(r1 - r0);
         dyd = (float)(r3 - r2);
       }
-      const float* grow = g + (size_t)y * W + x0;
+      const float* grow = g + (size_t)y * gpitch + x0;
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
         if (kFull || x0 + q < W) {
@@ -435,10 +476,10 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
       const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
       const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
       if (full) {
-        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
         box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
       } else {
-        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
         box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
       }
     }
@@ -500,10 +541,10 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
       const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
       const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
       if (full) {
-        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
         box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
       } else {
-        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, g4);
+        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
         box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
       }
     }
