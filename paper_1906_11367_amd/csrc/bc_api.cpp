@@ -29,8 +29,8 @@ size_t table_elems(int H, int W) { return (size_t)(H + 1) * (W + 1); }
 bool fwd_lds_fits(int H, int W) {
   return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget;
 }
-bool bwd_lds_fits(int N, int C, int H, int W) {
-  return (size_t)2 * (H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(N, C, H, W) > 0;
+bool bwd_lds_fits(int H, int W) {
+  return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(H, W) > 0;
 }
 
 struct FwdWs { size_t sat, means, total; };
@@ -42,21 +42,18 @@ FwdWs fwd_ws(int N, int C, int H, int W) {
   return w;
 }
 
-struct BwdWs { size_t sat_x, means, sat_g, partials, total; int P; };
+struct BwdWs { size_t sat_g, partials, total; int P; };
 BwdWs bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
   BwdWs w{};
   if (!hbm) {
-    w.P = N;
+    w.P = N * bc::box_bwd_lds_waves(H, W);
     w.partials = 0;
-    w.total = align_up((size_t)N * C * B * 4 * 4);
+    w.total = align_up((size_t)w.P * C * B * 4 * 4);
     return w;
   }
-  const int nblk = bc::box_bwd_gather_blocks(H, W);
-  w.P = N * nblk;
-  w.sat_x = 0;
-  w.means = align_up((size_t)N * C * table_elems(H, W) * 4);
-  w.sat_g = w.means + align_up((size_t)N * C * 4);
-  w.partials = w.sat_g + align_up((size_t)N * C * B * table_elems(H, W) * 4);
+  w.P = N * bc::box_bwd_gather_blocks(H, W) * 4;
+  w.sat_g = 0;
+  w.partials = align_up((size_t)N * C * B * table_elems(H, W) * 4);
   w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
   return w;
 }
@@ -107,7 +104,7 @@ size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigne
     return hbm ? fwd_ws(N, C, H, W).total : 0;
   }
   if (op == 1) {
-    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(N, C, H, W);
+    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W);
     return bwd_ws(N, C, H, W, B, hbm).total;
   }
   return 0;
@@ -149,8 +146,9 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
       (grad_boxes && !aligned16(grad_boxes)))
     return BC_ERR_ALIGN;
   if (!grad_x && !grad_boxes) return BC_OK;
-  const bool offset = (flags & BC_FLAG_MEAN_OFFSET) != 0;
-  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(N, C, H, W);
+  // BC_FLAG_MEAN_OFFSET is accepted and has no effect here: the backward
+  // tabulates only the upstream gradient, never x.
+  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W);
   if (hbm && W > 1024) return BC_ERR_SHAPE;
   const BwdWs L = bwd_ws(N, C, H, W, B, hbm);
   if (!ws) return BC_ERR_WORKSPACE;
@@ -160,15 +158,11 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   float* partials = reinterpret_cast<float*>(base + L.partials);
   hipError_t e;
   if (!hbm) {
-    e = bc::launch_box_bwd_lds(x, boxes, grad_y, grad_x, partials, N, C, H, W, B, offset, stream);
+    e = bc::launch_box_bwd_lds(x, boxes, grad_y, grad_x, partials, N, C, H, W, B, stream);
   } else {
-    float* sat_x = reinterpret_cast<float*>(base + L.sat_x);
-    float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
-    e = bc::launch_sat_build(x, false, sat_x, means, N * C, H, W, stream);
-    if (e == hipSuccess) e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
-    if (e == hipSuccess)
-      e = bc::launch_box_bwd_gather(sat_x, means, sat_g, boxes, grad_y, grad_x, partials, N, C, H, W, B, stream);
+    e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
+    if (e == hipSuccess) e = bc::launch_box_bwd_gather(x, sat_g, boxes, grad_x, partials, N, C, H, W, B, stream);
   }
   if (e != hipSuccess) return BC_ERR_HIP;
   if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);

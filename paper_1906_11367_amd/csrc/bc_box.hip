@@ -8,7 +8,7 @@ namespace bc {
 // ---------------------------------------------------------------------------
 // Helpers
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int lds_pitch_dev(int W) { return ((W + 1) & 1) ? (W + 1) : (W + 2); }
+__device__ __forceinline__ int lds_pitch_dev(int W) { return (W + 7) | 1; }
 
 template <typename T> __device__ __forceinline__ Taps<T> taps_for(const float* p, int limx, int limy);
 template <> __device__ __forceinline__ Taps<float> taps_for<float>(const float* p, int limx, int limy) {
@@ -50,46 +50,31 @@ __device__ float block_mean(const float* __restrict__ src, int n, float* red) {
   return tot / (float)n;
 }
 
-// Sum of 4 values over the block; result valid in thread 0 (fixed order).
-__device__ void block_sum4(float* v, float* red) {
-  const int wave = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) v[k] = wave_sum(v[k]);
-  if ((threadIdx.x & 63) == 0) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) red[wave * 4 + k] = v[k];
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int k = 0; k < 4; ++k) {
-      float t = 0.f;
-      for (int w = 0; w < nw; ++w) t += red[w * 4 + k];
-      v[k] = t;
-    }
-  }
-  __syncthreads();
-}
-
 // 16-byte vector of the map element type.
 template <typename T> struct Vec4;
 template <> struct Vec4<float> { using type = float4; };
 template <> struct Vec4<int> { using type = int4; };
 
-// Exclusive table of one H x W map in LDS, S[u * pitch + v].  The map is first
-// copied into the table's interior with every thread issuing 16-byte loads in
-// batches (the loads of a batch are all in flight together; out-of-range
-// slots re-read the last vector and are not stored, so no lane branches around
-// a load), optionally also into a plain copy P[i * pitch + j].  Then a column
-// pass (lanes own columns) and a row pass (lanes own rows; odd pitch: no bank
-// conflicts) in LDS.  With `sub`, mu is subtracted from the tabulated values.
+// Exclusive table of one H x W map in LDS, padded (LdsTable): S(u, v) at
+// S[u * pitch + kPad + v].  The map is first copied into the table's interior
+// with every thread issuing 16-byte loads in batches (the loads of a batch are
+// all in flight together; out-of-range slots re-read the last vector and are
+// not stored, so no lane branches around a load).  Then a column pass (lanes
+// own columns) and a row pass (lanes own rows; odd pitch: no bank conflicts),
+// each reading kScan elements ahead before it writes, so that a lane's LDS
+// reads overlap instead of waiting on one another; the row pass also fills
+// the right padding.  With `sub`, mu is subtracted from the tabulated values.
 template <typename T>
-__device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch,
-                                float mu, bool sub, T* P = nullptr) {
+__device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch, float mu, bool sub) {
   using V = typename Vec4<T>::type;
-  constexpr int kBatch = 8;
+  constexpr int kBatch = 8, kScan = 16;
   const int tid = threadIdx.x, nt = blockDim.x;
-  for (int u = tid; u <= H; u += nt) S[u * pitch] = (T)0;
-  for (int v = tid; v <= W; v += nt) S[v] = (T)0;
+  T* R = S + kPad;
+  for (int v = tid; v < pitch; v += nt) S[v] = (T)0;
+  for (int k = tid; k < H * (kPad + 1); k += nt) {
+    const int u = 1 + k / (kPad + 1);
+    S[u * pitch + k % (kPad + 1)] = (T)0;
+  }
   const int n = H * W;
   if ((W & 3) == 0 && ((uintptr_t)src & 15) == 0) {
     const int n4 = n >> 2;
@@ -103,15 +88,10 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
         const int k = base + b * nt + tid;
         if (k < n4) {
           const int e = k << 2, i = e / W, j = e - i * W;
-          T* d = S + (i + 1) * pitch + j + 1;
+          T* d = R + (i + 1) * pitch + j + 1;
           const T w4[4] = {(T)q[b].x, (T)q[b].y, (T)q[b].z, (T)q[b].w};
 #pragma unroll
           for (int t = 0; t < 4; ++t) d[t] = sub ? (T)((float)w4[t] - mu) : w4[t];
-          if (P) {
-            T* pp = P + i * pitch + j;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) pp[t] = w4[t];
-          }
         }
       }
     }
@@ -119,28 +99,49 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
     for (int k = tid; k < n; k += nt) {
       const int i = k / W, j = k - i * W;
       const T v = src[k];
-      S[(i + 1) * pitch + j + 1] = sub ? (T)((float)v - mu) : v;
-      if (P) P[i * pitch + j] = v;
+      R[(i + 1) * pitch + j + 1] = sub ? (T)((float)v - mu) : v;
     }
   }
   __syncthreads();
   for (int v = tid + 1; v <= W; v += nt) {
     T run = (T)0;
-#pragma unroll 8
-    for (int u = 1; u <= H; ++u) {
-      run += S[u * pitch + v];
-      S[u * pitch + v] = run;
+    int u = 1;
+    for (; u + kScan - 1 <= H; u += kScan) {
+      T r[kScan];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) r[k] = R[(u + k) * pitch + v];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) {
+        run += r[k];
+        R[(u + k) * pitch + v] = run;
+      }
+    }
+    for (; u <= H; ++u) {
+      run += R[u * pitch + v];
+      R[u * pitch + v] = run;
     }
   }
   __syncthreads();
   for (int u = tid + 1; u <= H; u += nt) {
-    T* row = S + u * pitch;
+    T* row = R + u * pitch;
     T run = (T)0;
-#pragma unroll 8
-    for (int v = 1; v <= W; ++v) {
+    int v = 1;
+    for (; v + kScan - 1 <= W; v += kScan) {
+      T r[kScan];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) r[k] = row[v + k];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) {
+        run += r[k];
+        row[v + k] = run;
+      }
+    }
+    for (; v <= W; ++v) {
       run += row[v];
       row[v] = run;
     }
+#pragma unroll
+    for (int k = 1; k <= kPad; ++k) row[W + k] = run;
   }
   __syncthreads();
 }
@@ -155,25 +156,24 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
 template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
 __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H, int W, int x0,
                                          int y0, int y1, float mu, Emit& emit) {
-  int ca[kQ + 1], cb[kQ + 1];
-  column_indices(tp, x0, W, ca, cb);
+  const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
   T uc[kQ], ud[kQ];
-  table_row(S, clampi(y0 + tp.oy[0], 0, H), ca, cb, tp, uc);
-  table_row(S, clampi(y0 + tp.oy[2], 0, H), ca, cb, tp, ud);
+  table_row(S, clampi(y0 + tp.oy[0], 0, H), ba, bb, tp, uc);
+  table_row(S, clampi(y0 + tp.oy[2], 0, H), ba, bb, tp, ud);
   float ex[kQ];
   if (kOffset) {
 #pragma unroll
     for (int q = 0; q < kQ; ++q)
-      ex[q] = (float)tp.wx[0] * (float)ca[q] + (float)tp.wx[1] * (float)ca[q + 1] +
-              (float)tp.wx[2] * (float)cb[q] + (float)tp.wx[3] * (float)cb[q + 1];
+      ex[q] = (float)tp.wx[0] * (float)clampi(ba + q, 0, W) + (float)tp.wx[1] * (float)clampi(ba + q + 1, 0, W) +
+              (float)tp.wx[2] * (float)clampi(bb + q, 0, W) + (float)tp.wx[3] * (float)clampi(bb + q + 1, 0, W);
   }
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
     if (kFull || y < y1) {
       T uc1[kQ], ud1[kQ];
-      table_row(S, clampi(y + tp.oy[1], 0, H), ca, cb, tp, uc1);
-      table_row(S, clampi(y + tp.oy[3], 0, H), ca, cb, tp, ud1);
+      table_row(S, clampi(y + tp.oy[1], 0, H), ba, bb, tp, uc1);
+      table_row(S, clampi(y + tp.oy[3], 0, H), ba, bb, tp, ud1);
       T o[kQ];
 #pragma unroll
       for (int q = 0; q < kQ; ++q)
@@ -193,78 +193,60 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
   }
 }
 
-// Box-parameter gradient walk over one item: accumulates
-//   acc[0..3] += sum_{y,x} g(y,x) * dO(y,x)/d(a, b, c, d).
-// dO/da = -sum_r wy[r] * (S(u_r, x+fa+1) - S(u_r, x+fa)): minus the integral
-// of the edge column floor(x+a) between the box's y edges (Eq. 4 along x,
-// differenced between the two y corners); dO/db likewise at floor(x+b), with
-// a plus sign; dO/dc = -(U(fc+1) - U(fc)), dO/dd = U(fd+1) - U(fd) with U the
-// x-interpolated table rows (Eq. 4 along y).  With an offset table the
-// analytic derivative of mu * (clipped area) is added.
-template <int SEG, bool kOffset, bool kFull, typename Src>
-__device__ __forceinline__ void grad_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0,
-                                          int y0, int y1, float mu, const float* __restrict__ g,
-                                          int gpitch, float* acc) {
-  int ca[kQ + 1], cb[kQ + 1];
-  column_indices(tp, x0, W, ca, cb);
-  float Uc[kQ], DAc[kQ], DBc[kQ], Ud[kQ], DAd[kQ], DBd[kQ];
-  table_row_grad(S, clampi(y0 + tp.oy[0], 0, H), ca, cb, tp, Uc, DAc, DBc);
-  table_row_grad(S, clampi(y0 + tp.oy[2], 0, H), ca, cb, tp, Ud, DAd, DBd);
-  float ex[kQ], dxa[kQ], dxb[kQ];
-  if (kOffset) {
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) {
-      ex[q] = tp.wx[0] * (float)ca[q] + tp.wx[1] * (float)ca[q + 1] + tp.wx[2] * (float)cb[q] +
-              tp.wx[3] * (float)cb[q + 1];
-      dxa[q] = (float)(ca[q + 1] - ca[q]);
-      dxb[q] = (float)(cb[q + 1] - cb[q]);
-    }
-  }
+// Backward walk over one item on the table of one upstream-gradient map G,
+// with the adjoint taps of the box (make_taps_adjoint).  For each input pixel
+// (y, x) = (y0 + s, x0 + q):
+//   acc[s][q] += D(y, x), the adjoint box sum of G (the input gradient);
+// and, since <G, box(I)> = <I, D> for every placement of the box, the four
+// edge gradients of the original box follow from the derivatives of D with
+// respect to the adjoint's edges, weighted by the map value v[s][q] = I(y, x)
+// (0 outside the map).  The adjoint's edges are a' = 1 - b, b' = 1 - a,
+// c' = 1 - d, d' = 1 - c, so
+//   dL/da = -sum v * (G integrated over the adjoint's y extent along the
+//           column just below x + b'):  minus the y-weighted differences of
+//           the two table columns at b';
+//   dL/db = +sum v * (the same at a');
+//   dL/dc = -sum v * (G integrated over the x extent along the row below
+//           y + d'):  the difference of the x-interpolated rows at d';
+//   dL/dd = +sum v * (the same at c').
+// These are Eq. 4's edge integrals moved to the gradient's table; the split
+// of the adjoint's edges puts the one-sided derivative between each edge's
+// two taps.  g4 += (dL/da, dL/db, dL/dc, dL/dd) summed over the item.
+template <int SEG, bool kFull, typename Src>
+__device__ __forceinline__ void adjoint_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0, int y0,
+                                             int y1, const float (&v)[SEG][kQ], float (&acc)[SEG][kQ],
+                                             float* g4) {
+  const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
+  float Uc[kQ], Ac[kQ], Bc[kQ], Ud[kQ], Ad[kQ], Bd[kQ];
+  table_row_grad(S, clampi(y0 + tp.oy[0], 0, H), ba, bb, tp, Uc, Ac, Bc);
+  table_row_grad(S, clampi(y0 + tp.oy[2], 0, H), ba, bb, tp, Ud, Ad, Bd);
   float ga = 0.f, gb = 0.f, gc = 0.f, gd = 0.f;
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
     if (kFull || y < y1) {
-      float Uc1[kQ], DAc1[kQ], DBc1[kQ], Ud1[kQ], DAd1[kQ], DBd1[kQ];
-      const int r0 = clampi(y + tp.oy[0], 0, H), r1 = clampi(y + tp.oy[1], 0, H);
-      const int r2 = clampi(y + tp.oy[2], 0, H), r3 = clampi(y + tp.oy[3], 0, H);
-      table_row_grad(S, r1, ca, cb, tp, Uc1, DAc1, DBc1);
-      table_row_grad(S, r3, ca, cb, tp, Ud1, DAd1, DBd1);
-      float ey = 0.f, dyc = 0.f, dyd = 0.f;
-      if (kOffset) {
-        ey = tp.wy[0] * (float)r0 + tp.wy[1] * (float)r1 + tp.wy[2] * (float)r2 + tp.wy[3] * (float)r3;
-        dyc = (float)(r1 - r0);
-        dyd = (float)(r3 - r2);
-      }
-      const float* grow = g + (size_t)y * gpitch + x0;
+      float Uc1[kQ], Ac1[kQ], Bc1[kQ], Ud1[kQ], Ad1[kQ], Bd1[kQ];
+      table_row_grad(S, clampi(y + tp.oy[1], 0, H), ba, bb, tp, Uc1, Ac1, Bc1);
+      table_row_grad(S, clampi(y + tp.oy[3], 0, H), ba, bb, tp, Ud1, Ad1, Bd1);
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
-        if (kFull || x0 + q < W) {
-          const float gv = grow[q];
-          float oa = -(tp.wy[0] * DAc[q] + tp.wy[1] * DAc1[q] + tp.wy[2] * DAd[q] + tp.wy[3] * DAd1[q]);
-          float ob = tp.wy[0] * DBc[q] + tp.wy[1] * DBc1[q] + tp.wy[2] * DBd[q] + tp.wy[3] * DBd1[q];
-          float oc = Uc[q] - Uc1[q];
-          float od = Ud1[q] - Ud[q];
-          if (kOffset) {
-            oa -= mu * (ey * dxa[q]);
-            ob += mu * (ey * dxb[q]);
-            oc -= mu * (ex[q] * dyc);
-            od += mu * (ex[q] * dyd);
-          }
-          ga += gv * oa;
-          gb += gv * ob;
-          gc += gv * oc;
-          gd += gv * od;
-        }
+        acc[s][q] += tp.wy[0] * Uc[q] + tp.wy[1] * Uc1[q] + tp.wy[2] * Ud[q] + tp.wy[3] * Ud1[q];
+        const float colA = tp.wy[0] * Ac[q] + tp.wy[1] * Ac1[q] + tp.wy[2] * Ad[q] + tp.wy[3] * Ad1[q];
+        const float colB = tp.wy[0] * Bc[q] + tp.wy[1] * Bc1[q] + tp.wy[2] * Bd[q] + tp.wy[3] * Bd1[q];
+        const float val = v[s][q];
+        ga -= val * colB;
+        gb += val * colA;
+        gc -= val * (Ud1[q] - Ud[q]);
+        gd += val * (Uc1[q] - Uc[q]);
       }
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
-        Uc[q] = Uc1[q]; DAc[q] = DAc1[q]; DBc[q] = DBc1[q];
-        Ud[q] = Ud1[q]; DAd[q] = DAd1[q]; DBd[q] = DBd1[q];
+        Uc[q] = Uc1[q]; Ac[q] = Ac1[q]; Bc[q] = Bc1[q];
+        Ud[q] = Ud1[q]; Ad[q] = Ad1[q]; Bd[q] = Bd1[q];
       }
     }
   }
-  acc[0] += ga; acc[1] += gb; acc[2] += gc; acc[3] += gd;
+  g4[0] += ga; g4[1] += gb; g4[2] += gc; g4[3] += gd;
 }
 
 // Emitters of walk outputs.
@@ -278,16 +260,6 @@ struct StoreRows {  // forward: write the kQ outputs of row y
 #pragma unroll
     for (int q = 0; q < kQ; ++q)
       if (kFull || x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
-  }
-};
-
-template <int SEG>
-struct AccumRows {  // backward: add the walk's outputs into per-thread registers
-  float acc[SEG][kQ];
-  template <bool kFull>
-  __device__ __forceinline__ void put(int s, int, const float* o) {
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
   }
 };
 
@@ -396,7 +368,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
   build_table_lds(src, S, H, W, pitch, mu, kOffset);
   const int b0 = grp * bpg, nb = min(bpg, B - b0);
   const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
-  const LdsTable<T> tab{S, pitch};
+  const LdsTable<T> tab{S, pitch, W};
   for (int it = threadIdx.x; it < nb * per_box; it += blockDim.x) {
     const int bl = it / per_box, r = it - bl * per_box;
     const int seg = r / nch, ch = r - seg * nch;
@@ -424,7 +396,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   const int it = blk * 256 + threadIdx.x;
   if (it >= nch * nseg) return;
   const int seg = it / nch, ch = it - seg * nch;
-  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1};
+  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W};
   const float mu = kOffset ? means[map] : 0.f;
   const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
   OutT* out = y + ((size_t)map * B + b) * H * W;
@@ -434,139 +406,123 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
 
-// Backward, tables in LDS: one block per map (n, c); items (row segment,
-// chunk), one per thread.  For each box b: the table of grad_y[n][c*B+b] is
-// built in LDS; the thread accumulates the box-parameter gradient from the
-// table of x and the input gradient from the mirrored box on the gradient's
-// table (in registers, summed over b); the block reduces the 4 edge
-// gradients of box b into partials[n][c*B+b][4].
-template <int SEG, bool kOffset>
+// Map values of one item, 0 outside the map (they then add nothing to the
+// parameter gradients).
+template <int SEG>
+__device__ __forceinline__ void load_item(const float* __restrict__ xs, int H, int W, int x0, int y0, bool active,
+                                          float (&v)[SEG][kQ]) {
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const int yy = y0 + s, xx = x0 + q;
+      v[s][q] = (active && yy < H && xx < W) ? xs[(size_t)yy * W + xx] : 0.f;
+    }
+}
+
+template <int SEG>
+__device__ __forceinline__ void store_item(float* __restrict__ out, int H, int W, int x0, int y0,
+                                           const float (&acc)[SEG][kQ]) {
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    const int yy = y0 + s;
+    if (yy < H) {
+#pragma unroll
+      for (int q = 0; q < kQ; ++q)
+        if (x0 + q < W) out[(size_t)yy * W + x0 + q] = acc[s][q];
+    }
+  }
+}
+
+// The wave's sums of the four edge gradients, written by lane 0 to pp[0..3].
+__device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict__ pp) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) g4[k] = wave_sum_dpp(g4[k]);
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pp[k] = g4[k];
+  }
+}
+
+// Backward, table in LDS: one block per map (n, c); items (row segment,
+// chunk), one per thread, whose map values stay in registers.  For each box
+// b the table of grad_y[n][c*B+b] is built in LDS and the adjoint walk adds
+// the input gradient (in registers, summed over b) and the edge gradients;
+// each wave writes its edge-gradient sums to
+// partials[(n * nw + wave) * C*B + c*B + b][4].
+template <int SEG>
 __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const float* __restrict__ boxes,
                                                      const float* __restrict__ gy, float* __restrict__ gx,
                                                      float* __restrict__ partials, int C, int H, int W, int B) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
-  float* SI = reinterpret_cast<float*>(smem_raw);
-  float* SG = SI + (H + 1) * pitch;
-  __shared__ float red[64];
-  const int map = blockIdx.x, c = map % C;
-  const float* xs = x + (size_t)map * H * W;
-  float mu = 0.f;
-  if (kOffset) mu = block_mean(xs, H * W, red);
-  build_table_lds(xs, SI, H, W, pitch, mu, kOffset);
+  float* SG = reinterpret_cast<float*>(smem_raw);
+  const int map = blockIdx.x, n = map / C, c = map - n * C;
+  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6;
   const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
   const int it = threadIdx.x;
   const bool active = it < nch * nseg;
   const int seg = it / nch, ch = it - seg * nch;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  AccumRows<SEG> dx;
   const bool full = y0 + SEG <= H && x0 + kQ <= W;
+  float v[SEG][kQ], acc[SEG][kQ];
+  load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
-    for (int q = 0; q < kQ; ++q) dx.acc[s][q] = 0.f;
-  const LdsTable<float> ti{SI, pitch}, tg{SG, pitch};
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  const LdsTable<float> tg{SG, pitch, W};
   for (int b = 0; b < B; ++b) {
-    const float* gp = gy + ((size_t)map * B + b) * H * W;
     __syncthreads();
-    build_table_lds(gp, SG, H, W, pitch, 0.f, false);
+    build_table_lds(gy + ((size_t)map * B + b) * H * W, SG, H, W, pitch, 0.f, false);
     float g4[4] = {0.f, 0.f, 0.f, 0.f};
     if (active) {
-      const float* p = boxes + (size_t)(c * B + b) * 4;
-      const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
-      const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
-      if (full) {
-        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
-        box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
-      } else {
-        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
-        box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
-      }
+      const Taps<float> tp = make_taps_adjoint(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
+      if (full) adjoint_walk<SEG, true>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
+      else adjoint_walk<SEG, false>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
     }
-    block_sum4(g4, red);
-    if (threadIdx.x == 0) {
-      float* pp = partials + ((size_t)map * B + b) * 4;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) pp[k] = g4[k];
-    }
+    store_wave_partial(g4, partials + (((size_t)n * nw + wave) * C * B + (size_t)c * B + b) * 4);
   }
-  if (active && gx != nullptr) {
-    float* out = gx + (size_t)map * H * W;
-#pragma unroll
-    for (int s = 0; s < SEG; ++s) {
-      const int yy = y0 + s;
-      if (yy < y1) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q)
-          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = dx.acc[s][q];
-      }
-    }
-  }
+  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
 }
 
-// Backward, tables in HBM (built beforehand: table of x, one table per
-// gradient map).  One block per (map, block of 256 items); loops over boxes.
-// partials: [n * nblk + blk][c*B+b][4].
-template <int SEG, bool kOffset>
-__global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict__ sat_x, const float* __restrict__ means,
-                                                        const float* __restrict__ sat_g, const float* __restrict__ boxes,
-                                                        const float* __restrict__ gy, float* __restrict__ gx,
+// Backward, tables in HBM (one table per gradient map, built beforehand).
+// One 256-thread block per (map, block of 256 items); loops over boxes.
+// partials: [((n * nblk + blk) * 4 + wave) * C*B + c*B + b][4].
+template <int SEG>
+__global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict__ x, const float* __restrict__ sat_g,
+                                                        const float* __restrict__ boxes, float* __restrict__ gx,
                                                         float* __restrict__ partials, int C, int H, int W, int B,
                                                         int nblk, int total) {
-  __shared__ float red[64];
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   if (L >= total) return;
   const int blk = L % nblk, map = L / nblk;
   const int n = map / C, c = map - n * C;
+  const int wave = threadIdx.x >> 6;
   const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
   const int it = blk * 256 + threadIdx.x;
   const bool active = it < nch * nseg;
   const int seg = it / nch, ch = it - seg * nch;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  const size_t tsz = (size_t)(H + 1) * (W + 1);
-  const GlobalTable<float> ti{sat_x + (size_t)map * tsz, W + 1};
-  const float mu = kOffset ? means[map] : 0.f;
-  AccumRows<SEG> dx;
   const bool full = y0 + SEG <= H && x0 + kQ <= W;
+  const size_t tsz = (size_t)(H + 1) * (W + 1);
+  float v[SEG][kQ], acc[SEG][kQ];
+  load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
-    for (int q = 0; q < kQ; ++q) dx.acc[s][q] = 0.f;
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
   for (int b = 0; b < B; ++b) {
-    const float* gp = gy + ((size_t)map * B + b) * H * W;
-    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1};
+    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1, W};
     float g4[4] = {0.f, 0.f, 0.f, 0.f};
     if (active) {
-      const float* p = boxes + (size_t)(c * B + b) * 4;
-      const Taps<float> tp = make_taps_f32(p, false, W + 1, H + 1);
-      const Taps<float> tm = make_taps_f32(p, true, W + 1, H + 1);
-      if (full) {
-        grad_walk<SEG, kOffset, true>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
-        box_walk<SEG, float, false, true>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
-      } else {
-        grad_walk<SEG, kOffset, false>(ti, tp, H, W, x0, y0, y1, mu, gp, W, g4);
-        box_walk<SEG, float, false, false>(tg, tm, H, W, x0, y0, y1, 0.f, dx);
-      }
+      const Taps<float> tp = make_taps_adjoint(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
+      if (full) adjoint_walk<SEG, true>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
+      else adjoint_walk<SEG, false>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
     }
-    block_sum4(g4, red);
-    if (threadIdx.x == 0) {
-      float* pp = partials + (((size_t)n * nblk + blk) * C * B + (size_t)c * B + b) * 4;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) pp[k] = g4[k];
-    }
+    store_wave_partial(g4, partials + ((((size_t)n * nblk + blk) * 4 + wave) * C * B + (size_t)c * B + b) * 4);
   }
-  if (active && gx != nullptr) {
-    float* out = gx + (size_t)map * H * W;
-#pragma unroll
-    for (int s = 0; s < SEG; ++s) {
-      const int yy = y0 + s;
-      if (yy < y1) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q)
-          if (x0 + q < W) out[(size_t)yy * W + x0 + q] = dx.acc[s][q];
-      }
-    }
-  }
+  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
 }
 
 // Second stage of the box-parameter gradient: fixed-order sum of the partial
@@ -668,54 +624,48 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
   return last_error();
 }
 
-template <int SEG, bool kOffset>
+template <int SEG>
 static void bwd_lds_t(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N, int C,
                       int H, int W, int B, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int threads = ((items + 63) / 64) * 64;
-  const size_t shm = (size_t)2 * (H + 1) * lds_pitch(W) * sizeof(float);
-  hipLaunchKernelGGL((k_box_bwd_lds<SEG, kOffset>), dim3(N * C), dim3(threads), shm, s, x, boxes, gy, gx, partials, C,
-                     H, W, B);
+  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
+  hipLaunchKernelGGL((k_box_bwd_lds<SEG>), dim3(N * C), dim3(threads), shm, s, x, boxes, gy, gx, partials, C, H, W,
+                     B);
 }
 
-// Segment length of the LDS backward: the longest that still gives >= 4096
-// waves (16 per CU), and whose item count fits one 256-thread block.
-int box_bwd_lds_seg(int N, int C, int H, int W) {
-  const int segs[3] = {16, 8, 4};
-  int pick = 0;
-  for (int i = 0; i < 3; ++i) {
-    const int items = n_chunks(W) * n_segs(H, segs[i]);
-    if (items > 256) break;
-    pick = segs[i];
-    const long waves = (long)N * C * ((items + 63) / 64);
-    if (waves >= 4096) break;
-  }
-  return pick;
+// Segment length of the LDS backward: 8 rows when the map's items fit one
+// 256-thread block, else 4; 0 = the map needs more than 256 items.
+int box_bwd_lds_seg(int H, int W) {
+  if (n_chunks(W) * n_segs(H, 8) <= 256) return 8;
+  if (n_chunks(W) * n_segs(H, 4) <= 256) return 4;
+  return 0;
+}
+
+int box_bwd_lds_waves(int H, int W) {
+  const int seg = box_bwd_lds_seg(H, W);
+  return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
 }
 
 hipError_t launch_box_bwd_lds(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N,
-                              int C, int H, int W, int B, bool offset, hipStream_t s) {
-  const int seg = box_bwd_lds_seg(N, C, H, W);
-  if (seg == 0) return hipErrorInvalidValue;
-  if (seg == 16) { if (offset) bwd_lds_t<16, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<16, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
-  else if (seg == 8) { if (offset) bwd_lds_t<8, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<8, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
-  else { if (offset) bwd_lds_t<4, true>(x, boxes, gy, gx, partials, N, C, H, W, B, s); else bwd_lds_t<4, false>(x, boxes, gy, gx, partials, N, C, H, W, B, s); }
+                              int C, int H, int W, int B, hipStream_t s) {
+  const int seg = box_bwd_lds_seg(H, W);
+  if (seg == 8) bwd_lds_t<8>(x, boxes, gy, gx, partials, N, C, H, W, B, s);
+  else if (seg == 4) bwd_lds_t<4>(x, boxes, gy, gx, partials, N, C, H, W, B, s);
+  else return hipErrorInvalidValue;
   return last_error();
 }
 
-int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, 16) + 255) / 256; }
+constexpr int kBwdGatherSeg = 8;
 
-hipError_t launch_box_bwd_gather(const float* sat_x, const float* means, const float* sat_g, const float* boxes,
-                                 const float* gy, float* gx, float* partials, int N, int C, int H, int W, int B,
-                                 hipStream_t s) {
+int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, kBwdGatherSeg) + 255) / 256; }
+
+hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const float* boxes, float* gx, float* partials,
+                                 int N, int C, int H, int W, int B, hipStream_t s) {
   const int nblk = box_bwd_gather_blocks(H, W);
   const int total = N * C * nblk;
-  if (means != nullptr)
-    hipLaunchKernelGGL((k_box_bwd_gather<16, true>), dim3(pad8(total)), dim3(256), 0, s, sat_x, means, sat_g, boxes,
-                       gy, gx, partials, C, H, W, B, nblk, total);
-  else
-    hipLaunchKernelGGL((k_box_bwd_gather<16, false>), dim3(pad8(total)), dim3(256), 0, s, sat_x, means, sat_g, boxes,
-                       gy, gx, partials, C, H, W, B, nblk, total);
+  hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg>), dim3(pad8(total)), dim3(256), 0, s, x, sat_g, boxes, gx,
+                     partials, C, H, W, B, nblk, total);
   return last_error();
 }
 

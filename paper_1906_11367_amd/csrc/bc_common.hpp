@@ -19,12 +19,14 @@ namespace bc {
 // Output columns per thread item.  Odd, so that the 64 lanes of a wave,
 // reading consecutive 3-column groups of one table row, hit distinct banks.
 constexpr int kQ = 3;
-// Output rows per thread item (the length of one sliding-window walk).
-constexpr int kSeg = 16;
 
-__device__ __forceinline__ int clampi(int v, int lo, int hi) {
-  return v < lo ? lo : (v > hi ? hi : v);
-}
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return min(max(v, lo), hi); }
+
+// Columns of padding on each side of a table row kept in LDS: left pads hold
+// 0 (= the table's column 0), right pads repeat column W.  A run of kQ + 1
+// consecutive table columns starting anywhere then reads correctly clamped
+// values once its start is clamped to [-kPad, W].
+constexpr int kPad = 3;
 
 // One box, ready to evaluate on a map: tap offsets and separable weights.
 template <typename T>
@@ -69,6 +71,40 @@ __device__ __forceinline__ Taps<float> make_taps_f32(const float* p, bool mirror
   return t;
 }
 
+// Taps of the adjoint (mirrored) box as the backward pass uses them.  Each
+// edge e is split as e = f + alpha with alpha in (0, 1], i.e. f = ceil(e) - 1:
+// the same table lookups as the floor split (interpolation is continuous),
+// but at an edge on a pixel boundary the table difference between the edge's
+// two taps is the column (row) just below the edge.  In the adjoint the
+// original box's right derivative (Section 3.1, Eq. 4) is that one-sided
+// derivative from below, so the backward reads it straight from the taps.
+__device__ __forceinline__ void edge_split_upper(double e, int lim, int& f, double& frac) {
+  double fl = ceil(e) - 1.0;
+  if (!(fl >= -(double)lim)) fl = -(double)lim;
+  if (fl > (double)lim) fl = (double)lim;
+  frac = e - fl;
+  f = (int)fl;
+}
+
+__device__ __forceinline__ Taps<float> make_taps_adjoint(const float* p, int limx, int limy) {
+  const double cx = -(double)p[0], cy = -(double)p[1];
+  const double rx = (double)p[2], ry = (double)p[3];
+  Taps<float> t;
+  int fa, fb, fc, fd;
+  double aa, ab, ac, ad;
+  edge_split_upper(0.5 + cx - rx, limx, fa, aa);
+  edge_split_upper(0.5 + cx + rx, limx, fb, ab);
+  edge_split_upper(0.5 + cy - ry, limy, fc, ac);
+  edge_split_upper(0.5 + cy + ry, limy, fd, ad);
+  t.ox[0] = fa; t.ox[1] = fa + 1; t.ox[2] = fb; t.ox[3] = fb + 1;
+  t.oy[0] = fc; t.oy[1] = fc + 1; t.oy[2] = fd; t.oy[3] = fd + 1;
+  t.wx[0] = (float)(aa - 1.0); t.wx[1] = (float)(-aa);
+  t.wx[2] = (float)(1.0 - ab); t.wx[3] = (float)ab;
+  t.wy[0] = (float)(ac - 1.0); t.wy[1] = (float)(-ac);
+  t.wy[2] = (float)(1.0 - ad); t.wy[3] = (float)ad;
+  return t;
+}
+
 // Integer maps: corners are floored (the fractions are ignored), so the box is
 // the plain sum of Eq. 1 and only the four corner taps have weight.
 __device__ __forceinline__ Taps<int> make_taps_i32(const float* p, int limx, int limy) {
@@ -93,43 +129,56 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
 }
 
-// Table accessors.  Indices passed in are already clamped.
+// Table accessors.  run(u, base, out) returns the kQ + 1 table values
+// S(u, clamp(base + k, 0, W)), k in [0, kQ], of a row u already clamped to
+// [0, H].
+//
+// LDS table, padded: S(u, v) at p[u * pitch + kPad + v], v in [-kPad, W+kPad];
+// the run is kQ + 1 consecutive words from one address.
 template <typename T>
 struct LdsTable {
   const T* p;
-  int pitch;
-  __device__ __forceinline__ T operator()(int u, int v) const { return p[u * pitch + v]; }
+  int pitch, W;
+  __device__ __forceinline__ void run(int u, int base, T* out) const {
+    const T* r = p + __mul24(u, pitch) + kPad + clampi(base, -kPad, W);
+#pragma unroll
+    for (int k = 0; k <= kQ; ++k) out[k] = r[k];
+  }
 };
 
+// Table in HBM, (H+1) x (W+1), unpadded: every index is clamped.
 template <typename T>
 struct GlobalTable {
   const T* __restrict__ p;
-  int pitch;
-  __device__ __forceinline__ T operator()(int u, int v) const { return p[(size_t)u * pitch + v]; }
+  int pitch, W;
+  __device__ __forceinline__ void run(int u, int base, T* out) const {
+    const T* r = p + (size_t)u * pitch;
+#pragma unroll
+    for (int k = 0; k <= kQ; ++k) out[k] = r[clampi(base + k, 0, W)];
+  }
 };
 
-// The x-interpolated table row for kQ consecutive outputs: for q in [0,kQ)
-//   U[q] = sum_k wx[k] * S(u, clamp(x0 + q + ox[k]))
-// ca[k] = clamp(x0 + fa + k), cb[k] = clamp(x0 + fb + k), k in [0, kQ].
+// The x-interpolated table row for kQ consecutive outputs x0 + q: for q in
+// [0, kQ),  U[q] = sum_k wx[k] * S(u, clamp(x0 + q + ox[k])).
+// ba = x0 + fa, bb = x0 + fb (unclamped).
 template <typename T, typename Src>
-__device__ __forceinline__ void table_row(const Src& S, int u, const int* ca, const int* cb,
-                                          const Taps<T>& tp, T* U) {
+__device__ __forceinline__ void table_row(const Src& S, int u, int ba, int bb, const Taps<T>& tp, T* U) {
   T sa[kQ + 1], sb[kQ + 1];
-#pragma unroll
-  for (int k = 0; k <= kQ; ++k) { sa[k] = S(u, ca[k]); sb[k] = S(u, cb[k]); }
+  S.run(u, ba, sa);
+  S.run(u, bb, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q)
     U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
 }
 
 // Same row, also returning the column differences at the two x edges
-// (the edge-column prefix integrals used by the box-parameter gradient).
+// (the table differences across each edge column).
 template <typename Src>
-__device__ __forceinline__ void table_row_grad(const Src& S, int u, const int* ca, const int* cb,
-                                               const Taps<float>& tp, float* U, float* DA, float* DB) {
+__device__ __forceinline__ void table_row_grad(const Src& S, int u, int ba, int bb, const Taps<float>& tp, float* U,
+                                               float* DA, float* DB) {
   float sa[kQ + 1], sb[kQ + 1];
-#pragma unroll
-  for (int k = 0; k <= kQ; ++k) { sa[k] = S(u, ca[k]); sb[k] = S(u, cb[k]); }
+  S.run(u, ba, sa);
+  S.run(u, bb, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
     U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
@@ -138,56 +187,25 @@ __device__ __forceinline__ void table_row_grad(const Src& S, int u, const int* c
   }
 }
 
-template <typename T>
-__device__ __forceinline__ void column_indices(const Taps<T>& tp, int x0, int W, int* ca, int* cb) {
-#pragma unroll
-  for (int k = 0; k <= kQ; ++k) {
-    ca[k] = clampi(x0 + tp.ox[0] + k, 0, W);
-    cb[k] = clampi(x0 + tp.ox[2] + k, 0, W);
-  }
+// Sum over the 16 lanes of each DPP row, in every lane of the row: pair,
+// quad, half-row and row steps through data-parallel lane moves (no LDS).
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));  // row_half_mirror
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));  // row_mirror
+  return v;
 }
 
-// Box evaluation for one item: kQ columns starting at x0, rows [y0, y1).
-// Each step reads two new table rows (one per y edge) and reuses the two
-// from the step before.  `emit(y, o)` receives the kQ outputs of row y.
-// With `offset`, the table holds the map minus mu and mu * (clipped box area)
-// is added back; the clipped area is the same tap combination applied to the
-// clamped coordinates (the table of a constant image is mu * u * v).
-template <typename T, bool kOffset, typename Src, typename Emit>
-__device__ __forceinline__ void box_item(const Src& S, const Taps<T>& tp, int H, int W,
-                                         int x0, int y0, int y1, float mu, Emit emit) {
-  int ca[kQ + 1], cb[kQ + 1];
-  column_indices(tp, x0, W, ca, cb);
-  T uc[kQ], ud[kQ];
-  table_row(S, clampi(y0 + tp.oy[0], 0, H), ca, cb, tp, uc);
-  table_row(S, clampi(y0 + tp.oy[2], 0, H), ca, cb, tp, ud);
-  float ex[kQ];
-  if (kOffset) {
-#pragma unroll
-    for (int q = 0; q < kQ; ++q)
-      ex[q] = (float)tp.wx[0] * (float)ca[q] + (float)tp.wx[1] * (float)ca[q + 1] +
-              (float)tp.wx[2] * (float)cb[q] + (float)tp.wx[3] * (float)cb[q + 1];
-  }
-  for (int y = y0; y < y1; ++y) {
-    T uc1[kQ], ud1[kQ];
-    table_row(S, clampi(y + tp.oy[1], 0, H), ca, cb, tp, uc1);
-    table_row(S, clampi(y + tp.oy[3], 0, H), ca, cb, tp, ud1);
-    T o[kQ];
-#pragma unroll
-    for (int q = 0; q < kQ; ++q)
-      o[q] = tp.wy[0] * uc[q] + tp.wy[1] * uc1[q] + tp.wy[2] * ud[q] + tp.wy[3] * ud1[q];
-    if (kOffset) {
-      const float ey = (float)tp.wy[0] * (float)clampi(y + tp.oy[0], 0, H) +
-                       (float)tp.wy[1] * (float)clampi(y + tp.oy[1], 0, H) +
-                       (float)tp.wy[2] * (float)clampi(y + tp.oy[2], 0, H) +
-                       (float)tp.wy[3] * (float)clampi(y + tp.oy[3], 0, H);
-#pragma unroll
-      for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
-    }
-    emit(y, o);
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
-  }
+// Wave64 sum, wave-uniform result: row sums, then the four rows' values read
+// from lanes 0, 16, 32, 48 (added in a fixed order).
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v = row16_sum(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 
 // Wave-level sum (wave64), result valid in every lane.

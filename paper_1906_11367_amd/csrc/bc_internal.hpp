@@ -7,9 +7,10 @@
 
 namespace bc {
 
-// Row pitch (elements) of a table kept in LDS: W+1 rounded up to odd, so
-// lanes walking down different rows of one column hit distinct banks.
-inline int lds_pitch(int W) { return ((W + 1) & 1) ? (W + 1) : (W + 2); }
+// Row pitch (elements) of a table kept in LDS: W+1 columns plus 3 columns of
+// padding on each side, rounded up to odd so that lanes walking down
+// different rows of one column hit distinct banks.
+inline int lds_pitch(int W) { return (W + 7) | 1; }
 
 // Items of the sliding-window walk: kQ-column chunks x seg-row segments.
 inline int n_chunks(int W) { return (W + 2) / 3; }
@@ -29,15 +30,17 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
                                  hipStream_t s);
 
 // Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
+// LDS path: one block of box_bwd_lds_waves() waves per map, P = N * waves;
+// box_bwd_lds_seg() == 0 means the map has too many items for one block.
 hipError_t launch_box_bwd_lds(const float* x, const float* boxes, const float* gy, float* gx,
-                              float* partials, int N, int C, int H, int W, int B, bool offset,
-                              hipStream_t s);
+                              float* partials, int N, int C, int H, int W, int B, hipStream_t s);
+int box_bwd_lds_seg(int H, int W);
+int box_bwd_lds_waves(int H, int W);
+// HBM path: tables of every gradient map in sat_g (built by sat_build);
+// P = N * box_bwd_gather_blocks() * 4.
 int box_bwd_gather_blocks(int H, int W);
-// Segment length the LDS backward uses for this shape; 0 = does not fit.
-int box_bwd_lds_seg(int N, int C, int H, int W);
-hipError_t launch_box_bwd_gather(const float* sat_x, const float* means, const float* sat_g,
-                                 const float* boxes, const float* gy, float* gx, float* partials,
-                                 int N, int C, int H, int W, int B, hipStream_t s);
+hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const float* boxes, float* gx,
+                                 float* partials, int N, int C, int H, int W, int B, hipStream_t s);
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 
