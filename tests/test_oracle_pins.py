@@ -154,6 +154,71 @@ def test_box_taps_reproduce_forward_on_exact_table():
     np.testing.assert_array_equal(flm[..., 0], np.floor(a))
 
 
+def test_adjoint_taps_match_mirror_taps_off_integer_edges():
+    """Away from integer edges the adjoint split is the floor split of the
+    mirrored box; on an integer edge the floor is one lower and the weights
+    put all of the edge on the upper tap."""
+    rng = np.random.default_rng(21)
+    bx = _real_boxes(rng, 3, 5, cmax=6.0, rmin=0.3, rmax=7.0)
+    fa, wxa, wya = O.adjoint_taps(bx)
+    fm, wxm, wym = O.box_taps(bx, mirror=True)
+    np.testing.assert_array_equal(fa, fm)
+    np.testing.assert_array_equal(wxa, wxm)
+    np.testing.assert_array_equal(wya, wym)
+    bi = np.array([[[1.5, -2.0, 1.0, 2.5]]], dtype=np.float32)   # all four edges integer
+    fa, wxa, wya = O.adjoint_taps(bi)
+    fm, _, _ = O.box_taps(bi, mirror=True)
+    np.testing.assert_array_equal(fa, fm - 1)
+    np.testing.assert_array_equal(wxa[0, 0], np.array([0, -1, 0, 1], np.float32))
+    np.testing.assert_array_equal(wya[0, 0], np.array([0, -1, 0, 1], np.float32))
+
+
+def _adjoint_param_grad(x, g, box):
+    """d<g, box(x)>/d(cx, cy, rx, ry) for one map through the adjoint:
+    <g, box(x)> = <x, D> with D the adjoint box sum of g read from g's
+    exclusive table at adjoint_taps; each edge derivative of D is a difference
+    of the two taps around that edge (small loops, independent of
+    box_backward_params)."""
+    H, W = x.shape
+    S = O.sat_exclusive(g[None, None])[0, 0]
+    fl, wx, wy = O.adjoint_taps(box[None, None])
+    fa, fb, fc, fd = fl[0, 0]
+    wx, wy = wx[0, 0].astype(np.float64), wy[0, 0].astype(np.float64)
+    ox, oy = [fa, fa + 1, fb, fb + 1], [fc, fc + 1, fd, fd + 1]
+    T = lambda u, v: S[min(max(u, 0), H), min(max(v, 0), W)]
+    ga = gb = gc = gd = 0.0
+    for i in range(H):
+        for j in range(W):
+            U = [sum(wx[k] * T(i + oy[r], j + ox[k]) for k in range(4)) for r in range(4)]
+            colA = sum(wy[r] * (T(i + oy[r], j + ox[1]) - T(i + oy[r], j + ox[0])) for r in range(4))
+            colB = sum(wy[r] * (T(i + oy[r], j + ox[3]) - T(i + oy[r], j + ox[2])) for r in range(4))
+            v = x[i, j]
+            ga -= v * colB          # a = 1 - b'
+            gb += v * colA          # b = 1 - a'
+            gc -= v * (U[3] - U[2])  # c = 1 - d'
+            gd += v * (U[1] - U[0])  # d = 1 - c'
+    return np.array([ga + gb, gc + gd, gb - ga, gd - gc])
+
+
+def test_adjoint_taps_carry_param_gradient():
+    """Through <g, box(x)> = <x, adjoint box(g)>, the table differences at
+    adjoint_taps reproduce the parameter gradient, including boxes whose
+    edges sit on pixel boundaries (where the one-sided derivative matters)."""
+    rng = np.random.default_rng(22)
+    H, W = 7, 6
+    boxes = [np.array([rng.uniform(-4, 4), rng.uniform(-4, 4), rng.uniform(0.3, 4), rng.uniform(0.3, 4)],
+                      np.float32) for _ in range(3)]
+    boxes += [np.array([0.5, -1.0, 1.0, 1.5], np.float32), np.array([-2.5, 2.0, 2.0, 0.5], np.float32),
+              np.array([3.0, 0.5, 1.5, 3.0], np.float32)]
+    for box in boxes:
+        x = rng.standard_normal((H, W))
+        g = rng.standard_normal((H, W))
+        want = O.box_backward_params(x[None, None], g[None, None], box[None, None])[0, 0]
+        got = _adjoint_param_grad(x, g, box)
+        # the tap weights are fp32 (reading R5): ~1e-7 relative per weight
+        assert np.all(np.abs(got - want) <= 1e-6 * (1.0 + np.abs(want))), (box, got, want)
+
+
 def test_forward_identity_box_exact():
     rng = np.random.default_rng(3)
     x = rng.standard_normal((2, 3, 8, 6)).astype(np.float32)
@@ -517,6 +582,10 @@ def _mut_param_sign(x, grad_y, boxes):
     return np.stack([ga + gb, gc + gd, ga - gb, gd - gc], axis=-1)
 
 
+def _mut_adjoint_floor_split(boxes):
+    return _OM.box_taps(boxes, mirror=True)
+
+
 def _mut_bf16_truncate(v):
     f = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
     u = (f.view(np.uint32) >> np.uint32(16)) << np.uint32(16)
@@ -548,6 +617,7 @@ _MUTATIONS = {
     "edge_selector_ceil": ("_edge_selector", _mut_edge_selector_ceil),
     "param_sign": ("box_backward_params", _mut_param_sign),
     "bf16_truncate": ("bf16_round", _mut_bf16_truncate),
+    "adjoint_floor_split": ("adjoint_taps", _mut_adjoint_floor_split),
     "bwd_input_no_transpose": ("box_backward_input", _mut_backward_input_no_transpose),
 }
 
@@ -558,6 +628,7 @@ _PINS = [
     test_input_grad_adjoint_and_mirrored_box, test_input_grad_finite_difference,
     test_param_grad_finite_difference_exact, test_param_grad_edges_clipped_at_border,
     test_param_grad_constant_image_closed_form, test_bf16_round_matches_torch,
+    test_adjoint_taps_carry_param_gradient,
 ]
 
 
