@@ -81,19 +81,23 @@ typedef enum {
  *
  * boxes : device fp32 [C][B][4] (cx, cy, rx, ry).
  * table : device, 2*C*B records of 16 32-bit words.  Record r < C*B is box r
- *         (r = c*B + b); record C*B + r is its mirror (centre offset negated:
- *         the box whose correlation is the transpose of box r's).  Words:
- *           0..3  int32  floor(a), floor(b), floor(c), floor(d), each clamped
- *                        to [-2^20, 2^20]; edges evaluated in fp64;
- *           4..7  fp32   x weights of columns floor(a), floor(a)+1, floor(b),
- *                        floor(b)+1: alpha_a - 1, -alpha_a, 1 - alpha_b,
- *                        alpha_b (alpha = edge - floor(edge), in fp64, then
- *                        rounded once to fp32);
+ *         (r = c*B + b); record C*B + r is its adjoint: the mirrored box
+ *         (centre offset negated), whose correlation is the transpose of box
+ *         r's.  Words:
+ *           0..3  int32  floors of the edges a, b, c, d, each clamped to
+ *                        [-2^20, 2^20]; edges evaluated in fp64.  Forward
+ *                        records use floor(e); adjoint records split each
+ *                        edge as e = f + alpha with alpha in (0, 1], i.e.
+ *                        f = ceil(e) - 1, which equals floor(e) except on
+ *                        integer edges (see box_conv_bwd);
+ *           4..7  fp32   x weights of columns f_a, f_a+1, f_b, f_b+1:
+ *                        alpha_a - 1, -alpha_a, 1 - alpha_b, alpha_b
+ *                        (alpha = e - f, in fp64, then rounded once to fp32);
  *           8..11 fp32   y weights, same for c, d;
  *          12..15        zero.
  *         The 16 tap weights of the paper are the products of an x and a y
- *         weight.  The other entry points compute this internally; it is
- *         exported for inspection and testing.
+ *         weight.  box_conv_fwd and box_conv_bwd run this first, into their
+ *         workspace, and read their taps from it.
  * ---------------------------------------------------------------------- */
 bc_status box_prep(const float* boxes, int C, int B, void* table, hipStream_t stream);
 
@@ -125,8 +129,9 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
  * BC_I32 : corners are floored (fractions ignored) and the sum is exact int32
  *          arithmetic -- callers pass integer corners (half-integer cx - rx).
  * flags  : BC_FLAG_MEAN_OFFSET (BC_F32), BC_FLAG_FORCE_HBM.
- * ws     : >= bc_box_workspace_bytes(0, ...) bytes (0 when the map's table fits
- *          in LDS and BC_FLAG_FORCE_HBM is not set).
+ * ws     : >= bc_box_workspace_bytes(0, ...) bytes: the tap records of
+ *          box_prep (2*C*B*64 bytes), plus the maps' tables when a table does
+ *          not fit in LDS or BC_FLAG_FORCE_HBM is set.
  * ---------------------------------------------------------------------- */
 bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
                        int N, int C, int H, int W, int B,
@@ -136,19 +141,24 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
 /* ------------------------------------------------------------------------
  * box_conv_bwd -- gradients of L = <grad_y, y> (fp32):
  *   grad_x[n][c] = sum_b (box (c,b))^T grad_y[n][c*B+b]: the transposed box
- *     sum, evaluated as the mirrored box (centre offset negated) read from the
+ *     sum, evaluated as the adjoint box (centre offset negated) read from the
  *     summed-area table of each upstream-gradient map.
  *   grad_boxes[c][b] = d L / d(cx, cy, rx, ry): each edge's derivative is the
  *     integral of x along that edge (Eq. 4 differenced between the box's two
- *     corners on that edge), read from the table of x; at an edge lying
- *     exactly on a pixel boundary the right derivative is taken.
+ *     corners on that edge); at an edge lying exactly on a pixel boundary the
+ *     right derivative is taken.  Evaluated through L = <x, adjoint box sums
+ *     of grad_y>: the edge derivatives of the adjoint sums are differences of
+ *     the taps already read for grad_x, weighted by x.  Only the gradient maps
+ *     are tabulated, so BC_FLAG_MEAN_OFFSET has no effect here.
  *
  * x          : device fp32 [N][C][H][W]     (the forward input)
  * grad_y     : device fp32 [N][C*B][H][W]
  * grad_x     : device fp32 [N][C][H][W] or NULL (skip)
  * grad_boxes : device fp32 [C][B][4] or NULL (skip); summed over n with a
  *              fixed-order (deterministic) reduction.
- * ws         : >= bc_box_workspace_bytes(1, ...) bytes.
+ * ws         : >= bc_box_workspace_bytes(1, ...) bytes: the tap records,
+ *              the per-wave partial edge gradients, and with the HBM path
+ *              the tables of all N*C*B gradient maps.
  * ---------------------------------------------------------------------- */
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
                        int N, int C, int H, int W, int B,

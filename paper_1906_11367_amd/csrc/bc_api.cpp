@@ -33,27 +33,36 @@ bool bwd_lds_fits(int H, int W) {
   return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(H, W) > 0;
 }
 
-struct FwdWs { size_t sat, means, total; };
-FwdWs fwd_ws(int N, int C, int H, int W) {
-  FwdWs w;
-  w.sat = 0;
-  w.means = align_up((size_t)N * C * table_elems(H, W) * 4);
+// Workspace layouts.  Every box entry point first writes the tap records of
+// all boxes (box_prep) at offset 0; the HBM paths add their tables after it.
+struct FwdWs { size_t taps, sat, means, total; };
+FwdWs fwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+  FwdWs w{};
+  w.taps = 0;
+  w.sat = align_up(bc::tap_table_bytes(C, B));
+  if (!hbm) {
+    w.total = w.sat;
+    return w;
+  }
+  w.means = w.sat + align_up((size_t)N * C * table_elems(H, W) * 4);
   w.total = w.means + align_up((size_t)N * C * 4);
   return w;
 }
 
-struct BwdWs { size_t sat_g, partials, total; int P; };
+struct BwdWs { size_t taps, sat_g, partials, total; int P; };
 BwdWs bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
   BwdWs w{};
+  w.taps = 0;
+  const size_t after_taps = align_up(bc::tap_table_bytes(C, B));
   if (!hbm) {
     w.P = N * bc::box_bwd_lds_waves(H, W);
-    w.partials = 0;
-    w.total = align_up((size_t)w.P * C * B * 4 * 4);
+    w.partials = after_taps;
+    w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
     return w;
   }
   w.P = N * bc::box_bwd_gather_blocks(H, W) * 4;
-  w.sat_g = 0;
-  w.partials = align_up((size_t)N * C * B * table_elems(H, W) * 4);
+  w.sat_g = after_taps;
+  w.partials = w.sat_g + align_up((size_t)N * C * B * table_elems(H, W) * 4);
   w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
   return w;
 }
@@ -101,7 +110,7 @@ size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigne
   if (!dims_ok(N, C, H, W, B)) return 0;
   if (op == 0) {
     const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
-    return hbm ? fwd_ws(N, C, H, W).total : 0;
+    return fwd_ws(N, C, H, W, B, hbm).total;
   }
   if (op == 1) {
     const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W);
@@ -123,17 +132,21 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, 
   const int out_kind = y_dt == BC_BF16 ? 2 : (is_int ? 0 : 1);
   const bool offset = (flags & BC_FLAG_MEAN_OFFSET) != 0;
   const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
-  if (!hbm) return hip_status(bc::launch_box_fwd_lds(x, is_int, boxes, y, out_kind, N, C, H, W, B, offset, stream));
-  if (W > 1024) return BC_ERR_SHAPE;
-  const FwdWs L = fwd_ws(N, C, H, W);
+  if (hbm && W > 1024) return BC_ERR_SHAPE;
+  const FwdWs L = fwd_ws(N, C, H, W, B, hbm);
   if (!ws) return BC_ERR_WORKSPACE;
   if (ws_bytes < L.total) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
   char* base = static_cast<char*>(ws);
-  float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
-  hipError_t e = bc::launch_sat_build(x, is_int, base + L.sat, means, N * C, H, W, stream);
+  const int* taps = reinterpret_cast<const int*>(base + L.taps);
+  hipError_t e = bc::launch_box_prep(boxes, C, B, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  return hip_status(bc::launch_box_fwd_gather(base + L.sat, is_int, means, boxes, y, out_kind, N, C, H, W, B, stream));
+  if (!hbm) return hip_status(bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, stream));
+  float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
+  e = bc::launch_sat_build(x, is_int, base + L.sat, means, N * C, H, W, stream);
+  if (e != hipSuccess) return BC_ERR_HIP;
+  return hip_status(
+      bc::launch_box_fwd_gather(base + L.sat, is_int, means, taps, y, out_kind, N, C, H, W, B, stream));
 }
 
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,
@@ -156,13 +169,15 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   if (!aligned16(ws)) return BC_ERR_ALIGN;
   char* base = static_cast<char*>(ws);
   float* partials = reinterpret_cast<float*>(base + L.partials);
-  hipError_t e;
+  const int* taps = reinterpret_cast<const int*>(base + L.taps);
+  hipError_t e = bc::launch_box_prep(boxes, C, B, base + L.taps, stream);
+  if (e != hipSuccess) return BC_ERR_HIP;
   if (!hbm) {
-    e = bc::launch_box_bwd_lds(x, boxes, grad_y, grad_x, partials, N, C, H, W, B, stream);
+    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, stream);
   } else {
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
     e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
-    if (e == hipSuccess) e = bc::launch_box_bwd_gather(x, sat_g, boxes, grad_x, partials, N, C, H, W, B, stream);
+    if (e == hipSuccess) e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, stream);
   }
   if (e != hipSuccess) return BC_ERR_HIP;
   if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);

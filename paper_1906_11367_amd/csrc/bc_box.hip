@@ -10,14 +10,6 @@ namespace bc {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lds_pitch_dev(int W) { return (W + 7) | 1; }
 
-template <typename T> __device__ __forceinline__ Taps<T> taps_for(const float* p, int limx, int limy);
-template <> __device__ __forceinline__ Taps<float> taps_for<float>(const float* p, int limx, int limy) {
-  return make_taps_f32(p, false, limx, limy);
-}
-template <> __device__ __forceinline__ Taps<int> taps_for<int>(const float* p, int limx, int limy) {
-  return make_taps_i32(p, limx, limy);
-}
-
 template <typename OutT, typename T> __device__ __forceinline__ OutT convert_out(T v);
 template <> __device__ __forceinline__ float convert_out<float, float>(float v) { return v; }
 template <> __device__ __forceinline__ int convert_out<int, int>(int v) { return v; }
@@ -55,26 +47,61 @@ template <typename T> struct Vec4;
 template <> struct Vec4<float> { using type = float4; };
 template <> struct Vec4<int> { using type = int4; };
 
+// Zero row 0 and columns -kPad..0 of every row of a padded LDS table.
+template <typename T>
+__device__ __forceinline__ void table_zero_edges(T* S, int H, int pitch) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int v = tid; v < pitch; v += nt) S[v] = (T)0;
+  for (int k = tid; k < H * (kPad + 1); k += nt) {
+    const int u = 1 + k / (kPad + 1);
+    S[u * pitch + k - (u - 1) * (kPad + 1)] = (T)0;
+  }
+}
+
+// Row pass of a padded LDS table whose interior holds column prefix sums:
+// lanes own rows, reading kScan elements ahead before writing, so that a
+// lane's LDS reads overlap; also fills the right padding.
+template <typename T>
+__device__ __forceinline__ void table_row_pass(T* S, int H, int W, int pitch) {
+  constexpr int kScan = 16;
+  T* R = S + kPad;
+  for (int u = threadIdx.x + 1; u <= H; u += blockDim.x) {
+    T* row = R + u * pitch;
+    T run = (T)0;
+    int v = 1;
+    for (; v + kScan - 1 <= W; v += kScan) {
+      T r[kScan];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) r[k] = row[v + k];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) {
+        run += r[k];
+        row[v + k] = run;
+      }
+    }
+    for (; v <= W; ++v) {
+      run += row[v];
+      row[v] = run;
+    }
+#pragma unroll
+    for (int k = 1; k <= kPad; ++k) row[W + k] = run;
+  }
+}
+
 // Exclusive table of one H x W map in LDS, padded (LdsTable): S(u, v) at
 // S[u * pitch + kPad + v].  The map is first copied into the table's interior
 // with every thread issuing 16-byte loads in batches (the loads of a batch are
 // all in flight together; out-of-range slots re-read the last vector and are
 // not stored, so no lane branches around a load).  Then a column pass (lanes
-// own columns) and a row pass (lanes own rows; odd pitch: no bank conflicts),
-// each reading kScan elements ahead before it writes, so that a lane's LDS
-// reads overlap instead of waiting on one another; the row pass also fills
-// the right padding.  With `sub`, mu is subtracted from the tabulated values.
+// own columns) and the row pass, each reading kScan elements ahead before it
+// writes.  With `sub`, mu is subtracted from the tabulated values.
 template <typename T>
 __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch, float mu, bool sub) {
   using V = typename Vec4<T>::type;
   constexpr int kBatch = 8, kScan = 16;
   const int tid = threadIdx.x, nt = blockDim.x;
   T* R = S + kPad;
-  for (int v = tid; v < pitch; v += nt) S[v] = (T)0;
-  for (int k = tid; k < H * (kPad + 1); k += nt) {
-    const int u = 1 + k / (kPad + 1);
-    S[u * pitch + k % (kPad + 1)] = (T)0;
-  }
+  table_zero_edges(S, H, pitch);
   const int n = H * W;
   if ((W & 3) == 0 && ((uintptr_t)src & 15) == 0) {
     const int n4 = n >> 2;
@@ -122,27 +149,7 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
     }
   }
   __syncthreads();
-  for (int u = tid + 1; u <= H; u += nt) {
-    T* row = R + u * pitch;
-    T run = (T)0;
-    int v = 1;
-    for (; v + kScan - 1 <= W; v += kScan) {
-      T r[kScan];
-#pragma unroll
-      for (int k = 0; k < kScan; ++k) r[k] = row[v + k];
-#pragma unroll
-      for (int k = 0; k < kScan; ++k) {
-        run += r[k];
-        row[v + k] = run;
-      }
-    }
-    for (; v <= W; ++v) {
-      run += row[v];
-      row[v] = run;
-    }
-#pragma unroll
-    for (int k = 1; k <= kPad; ++k) row[W + k] = run;
-  }
+  table_row_pass(S, H, W, pitch);
   __syncthreads();
 }
 
@@ -150,16 +157,24 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
 // Walks with compile-time segment length (registers indexed statically)
 // ---------------------------------------------------------------------------
 
-// Forward walk: emit.put<kFull>(s, y, o) for s in [0, SEG) with y = y0 + s < y1.
+// Forward walk: emit.put<kFull>(s, o) for s in [0, SEG) with y0 + s < y1.
 // kFull: the item is known to be whole (y1 = y0 + SEG, x0 + kQ <= W), so no
 // step or column is guarded and the unrolled window needs no register copies.
+// Each step reads two new table rows (one per y edge) and reuses the two from
+// the step before.  With kOffset the table holds the map minus mu, and
+// mu * (clipped box area) is added back: the clipped area is the same tap
+// combination applied to the clamped coordinates (the table of a constant
+// image is mu * u * v).
 template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
 __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H, int W, int x0,
                                          int y0, int y1, float mu, Emit& emit) {
   const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
+  const typename Src::Cols cl = S.cols(ba, bb);
+  const int st = S.row_step();
+  const int rc = S.row_coord(y0 + tp.oy[0]), rd = S.row_coord(y0 + tp.oy[2]);
   T uc[kQ], ud[kQ];
-  table_row(S, clampi(y0 + tp.oy[0], 0, H), ba, bb, tp, uc);
-  table_row(S, clampi(y0 + tp.oy[2], 0, H), ba, bb, tp, ud);
+  table_row(S, rc, cl, tp, uc);
+  table_row(S, rd, cl, tp, ud);
   float ex[kQ];
   if (kOffset) {
 #pragma unroll
@@ -172,8 +187,8 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
     const int y = y0 + s;
     if (kFull || y < y1) {
       T uc1[kQ], ud1[kQ];
-      table_row(S, clampi(y + tp.oy[1], 0, H), ba, bb, tp, uc1);
-      table_row(S, clampi(y + tp.oy[3], 0, H), ba, bb, tp, ud1);
+      table_row(S, rc + (s + 1) * st, cl, tp, uc1);
+      table_row(S, rd + (s + 1) * st, cl, tp, ud1);
       T o[kQ];
 #pragma unroll
       for (int q = 0; q < kQ; ++q)
@@ -186,7 +201,7 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 #pragma unroll
         for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
       }
-      emit.template put<kFull>(s, y, o);
+      emit.template put<kFull>(s, o);
 #pragma unroll
       for (int q = 0; q < kQ; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
     }
@@ -194,8 +209,8 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 }
 
 // Backward walk over one item on the table of one upstream-gradient map G,
-// with the adjoint taps of the box (make_taps_adjoint).  For each input pixel
-// (y, x) = (y0 + s, x0 + q):
+// with the adjoint taps of the box.  For each input pixel (y, x) =
+// (y0 + s, x0 + q):
 //   acc[s][q] += D(y, x), the adjoint box sum of G (the input gradient);
 // and, since <G, box(I)> = <I, D> for every placement of the box, the four
 // edge gradients of the original box follow from the derivatives of D with
@@ -203,41 +218,54 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 // (0 outside the map).  The adjoint's edges are a' = 1 - b, b' = 1 - a,
 // c' = 1 - d, d' = 1 - c, so
 //   dL/da = -sum v * (G integrated over the adjoint's y extent along the
-//           column just below x + b'):  minus the y-weighted differences of
-//           the two table columns at b';
+//           column just below x + b'): the y-weighted differences of the two
+//           table columns at b';
 //   dL/db = +sum v * (the same at a');
 //   dL/dc = -sum v * (G integrated over the x extent along the row below
-//           y + d'):  the difference of the x-interpolated rows at d';
+//           y + d'): the difference of the x-interpolated rows at d';
 //   dL/dd = +sum v * (the same at c').
-// These are Eq. 4's edge integrals moved to the gradient's table; the split
-// of the adjoint's edges puts the one-sided derivative between each edge's
-// two taps.  g4 += (dL/da, dL/db, dL/dc, dL/dd) summed over the item.
+// These are Eq. 4's edge integrals moved to the gradient's table; the adjoint
+// split of the edges puts the one-sided derivative between each edge's two
+// taps.  The y weights are the same for every pixel, so the walk keeps one
+// sum per tap row and applies them once (edge_grads):
+//   P[r]     += v * (column difference at a', tap row r),
+//   P[4 + r] += v * (column difference at b', tap row r),
+//   P[8 + r] += v * (x-interpolated row r),  r = c'0, c'1, d'0, d'1.
 template <int SEG, bool kFull, typename Src>
-__device__ __forceinline__ void adjoint_walk(const Src& S, const Taps<float>& tp, int H, int W, int x0, int y0,
-                                             int y1, const float (&v)[SEG][kQ], float (&acc)[SEG][kQ],
-                                             float* g4) {
-  const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
+__device__ __forceinline__ void adjoint_walk(const Src& S, const Taps<float>& tp, int x0, int y0, int y1,
+                                             const float (&v)[SEG][kQ], float (&acc)[SEG][kQ], float (&P)[12]) {
+  const typename Src::Cols cl = S.cols(x0 + tp.ox[0], x0 + tp.ox[2]);
+  const int st = S.row_step();
+  const int rc = S.row_coord(y0 + tp.oy[0]), rd = S.row_coord(y0 + tp.oy[2]);
   float Uc[kQ], Ac[kQ], Bc[kQ], Ud[kQ], Ad[kQ], Bd[kQ];
-  table_row_grad(S, clampi(y0 + tp.oy[0], 0, H), ba, bb, tp, Uc, Ac, Bc);
-  table_row_grad(S, clampi(y0 + tp.oy[2], 0, H), ba, bb, tp, Ud, Ad, Bd);
-  float ga = 0.f, gb = 0.f, gc = 0.f, gd = 0.f;
+  table_row_grad(S, rc, cl, tp, Uc, Ac, Bc);
+  table_row_grad(S, rd, cl, tp, Ud, Ad, Bd);
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
-    const int y = y0 + s;
-    if (kFull || y < y1) {
+    if (kFull || y0 + s < y1) {
       float Uc1[kQ], Ac1[kQ], Bc1[kQ], Ud1[kQ], Ad1[kQ], Bd1[kQ];
-      table_row_grad(S, clampi(y + tp.oy[1], 0, H), ba, bb, tp, Uc1, Ac1, Bc1);
-      table_row_grad(S, clampi(y + tp.oy[3], 0, H), ba, bb, tp, Ud1, Ad1, Bd1);
+      table_row_grad(S, rc + (s + 1) * st, cl, tp, Uc1, Ac1, Bc1);
+      table_row_grad(S, rd + (s + 1) * st, cl, tp, Ud1, Ad1, Bd1);
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
-        acc[s][q] += tp.wy[0] * Uc[q] + tp.wy[1] * Uc1[q] + tp.wy[2] * Ud[q] + tp.wy[3] * Ud1[q];
-        const float colA = tp.wy[0] * Ac[q] + tp.wy[1] * Ac1[q] + tp.wy[2] * Ad[q] + tp.wy[3] * Ad1[q];
-        const float colB = tp.wy[0] * Bc[q] + tp.wy[1] * Bc1[q] + tp.wy[2] * Bd[q] + tp.wy[3] * Bd1[q];
+        float a = acc[s][q];
+        a = fmaf(tp.wy[0], Uc[q], a);
+        a = fmaf(tp.wy[1], Uc1[q], a);
+        a = fmaf(tp.wy[2], Ud[q], a);
+        acc[s][q] = fmaf(tp.wy[3], Ud1[q], a);
         const float val = v[s][q];
-        ga -= val * colB;
-        gb += val * colA;
-        gc -= val * (Ud1[q] - Ud[q]);
-        gd += val * (Uc1[q] - Uc[q]);
+        P[0] = fmaf(val, Ac[q], P[0]);
+        P[1] = fmaf(val, Ac1[q], P[1]);
+        P[2] = fmaf(val, Ad[q], P[2]);
+        P[3] = fmaf(val, Ad1[q], P[3]);
+        P[4] = fmaf(val, Bc[q], P[4]);
+        P[5] = fmaf(val, Bc1[q], P[5]);
+        P[6] = fmaf(val, Bd[q], P[6]);
+        P[7] = fmaf(val, Bd1[q], P[7]);
+        P[8] = fmaf(val, Uc[q], P[8]);
+        P[9] = fmaf(val, Uc1[q], P[9]);
+        P[10] = fmaf(val, Ud[q], P[10]);
+        P[11] = fmaf(val, Ud1[q], P[11]);
       }
 #pragma unroll
       for (int q = 0; q < kQ; ++q) {
@@ -246,17 +274,31 @@ __device__ __forceinline__ void adjoint_walk(const Src& S, const Taps<float>& tp
       }
     }
   }
-  g4[0] += ga; g4[1] += gb; g4[2] += gc; g4[3] += gd;
 }
 
-// Emitters of walk outputs.
+// (dL/da, dL/db, dL/dc, dL/dd) from the per-tap-row sums of adjoint_walk.
+__device__ __forceinline__ void edge_grads(const Taps<float>& tp, const float (&P)[12], float* g4) {
+  float ca = 0.f, cb = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    ca = fmaf(tp.wy[r], P[r], ca);
+    cb = fmaf(tp.wy[r], P[4 + r], cb);
+  }
+  g4[0] = -cb;
+  g4[1] = ca;
+  g4[2] = P[10] - P[11];
+  g4[3] = P[9] - P[8];
+}
+
+// Emitter of forward outputs: the kQ outputs of row y0 + s at plane offset
+// off0 + s * W (elements; off0 = y0 * W + x0).
 template <typename OutT, typename T>
-struct StoreRows {  // forward: write the kQ outputs of row y
+struct StoreRows {
   OutT* out;
-  int W, x0;
+  int W, x0, off0;
   template <bool kFull>
-  __device__ __forceinline__ void put(int, int y, const T* o) {
-    OutT* row = out + (size_t)y * W + x0;
+  __device__ __forceinline__ void put(int s, const T* o) {
+    OutT* row = out + (unsigned)(off0 + s * W);
 #pragma unroll
     for (int q = 0; q < kQ; ++q)
       if (kFull || x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
@@ -266,11 +308,14 @@ struct StoreRows {  // forward: write the kQ outputs of row y
 // ---------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------
+// Tap records (16 words each): record r < CB is box r's forward taps, record
+// CB + r its adjoint taps (make_taps_adjoint).
 __global__ void k_box_prep(const float* __restrict__ boxes, int CB, int* __restrict__ table) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= 2 * CB) return;
-  const bool mirror = i >= CB;
-  const Taps<float> t = make_taps_f32(boxes + (size_t)(mirror ? i - CB : i) * 4, mirror, 1 << 20, 1 << 20);
+  const bool adj = i >= CB;
+  const float* p = boxes + (size_t)(adj ? i - CB : i) * 4;
+  const Taps<float> t = adj ? make_taps_adjoint(p, 1 << 20, 1 << 20) : make_taps_f32(p, false, 1 << 20, 1 << 20);
   int* r = table + (size_t)i * 16;
   float* f = reinterpret_cast<float*>(r);
   r[0] = t.ox[0]; r[1] = t.ox[2]; r[2] = t.oy[0]; r[3] = t.oy[2];
@@ -348,45 +393,61 @@ __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* _
   }
 }
 
-// Forward, table in LDS: one block per (map, group of boxes).  The block
-// builds the map's table once and evaluates every box of its group; item
-// `it` is (box, row segment, 3-column chunk), chunk fastest so that adjacent
-// lanes write adjacent columns.
+template <typename T> __device__ __forceinline__ Taps<T> typed_taps(const Taps<float>& t);
+template <> __device__ __forceinline__ Taps<float> typed_taps<float>(const Taps<float>& t) { return t; }
+template <> __device__ __forceinline__ Taps<int> typed_taps<int>(const Taps<float>& t) { return int_taps(t); }
+
+// Forward on a map's table in LDS, for the boxes b0 .. b0+nb-1 of channel c.
+// Items of one box are (row segment, 3-column chunk), chunk fastest so that
+// adjacent lanes write adjacent columns; each box's items are padded to a
+// multiple of 64 (per_box_p) so that a wave works on one box and reads its
+// taps through scalar loads.
 template <typename T, typename OutT, int SEG, bool kOffset>
-__global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const float* __restrict__ boxes,
-                                                     OutT* __restrict__ y, int C, int H, int W, int B, int bpg) {
+__device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __restrict__ taps,
+                                          OutT* __restrict__ y, int map, int c, int b0, int nb, int H, int W,
+                                          int B, int per_box_p, float mu) {
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
+  for (int it = threadIdx.x; it < nb * per_box_p; it += blockDim.x) {
+    const int bl = __builtin_amdgcn_readfirstlane(it / per_box_p);
+    const int r = it - bl * per_box_p;
+    if (r >= per_box) continue;
+    const int seg = r / nch, ch = r - seg * nch;
+    const int b = b0 + bl;
+    const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
+    OutT* out = y + ((size_t)map * B + b) * H * W;
+    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+    StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
+    if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
+    else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
+  }
+}
+
+// Forward, table in LDS: one block per (map, group of bpg boxes).  The block
+// builds the map's table once and evaluates every box of its group.
+template <typename T, typename OutT, int SEG, bool kOffset>
+__global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const int* __restrict__ taps,
+                                                     OutT* __restrict__ y, int C, int H, int W, int B, int bpg,
+                                                     int per_box_p) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* S = reinterpret_cast<T*>(smem_raw);
   __shared__ float red[16];
   const int pitch = lds_pitch_dev(W);
   const int ngrp = (B + bpg - 1) / bpg;
   const int map = blockIdx.x / ngrp, grp = blockIdx.x - map * ngrp;
-  const int c = map % C;
   const T* src = x + (size_t)map * H * W;
   float mu = 0.f;
   if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
   build_table_lds(src, S, H, W, pitch, mu, kOffset);
-  const int b0 = grp * bpg, nb = min(bpg, B - b0);
-  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
-  const LdsTable<T> tab{S, pitch, W};
-  for (int it = threadIdx.x; it < nb * per_box; it += blockDim.x) {
-    const int bl = it / per_box, r = it - bl * per_box;
-    const int seg = r / nch, ch = r - seg * nch;
-    const int b = b0 + bl;
-    const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
-    OutT* out = y + ((size_t)map * B + b) * H * W;
-    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-    StoreRows<OutT, T> em{out, W, x0};
-    if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
-    else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
-  }
+  const int b0 = grp * bpg;
+  fwd_boxes<T, OutT, SEG, kOffset>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0, min(bpg, B - b0), H,
+                                   W, B, per_box_p, mu);
 }
 
 // Forward, table in HBM: one block per (map, box, block of 256 items), mapped
 // so that one map's blocks run on one XCD.
 template <typename T, typename OutT, int SEG, bool kOffset>
 __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sat, const float* __restrict__ means,
-                                                        const float* __restrict__ boxes, OutT* __restrict__ y,
+                                                        const int* __restrict__ taps, OutT* __restrict__ y,
                                                         int C, int H, int W, int B, int nblk, int total) {
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   if (L >= total) return;
@@ -396,12 +457,12 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   const int it = blk * 256 + threadIdx.x;
   if (it >= nch * nseg) return;
   const int seg = it / nch, ch = it - seg * nch;
-  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W};
+  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
   const float mu = kOffset ? means[map] : 0.f;
-  const Taps<T> tp = taps_for<T>(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
+  const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
   OutT* out = y + ((size_t)map * B + b) * H * W;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  StoreRows<OutT, T> em{out, W, x0};
+  StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
   if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
   else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
@@ -451,7 +512,7 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // each wave writes its edge-gradient sums to
 // partials[(n * nw + wave) * C*B + c*B + b][4].
 template <int SEG>
-__global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const float* __restrict__ boxes,
+__global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
                                                      const float* __restrict__ gy, float* __restrict__ gx,
                                                      float* __restrict__ partials, int C, int H, int W, int B) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -465,25 +526,32 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
   const int seg = it / nch, ch = it - seg * nch;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
   const bool full = y0 + SEG <= H && x0 + kQ <= W;
+  const size_t plane = (size_t)H * W;
+  const float* g0 = gy + (size_t)map * B * plane;
   float v[SEG][kQ], acc[SEG][kQ];
-  load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
+  load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
     for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
-  const LdsTable<float> tg{SG, pitch, W};
+  const LdsTable<float> tg{SG, pitch, W, H};
+  const int* adj = taps + (size_t)C * B * 16;
   for (int b = 0; b < B; ++b) {
     __syncthreads();
-    build_table_lds(gy + ((size_t)map * B + b) * H * W, SG, H, W, pitch, 0.f, false);
-    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+    build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
+    const Taps<float> tp = load_taps(adj + (size_t)(c * B + b) * 16, W, H);
+    float P[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) P[k] = 0.f;
     if (active) {
-      const Taps<float> tp = make_taps_adjoint(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
-      if (full) adjoint_walk<SEG, true>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
-      else adjoint_walk<SEG, false>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
+      if (full) adjoint_walk<SEG, true>(tg, tp, x0, y0, y1, v, acc, P);
+      else adjoint_walk<SEG, false>(tg, tp, x0, y0, y1, v, acc, P);
     }
+    float g4[4];
+    edge_grads(tp, P, g4);
     store_wave_partial(g4, partials + (((size_t)n * nw + wave) * C * B + (size_t)c * B + b) * 4);
   }
-  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
+  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * plane, H, W, x0, y0, acc);
 }
 
 // Backward, tables in HBM (one table per gradient map, built beforehand).
@@ -491,7 +559,7 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
 // partials: [((n * nblk + blk) * 4 + wave) * C*B + c*B + b][4].
 template <int SEG>
 __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict__ x, const float* __restrict__ sat_g,
-                                                        const float* __restrict__ boxes, float* __restrict__ gx,
+                                                        const int* __restrict__ taps, float* __restrict__ gx,
                                                         float* __restrict__ partials, int C, int H, int W, int B,
                                                         int nblk, int total) {
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -512,14 +580,19 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
     for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  const int* adj = taps + (size_t)C * B * 16;
   for (int b = 0; b < B; ++b) {
-    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1, W};
-    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1, W, H};
+    const Taps<float> tp = load_taps(adj + (size_t)(c * B + b) * 16, W, H);
+    float P[12];
+#pragma unroll
+    for (int k = 0; k < 12; ++k) P[k] = 0.f;
     if (active) {
-      const Taps<float> tp = make_taps_adjoint(boxes + (size_t)(c * B + b) * 4, W + 1, H + 1);
-      if (full) adjoint_walk<SEG, true>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
-      else adjoint_walk<SEG, false>(tg, tp, H, W, x0, y0, y1, v, acc, g4);
+      if (full) adjoint_walk<SEG, true>(tg, tp, x0, y0, y1, v, acc, P);
+      else adjoint_walk<SEG, false>(tg, tp, x0, y0, y1, v, acc, P);
     }
+    float g4[4];
+    edge_grads(tp, P, g4);
     store_wave_partial(g4, partials + ((((size_t)n * nblk + blk) * 4 + wave) * C * B + (size_t)c * B + b) * 4);
   }
   if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
@@ -566,71 +639,78 @@ hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, 
   return last_error();
 }
 
-template <typename T, typename OutT, bool kOffset>
-static void fwd_lds_t(const void* x, const float* boxes, void* y, int N, int C, int H, int W, int B, hipStream_t s) {
-  constexpr int SEG = 16;
-  const int per_box = n_chunks(W) * n_segs(H, SEG);
-  int bpg = 256 / per_box;
-  if (bpg < 1) bpg = 1;
-  if (bpg > B) bpg = B;
+// Forward launch geometry shared by both LDS kernels.
+struct FwdGeom { int per_box_p, bpg, ngrp, threads; };
+static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
+  FwdGeom g;
+  const int per_box = n_chunks(W) * n_segs(H, seg);
+  g.per_box_p = ((per_box + 63) / 64) * 64;
+  g.bpg = 256 / g.per_box_p;
+  if (g.bpg < 1) g.bpg = 1;
+  if (g.bpg > B) g.bpg = B;
   // keep enough blocks in flight to fill the chip
-  while (bpg > 1 && (long)N * C * ((B + bpg - 1) / bpg) < 2048) bpg = (bpg + 1) / 2;
-  const int ngrp = (B + bpg - 1) / bpg;
-  int threads = bpg * per_box;
-  threads = ((threads + 63) / 64) * 64;
-  if (threads > 256) threads = 256;
-  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
-  hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset>), dim3(N * C * ngrp), dim3(threads), shm, s,
-                     (const T*)x, boxes, (OutT*)y, C, H, W, B, bpg);
+  while (g.bpg > 1 && (long)N * C * ((B + g.bpg - 1) / g.bpg) < 2048) g.bpg = (g.bpg + 1) / 2;
+  g.ngrp = (B + g.bpg - 1) / g.bpg;
+  g.threads = min(g.bpg * g.per_box_p, 256);
+  return g;
 }
 
-hipError_t launch_box_fwd_lds(const void* x, bool is_int, const float* boxes, void* y, int out_kind, int N, int C,
+template <typename T, typename OutT, bool kOffset>
+static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int H, int W, int B, hipStream_t s) {
+  constexpr int SEG = 16;
+  const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
+  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
+  hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s,
+                     (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+}
+
+hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void* y, int out_kind, int N, int C,
                               int H, int W, int B, bool offset, hipStream_t s) {
   if (is_int) {
-    fwd_lds_t<int, int, false>(x, boxes, y, N, C, H, W, B, s);
+    fwd_lds_t<int, int, false>(x, taps, y, N, C, H, W, B, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_lds_t<float, uint16_t, true>(x, boxes, y, N, C, H, W, B, s);
-    else fwd_lds_t<float, uint16_t, false>(x, boxes, y, N, C, H, W, B, s);
+    if (offset) fwd_lds_t<float, uint16_t, true>(x, taps, y, N, C, H, W, B, s);
+    else fwd_lds_t<float, uint16_t, false>(x, taps, y, N, C, H, W, B, s);
   } else {
-    if (offset) fwd_lds_t<float, float, true>(x, boxes, y, N, C, H, W, B, s);
-    else fwd_lds_t<float, float, false>(x, boxes, y, N, C, H, W, B, s);
+    if (offset) fwd_lds_t<float, float, true>(x, taps, y, N, C, H, W, B, s);
+    else fwd_lds_t<float, float, false>(x, taps, y, N, C, H, W, B, s);
   }
   return last_error();
 }
 
 template <typename T, typename OutT, bool kOffset>
-static void fwd_gather_t(const void* sat, const float* means, const float* boxes, void* y, int N, int C, int H,
-                         int W, int B, hipStream_t s) {
+static void fwd_gather_t(const void* sat, const float* means, const int* taps, void* y, int N, int C, int H, int W,
+                         int B, hipStream_t s) {
   constexpr int SEG = 16;
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int nblk = (items + 255) / 256;
   const int total = N * C * B * nblk;
   hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset>), dim3(pad8(total)), dim3(256), 0, s,
-                     (const T*)sat, means, boxes, (OutT*)y, C, H, W, B, nblk, total);
+                     (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
 }
 
-hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const float* boxes, void* y,
+hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const int* taps, void* y,
                                  int out_kind, int N, int C, int H, int W, int B, hipStream_t s) {
   const bool offset = means != nullptr;
   if (is_int) {
-    fwd_gather_t<int, int, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+    fwd_gather_t<int, int, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, boxes, y, N, C, H, W, B, s);
-    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, taps, y, N, C, H, W, B, s);
+    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
   } else {
-    if (offset) fwd_gather_t<float, float, true>(sat, means, boxes, y, N, C, H, W, B, s);
-    else fwd_gather_t<float, float, false>(sat, nullptr, boxes, y, N, C, H, W, B, s);
+    if (offset) fwd_gather_t<float, float, true>(sat, means, taps, y, N, C, H, W, B, s);
+    else fwd_gather_t<float, float, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
   }
   return last_error();
 }
 
 template <int SEG>
-static void bwd_lds_t(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N, int C,
+static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N, int C,
                       int H, int W, int B, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int threads = ((items + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
-  hipLaunchKernelGGL((k_box_bwd_lds<SEG>), dim3(N * C), dim3(threads), shm, s, x, boxes, gy, gx, partials, C, H, W,
+  hipLaunchKernelGGL((k_box_bwd_lds<SEG>), dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W,
                      B);
 }
 
@@ -647,11 +727,11 @@ int box_bwd_lds_waves(int H, int W) {
   return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
 }
 
-hipError_t launch_box_bwd_lds(const float* x, const float* boxes, const float* gy, float* gx, float* partials, int N,
+hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N,
                               int C, int H, int W, int B, hipStream_t s) {
   const int seg = box_bwd_lds_seg(H, W);
-  if (seg == 8) bwd_lds_t<8>(x, boxes, gy, gx, partials, N, C, H, W, B, s);
-  else if (seg == 4) bwd_lds_t<4>(x, boxes, gy, gx, partials, N, C, H, W, B, s);
+  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, s);
+  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, s);
   else return hipErrorInvalidValue;
   return last_error();
 }
@@ -660,11 +740,11 @@ constexpr int kBwdGatherSeg = 8;
 
 int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, kBwdGatherSeg) + 255) / 256; }
 
-hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const float* boxes, float* gx, float* partials,
+hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx, float* partials,
                                  int N, int C, int H, int W, int B, hipStream_t s) {
   const int nblk = box_bwd_gather_blocks(H, W);
   const int total = N * C * nblk;
-  hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg>), dim3(pad8(total)), dim3(256), 0, s, x, sat_g, boxes, gx,
+  hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg>), dim3(pad8(total)), dim3(256), 0, s, x, sat_g, taps, gx,
                      partials, C, H, W, B, nblk, total);
   return last_error();
 }

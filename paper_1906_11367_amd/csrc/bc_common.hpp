@@ -105,17 +105,6 @@ __device__ __forceinline__ Taps<float> make_taps_adjoint(const float* p, int lim
   return t;
 }
 
-// Integer maps: corners are floored (the fractions are ignored), so the box is
-// the plain sum of Eq. 1 and only the four corner taps have weight.
-__device__ __forceinline__ Taps<int> make_taps_i32(const float* p, int limx, int limy) {
-  Taps<float> f = make_taps_f32(p, false, limx, limy);
-  Taps<int> t;
-  for (int k = 0; k < 4; ++k) { t.ox[k] = f.ox[k]; t.oy[k] = f.oy[k]; }
-  t.wx[0] = -1; t.wx[1] = 0; t.wx[2] = 1; t.wx[3] = 0;
-  t.wy[0] = -1; t.wy[1] = 0; t.wy[2] = 1; t.wy[3] = 0;
-  return t;
-}
-
 // fp32 -> bf16, round to nearest even; NaN stays NaN (quiet).  Branch-free
 // (a select), so that it never splits a wave.
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
@@ -129,43 +118,67 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
 }
 
-// Table accessors.  run(u, base, out) returns the kQ + 1 table values
-// S(u, clamp(base + k, 0, W)), k in [0, kQ], of a row u already clamped to
-// [0, H].
+// v clamped to [lo, hi] in one instruction (hi wave-uniform).
+__device__ __forceinline__ int med3_i32(int v, int hi) {
+  int r;
+  asm("v_med3_i32 %0, %1, 0, %2" : "=v"(r) : "v"(v), "s"(hi));
+  return r;
+}
+
+// Table accessors.  A walk addresses a table row by an unclamped row
+// coordinate in the table's own units (row_coord(v) for table row v; one row
+// further is + row_step()), and the two runs of kQ + 1 columns it reads by
+// cols(ba, bb) with ba = x0 + fa, bb = x0 + fb unclamped.  runs(coord, c, sa,
+// sb) returns S(clamp(v, 0, H), clamp(ba + k, 0, W)) and the same at bb,
+// k in [0, kQ].
 //
 // LDS table, padded: S(u, v) at p[u * pitch + kPad + v], v in [-kPad, W+kPad];
-// the run is kQ + 1 consecutive words from one address.
+// coordinates are byte offsets, a row is clamped once (v_med3) and each run
+// is kQ + 1 consecutive words from one address.
 template <typename T>
 struct LdsTable {
   const T* p;
-  int pitch, W;
-  __device__ __forceinline__ void run(int u, int base, T* out) const {
-    const T* r = p + __mul24(u, pitch) + kPad + clampi(base, -kPad, W);
+  int pitch, W, H;
+  struct Cols { const char* a; const char* b; };  // first word of each run in table row 0
+  __device__ __forceinline__ Cols cols(int ba, int bb) const {
+    const char* base = reinterpret_cast<const char*>(p + kPad);
+    return {base + clampi(ba, -kPad, W) * (int)sizeof(T), base + clampi(bb, -kPad, W) * (int)sizeof(T)};
+  }
+  __device__ __forceinline__ int row_step() const { return pitch * (int)sizeof(T); }
+  __device__ __forceinline__ int row_coord(int v) const { return v * row_step(); }
+  __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
+    const int row = med3_i32(coord, H * row_step());
+    const T* ra = reinterpret_cast<const T*>(c.a + row);
+    const T* rb = reinterpret_cast<const T*>(c.b + row);
 #pragma unroll
-    for (int k = 0; k <= kQ; ++k) out[k] = r[k];
+    for (int k = 0; k <= kQ; ++k) { sa[k] = ra[k]; sb[k] = rb[k]; }
   }
 };
 
-// Table in HBM, (H+1) x (W+1), unpadded: every index is clamped.
+// Table in HBM, (H+1) x (W+1), unpadded: row coordinates are row indices and
+// every index is clamped.
 template <typename T>
 struct GlobalTable {
   const T* __restrict__ p;
-  int pitch, W;
-  __device__ __forceinline__ void run(int u, int base, T* out) const {
-    const T* r = p + (size_t)u * pitch;
+  int pitch, W, H;
+  struct Cols { int a, b; };
+  __device__ __forceinline__ Cols cols(int ba, int bb) const { return {ba, bb}; }
+  __device__ __forceinline__ int row_step() const { return 1; }
+  __device__ __forceinline__ int row_coord(int v) const { return v; }
+  __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
+    const T* r = p + (size_t)clampi(coord, 0, H) * pitch;
 #pragma unroll
-    for (int k = 0; k <= kQ; ++k) out[k] = r[clampi(base + k, 0, W)];
+    for (int k = 0; k <= kQ; ++k) { sa[k] = r[clampi(c.a + k, 0, W)]; sb[k] = r[clampi(c.b + k, 0, W)]; }
   }
 };
 
 // The x-interpolated table row for kQ consecutive outputs x0 + q: for q in
-// [0, kQ),  U[q] = sum_k wx[k] * S(u, clamp(x0 + q + ox[k])).
-// ba = x0 + fa, bb = x0 + fb (unclamped).
+// [0, kQ),  U[q] = sum_k wx[k] * S(v, clamp(x0 + q + ox[k])).
 template <typename T, typename Src>
-__device__ __forceinline__ void table_row(const Src& S, int u, int ba, int bb, const Taps<T>& tp, T* U) {
+__device__ __forceinline__ void table_row(const Src& S, int coord, const typename Src::Cols& c, const Taps<T>& tp,
+                                          T* U) {
   T sa[kQ + 1], sb[kQ + 1];
-  S.run(u, ba, sa);
-  S.run(u, bb, sb);
+  S.runs(coord, c, sa, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q)
     U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
@@ -174,17 +187,44 @@ __device__ __forceinline__ void table_row(const Src& S, int u, int ba, int bb, c
 // Same row, also returning the column differences at the two x edges
 // (the table differences across each edge column).
 template <typename Src>
-__device__ __forceinline__ void table_row_grad(const Src& S, int u, int ba, int bb, const Taps<float>& tp, float* U,
-                                               float* DA, float* DB) {
+__device__ __forceinline__ void table_row_grad(const Src& S, int coord, const typename Src::Cols& c,
+                                               const Taps<float>& tp, float* U, float* DA, float* DB) {
   float sa[kQ + 1], sb[kQ + 1];
-  S.run(u, ba, sa);
-  S.run(u, bb, sb);
+  S.runs(coord, c, sa, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
     U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
     DA[q] = sa[q + 1] - sa[q];
     DB[q] = sb[q + 1] - sb[q];
   }
+}
+
+// Taps of one box from its record in the table box_prep writes (16 words:
+// floors of a, b, c, d; x weights; y weights).  Called with a wave-uniform
+// record, so the record comes in through scalar loads.  The floors are
+// clamped to [-(n+1), n+1] for a map of extent n, which leaves every clamped
+// tap index unchanged and keeps row and column arithmetic in range.
+__device__ __forceinline__ Taps<float> load_taps(const int* __restrict__ rec, int W, int H) {
+  const float* f = reinterpret_cast<const float*>(rec);
+  Taps<float> t;
+  const int fa = clampi(rec[0], -(W + 1), W + 1), fb = clampi(rec[1], -(W + 1), W + 1);
+  const int fc = clampi(rec[2], -(H + 1), H + 1), fd = clampi(rec[3], -(H + 1), H + 1);
+  t.ox[0] = fa; t.ox[1] = fa + 1; t.ox[2] = fb; t.ox[3] = fb + 1;
+  t.oy[0] = fc; t.oy[1] = fc + 1; t.oy[2] = fd; t.oy[3] = fd + 1;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { t.wx[k] = f[4 + k]; t.wy[k] = f[8 + k]; }
+  return t;
+}
+
+// Integer maps: corners are floored (the fractions are ignored), so the box is
+// the plain sum of Eq. 1 and only the four corner taps have weight.
+__device__ __forceinline__ Taps<int> int_taps(const Taps<float>& f) {
+  Taps<int> t;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { t.ox[k] = f.ox[k]; t.oy[k] = f.oy[k]; }
+  t.wx[0] = -1; t.wx[1] = 0; t.wx[2] = 1; t.wx[3] = 0;
+  t.wy[0] = -1; t.wy[1] = 0; t.wy[2] = 1; t.wy[3] = 0;
+  return t;
 }
 
 // Sum over the 16 lanes of each DPP row, in every lane of the row: pair,

@@ -68,10 +68,13 @@ def test_fwd_argument_errors():
     assert lib.box_conv_fwd(*a) == 4
     a = list(ok); a[10] = 1 << 7
     assert lib.box_conv_fwd(*a) == 7
-    # a map whose table does not fit LDS needs a workspace
-    a = list(ok); a[5] = 300; a[6] = 300
+    # every forward needs a workspace (the boxes' tap records), larger when a
+    # map's table does not fit LDS
+    assert lib.box_conv_fwd(*ok) == 5
+    a = list(ok); a[11] = FAKE; a[12] = 16
     assert lib.box_conv_fwd(*a) == 5
-    a[11] = FAKE; a[12] = 16
+    a = list(ok); a[5] = 300; a[6] = 300
+    a[11] = FAKE; a[12] = lib.bc_box_workspace_bytes(0, 2, 3, 8, 8, 4, 0)
     assert lib.box_conv_fwd(*a) == 5
     a = list(ok); a[10] = bc.BC_FLAG_FORCE_HBM
     assert lib.box_conv_fwd(*a) == 5
@@ -128,9 +131,11 @@ def test_sat_and_prep_argument_errors():
 
 def test_workspace_queries():
     lib = bc.load_library()
-    # 64x48 maps: tables fit LDS -> forward needs none; backward needs partials
-    assert lib.bc_box_workspace_bytes(0, 32, 256, 64, 48, 4, 0) == 0
-    assert lib.bc_box_workspace_bytes(1, 32, 256, 64, 48, 4, 0) >= 32 * 256 * 4 * 16
+    # 64x48 maps: tables fit LDS -> the forward needs the tap records only (2 per
+    # box, 64 bytes each); the backward also needs its gradient partials
+    taps = 2 * 256 * 4 * 64
+    assert lib.bc_box_workspace_bytes(0, 32, 256, 64, 48, 4, 0) == taps
+    assert lib.bc_box_workspace_bytes(1, 32, 256, 64, 48, 4, 0) >= taps + 32 * 256 * 4 * 16
     # forced HBM path and 256x256 maps need tables in the workspace
     big = lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, 0)
     assert big >= 4 * 128 * 257 * 257 * 4

@@ -67,11 +67,11 @@ def test_box_prep_bit_exact():
     bc.box_prep(dev(bx), table)
     torch.cuda.synchronize()
     t = table.cpu().numpy().reshape(2, C, B, 16)
-    for mirror in (0, 1):
-        fl, wx, wy = O.box_taps(bx, mirror=bool(mirror))
-        np.testing.assert_array_equal(t[mirror, ..., 0:4], fl)
-        np.testing.assert_array_equal(t[mirror, ..., 4:8].view(np.float32), wx)
-        np.testing.assert_array_equal(t[mirror, ..., 8:12].view(np.float32), wy)
+    for half, (fl, wx, wy) in enumerate([O.box_taps(bx), O.adjoint_taps(bx)]):
+        np.testing.assert_array_equal(t[half, ..., 0:4], fl)
+        np.testing.assert_array_equal(t[half, ..., 4:8].view(np.float32), wx)
+        np.testing.assert_array_equal(t[half, ..., 8:12].view(np.float32), wy)
+        np.testing.assert_array_equal(t[half, ..., 12:16], 0)
 
 
 # ---------------------------------------------------------------------------
@@ -236,6 +236,29 @@ def test_bwd(key, scale, flags):
     gx, gb = _bwd(d["x"], d["boxes"], g, flags)
     check(gx, O.box_backward_input(g, d["boxes"], wl.H, wl.W), RTOL_F32, "dx")
     check(gb, O.box_backward_params(d["x"], g, d["boxes"]), RTOL_F32, "dboxes")
+
+
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_bwd_integer_edges(flags):
+    """Boxes whose edges all sit on pixel boundaries: the parameter gradient
+    is one-sided there (right derivative), which the backward takes through
+    the adjoint split of the taps."""
+    rng = np.random.default_rng(107)
+    N, C, B, H, W = 2, 3, 4, 23, 19
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    g = rng.standard_normal((N, C * B, H, W)).astype(np.float32)
+    bx = np.empty((C, B, 4), dtype=np.float32)
+    for ax in range(2):
+        size = rng.integers(1, 9, size=(C, B))
+        lo = rng.integers(-10, 10, size=(C, B))
+        bx[..., ax] = lo + (size - 1) / 2.0
+        bx[..., 2 + ax] = size / 2.0
+    a, b, c, d = O.box_edges(bx)
+    assert np.all(a == np.floor(a)) and np.all(d == np.floor(d))
+    say(f"bwd integer edges flags={flags}")
+    gx, gb = _bwd(x, bx, g, flags)
+    check(gx, O.box_backward_input(g, bx, H, W), RTOL_F32, "dx")
+    check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
 
 
 def test_bwd_deterministic():
