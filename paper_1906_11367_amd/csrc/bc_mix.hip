@@ -281,10 +281,26 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[2][2], char* cbas
       }
 }
 
+// Occupancy target (waves per SIMD) of one GEMM variant.  The kernel is
+// bound by global-load latency (one K-step of each operand in flight per
+// block), so a third resident block per CU pays whenever the variant still
+// fits in 168 registers without spilling -- the accumulators then move from
+// AGPRs to VGPRs.  Variants that would spill (l-contiguous masked or fp32
+// operands in bf16 compute, the bf16 weight-gradient GEMM) keep two.
+template <bool BF16, int ADT, bool AKC, bool AMASK, int BDT, bool BKC, bool BMASK>
+constexpr int mix_waves() {
+  if (!BF16) return (AKC && AMASK) ? 2 : 3;
+  if (AMASK || BMASK) return 2;
+  if (AKC && !BKC) return (ADT == 2 && BDT == 2) ? 3 : 2;
+  if (!AKC && !BKC) return (ADT == 1 && BDT == 1) ? 2 : 3;
+  return 2;
+}
+
 // out-kind: 0 = store fp32 (relu optional), 1 = store int32 (exact integers),
 // 2 = store fp32 partial (BWD_WEIGHT split), 3 = fp32 with accumulate.
 template <bool BF16, int ADT, bool AKC, bool AMASK, int BDT, bool BKC, bool BMASK>
-__global__ __launch_bounds__(kMixThreads) void k_mix_gemm(
+__global__ __launch_bounds__(kMixThreads)
+__attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BMASK>(), 8))) void k_mix_gemm(
     const void* __restrict__ a, const void* __restrict__ b, const float* __restrict__ aux, void* __restrict__ out,
     int rows, int cols, int depth, long lda, long ldb, long ldc, long a_bs, long b_bs, long c_bs,
     int mt, int nt, int zt, int nsplit_p, int pchunk, int out_kind, int relu) {
