@@ -60,6 +60,43 @@ __device__ __forceinline__ void ld_run(const char* base, size_t idx, bool vec, i
   }
 }
 
+// Buffer-resource loads: a wave-uniform descriptor of one operand (base and
+// byte size, so that the hardware returns zeros past its end), a per-thread
+// byte offset and a wave-uniform byte offset.
+constexpr int kBufWord3 = 0x00020000;  // raw 32-bit data, no format conversion
+
+__device__ __forceinline__ uint4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const auto q = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(q[0], q[1], q[2], q[3]);
+}
+__device__ __forceinline__ uint2 buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const auto q = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+  return make_uint2(q[0], q[1]);
+}
+
+// N consecutive elements through a buffer descriptor, as raw bits (one word
+// per element; bf16 in the low half).
+template <int DT, int N>
+__device__ __forceinline__ void buf_run(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint32_t* w) {
+  if constexpr (DT == 2) {
+    if constexpr (N == 8) {
+      const uint4 q = buf_ld16(r, voff, soff);
+      const uint32_t p[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) { w[2 * k] = p[k] & 0xffffu; w[2 * k + 1] = p[k] >> 16; }
+    } else {
+      const uint2 q = buf_ld8(r, voff, soff);
+      w[0] = q.x & 0xffffu; w[1] = q.x >> 16; w[2] = q.y & 0xffffu; w[3] = q.y >> 16;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < N; k += 4) {
+      const uint4 q = buf_ld16(r, voff, soff + k * 4);
+      w[k] = q.x; w[k + 1] = q.y; w[k + 2] = q.z; w[k + 3] = q.w;
+    }
+  }
+}
+
 // Storage bits -> fp32 value.
 template <int DT>
 __device__ __forceinline__ float bits_to_f32(uint32_t b) {
@@ -117,20 +154,80 @@ struct Stager {
   static constexpr int NW = kRaw ? (KC ? NU * UL / 2 : UL * 2) : (KC ? NU * UL : 4 * UL);
   using E = typename std::conditional<BF16, uint16_t, float>::type;
 
+  // Byte offset of this thread's first load inside a tile (the same for every
+  // K-step); its other loads sit a wave-uniform step further each: KC units
+  // are kMixThreads / (BK / UL) rows apart, non-KC rows one l apart.
+  static constexpr int SB = DT == 2 ? 2 : 4;
+
   const char* p;
   const float* mask;
   long ld;
   int rows, depth;
   bool vec_ok;
+  uint32_t off0;
+  __amdgpu_buffer_rsrc_t rs, mrs;
   uint32_t v[NW];
   uint32_t m[MASK ? NW : 1];
 
+  // Offsets, and buffer descriptors covering this image's operand (and mask).
+  __device__ __forceinline__ void init_offsets() {
+    const int tid = threadIdx.x;
+    if constexpr (KC) off0 = (uint32_t)(((long)(tid / (BK / UL)) * ld + (tid % (BK / UL)) * UL) * SB);
+    else off0 = (uint32_t)(((long)((tid / (kBM / 4)) * UL) * ld + (tid % (kBM / 4)) * 4) * SB);
+    const long extent = KC ? (long)(rows - 1) * ld + depth : (long)(depth - 1) * ld + rows;  // elements
+    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(p), (short)0, (int)(extent * SB), kBufWord3);
+    if constexpr (MASK)
+      mrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(mask), (short)0, (int)(extent * 4), kBufWord3);
+  }
+  __device__ __forceinline__ long unit_step() const {
+    return KC ? (long)(kMixThreads / (BK / UL)) * ld * SB : ld * SB;
+  }
+  // Whether an image's operand fits the 32-bit byte offsets of the buffer path.
+  __device__ __forceinline__ bool buf_ok() const {
+    const long extent = KC ? (long)(rows - 1) * ld + depth : (long)(depth - 1) * ld + rows;
+    return extent * 4 < (1L << 31);
+  }
+
   // Whole tile in range and aligned: the block takes the unguarded path
   // (the condition is uniform, so no lane diverges and the wide loads stay in
-  // flight until store() consumes them).
+  // flight until store() consumes them).  The unguarded path reads through
+  // the buffer descriptor: the thread's one offset plus a wave-uniform offset
+  // per K-step and unit, so no address is computed in the loop.
   __device__ __forceinline__ void load(int r0, int l0) {
-    if (vec_ok && r0 + kBM <= rows && l0 + BK <= depth) load_tile<true>(r0, l0);
+    if (vec_ok && r0 + kBM <= rows && l0 + BK <= depth) load_full(r0, l0);
     else load_tile<false>(r0, l0);
+  }
+
+  __device__ __forceinline__ void load_full(int r0, int l0) {
+    const uint32_t origin = (uint32_t)(KC ? (long)r0 * ld + l0 : (long)l0 * ld + r0);
+    const uint32_t step = (uint32_t)unit_step();
+    const uint32_t moff = off0 / SB * 4;
+    if constexpr (KC) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const uint32_t so = origin * SB + u * step;
+        if constexpr (kRaw) {
+          const uint4 q = buf_ld16(rs, off0, so);
+          uint32_t* w = v + u * (UL / 2);
+          w[0] = q.x; w[1] = q.y; w[2] = q.z; w[3] = q.w;
+        } else {
+          buf_run<DT, UL>(rs, off0, so, v + u * UL);
+          if constexpr (MASK) buf_run<1, UL>(mrs, moff, origin * 4 + u * (step / SB * 4), m + u * UL);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < UL; ++e) {
+        const uint32_t so = origin * SB + e * step;
+        if constexpr (kRaw) {
+          const uint2 q = buf_ld8(rs, off0, so);
+          v[e * 2] = q.x; v[e * 2 + 1] = q.y;
+        } else {
+          buf_run<DT, 4>(rs, off0, so, v + e * 4);
+          if constexpr (MASK) buf_run<1, 4>(mrs, moff, origin * 4 + e * (step / SB * 4), m + e * 4);
+        }
+      }
+    }
   }
 
   template <bool kFull>
@@ -337,6 +434,10 @@ __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BM
   sb.mask = BMASK ? aux + (size_t)n * b_bs : nullptr;
   sb.ld = ldb; sb.rows = cols; sb.depth = depth;
   sb.vec_ok = (ldb & 7) == 0 && ((uintptr_t)sb.p & 15) == 0 && (!BMASK || ((uintptr_t)sb.mask & 15) == 0);
+  sa.init_offsets();
+  sb.init_offsets();
+  sa.vec_ok = sa.vec_ok && sa.buf_ok();
+  sb.vec_ok = sb.vec_ok && sb.buf_ok();
 
   const int i0 = tm * kBM, j0 = tn * kBN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
