@@ -102,9 +102,16 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
   const int tid = threadIdx.x, nt = blockDim.x;
   T* R = S + kPad;
   table_zero_edges(S, H, pitch);
+  // Slot k of this thread is element (vector) tid + k * nt; its row and
+  // column advance by the same (nt / width, nt % width) every slot, so only
+  // the first position takes a division.
   const int n = H * W;
   if ((W & 3) == 0 && ((uintptr_t)src & 15) == 0) {
-    const int n4 = n >> 2;
+    const int n4 = n >> 2, W4 = W >> 2;
+    const int di = nt / W4, dj = nt - di * W4;
+    int j = tid % W4;
+    int o = (tid / W4 + 1) * pitch + 4 * j + 1;  // table offset of the slot's first element
+    const int step = di * pitch + 4 * dj, wrap = pitch - W;
     const V* s4 = reinterpret_cast<const V*>(src);
     for (int base = 0; base < n4; base += nt * kBatch) {
       V q[kBatch];
@@ -112,21 +119,25 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
       for (int b = 0; b < kBatch; ++b) q[b] = s4[min(base + b * nt + tid, n4 - 1)];
 #pragma unroll
       for (int b = 0; b < kBatch; ++b) {
-        const int k = base + b * nt + tid;
-        if (k < n4) {
-          const int e = k << 2, i = e / W, j = e - i * W;
-          T* d = R + (i + 1) * pitch + j + 1;
+        if (tid < n4 - base - b * nt) {
           const T w4[4] = {(T)q[b].x, (T)q[b].y, (T)q[b].z, (T)q[b].w};
 #pragma unroll
-          for (int t = 0; t < 4; ++t) d[t] = sub ? (T)((float)w4[t] - mu) : w4[t];
+          for (int t = 0; t < 4; ++t) R[o + t] = sub ? (T)((float)w4[t] - mu) : w4[t];
         }
+        o += step;
+        j += dj;
+        if (j >= W4) { j -= W4; o += wrap; }
       }
     }
   } else {
+    const int di = nt / W, dj = nt - di * W;
+    int i = tid / W, j = tid - i * W;
     for (int k = tid; k < n; k += nt) {
-      const int i = k / W, j = k - i * W;
       const T v = src[k];
       R[(i + 1) * pitch + j + 1] = sub ? (T)((float)v - mu) : v;
+      i += di;
+      j += dj;
+      if (j >= W) { j -= W; ++i; }
     }
   }
   __syncthreads();
@@ -602,20 +613,39 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
 // edge gradients, then the change of variables a = 1/2+cx-rx, b = 1/2+cx+rx,
 // c = 1/2+cy-ry, d = 1/2+cy+ry:  dcx = ga+gb, dcy = gc+gd, drx = gb-ga,
 // dry = gd-gc.
-__global__ void k_box_grad_reduce(const float* __restrict__ partials, int P, int CB, float* __restrict__ out) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= CB) return;
-  float s[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int p = 0; p < P; ++p) {
-    const float* pp = partials + ((size_t)p * CB + i) * 4;
+// One block per 16 boxes: thread (q, j) sums rows p = q, q + 16, ... of box
+// j (a wave's load covers 4 rows x 16 consecutive boxes, 256 contiguous
+// bytes each), then the 16 row-sums of each box combine in a fixed tree
+// (lane shuffles across the wave's 4 row groups, then the 4 waves in LDS).
+constexpr int kReduceBoxes = 16;
+__global__ __launch_bounds__(256) void k_box_grad_reduce(const float* __restrict__ partials, int P, int CB,
+                                                         float* __restrict__ out) {
+  __shared__ float4 red[4][kReduceBoxes];
+  const int j = threadIdx.x % kReduceBoxes, q = threadIdx.x / kReduceBoxes;
+  const int i = blockIdx.x * kReduceBoxes + j;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < CB)
+    for (int p = q; p < P; p += 256 / kReduceBoxes) {
+      const float4 v = *reinterpret_cast<const float4*>(partials + ((size_t)p * CB + i) * 4);
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] += pp[k];
+  for (int m = 16; m < 64; m <<= 1) {
+    s.x += __shfl_xor(s.x, m); s.y += __shfl_xor(s.y, m);
+    s.z += __shfl_xor(s.z, m); s.w += __shfl_xor(s.w, m);
   }
-  float* o = out + (size_t)i * 4;
-  o[0] = s[0] + s[1];
-  o[1] = s[2] + s[3];
-  o[2] = s[1] - s[0];
-  o[3] = s[3] - s[2];
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) < kReduceBoxes) red[wave][j] = s;
+  __syncthreads();
+  if (threadIdx.x < kReduceBoxes && i < CB) {
+    float4 t = red[0][j];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float4 u = red[w][j];
+      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
+    }
+    *reinterpret_cast<float4*>(out + (size_t)i * 4) = make_float4(t.x + t.y, t.z + t.w, t.y - t.x, t.w - t.z);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -750,7 +780,8 @@ hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* 
 }
 
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes, hipStream_t s) {
-  hipLaunchKernelGGL(k_box_grad_reduce, dim3((CB + 255) / 256), dim3(256), 0, s, partials, P, CB, grad_boxes);
+  hipLaunchKernelGGL(k_box_grad_reduce, dim3((CB + kReduceBoxes - 1) / kReduceBoxes), dim3(256), 0, s, partials, P, CB,
+                     grad_boxes);
   return last_error();
 }
 
