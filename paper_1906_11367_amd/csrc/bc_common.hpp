@@ -184,8 +184,10 @@ __device__ __forceinline__ void table_row(const Src& S, int coord, const typenam
     U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
 }
 
-// Same row, also returning the column differences at the two x edges
-// (the table differences across each edge column).
+// Same row for adjoint taps, also returning the column differences at the
+// two x edges (the table differences across each edge column).  Adjoint x
+// weights are (alpha - 1, -alpha) and (1 - beta, beta), so the interpolated
+// row is (sb - sa) - alpha * DA + beta * DB.
 template <typename Src>
 __device__ __forceinline__ void table_row_grad(const Src& S, int coord, const typename Src::Cols& c,
                                                const Taps<float>& tp, float* U, float* DA, float* DB) {
@@ -193,9 +195,9 @@ __device__ __forceinline__ void table_row_grad(const Src& S, int coord, const ty
   S.runs(coord, c, sa, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
-    U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
     DA[q] = sa[q + 1] - sa[q];
     DB[q] = sb[q + 1] - sb[q];
+    U[q] = fmaf(tp.wx[3], DB[q], fmaf(tp.wx[1], DA[q], sb[q] - sa[q]));
   }
 }
 
