@@ -73,6 +73,14 @@ typedef enum {
                                     large tables. */
 #define BC_FLAG_FORCE_HBM 2u     /* use the HBM-table path even when a map's table
                                     fits in LDS (both paths compute the same). */
+#define BC_FLAG_INTEGER_CORNERS 4u  /* inference form of the Conclusions: each box
+                                    edge (a, b, c, d, in fp64) is rounded to the
+                                    nearest integer, ties up (floor(e + 1/2)),
+                                    and each corner is one table sample: four
+                                    samples per box instead of sixteen, no
+                                    interpolation.  The boxes are then frozen
+                                    (rounding is not differentiable):
+                                    box_conv_bwd computes grad_x only. */
 
 /* ------------------------------------------------------------------------
  * box_prep -- the per-box precomputation of Section 3.1 (after Eq. 4): since
@@ -80,6 +88,10 @@ typedef enum {
  * once to integer tap offsets and bilinear weights.
  *
  * boxes : device fp32 [C][B][4] (cx, cy, rx, ry).
+ * flags : 0, or BC_FLAG_INTEGER_CORNERS: the records of the boxes with
+ *         rounded corners (floors = the rounded edges, and for the adjoint
+ *         1 - b, 1 - a, 1 - d, 1 - c of them; weights -1, 0, 1, 0).  Other
+ *         flags: BC_ERR_UNSUPPORTED.
  * table : device, 2*C*B records of 16 32-bit words.  Record r < C*B is box r
  *         (r = c*B + b); record C*B + r is its adjoint: the mirrored box
  *         (centre offset negated), whose correlation is the transpose of box
@@ -99,7 +111,7 @@ typedef enum {
  *         weight.  box_conv_fwd and box_conv_bwd run this first, into their
  *         workspace, and read their taps from it.
  * ---------------------------------------------------------------------- */
-bc_status box_prep(const float* boxes, int C, int B, void* table, hipStream_t stream);
+bc_status box_prep(const float* boxes, int C, int B, unsigned flags, void* table, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * sat_build -- the summed-area table (Section 3.1, before Eq. 2), exclusive
@@ -128,7 +140,9 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
  *          BC_F32 or BC_BF16 (the fp32 result rounded to nearest even).
  * BC_I32 : corners are floored (fractions ignored) and the sum is exact int32
  *          arithmetic -- callers pass integer corners (half-integer cx - rx).
- * flags  : BC_FLAG_MEAN_OFFSET (BC_F32), BC_FLAG_FORCE_HBM.
+ * flags  : BC_FLAG_MEAN_OFFSET (BC_F32), BC_FLAG_FORCE_HBM,
+ *          BC_FLAG_INTEGER_CORNERS (the box with rounded corners: the
+ *          four-sample sum of Eq. 2, exact int32 for BC_I32 maps).
  * ws     : >= bc_box_workspace_bytes(0, ...) bytes: the tap records of
  *          box_prep (2*C*B*64 bytes), plus the maps' tables when a table does
  *          not fit in LDS or BC_FLAG_FORCE_HBM is set.
@@ -150,6 +164,9 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
  *     of grad_y>: the edge derivatives of the adjoint sums are differences of
  *     the taps already read for grad_x, weighted by x.  Only the gradient maps
  *     are tabulated, so BC_FLAG_MEAN_OFFSET has no effect here.
+ *   With BC_FLAG_INTEGER_CORNERS: grad_x of the boxes with rounded corners
+ *     (the adjoint four-sample sums); grad_boxes must be NULL
+ *     (BC_ERR_UNSUPPORTED otherwise) and x is not read.
  *
  * x          : device fp32 [N][C][H][W]     (the forward input)
  * grad_y     : device fp32 [N][C*B][H][W]

@@ -44,13 +44,19 @@ R6  No area normalisation and no bias (Eq. 1 is a plain sum).
 R7  Output channel of box b on input channel c is c*B + b.
 R8  A bf16 1x1 mix rounds both operands to bf16 (round to nearest even) and
     accumulates exactly; the oracle accumulates in fp64.
+R12 Integer corners for inference (Conclusions: once the boxes have
+    converged, round the sampling points to integers so that no interpolation
+    is needed): each edge a, b, c, d is rounded to the nearest integer, a tie
+    (an edge exactly halfway between two integers) rounding up:
+    floor(e + 1/2).  The boxes are then fixed; only the input gradient is
+    defined.
 """
 from __future__ import annotations
 
 import numpy as np
 
 __all__ = [
-    "box_edges", "mirrored_boxes", "box_taps", "adjoint_taps", "overlap_matrix", "sat_exclusive",
+    "box_edges", "rounded_edges", "mirrored_boxes", "box_taps", "adjoint_taps", "overlap_matrix", "sat_exclusive",
     "map_mean", "box_forward", "box_backward_input", "box_backward_params",
     "box_param_grad_from_edges", "bf16_round", "mix_forward",
     "mix_backward_data", "mix_backward_weight", "relu", "layer_forward",
@@ -72,6 +78,13 @@ def box_edges(boxes):
     p = np.asarray(boxes, dtype=np.float32).astype(np.float64)
     cx, cy, rx, ry = p[..., 0], p[..., 1], p[..., 2], p[..., 3]
     return 0.5 + cx - rx, 0.5 + cx + rx, 0.5 + cy - ry, 0.5 + cy + ry
+
+
+def rounded_edges(boxes):
+    """Edges (a, b, c, d) of the boxes with their corners rounded to integers
+    (reading R12): each fp64 edge e becomes floor(e + 1/2), so a tie rounds
+    up.  Returns four fp64 arrays holding integers."""
+    return tuple(np.floor(e + 0.5) for e in box_edges(boxes))
 
 
 def mirrored_boxes(boxes):
@@ -176,18 +189,20 @@ def _is_int(x):
     return np.issubdtype(np.asarray(x).dtype, np.integer)
 
 
-def box_forward(x, boxes):
+def box_forward(x, boxes, integer_corners=False):
     """O[n, c*B+b] = integral of zero-padded x[n, c] over each box (fp64/int64).
 
     x: [N, C, H, W]; boxes: [C, B, 4] fp32 (cx, cy, rx, ry).
     Computed as O = Wy @ I @ Wx^T with the overlap matrices of each box.  For
     integer x the boxes must have integer corners (then every weight is 0 or
-    1) and the result is exact int64.
+    1) and the result is exact int64.  integer_corners: the boxes with their
+    corners rounded (reading R12) -- the plain sum of Eq. 1 over the rounded
+    box, for any map type.
     """
     x = np.asarray(x)
     N, C, H, W = x.shape
     B = boxes.shape[1]
-    a, b, c, d = box_edges(boxes)
+    a, b, c, d = rounded_edges(boxes) if integer_corners else box_edges(boxes)
     integer = _is_int(x)
     dt = np.int64 if integer else np.float64
     xf = x.astype(dt)
@@ -205,18 +220,19 @@ def box_forward(x, boxes):
     return out.reshape(N, C * B, H, W)
 
 
-def box_backward_input(grad_y, boxes, H, W):
+def box_backward_input(grad_y, boxes, H, W, integer_corners=False):
     """dI[n, c] = sum_b Wy^T @ dO[n, c*B+b] @ Wx  (transpose of box_forward).
 
     grad_y: [N, C*B, H, W]; returns fp64 [N, C, H, W].  The paper states only
     the local derivative of a table sample (its bilinear weight, the text after
-    Eq. 4); this is the chain rule of the whole forward map.
+    Eq. 4); this is the chain rule of the whole forward map.  integer_corners:
+    the transpose of box_forward(..., integer_corners=True).
     """
     g = np.asarray(grad_y, dtype=np.float64)
     C, B = boxes.shape[0], boxes.shape[1]
     N = g.shape[0]
     g = g.reshape(N, C, B, H, W)
-    a, b, c, d = box_edges(boxes)
+    a, b, c, d = rounded_edges(boxes) if integer_corners else box_edges(boxes)
     out = np.zeros((N, C, H, W), dtype=np.float64)
     for ci in range(C):
         for bi in range(B):

@@ -20,14 +20,14 @@ LIB_PATH = os.path.join(_HERE, "libboxconv.so")
 
 BC_I32, BC_F32, BC_BF16 = 0, 1, 2
 BC_MIX_FWD, BC_MIX_BWD_DATA, BC_MIX_BWD_WEIGHT = 0, 1, 2
-BC_FLAG_MEAN_OFFSET, BC_FLAG_FORCE_HBM = 1, 2
+BC_FLAG_MEAN_OFFSET, BC_FLAG_FORCE_HBM, BC_FLAG_INTEGER_CORNERS = 1, 2, 4
 STATUS = {0: "BC_OK", 1: "BC_ERR_NULL", 2: "BC_ERR_SHAPE", 3: "BC_ERR_DTYPE", 4: "BC_ERR_ALIGN",
           5: "BC_ERR_WORKSPACE", 6: "BC_ERR_HIP", 7: "BC_ERR_UNSUPPORTED"}
 
 # Exported symbols and their C signatures (kept in step with boxconv.h).
 _vp, _i, _u, _sz, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint, ctypes.c_size_t, ctypes.c_float
 SIGNATURES = {
-    "box_prep": (_i, [_vp, _i, _i, _vp, _vp]),
+    "box_prep": (_i, [_vp, _i, _i, _u, _vp, _vp]),
     "sat_build": (_i, [_vp, _i, _vp, _vp, _i, _i, _i, _i, _vp]),
     "box_conv_fwd": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
     "box_conv_bwd": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
@@ -107,10 +107,10 @@ def mix_workspace_bytes(mode: int, N, M, K, P, compute_dt) -> int:
     return int(load_library().bc_mix_workspace_bytes(mode, N, M, K, P, compute_dt))
 
 
-def box_prep(boxes: torch.Tensor, table: torch.Tensor):
+def box_prep(boxes: torch.Tensor, table: torch.Tensor, flags: int = 0):
     """table: int32 tensor of 2*C*B*16 words (see boxconv.h)."""
     C, B = boxes.shape[0], boxes.shape[1]
-    _check(load_library().box_prep(_ptr(boxes), C, B, _ptr(table), _stream()), "box_prep")
+    _check(load_library().box_prep(_ptr(boxes), C, B, flags, _ptr(table), _stream()), "box_prep")
     return table
 
 

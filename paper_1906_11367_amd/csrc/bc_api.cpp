@@ -73,7 +73,7 @@ bc_status hip_status(hipError_t e) { return e == hipSuccess ? BC_OK : BC_ERR_HIP
 
 extern "C" {
 
-int bc_abi_version(void) { return 1; }
+int bc_abi_version(void) { return 2; }
 
 const char* bc_status_string(bc_status s) {
   switch (s) {
@@ -89,11 +89,12 @@ const char* bc_status_string(bc_status s) {
   return "unknown status";
 }
 
-bc_status box_prep(const float* boxes, int C, int B, void* table, hipStream_t stream) {
+bc_status box_prep(const float* boxes, int C, int B, unsigned flags, void* table, hipStream_t stream) {
   if (!boxes || !table) return BC_ERR_NULL;
   if (C <= 0 || B <= 0 || (long)C * B > (1L << 28)) return BC_ERR_SHAPE;
+  if (flags & ~BC_FLAG_INTEGER_CORNERS) return BC_ERR_UNSUPPORTED;
   if (!aligned16(boxes) || !aligned16(table)) return BC_ERR_ALIGN;
-  return hip_status(bc::launch_box_prep(boxes, C, B, table, stream));
+  return hip_status(bc::launch_box_prep(boxes, C, B, (flags & BC_FLAG_INTEGER_CORNERS) != 0, table, stream));
 }
 
 bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean, int N, int C, int H, int W,
@@ -123,8 +124,9 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, 
                        void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!x || !boxes || !y) return BC_ERR_NULL;
   if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
-  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM)) return BC_ERR_UNSUPPORTED;
+  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM | BC_FLAG_INTEGER_CORNERS)) return BC_ERR_UNSUPPORTED;
   const bool is_int = x_dt == BC_I32;
+  const bool rounded = (flags & BC_FLAG_INTEGER_CORNERS) != 0;
   if (x_dt != BC_I32 && x_dt != BC_F32) return BC_ERR_DTYPE;
   if (is_int ? (y_dt != BC_I32) : (y_dt != BC_F32 && y_dt != BC_BF16)) return BC_ERR_DTYPE;
   if (is_int && (flags & BC_FLAG_MEAN_OFFSET)) return BC_ERR_DTYPE;
@@ -139,14 +141,16 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, 
   if (!aligned16(ws)) return BC_ERR_ALIGN;
   char* base = static_cast<char*>(ws);
   const int* taps = reinterpret_cast<const int*>(base + L.taps);
-  hipError_t e = bc::launch_box_prep(boxes, C, B, base + L.taps, stream);
+  hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  if (!hbm) return hip_status(bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, stream));
+  if (!hbm)
+    return hip_status(
+        bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, rounded, stream));
   float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
   e = bc::launch_sat_build(x, is_int, base + L.sat, means, N * C, H, W, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
   return hip_status(
-      bc::launch_box_fwd_gather(base + L.sat, is_int, means, taps, y, out_kind, N, C, H, W, B, stream));
+      bc::launch_box_fwd_gather(base + L.sat, is_int, means, taps, y, out_kind, N, C, H, W, B, rounded, stream));
 }
 
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,
@@ -154,7 +158,11 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
                        hipStream_t stream) {
   if (!x || !boxes || !grad_y) return BC_ERR_NULL;
   if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
-  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM)) return BC_ERR_UNSUPPORTED;
+  if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM | BC_FLAG_INTEGER_CORNERS)) return BC_ERR_UNSUPPORTED;
+  const bool rounded = (flags & BC_FLAG_INTEGER_CORNERS) != 0;
+  // rounding the corners is not differentiable: with rounded corners the
+  // boxes are frozen and only the input gradient is defined
+  if (rounded && grad_boxes) return BC_ERR_UNSUPPORTED;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(grad_y) || (grad_x && !aligned16(grad_x)) ||
       (grad_boxes && !aligned16(grad_boxes)))
     return BC_ERR_ALIGN;
@@ -170,14 +178,15 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   char* base = static_cast<char*>(ws);
   float* partials = reinterpret_cast<float*>(base + L.partials);
   const int* taps = reinterpret_cast<const int*>(base + L.taps);
-  hipError_t e = bc::launch_box_prep(boxes, C, B, base + L.taps, stream);
+  hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
   if (!hbm) {
-    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, stream);
+    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, stream);
   } else {
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
     e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
-    if (e == hipSuccess) e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, stream);
+    if (e == hipSuccess)
+      e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, rounded, stream);
   }
   if (e != hipSuccess) return BC_ERR_HIP;
   if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);

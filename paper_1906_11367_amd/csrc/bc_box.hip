@@ -3,6 +3,8 @@
 #include "bc_common.hpp"
 #include "bc_internal.hpp"
 
+#include <type_traits>
+
 namespace bc {
 
 // ---------------------------------------------------------------------------
@@ -219,6 +221,65 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
   }
 }
 
+// Walk for boxes with integer corners (make_taps_rounded records): each
+// output is Eq. 2's four-corner difference with no interpolation, so per
+// output row the walk reads one table row per y edge, each a run of kQ
+// columns at both x edges:  o = (S(y+d, x+b) - S(y+d, x+a)) - (S(y+c, x+b) -
+// S(y+c, x+a)).  emit.put<kFull>(s, o) for s in [0, SEG) with y0 + s < y1.
+// With kOffset the table holds the map minus mu, and mu * (clipped area) is
+// added back.
+template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
+__device__ __forceinline__ void box_walk_int(const Src& S, const Taps<T>& tp, int H, int W, int x0, int y0,
+                                             int y1, float mu, Emit& emit) {
+  const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
+  const typename Src::Cols cl = S.cols(ba, bb);
+  const int st = S.row_step();
+  const int rc = S.row_coord(y0 + tp.oy[0]), rd = S.row_coord(y0 + tp.oy[2]);
+  float ex[kQ];
+  if (kOffset) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) ex[q] = (float)(clampi(bb + q, 0, W) - clampi(ba + q, 0, W));
+  }
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    const int y = y0 + s;
+    if (kFull || y < y1) {
+      T ca[kQ], cb[kQ], da[kQ], db[kQ];
+      S.template runs<kQ>(rc + s * st, cl, ca, cb);
+      S.template runs<kQ>(rd + s * st, cl, da, db);
+      T o[kQ];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) o[q] = (db[q] - da[q]) - (cb[q] - ca[q]);
+      if (kOffset) {
+        const float ey = (float)(clampi(y + tp.oy[2], 0, H) - clampi(y + tp.oy[0], 0, H));
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
+      }
+      emit.template put<kFull>(s, o);
+    }
+  }
+}
+
+// Forward walk of one item: integer-corner or interpolated.
+template <int SEG, typename T, bool kOffset, bool kFull, bool kInt, typename Src, typename Emit>
+__device__ __forceinline__ void walk_fwd(const Src& S, const Taps<T>& tp, int H, int W, int x0, int y0, int y1,
+                                         float mu, Emit& emit) {
+  if constexpr (kInt) box_walk_int<SEG, T, kOffset, kFull>(S, tp, H, W, x0, y0, y1, mu, emit);
+  else box_walk<SEG, T, kOffset, kFull>(S, tp, H, W, x0, y0, y1, mu, emit);
+}
+
+// Emitter that adds an item's outputs to its register accumulator (the
+// input gradient, summed over boxes).
+template <int SEG>
+struct AccRows {
+  float (&acc)[SEG][kQ];
+  template <bool kFull>
+  __device__ __forceinline__ void put(int s, const float* o) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] += o[q];
+  }
+};
+
 // Backward walk over one item on the table of one upstream-gradient map G,
 // with the adjoint taps of the box.  For each input pixel (y, x) =
 // (y0 + s, x0 + q):
@@ -320,13 +381,16 @@ struct StoreRows {
 // Kernels
 // ---------------------------------------------------------------------------
 // Tap records (16 words each): record r < CB is box r's forward taps, record
-// CB + r its adjoint taps (make_taps_adjoint).
-__global__ void k_box_prep(const float* __restrict__ boxes, int CB, int* __restrict__ table) {
+// CB + r its adjoint taps (make_taps_adjoint); with `rounded`, the taps of
+// the boxes with rounded (integer) corners and of their adjoints.
+__global__ void k_box_prep(const float* __restrict__ boxes, int CB, int rounded, int* __restrict__ table) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= 2 * CB) return;
   const bool adj = i >= CB;
   const float* p = boxes + (size_t)(adj ? i - CB : i) * 4;
-  const Taps<float> t = adj ? make_taps_adjoint(p, 1 << 20, 1 << 20) : make_taps_f32(p, false, 1 << 20, 1 << 20);
+  const Taps<float> t = rounded ? make_taps_rounded(p, adj, 1 << 20, 1 << 20)
+                        : adj   ? make_taps_adjoint(p, 1 << 20, 1 << 20)
+                                : make_taps_f32(p, false, 1 << 20, 1 << 20);
   int* r = table + (size_t)i * 16;
   float* f = reinterpret_cast<float*>(r);
   r[0] = t.ox[0]; r[1] = t.ox[2]; r[2] = t.oy[0]; r[3] = t.oy[2];
@@ -413,7 +477,7 @@ template <> __device__ __forceinline__ Taps<int> typed_taps<int>(const Taps<floa
 // adjacent lanes write adjacent columns; each box's items are padded to a
 // multiple of 64 (per_box_p) so that a wave works on one box and reads its
 // taps through scalar loads.
-template <typename T, typename OutT, int SEG, bool kOffset>
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
 __device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __restrict__ taps,
                                           OutT* __restrict__ y, int map, int c, int b0, int nb, int H, int W,
                                           int B, int per_box_p, float mu) {
@@ -428,14 +492,14 @@ __device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __r
     OutT* out = y + ((size_t)map * B + b) * H * W;
     const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
     StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
-    if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
-    else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
+    if (y0 + SEG <= H && x0 + kQ <= W) walk_fwd<SEG, T, kOffset, true, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
+    else walk_fwd<SEG, T, kOffset, false, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
   }
 }
 
 // Forward, table in LDS: one block per (map, group of bpg boxes).  The block
 // builds the map's table once and evaluates every box of its group.
-template <typename T, typename OutT, int SEG, bool kOffset>
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
 __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const int* __restrict__ taps,
                                                      OutT* __restrict__ y, int C, int H, int W, int B, int bpg,
                                                      int per_box_p) {
@@ -450,13 +514,13 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
   if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
   build_table_lds(src, S, H, W, pitch, mu, kOffset);
   const int b0 = grp * bpg;
-  fwd_boxes<T, OutT, SEG, kOffset>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0, min(bpg, B - b0), H,
+  fwd_boxes<T, OutT, SEG, kOffset, kInt>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0, min(bpg, B - b0), H,
                                    W, B, per_box_p, mu);
 }
 
 // Forward, table in HBM: one block per (map, box, block of 256 items), mapped
 // so that one map's blocks run on one XCD.
-template <typename T, typename OutT, int SEG, bool kOffset>
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
 __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sat, const float* __restrict__ means,
                                                         const int* __restrict__ taps, OutT* __restrict__ y,
                                                         int C, int H, int W, int B, int nblk, int total) {
@@ -474,8 +538,8 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   OutT* out = y + ((size_t)map * B + b) * H * W;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
   StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
-  if (y0 + SEG <= H && x0 + kQ <= W) box_walk<SEG, T, kOffset, true>(tab, tp, H, W, x0, y0, y1, mu, em);
-  else box_walk<SEG, T, kOffset, false>(tab, tp, H, W, x0, y0, y1, mu, em);
+  if (y0 + SEG <= H && x0 + kQ <= W) walk_fwd<SEG, T, kOffset, true, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
+  else walk_fwd<SEG, T, kOffset, false, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
 
 // Map values of one item, 0 outside the map (they then add nothing to the
@@ -521,8 +585,9 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // b the table of grad_y[n][c*B+b] is built in LDS and the adjoint walk adds
 // the input gradient (in registers, summed over b) and the edge gradients;
 // each wave writes its edge-gradient sums to
-// partials[(n * nw + wave) * C*B + c*B + b][4].
-template <int SEG>
+// partials[(n * nw + wave) * C*B + c*B + b][4].  kInt (boxes with integer
+// corners): the adjoint four-corner sums only, no edge gradients.
+template <int SEG, bool kInt>
 __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
                                                      const float* __restrict__ gy, float* __restrict__ gx,
                                                      float* __restrict__ partials, int C, int H, int W, int B) {
@@ -540,7 +605,7 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
   const size_t plane = (size_t)H * W;
   const float* g0 = gy + (size_t)map * B * plane;
   float v[SEG][kQ], acc[SEG][kQ];
-  load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
+  if constexpr (!kInt) load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
@@ -551,6 +616,14 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
     __syncthreads();
     build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
     const Taps<float> tp = load_taps(adj + (size_t)(c * B + b) * 16, W, H);
+    if constexpr (kInt) {  // integer corners: input gradient only
+      AccRows<SEG> em{acc};
+      if (active) {
+        if (full) box_walk_int<SEG, float, false, true>(tg, tp, H, W, x0, y0, y1, 0.f, em);
+        else box_walk_int<SEG, float, false, false>(tg, tp, H, W, x0, y0, y1, 0.f, em);
+      }
+      continue;
+    }
     float P[12];
 #pragma unroll
     for (int k = 0; k < 12; ++k) P[k] = 0.f;
@@ -567,9 +640,10 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
 
 // Backward, tables in HBM (one table per gradient map, built beforehand).
 // One 256-thread block per (map, block of 256 items); loops over boxes.
-// partials: [((n * nblk + blk) * 4 + wave) * C*B + c*B + b][4].
-template <int SEG>
-__global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict__ x, const float* __restrict__ sat_g,
+// partials: [((n * nblk + blk) * 4 + wave) * C*B + c*B + b][4]; kInt as in
+// k_box_bwd_lds.
+template <int SEG, bool kInt>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_box_bwd_gather(const float* __restrict__ x, const float* __restrict__ sat_g,
                                                         const int* __restrict__ taps, float* __restrict__ gx,
                                                         float* __restrict__ partials, int C, int H, int W, int B,
                                                         int nblk, int total) {
@@ -586,7 +660,7 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
   const bool full = y0 + SEG <= H && x0 + kQ <= W;
   const size_t tsz = (size_t)(H + 1) * (W + 1);
   float v[SEG][kQ], acc[SEG][kQ];
-  load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
+  if constexpr (!kInt) load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
@@ -595,6 +669,14 @@ __global__ __launch_bounds__(256) void k_box_bwd_gather(const float* __restrict_
   for (int b = 0; b < B; ++b) {
     const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1, W, H};
     const Taps<float> tp = load_taps(adj + (size_t)(c * B + b) * 16, W, H);
+    if constexpr (kInt) {  // integer corners: input gradient only
+      AccRows<SEG> em{acc};
+      if (active) {
+        if (full) box_walk_int<SEG, float, false, true>(tg, tp, H, W, x0, y0, y1, 0.f, em);
+        else box_walk_int<SEG, float, false, false>(tg, tp, H, W, x0, y0, y1, 0.f, em);
+      }
+      continue;
+    }
     float P[12];
 #pragma unroll
     for (int k = 0; k < 12; ++k) P[k] = 0.f;
@@ -653,10 +735,17 @@ __global__ __launch_bounds__(256) void k_box_grad_reduce(const float* __restrict
 // ---------------------------------------------------------------------------
 static hipError_t last_error() { return hipGetLastError(); }
 
-hipError_t launch_box_prep(const float* boxes, int C, int B, void* table, hipStream_t s) {
+hipError_t launch_box_prep(const float* boxes, int C, int B, bool rounded, void* table, hipStream_t s) {
   const int n = 2 * C * B;
-  hipLaunchKernelGGL(k_box_prep, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, (int*)table);
+  hipLaunchKernelGGL(k_box_prep, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, (int)rounded, (int*)table);
   return last_error();
+}
+
+// f(std::integral_constant<bool, v>) for the runtime flag v.
+template <typename F>
+static void with_flag(bool v, F&& f) {
+  if (v) f(std::integral_constant<bool, true>{});
+  else f(std::integral_constant<bool, false>{});
 }
 
 hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W,
@@ -686,62 +775,69 @@ static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
 }
 
 template <typename T, typename OutT, bool kOffset>
-static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int H, int W, int B, hipStream_t s) {
+static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int H, int W, int B, bool rounded,
+                      hipStream_t s) {
   constexpr int SEG = 16;
   const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
-  hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s,
-                     (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+  with_flag(rounded, [&](auto ki) {
+    hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
+                       dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+  });
 }
 
 hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void* y, int out_kind, int N, int C,
-                              int H, int W, int B, bool offset, hipStream_t s) {
+                              int H, int W, int B, bool offset, bool rounded, hipStream_t s) {
   if (is_int) {
-    fwd_lds_t<int, int, false>(x, taps, y, N, C, H, W, B, s);
+    fwd_lds_t<int, int, false>(x, taps, y, N, C, H, W, B, rounded, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_lds_t<float, uint16_t, true>(x, taps, y, N, C, H, W, B, s);
-    else fwd_lds_t<float, uint16_t, false>(x, taps, y, N, C, H, W, B, s);
+    if (offset) fwd_lds_t<float, uint16_t, true>(x, taps, y, N, C, H, W, B, rounded, s);
+    else fwd_lds_t<float, uint16_t, false>(x, taps, y, N, C, H, W, B, rounded, s);
   } else {
-    if (offset) fwd_lds_t<float, float, true>(x, taps, y, N, C, H, W, B, s);
-    else fwd_lds_t<float, float, false>(x, taps, y, N, C, H, W, B, s);
+    if (offset) fwd_lds_t<float, float, true>(x, taps, y, N, C, H, W, B, rounded, s);
+    else fwd_lds_t<float, float, false>(x, taps, y, N, C, H, W, B, rounded, s);
   }
   return last_error();
 }
 
 template <typename T, typename OutT, bool kOffset>
 static void fwd_gather_t(const void* sat, const float* means, const int* taps, void* y, int N, int C, int H, int W,
-                         int B, hipStream_t s) {
+                         int B, bool rounded, hipStream_t s) {
   constexpr int SEG = 16;
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int nblk = (items + 255) / 256;
   const int total = N * C * B * nblk;
-  hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset>), dim3(pad8(total)), dim3(256), 0, s,
-                     (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
+  with_flag(rounded, [&](auto ki) {
+    hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(pad8(total)), dim3(256),
+                       0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
+  });
 }
 
 hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const int* taps, void* y,
-                                 int out_kind, int N, int C, int H, int W, int B, hipStream_t s) {
+                                 int out_kind, int N, int C, int H, int W, int B, bool rounded, hipStream_t s) {
   const bool offset = means != nullptr;
   if (is_int) {
-    fwd_gather_t<int, int, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
+    fwd_gather_t<int, int, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, taps, y, N, C, H, W, B, s);
-    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
+    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, taps, y, N, C, H, W, B, rounded, s);
+    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
   } else {
-    if (offset) fwd_gather_t<float, float, true>(sat, means, taps, y, N, C, H, W, B, s);
-    else fwd_gather_t<float, float, false>(sat, nullptr, taps, y, N, C, H, W, B, s);
+    if (offset) fwd_gather_t<float, float, true>(sat, means, taps, y, N, C, H, W, B, rounded, s);
+    else fwd_gather_t<float, float, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
   }
   return last_error();
 }
 
 template <int SEG>
 static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N, int C,
-                      int H, int W, int B, hipStream_t s) {
+                      int H, int W, int B, bool rounded, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int threads = ((items + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
-  hipLaunchKernelGGL((k_box_bwd_lds<SEG>), dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W,
-                     B);
+  with_flag(rounded, [&](auto ki) {
+    hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value>), dim3(N * C), dim3(threads), shm, s, x, taps, gy,
+                       gx, partials, C, H, W, B);
+  });
 }
 
 // Segment length of the LDS backward: 8 rows when the map's items fit one
@@ -758,10 +854,10 @@ int box_bwd_lds_waves(int H, int W) {
 }
 
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N,
-                              int C, int H, int W, int B, hipStream_t s) {
+                              int C, int H, int W, int B, bool rounded, hipStream_t s) {
   const int seg = box_bwd_lds_seg(H, W);
-  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, s);
-  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, s);
+  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, s);
+  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, s);
   else return hipErrorInvalidValue;
   return last_error();
 }
@@ -771,11 +867,13 @@ constexpr int kBwdGatherSeg = 8;
 int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, kBwdGatherSeg) + 255) / 256; }
 
 hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx, float* partials,
-                                 int N, int C, int H, int W, int B, hipStream_t s) {
+                                 int N, int C, int H, int W, int B, bool rounded, hipStream_t s) {
   const int nblk = box_bwd_gather_blocks(H, W);
   const int total = N * C * nblk;
-  hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg>), dim3(pad8(total)), dim3(256), 0, s, x, sat_g, taps, gx,
-                     partials, C, H, W, B, nblk, total);
+  with_flag(rounded, [&](auto ki) {
+    hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg, decltype(ki)::value>), dim3(pad8(total)), dim3(256), 0, s, x,
+                       sat_g, taps, gx, partials, C, H, W, B, nblk, total);
+  });
   return last_error();
 }
 

@@ -105,6 +105,35 @@ __device__ __forceinline__ Taps<float> make_taps_adjoint(const float* p, int lim
   return t;
 }
 
+// Taps of a box whose corners are rounded to integers (the inference form of
+// the Conclusions: once the boxes have converged the sampling points are
+// rounded, and each corner is one table sample).  Each edge e (fp64) is
+// rounded to floor(e + 1/2), ties up.  The adjoint (mirrored) box of the
+// rounded box has the integer edges 1 - b, 1 - a, 1 - d, 1 - c.  Weights are
+// those of an integer edge, (-1, 0) and (1, 0): the general 16-tap walk reads
+// the same sums from these records as the 4-tap walk.
+__device__ __forceinline__ Taps<float> make_taps_rounded(const float* p, bool adjoint, int limx, int limy) {
+  const double cx = (double)p[0], cy = (double)p[1], rx = (double)p[2], ry = (double)p[3];
+  auto rnd = [](double e, int lim) {
+    double r = floor(e + 0.5);
+    if (!(r >= -(double)lim)) r = -(double)lim;
+    if (r > (double)lim) r = (double)lim;
+    return (int)r;
+  };
+  int a = rnd(0.5 + cx - rx, limx), b = rnd(0.5 + cx + rx, limx);
+  int c = rnd(0.5 + cy - ry, limy), d = rnd(0.5 + cy + ry, limy);
+  if (adjoint) {
+    const int a2 = 1 - b, b2 = 1 - a, c2 = 1 - d, d2 = 1 - c;
+    a = a2; b = b2; c = c2; d = d2;
+  }
+  Taps<float> t;
+  t.ox[0] = a; t.ox[1] = a + 1; t.ox[2] = b; t.ox[3] = b + 1;
+  t.oy[0] = c; t.oy[1] = c + 1; t.oy[2] = d; t.oy[3] = d + 1;
+  t.wx[0] = -1.f; t.wx[1] = 0.f; t.wx[2] = 1.f; t.wx[3] = 0.f;
+  t.wy[0] = -1.f; t.wy[1] = 0.f; t.wy[2] = 1.f; t.wy[3] = 0.f;
+  return t;
+}
+
 // fp32 -> bf16, round to nearest even; NaN stays NaN (quiet).  Branch-free
 // (a select), so that it never splits a wave.
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
@@ -127,10 +156,10 @@ __device__ __forceinline__ int med3_i32(int v, int hi) {
 
 // Table accessors.  A walk addresses a table row by an unclamped row
 // coordinate in the table's own units (row_coord(v) for table row v; one row
-// further is + row_step()), and the two runs of kQ + 1 columns it reads by
-// cols(ba, bb) with ba = x0 + fa, bb = x0 + fb unclamped.  runs(coord, c, sa,
-// sb) returns S(clamp(v, 0, H), clamp(ba + k, 0, W)) and the same at bb,
-// k in [0, kQ].
+// further is + row_step()), and the two runs of columns it reads by
+// cols(ba, bb) with ba = x0 + fa, bb = x0 + fb unclamped.  runs<N>(coord, c,
+// sa, sb) returns S(clamp(v, 0, H), clamp(ba + k, 0, W)) and the same at bb,
+// k in [0, N); N = kQ + 1 for interpolated edges, kQ for integer ones.
 //
 // LDS table, padded: S(u, v) at p[u * pitch + kPad + v], v in [-kPad, W+kPad];
 // coordinates are byte offsets, a row is clamped once (v_med3) and each run
@@ -146,12 +175,13 @@ struct LdsTable {
   }
   __device__ __forceinline__ int row_step() const { return pitch * (int)sizeof(T); }
   __device__ __forceinline__ int row_coord(int v) const { return v * row_step(); }
+  template <int N = kQ + 1>
   __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
     const int row = med3_i32(coord, H * row_step());
     const T* ra = reinterpret_cast<const T*>(c.a + row);
     const T* rb = reinterpret_cast<const T*>(c.b + row);
 #pragma unroll
-    for (int k = 0; k <= kQ; ++k) { sa[k] = ra[k]; sb[k] = rb[k]; }
+    for (int k = 0; k < N; ++k) { sa[k] = ra[k]; sb[k] = rb[k]; }
   }
 };
 
@@ -165,10 +195,11 @@ struct GlobalTable {
   __device__ __forceinline__ Cols cols(int ba, int bb) const { return {ba, bb}; }
   __device__ __forceinline__ int row_step() const { return 1; }
   __device__ __forceinline__ int row_coord(int v) const { return v; }
+  template <int N = kQ + 1>
   __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
     const T* r = p + (size_t)clampi(coord, 0, H) * pitch;
 #pragma unroll
-    for (int k = 0; k <= kQ; ++k) { sa[k] = r[clampi(c.a + k, 0, W)]; sb[k] = r[clampi(c.b + k, 0, W)]; }
+    for (int k = 0; k < N; ++k) { sa[k] = r[clampi(c.a + k, 0, W)]; sb[k] = r[clampi(c.b + k, 0, W)]; }
   }
 };
 

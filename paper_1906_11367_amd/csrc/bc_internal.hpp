@@ -17,8 +17,9 @@ inline int n_chunks(int W) { return (W + 2) / 3; }
 inline int n_segs(int H, int seg) { return (H + seg - 1) / seg; }
 
 // Tap records of every box (2*C*B records of 16 words: forward, then adjoint);
-// the box kernels read their taps from this table.
-hipError_t launch_box_prep(const float* boxes, int C, int B, void* table, hipStream_t s);
+// the box kernels read their taps from this table.  rounded: boxes with their
+// corners rounded to integers (the kernels then take the 4-tap walks).
+hipError_t launch_box_prep(const float* boxes, int C, int B, bool rounded, void* table, hipStream_t s);
 inline size_t tap_table_bytes(int C, int B) { return (size_t)2 * C * B * 16 * 4; }
 
 hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean,
@@ -26,24 +27,25 @@ hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean,
 
 // Forward, table in LDS.  out_kind: 0 = same type as x, 1 = fp32, 2 = bf16.
 hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void* y, int out_kind,
-                              int N, int C, int H, int W, int B, bool offset, hipStream_t s);
+                              int N, int C, int H, int W, int B, bool offset, bool rounded, hipStream_t s);
 // Forward, table read from HBM (built beforehand by sat_build into `sat`).
 hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const int* taps,
-                                 void* y, int out_kind, int N, int C, int H, int W, int B,
+                                 void* y, int out_kind, int N, int C, int H, int W, int B, bool rounded,
                                  hipStream_t s);
 
 // Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
 // LDS path: one block of box_bwd_lds_waves() waves per map, P = N * waves;
 // box_bwd_lds_seg() == 0 means the map has too many items for one block.
+// rounded: input gradient only (partials unused).
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx,
-                              float* partials, int N, int C, int H, int W, int B, hipStream_t s);
+                              float* partials, int N, int C, int H, int W, int B, bool rounded, hipStream_t s);
 int box_bwd_lds_seg(int H, int W);
 int box_bwd_lds_waves(int H, int W);
 // HBM path: tables of every gradient map in sat_g (built by sat_build);
 // P = N * box_bwd_gather_blocks() * 4.
 int box_bwd_gather_blocks(int H, int W);
 hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx,
-                                 float* partials, int N, int C, int H, int W, int B, hipStream_t s);
+                                 float* partials, int N, int C, int H, int W, int B, bool rounded, hipStream_t s);
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 

@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     lib = bc.load_library()
-    assert lib.bc_abi_version() == 1
+    assert lib.bc_abi_version() == 2
     for s in range(8):
         assert lib.bc_status_string(s)
     assert lib.bc_status_string(99) == b"unknown status"
@@ -68,6 +68,8 @@ def test_fwd_argument_errors():
     assert lib.box_conv_fwd(*a) == 4
     a = list(ok); a[10] = 1 << 7
     assert lib.box_conv_fwd(*a) == 7
+    a = list(ok); a[10] = bc.BC_FLAG_INTEGER_CORNERS   # accepted: fails only for lack of a workspace
+    assert lib.box_conv_fwd(*a) == 5
     # every forward needs a workspace (the boxes' tap records), larger when a
     # map's table does not fit LDS
     assert lib.box_conv_fwd(*ok) == 5
@@ -93,6 +95,11 @@ def test_bwd_argument_errors():
     assert lib.box_conv_bwd(*a) == 4
     a = list(ok); a[8] = None; a[9] = None  # nothing requested: no-op
     assert lib.box_conv_bwd(*a) == 0
+    # rounded corners are not differentiable: no box gradient with them
+    a = list(ok); a[10] = bc.BC_FLAG_INTEGER_CORNERS
+    assert lib.box_conv_bwd(*a) == 7
+    a[9] = None                             # grad_x only: fails only for lack of a workspace
+    assert lib.box_conv_bwd(*a) == 5
 
 
 def test_mix_argument_errors():
@@ -125,8 +132,10 @@ def test_sat_and_prep_argument_errors():
     assert lib.sat_build(FAKE, bc.BC_BF16, FAKE, None, 1, 1, 8, 8, None) == 3
     assert lib.sat_build(FAKE, bc.BC_I32, FAKE, FAKE, 1, 1, 8, 8, None) == 3      # mean needs fp32
     assert lib.sat_build(None, bc.BC_F32, FAKE, None, 1, 1, 8, 8, None) == 1
-    assert lib.box_prep(FAKE, 0, 4, FAKE, None) == 2
-    assert lib.box_prep(FAKE_MISALIGNED, 2, 4, FAKE, None) == 4
+    assert lib.box_prep(FAKE, 0, 4, 0, FAKE, None) == 2
+    assert lib.box_prep(FAKE_MISALIGNED, 2, 4, 0, FAKE, None) == 4
+    assert lib.box_prep(FAKE, 2, 4, bc.BC_FLAG_MEAN_OFFSET, FAKE, None) == 7      # only INTEGER_CORNERS
+    assert lib.box_prep(None, 2, 4, bc.BC_FLAG_INTEGER_CORNERS, FAKE, None) == 1
 
 
 def test_workspace_queries():

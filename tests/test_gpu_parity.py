@@ -208,6 +208,113 @@ def test_fwd_deterministic():
 
 
 # ---------------------------------------------------------------------------
+# Integer corners (the inference form): the rounded box, four samples per box
+# ---------------------------------------------------------------------------
+INT_CORNERS = bc.BC_FLAG_INTEGER_CORNERS
+
+
+def rounding_boxes(rng, C, B):
+    """Real-valued boxes, plus boxes whose edges are exact ties."""
+    bx = real_boxes(rng, C, B, 20.0, 0.0, 30.0)
+    bx[0, 0] = [0.0, 0.0, 1.0, 2.0]        # edges -0.5, 1.5, -1.5, 2.5
+    bx[0, 1] = [-3.25, 2.0, 0.25, 0.75]    # edges -3.0, -2.5, 1.75, 3.25
+    bx[1, 0] = [0.0, 0.0, 0.5, 0.5]        # identity
+    bx[1, 1] = [0.1, 0.0, 0.2, 0.1]        # rounds to an empty box
+    return bx
+
+
+def test_box_prep_rounded_bit_exact():
+    rng = np.random.default_rng(110)
+    C, B = 5, 4
+    bx = rounding_boxes(rng, C, B)
+    table = torch.zeros(2 * C * B * 16, dtype=torch.int32, device="cuda")
+    bc.box_prep(dev(bx), table, INT_CORNERS)
+    torch.cuda.synchronize()
+    t = table.cpu().numpy().reshape(2, C, B, 16)
+    a, b, c, d = O.rounded_edges(bx)
+    np.testing.assert_array_equal(t[0, ..., 0:4], np.stack([a, b, c, d], axis=-1))
+    # the adjoint: the mirrored box [1-b, 1-a) x [1-d, 1-c) of the rounded box
+    np.testing.assert_array_equal(t[1, ..., 0:4], np.stack([1 - b, 1 - a, 1 - d, 1 - c], axis=-1))
+    w = np.broadcast_to(np.array([-1, 0, 1, 0], dtype=np.float32), (C, B, 4))
+    for half in range(2):
+        np.testing.assert_array_equal(t[half, ..., 4:8].view(np.float32), w)
+        np.testing.assert_array_equal(t[half, ..., 8:12].view(np.float32), w)
+        np.testing.assert_array_equal(t[half, ..., 12:16], 0)
+
+
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+@pytest.mark.parametrize("shape", [(2, 3, 32, 32), (1, 2, 37, 29)])
+def test_fwd_integer_corners_int_bit_exact(flags, shape):
+    say(f"fwd integer corners int32 {shape} flags={flags}")
+    rng = np.random.default_rng(111)
+    x = rng.integers(-8, 9, size=shape).astype(np.int32)
+    bx = rounding_boxes(rng, shape[1], 4)
+    got = _fwd(x, bx, torch.int32, flags | INT_CORNERS)
+    np.testing.assert_array_equal(got, O.box_forward(x, bx, integer_corners=True))
+
+
+@pytest.mark.parametrize("key,scale", [
+    (3, dict(N=2, C=8)),
+    (2, dict(N=1, C=3, H=37, W=29, B=5)),   # ragged chunks and segments
+    (3, dict(N=1, C=2, H=17, W=100, B=3)),
+])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM, bc.BC_FLAG_MEAN_OFFSET])
+def test_fwd_integer_corners_f32(key, scale, flags):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
+    d = wlmod.make_inputs(wl)
+    say(f"fwd integer corners {wl.key} {scale} flags={flags}")
+    got = _fwd(d["x"], d["boxes"], torch.float32, flags | INT_CORNERS)
+    check(got, O.box_forward(d["x"], d["boxes"], integer_corners=True), RTOL_F32, "O")
+
+
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_MEAN_OFFSET])
+def test_fwd_integer_corners_large_maps(flags):
+    wl = wlmod.WORKLOADS[4].scaled(N=1, C=2)
+    d = wlmod.make_inputs(wl)
+    say(f"fwd integer corners {wl.key} reduced flags={flags}")
+    got = _fwd(d["x"], d["boxes"], torch.float32, flags | INT_CORNERS)
+    check(got, O.box_forward(d["x"], d["boxes"], integer_corners=True), RTOL_F32, "O")
+
+
+def test_fwd_integer_corners_bf16_output():
+    wl = wlmod.WORKLOADS[3].scaled(N=1, C=4)
+    d = wlmod.make_inputs(wl)
+    got = _fwd(d["x"], d["boxes"], torch.bfloat16, INT_CORNERS)
+    ref = O.box_forward(d["x"], d["boxes"], integer_corners=True)
+    e = bb.scale_err(ref, bb.E_F32)
+    assert np.all(np.abs(got - O.bf16_round(ref)) <= bb.bf16_band(ref, e))
+    assert np.mean(got == O.bf16_round(ref)) > 0.9
+
+
+@pytest.mark.parametrize("key,scale", [
+    (3, dict(N=3, C=4)),
+    (2, dict(N=1, C=3, H=37, W=29, B=5)),
+    (3, dict(N=2, C=2, H=17, W=100, B=3)),
+    (4, dict(N=1, C=1, B=3)),
+])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_bwd_integer_corners(key, scale, flags):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
+    d = wlmod.make_inputs(wl)
+    rng = np.random.default_rng(112)
+    g = rng.standard_normal((wl.N, wl.C * wl.B, wl.H, wl.W)).astype(np.float32)
+    say(f"bwd integer corners {wl.key} {scale} flags={flags}")
+    gx = torch.empty((wl.N, wl.C, wl.H, wl.W), dtype=torch.float32, device="cuda")
+    bc.box_conv_bwd(dev(d["x"]), dev(d["boxes"]), dev(g), gx, None, flags | INT_CORNERS)
+    check(host(gx), O.box_backward_input(g, d["boxes"], wl.H, wl.W, integer_corners=True), RTOL_F32, "dx")
+
+
+def test_integer_corners_box_grad_rejected():
+    x = torch.zeros((1, 1, 8, 8), device="cuda")
+    bx = torch.zeros((1, 2, 4), device="cuda")
+    g = torch.zeros((1, 2, 8, 8), device="cuda")
+    gx = torch.empty_like(x)
+    gb = torch.empty((1, 2, 4), device="cuda")
+    with pytest.raises(bc.BoxConvError):
+        bc.box_conv_bwd(x, bx, g, gx, gb, INT_CORNERS)
+
+
+# ---------------------------------------------------------------------------
 # a7 / a8: backward of the box filter
 # ---------------------------------------------------------------------------
 def _bwd(x, bx, g, flags=0):

@@ -296,6 +296,64 @@ def test_forward_naive_overlap_loop_matches():
 
 
 # --------------------------------------------------------------------------
+# Integer corners: the inference form of the Conclusions (reading R12)
+# --------------------------------------------------------------------------
+def test_rounded_edges_closed_form():
+    # edges worked out by hand: plain values, ties (halfway: up), negatives
+    bx = np.array([[[0.3, -0.2, 1.1, 0.4],     # a=-0.3, b=1.9, c=-0.1, d=0.7
+                    [0.0, 0.0, 1.0, 2.0],      # a=-0.5, b=1.5, c=-1.5, d=2.5 (all ties)
+                    [-3.25, 2.0, 0.25, 0.75]]],  # a=-3.0, b=-2.5, c=1.75, d=3.25
+                  dtype=np.float32)
+    a, b, c, d = O.rounded_edges(bx)
+    np.testing.assert_array_equal(a[0], [0, 0, -3])
+    np.testing.assert_array_equal(b[0], [2, 2, -2])
+    np.testing.assert_array_equal(c[0], [0, -1, 2])
+    np.testing.assert_array_equal(d[0], [1, 3, 3])
+
+
+def _integer_corner_case(kind, seed=21):
+    rng = np.random.default_rng(seed)
+    N, C, B, H, W = 1, 2, 3, 7, 6
+    x = (rng.integers(-8, 9, size=(N, C, H, W)) if kind == "int"
+         else rng.standard_normal((N, C, H, W)))
+    bx = _real_boxes(rng, C, B, cmax=4.0, rmin=0.1, rmax=4.0)
+    return x, bx
+
+
+@pytest.mark.parametrize("kind", ["int", "float"])
+def test_integer_corners_forward_equals_eq1_loops(kind):
+    x, bx = _integer_corner_case(kind)
+    a, b, c, d = O.rounded_edges(bx)
+    # the same boxes written with their rounded corners (half-integers, exact
+    # in fp32), summed by the Eq. 1 loops
+    br = np.stack([(a + b - 1) / 2, (c + d - 1) / 2, (b - a) / 2, (d - c) / 2], axis=-1).astype(np.float32)
+    got = O.box_forward(x, bx, integer_corners=True)
+    want = O.naive_box_forward_eq1(x, br)
+    if kind == "int":
+        np.testing.assert_array_equal(got, want)
+    else:
+        np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_integer_corners_keep_integer_boxes():
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((1, 2, 9, 8))
+    bx = _int_boxes(rng, 2, 3, smax=7, span=5)
+    np.testing.assert_array_equal(O.box_forward(x, bx, integer_corners=True), O.box_forward(x, bx))
+
+
+def test_integer_corners_backward_is_adjoint():
+    rng = np.random.default_rng(23)
+    N, C, B, H, W = 2, 2, 3, 9, 7
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = _real_boxes(rng, C, B, cmax=4.0, rmin=0.1, rmax=5.0)
+    dx = O.box_backward_input(g, bx, H, W, integer_corners=True)
+    lhs = np.sum(O.box_forward(x, bx, integer_corners=True) * g)
+    assert abs(lhs - np.sum(x * dx)) <= 1e-12 * (1 + abs(lhs))
+
+
+# --------------------------------------------------------------------------
 # Input gradient: adjoint of the forward map
 # --------------------------------------------------------------------------
 def test_input_grad_adjoint_and_mirrored_box():
@@ -592,12 +650,12 @@ def _mut_bf16_truncate(v):
     return u.view(np.float32).astype(np.float64)
 
 
-def _mut_backward_input_no_transpose(grad_y, boxes, H, W):
+def _mut_backward_input_no_transpose(grad_y, boxes, H, W, integer_corners=False):
     g = np.asarray(grad_y, dtype=np.float64)
     C, B = boxes.shape[0], boxes.shape[1]
     N = g.shape[0]
     g = g.reshape(N, C, B, H, W)
-    a, b, c, d = _OM.box_edges(boxes)
+    a, b, c, d = _OM.rounded_edges(boxes) if integer_corners else _OM.box_edges(boxes)
     out = np.zeros((N, C, H, W))
     for ci in range(C):
         for bi in range(B):
@@ -605,6 +663,14 @@ def _mut_backward_input_no_transpose(grad_y, boxes, H, W):
             wy = _OM.overlap_matrix(H, c[ci, bi], d[ci, bi])
             out[:, ci] += wy @ g[:, ci, bi] @ wx.T
     return out
+
+
+def _mut_rounded_half_even(boxes):
+    return tuple(np.round(e) for e in _OM.box_edges(boxes))
+
+
+def _mut_rounded_floor(boxes):
+    return tuple(np.floor(e) for e in _OM.box_edges(boxes))
 
 
 _ORIG = {k: getattr(_OM, k) for k in ("overlap_matrix", "_edge_selector")}
@@ -619,6 +685,8 @@ _MUTATIONS = {
     "bf16_truncate": ("bf16_round", _mut_bf16_truncate),
     "adjoint_floor_split": ("adjoint_taps", _mut_adjoint_floor_split),
     "bwd_input_no_transpose": ("box_backward_input", _mut_backward_input_no_transpose),
+    "rounded_half_even": ("rounded_edges", _mut_rounded_half_even),
+    "rounded_floor": ("rounded_edges", _mut_rounded_floor),
 }
 
 _PINS = [
@@ -628,7 +696,8 @@ _PINS = [
     test_input_grad_adjoint_and_mirrored_box, test_input_grad_finite_difference,
     test_param_grad_finite_difference_exact, test_param_grad_edges_clipped_at_border,
     test_param_grad_constant_image_closed_form, test_bf16_round_matches_torch,
-    test_adjoint_taps_carry_param_gradient,
+    test_adjoint_taps_carry_param_gradient, test_rounded_edges_closed_form,
+    lambda: test_integer_corners_forward_equals_eq1_loops("int"), test_integer_corners_backward_is_adjoint,
 ]
 
 
