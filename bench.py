@@ -8,10 +8,12 @@ and box-parameter gradients).  Inputs are seeded synthetic arrays shaped like
 pose-estimation feature maps, already resident in HBM when timing starts.
 
 Prints ONE JSON line.  `value` is filtered-map elements (pixel*box, summed over
-layers) per second of the whole step, in Gpix*box/s.  `roofline` reports the
-dominant library call, timed with HIP events in a second pass that records an
-event after every call (`serial_ms_per_step` is that pass's step);
-`cpu_baseline` times the CPU oracle on a bounded sample on this host.
+layers) per second of the whole step, in Gpix*box/s, timed on steps run as the
+layer runs them (the weight gradient overlapped on a second stream).
+`roofline` reports the dominant library call, timed with HIP events in a
+second pass where every call runs in order on one stream (`serial_ms_per_step`
+is that pass's step); `cpu_baseline` times the CPU oracle on a bounded sample
+on this host.
 """
 from __future__ import annotations
 
@@ -187,7 +189,9 @@ def main():
             timing["events"].append((label, e))
 
     def step():
-        # the per-call pass records an event after every call
+        # The plain pass runs the layer as a user would (the weight gradient
+        # overlapped on a second stream); the per-call pass records an event
+        # after every call, in order on one stream.
         t = tap if timing["on"] else None
         if t:
             t("start")
@@ -219,7 +223,7 @@ def main():
         if l1 == "start":
             continue
         per.setdefault(l1, []).append(a.elapsed_time(b))
-    # one step of the per-call pass
+    # one step with every call in order on one stream (the per-call pass)
     serial_ms = sum(sum(ts) for ts in per.values()) / args.steps
     o_bytes = 2 if (wl.mix_out is not None and wl.mix_dtype == "bf16") else 4
     src_hash = source_hash()

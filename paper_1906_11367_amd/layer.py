@@ -5,8 +5,12 @@ Forward:  O = box_conv_fwd(x)            (bf16 copy when the mix runs in bf16)
 Backward: dW = pointwise_mix(BWD_WEIGHT, dZ, O)
           dO = pointwise_mix(BWD_DATA, w, dZ)
           dx, dboxes = box_conv_bwd(x, dO)
+The weight gradient depends on neither of the other two backward calls; it
+runs on a second stream (default priority) alongside them, and the caller's
+stream waits for it before the backward returns.
 All buffers and workspaces are allocated once per plan (torch is used for
-device memory only); every arithmetic step runs in libboxconv's kernels.
+device memory and streams only); every arithmetic step runs in libboxconv's
+kernels.
 """
 from __future__ import annotations
 
@@ -62,6 +66,9 @@ class LayerPlan:
                 self.dw = torch.empty((self.M, K), dtype=torch.float32, device=dev)
                 self.ws_mixw = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, N, self.M, K, P,
                                                           self.compute), dev)
+                self.side = torch.cuda.Stream(device=dev)   # default priority
+                self.ev_in = torch.cuda.Event()
+                self.ev_dw = torch.cuda.Event()
 
     def forward(self, x: torch.Tensor, boxes: torch.Tensor, w: torch.Tensor | None, tap=None):
         """tap(label), if given, is called after each library call (the benchmark
@@ -81,16 +88,30 @@ class LayerPlan:
 
     def backward(self, x: torch.Tensor, boxes: torch.Tensor, w: torch.Tensor | None, grad_out: torch.Tensor,
                  tap=None):
-        """grad_out: dL/dZ (or dL/dO without a mix).  Returns (dx, dboxes, dw)."""
+        """grad_out: dL/dZ (or dL/dO without a mix).  Returns (dx, dboxes, dw).
+
+        With a mix, the weight gradient runs on the plan's second stream; given
+        `tap`, every call runs in order on the current stream instead, so that
+        the events the benchmark records there time each call alone."""
+        overlap = tap is None
         tap = tap or _no_tap
         if self.M is None:
             do = grad_out
             dw = None
         else:
             aux = self.z if self.relu else None
-            bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, grad_out, self.o, self.dw, self.N, self.M, self.K, self.P,
-                             self.compute, relu=int(self.relu), aux=aux, ws=self.ws_mixw)
-            tap("mix_bwd_weight")
+            main = torch.cuda.current_stream()
+            if overlap:
+                self.ev_in.record(main)         # O, Z and dZ are ready on the caller's stream
+                self.side.wait_event(self.ev_in)
+                with torch.cuda.stream(self.side):
+                    bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, grad_out, self.o, self.dw, self.N, self.M, self.K,
+                                     self.P, self.compute, relu=int(self.relu), aux=aux, ws=self.ws_mixw)
+                self.ev_dw.record(self.side)
+            else:
+                bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, grad_out, self.o, self.dw, self.N, self.M, self.K, self.P,
+                                 self.compute, relu=int(self.relu), aux=aux, ws=self.ws_mixw)
+                tap("mix_bwd_weight")
             if self.w_c is not None:
                 w = self.w_c
             bc.pointwise_mix(bc.BC_MIX_BWD_DATA, w, grad_out, self.do, self.N, self.M, self.K, self.P,
@@ -100,6 +121,8 @@ class LayerPlan:
             dw = self.dw
         bc.box_conv_bwd(x, boxes, do, self.dx, self.dboxes, self.flags, self.ws_bwd)
         tap("box_conv_bwd")
+        if self.M is not None and overlap:
+            main.wait_event(self.ev_dw)         # dW (and the reuse of O, dZ) ordered after the side stream
         return self.dx, self.dboxes, dw
 
 
