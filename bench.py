@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "box-conv fwd+bwd Gpix·box/s; SAT/box HBM GB/s and 1×1 MFMA util vs peak"
+METRIC_INFERENCE = "box-conv inference fwd Gpix·box/s (integer corners); box HBM GB/s and 1×1 MFMA util vs peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 DEFAULT_WORKLOAD = 3
@@ -42,6 +43,12 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=20.0,
                    help="rough CPU time the oracle sample may take")
+    p.add_argument("--inference", action="store_true",
+                   help="time the inference forward instead (boxes rounded to integer corners, "
+                        "four table samples per box, then the 1x1 mix); no backward")
+    p.add_argument("--serial", action="store_true",
+                   help="run every call in order on one stream in the timed pass too (no overlapped "
+                        "weight gradient): the configuration the per-kernel profiles are taken in")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain elementwise kernel that reads 256 MiB and writes 256 MiB, 5 "
                         "times (reference for the FETCH_SIZE / WRITE_SIZE counters), and exit")
@@ -96,8 +103,9 @@ def load_traffic(label, wl_key, src_hash):
         return None
 
 
-def cpu_baseline(wl, d, budget_s):
-    """Times the CPU oracle (fwd + bwd of the layer) on a sample of images.
+def cpu_baseline(wl, d, budget_s, inference=False):
+    """Times the CPU oracle (fwd + bwd of the layer; with `inference`, the
+    integer-corner forward only) on a sample of images.
 
     The sample keeps every channel and box of the workload and takes the
     first n images (n chosen from a one-image probe to fit the budget)."""
@@ -116,6 +124,11 @@ def cpu_baseline(wl, d, budget_s):
             layers = d["layers"][:1]   # one layer of the stack per sample image
             cache = O.stack_forward(x, layers, compute=wl.mix_dtype, apply_relu=wl.relu)
             O.stack_backward(cache, layers, g, compute=wl.mix_dtype, apply_relu=wl.relu)
+            return n * wl.C * wl.B * wl.H * wl.W
+        if inference:
+            o = O.box_forward(x, d["boxes"], integer_corners=True)
+            if wl.mix_out is not None:
+                O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
             return n * wl.C * wl.B * wl.H * wl.W
         o = O.box_forward(x, d["boxes"])
         if wl.mix_out is None:
@@ -139,9 +152,10 @@ def cpu_baseline(wl, d, budget_s):
         t0 = time.perf_counter()
         pb = run(n)
         t1 = time.perf_counter() - t0
+    what = "integer-corner fwd" if inference else "fwd+bwd"
     return {"value": pb / t1 / 1e9, "unit": "Gpix·box/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} of {wl.N} images, all {wl.C} channels x {wl.B} boxes, one layer, "
-                      f"fwd+bwd, fp64 NumPy, {t1:.1f} s"}
+                      f"{what}, fp64 NumPy, {t1:.1f} s"}
 
 
 def main():
@@ -177,8 +191,13 @@ def main():
     grad = dev(d["grad"]) if d["grad"] is not None else None
     x_dt = torch.int32 if wl.x_kind == "int8range" else torch.float32
     flags = bc.BC_FLAG_MEAN_OFFSET if wl.mean_offset else 0
+    backward = wl.backward and not args.inference
+    if args.inference:
+        flags |= bc.BC_FLAG_INTEGER_CORNERS
     st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, wl.mix_dtype, wl.relu, x_dt, flags,
-               wl.backward)
+               backward)
+    for plan in st.plans:
+        plan.overlap = not args.serial
     stream = torch.cuda.current_stream()
     timing = {"on": False, "events": []}
 
@@ -196,7 +215,7 @@ def main():
         if t:
             t("start")
         inputs, out = st.forward(x, params, t)
-        if wl.backward:
+        if backward:
             st.backward(inputs, params, grad, t)
 
     for _ in range(args.warmup):
@@ -253,7 +272,7 @@ def main():
         calls[label] = ent
     dom = max(calls, key=lambda k: calls[k]["avg_us"] * calls[k]["launches"])
     dc = calls[dom]
-    traffic = load_traffic(dom, wl.key, src_hash)
+    traffic = load_traffic(dom, wl.key + ("_inference" if args.inference else ""), src_hash)
     roofline = {"bound": dc["bound"], "achieved": dc["achieved"], "peak": dc["peak"], "unit": dc["unit"],
                 "frac": dc["frac"], "traffic": traffic, "kernel": dom, "avg_us": dc["avg_us"],
                 "per_launch": ("algo_bytes=%d" % dc["algo_bytes"]) if dc["bound"] == "hbm"
@@ -263,7 +282,7 @@ def main():
     value = pix_box / (ms * 1e-3) / 1e9
     box_ms = sum(calls[k]["avg_us"] * calls[k]["launches"] for k in calls if k.startswith("box")) / 1e3
     line = {
-        "metric": METRIC, "value": round(value, 3), "unit": "Gpix·box/s", "n_gpus": 1,
+        "metric": METRIC_INFERENCE if args.inference else METRIC, "value": round(value, 3), "unit": "Gpix·box/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "serial_ms_per_step": round(serial_ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32" if x_dt == torch.float32 else "i32",
@@ -271,6 +290,8 @@ def main():
         "config": {"workload": wl.key, "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "B": wl.B,
                    "mix": None if wl.mix_out is None else f"{wl.C * wl.B}->{wl.mix_out} {wl.mix_dtype}",
                    "layers": wl.layers, "relu": wl.relu, "mean_offset": wl.mean_offset,
+                   "integer_corners": bool(args.inference), "backward": backward,
+                   "overlap_weight_grad": backward and not args.serial,
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
         "roofline": roofline,
@@ -279,7 +300,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s)
+        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference)
     print(json.dumps(line), flush=True)
     return 0
 

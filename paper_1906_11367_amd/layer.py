@@ -35,6 +35,7 @@ class LayerPlan:
     flags: int = 0
     with_backward: bool = True
     device: str = "cuda"
+    overlap: bool = True       # weight gradient on a second stream during the backward
 
     def __post_init__(self):
         dev = torch.device(self.device)
@@ -90,10 +91,11 @@ class LayerPlan:
                  tap=None):
         """grad_out: dL/dZ (or dL/dO without a mix).  Returns (dx, dboxes, dw).
 
-        With a mix, the weight gradient runs on the plan's second stream; given
-        `tap`, every call runs in order on the current stream instead, so that
-        the events the benchmark records there time each call alone."""
-        overlap = tap is None
+        With a mix (and `overlap`), the weight gradient runs on the plan's
+        second stream; given `tap`, every call runs in order on the current
+        stream instead, so that the events the benchmark records there time
+        each call alone."""
+        overlap = tap is None and self.overlap
         tap = tap or _no_tap
         if self.M is None:
             do = grad_out
