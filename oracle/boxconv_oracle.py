@@ -44,6 +44,10 @@ R6  No area normalisation and no bias (Eq. 1 is a plain sum).
 R7  Output channel of box b on input channel c is c*B + b.
 R8  A bf16 1x1 mix rounds both operands to bf16 (round to nearest even) and
     accumulates exactly; the oracle accumulates in fp64.
+R13 Integer stride s (Section 3.1 assumes an integer stride so that the
+    interpolation weights stay fixed): output pixel (i, j) is the box placed
+    at input pixel (s*i, s*j); the output is ceil(H/s) x ceil(W/s).  Stride 1
+    is the plain layer.
 R12 Integer corners for inference (Conclusions: once the boxes have
     converged, round the sampling points to integers so that no interpolation
     is needed): each edge a, b, c, d is rounded to the nearest integer, a tie
@@ -60,7 +64,7 @@ __all__ = [
     "map_mean", "box_forward", "box_backward_input", "box_backward_params",
     "box_param_grad_from_edges", "bf16_round", "mix_forward",
     "mix_backward_data", "mix_backward_weight", "relu", "layer_forward",
-    "stack_forward", "stack_backward", "naive_box_forward_eq1",
+    "stack_forward", "stack_backward", "naive_box_forward_eq1", "strided_size", "zero_upsample",
     "naive_box_forward_overlap", "tolerance_ok", "rel_errors",
 ]
 
@@ -189,7 +193,23 @@ def _is_int(x):
     return np.issubdtype(np.asarray(x).dtype, np.integer)
 
 
-def box_forward(x, boxes, integer_corners=False):
+def strided_size(n, stride):
+    """Output extent of a stride-s filter over n pixels (reading R13)."""
+    return (n + stride - 1) // stride
+
+
+def zero_upsample(g, H, W, stride):
+    """[..., ceil(H/s), ceil(W/s)] -> [..., H, W]: g[..., i, j] at (s*i, s*j),
+    zero elsewhere.  The transpose of sampling every s-th pixel."""
+    g = np.asarray(g)
+    if stride == 1:
+        return g
+    out = np.zeros(g.shape[:-2] + (H, W), dtype=g.dtype)
+    out[..., ::stride, ::stride] = g
+    return out
+
+
+def box_forward(x, boxes, integer_corners=False, stride=1):
     """O[n, c*B+b] = integral of zero-padded x[n, c] over each box (fp64/int64).
 
     x: [N, C, H, W]; boxes: [C, B, 4] fp32 (cx, cy, rx, ry).
@@ -197,7 +217,8 @@ def box_forward(x, boxes, integer_corners=False):
     integer x the boxes must have integer corners (then every weight is 0 or
     1) and the result is exact int64.  integer_corners: the boxes with their
     corners rounded (reading R12) -- the plain sum of Eq. 1 over the rounded
-    box, for any map type.
+    box, for any map type.  stride: the output at every stride-th pixel
+    (reading R13), [N, C*B, ceil(H/s), ceil(W/s)].
     """
     x = np.asarray(x)
     N, C, H, W = x.shape
@@ -217,18 +238,20 @@ def box_forward(x, boxes, integer_corners=False):
                 wx = wx.astype(np.int64)
                 wy = wy.astype(np.int64)
             out[:, ci, bi] = wy @ xf[:, ci] @ wx.T
-    return out.reshape(N, C * B, H, W)
+    return out.reshape(N, C * B, H, W)[..., ::stride, ::stride]
 
 
-def box_backward_input(grad_y, boxes, H, W, integer_corners=False):
+def box_backward_input(grad_y, boxes, H, W, integer_corners=False, stride=1):
     """dI[n, c] = sum_b Wy^T @ dO[n, c*B+b] @ Wx  (transpose of box_forward).
 
     grad_y: [N, C*B, H, W]; returns fp64 [N, C, H, W].  The paper states only
     the local derivative of a table sample (its bilinear weight, the text after
     Eq. 4); this is the chain rule of the whole forward map.  integer_corners:
-    the transpose of box_forward(..., integer_corners=True).
+    the transpose of box_forward(..., integer_corners=True).  stride: grad_y
+    is [N, C*B, ceil(H/s), ceil(W/s)]; the transpose of sampling every s-th
+    pixel places it on the full grid (zero_upsample) first.
     """
-    g = np.asarray(grad_y, dtype=np.float64)
+    g = zero_upsample(np.asarray(grad_y, dtype=np.float64), H, W, stride)
     C, B = boxes.shape[0], boxes.shape[1]
     N = g.shape[0]
     g = g.reshape(N, C, B, H, W)
@@ -289,13 +312,17 @@ def box_param_grad_from_edges(x, grad_y, boxes):
     return out
 
 
-def box_backward_params(x, grad_y, boxes):
+def box_backward_params(x, grad_y, boxes, stride=1):
     """Gradient of L = <grad_y, O> with respect to (cx, cy, rx, ry), fp64 [C, B, 4].
 
     a = 1/2+cx-rx, b = 1/2+cx+rx, c = 1/2+cy-ry, d = 1/2+cy+ry, so
-    dcx = gA+gB, dcy = gC+gD, drx = gB-gA, dry = gD-gC.
+    dcx = gA+gB, dcy = gC+gD, drx = gB-gA, dry = gD-gC.  stride: as in
+    box_backward_input (the strided output is the full output sampled, so its
+    gradient is the full one of the zero-upsampled grad_y).
     """
-    e = box_param_grad_from_edges(x, grad_y, boxes)
+    H, W = np.asarray(x).shape[-2:]
+    g = zero_upsample(np.asarray(grad_y, dtype=np.float64), H, W, stride)
+    e = box_param_grad_from_edges(x, g, boxes)
     ga, gb, gc, gd = e[..., 0], e[..., 1], e[..., 2], e[..., 3]
     return np.stack([ga + gb, gc + gd, gb - ga, gd - gc], axis=-1)
 

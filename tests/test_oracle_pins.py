@@ -354,6 +354,52 @@ def test_integer_corners_backward_is_adjoint():
 
 
 # --------------------------------------------------------------------------
+# Integer stride (reading R13): the box placed at every s-th pixel
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("stride", [2, 3])
+def test_strided_forward_equals_eq1_loops(stride):
+    rng = np.random.default_rng(24)
+    x = rng.integers(-8, 9, size=(1, 2, 8, 7))
+    bx = _int_boxes(rng, 2, 3, smax=5, span=3)
+    full = O.naive_box_forward_eq1(x, bx)
+    got = O.box_forward(x, bx, stride=stride)
+    Ho, Wo = O.strided_size(8, stride), O.strided_size(7, stride)
+    assert got.shape == (1, 6, Ho, Wo)
+    for i in range(Ho):
+        for j in range(Wo):
+            np.testing.assert_array_equal(got[..., i, j], full[..., stride * i, stride * j])
+
+
+def test_strided_input_grad_is_adjoint():
+    rng = np.random.default_rng(25)
+    N, C, B, H, W, s = 2, 2, 3, 11, 9, 2
+    x = rng.standard_normal((N, C, H, W))
+    bx = _real_boxes(rng, C, B, cmax=4.0, rmin=0.2, rmax=5.0)
+    g = rng.standard_normal((N, C * B, O.strided_size(H, s), O.strided_size(W, s)))
+    dx = O.box_backward_input(g, bx, H, W, stride=s)
+    lhs = np.sum(O.box_forward(x, bx, stride=s) * g)
+    assert abs(lhs - np.sum(x * dx)) <= 1e-12 * (1 + abs(lhs))
+
+
+def test_strided_param_grad_finite_difference_exact():
+    rng = np.random.default_rng(26)
+    N, C, B, H, W, s = 1, 2, 2, 12, 10, 3
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    g = rng.standard_normal((N, C * B, O.strided_size(H, s), O.strided_size(W, s)))
+    bx = _boxes_away_from_kinks(rng, C, B, 4.0, 0.4, 6.0)
+    grad = O.box_backward_params(x, g, bx, stride=s)
+    L0 = np.sum(O.box_forward(x, bx, stride=s) * g)
+    for c in range(C):
+        for b in range(B):
+            for k in range(4):
+                p = bx.copy()
+                p[c, b, k] = np.float32(p[c, b, k] + np.float32(0.01))
+                h = float(p[c, b, k]) - float(bx[c, b, k])
+                fd = (np.sum(O.box_forward(x, p, stride=s) * g) - L0) / h
+                assert abs(fd - grad[c, b, k]) <= 1e-8 * (1 + abs(fd)), (c, b, k, fd, grad[c, b, k])
+
+
+# --------------------------------------------------------------------------
 # Input gradient: adjoint of the forward map
 # --------------------------------------------------------------------------
 def test_input_grad_adjoint_and_mirrored_box():
@@ -634,8 +680,10 @@ def _mut_edge_selector_ceil(n, edge):
     return _ORIG["_edge_selector"](n, edge + 1.0)
 
 
-def _mut_param_sign(x, grad_y, boxes):
-    e = _OM.box_param_grad_from_edges(x, grad_y, boxes)
+def _mut_param_sign(x, grad_y, boxes, stride=1):
+    H, W = np.asarray(x).shape[-2:]
+    e = _OM.box_param_grad_from_edges(x, _OM.zero_upsample(np.asarray(grad_y, dtype=np.float64), H, W, stride),
+                                      boxes)
     ga, gb, gc, gd = e[..., 0], e[..., 1], e[..., 2], e[..., 3]
     return np.stack([ga + gb, gc + gd, ga - gb, gd - gc], axis=-1)
 
@@ -650,8 +698,8 @@ def _mut_bf16_truncate(v):
     return u.view(np.float32).astype(np.float64)
 
 
-def _mut_backward_input_no_transpose(grad_y, boxes, H, W, integer_corners=False):
-    g = np.asarray(grad_y, dtype=np.float64)
+def _mut_backward_input_no_transpose(grad_y, boxes, H, W, integer_corners=False, stride=1):
+    g = _OM.zero_upsample(np.asarray(grad_y, dtype=np.float64), H, W, stride)
     C, B = boxes.shape[0], boxes.shape[1]
     N = g.shape[0]
     g = g.reshape(N, C, B, H, W)
@@ -667,6 +715,17 @@ def _mut_backward_input_no_transpose(grad_y, boxes, H, W, integer_corners=False)
 
 def _mut_rounded_half_even(boxes):
     return tuple(np.round(e) for e in _OM.box_edges(boxes))
+
+
+def _mut_upsample_offset(g, H, W, stride):
+    # places the strided gradient one pixel off its sampling position
+    g = np.asarray(g)
+    if stride == 1:
+        return g
+    out = np.zeros(g.shape[:-2] + (H, W), dtype=g.dtype)
+    sub = out[..., 1::stride, 1::stride]
+    sub[...] = g[..., :sub.shape[-2], :sub.shape[-1]]
+    return out
 
 
 def _mut_rounded_floor(boxes):
@@ -687,6 +746,7 @@ _MUTATIONS = {
     "bwd_input_no_transpose": ("box_backward_input", _mut_backward_input_no_transpose),
     "rounded_half_even": ("rounded_edges", _mut_rounded_half_even),
     "rounded_floor": ("rounded_edges", _mut_rounded_floor),
+    "upsample_offset": ("zero_upsample", _mut_upsample_offset),
 }
 
 _PINS = [
@@ -698,6 +758,8 @@ _PINS = [
     test_param_grad_constant_image_closed_form, test_bf16_round_matches_torch,
     test_adjoint_taps_carry_param_gradient, test_rounded_edges_closed_form,
     lambda: test_integer_corners_forward_equals_eq1_loops("int"), test_integer_corners_backward_is_adjoint,
+    lambda: test_strided_forward_equals_eq1_loops(2), test_strided_input_grad_is_adjoint,
+    test_strided_param_grad_finite_difference_exact,
 ]
 
 
