@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--inference", action="store_true",
                    help="time the inference forward instead (boxes rounded to integer corners, "
                         "four table samples per box, then the 1x1 mix); no backward")
+    p.add_argument("--stride", type=int, default=1,
+                   help="box filter stride (outputs at every stride-th pixel; the 1x1 mix and the backward "
+                        "run on the strided grid)")
     p.add_argument("--serial", action="store_true",
                    help="run every call in order on one stream in the timed pass too (no overlapped "
                         "weight gradient): the configuration the per-kernel profiles are taken in")
@@ -64,24 +67,25 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def call_cost(label, wl, o_bytes):
+def call_cost(label, wl, o_bytes, stride=1):
     """Algorithmic bytes and FLOPs of one launch of a library call (one layer).
 
-    box_conv_fwd : read x (4 B/pixel) + write O (o_bytes per pixel*box)
-    box_conv_bwd : read x + read dO (4 B/pixel*box) + write dx (4 B/pixel)
+    box_conv_fwd : read x (4 B/pixel) + write O (o_bytes per output pixel*box)
+    box_conv_bwd : read x + read dO (4 B/output pixel*box) + write dx (4 B/pixel)
     mix_*        : 2*N*M*K*P FLOPs (one GEMM), reported against the MFMA
                    peak; also the operand bytes it must move (fwd: read O,
                    write Z; bwd_data: read dZ, write dO; bwd_weight: read dZ
                    and O), reported against the HBM peak
     """
     px = wl.N * wl.C * wl.H * wl.W
-    pb = px * wl.B
+    Ho, Wo = (wl.H + stride - 1) // stride, (wl.W + stride - 1) // stride
+    pb = wl.N * wl.C * wl.B * Ho * Wo          # output pixel*box
     if label == "box_conv_fwd":
         return {"bound": "hbm", "bytes": 4 * px + o_bytes * pb}
     if label == "box_conv_bwd":
         return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 4 * px}
-    flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * wl.H * wl.W
-    z = 4 * wl.N * wl.mix_out * wl.H * wl.W
+    flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * Ho * Wo
+    z = 4 * wl.N * wl.mix_out * Ho * Wo
     mix_bytes = {"mix_fwd": o_bytes * pb + z, "mix_bwd_data": z + 4 * pb, "mix_bwd_weight": z + o_bytes * pb}
     return {"bound": "mfma", "flops": flops, "bytes": mix_bytes.get(label)}
 
@@ -103,7 +107,7 @@ def load_traffic(label, wl_key, src_hash):
         return None
 
 
-def cpu_baseline(wl, d, budget_s, inference=False):
+def cpu_baseline(wl, d, budget_s, inference=False, stride=1):
     """Times the CPU oracle (fwd + bwd of the layer; with `inference`, the
     integer-corner forward only) on a sample of images.
 
@@ -119,30 +123,31 @@ def cpu_baseline(wl, d, budget_s, inference=False):
 
     def run(n):
         x = d["x"][:n]
-        g = d["grad"][:n] if d["grad"] is not None else None
+        g = d["grad"][:n, ..., ::stride, ::stride] if d["grad"] is not None else None
+        Ho, Wo = (wl.H + stride - 1) // stride, (wl.W + stride - 1) // stride
         if wl.layers > 1:
             layers = d["layers"][:1]   # one layer of the stack per sample image
             cache = O.stack_forward(x, layers, compute=wl.mix_dtype, apply_relu=wl.relu)
             O.stack_backward(cache, layers, g, compute=wl.mix_dtype, apply_relu=wl.relu)
             return n * wl.C * wl.B * wl.H * wl.W
         if inference:
-            o = O.box_forward(x, d["boxes"], integer_corners=True)
+            o = O.box_forward(x, d["boxes"], integer_corners=True, stride=stride)
             if wl.mix_out is not None:
                 O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
-            return n * wl.C * wl.B * wl.H * wl.W
-        o = O.box_forward(x, d["boxes"])
+            return n * wl.C * wl.B * Ho * Wo
+        o = O.box_forward(x, d["boxes"], stride=stride)
         if wl.mix_out is None:
             if g is not None:
-                O.box_backward_input(g, d["boxes"], wl.H, wl.W)
-                O.box_backward_params(x, g, d["boxes"])
-            return n * wl.C * wl.B * wl.H * wl.W
+                O.box_backward_input(g, d["boxes"], wl.H, wl.W, stride=stride)
+                O.box_backward_params(x, g, d["boxes"], stride=stride)
+            return n * wl.C * wl.B * Ho * Wo
         O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
         if g is not None:
             O.mix_backward_weight(g, o, compute=wl.mix_dtype)
             do = O.mix_backward_data(d["w"], g, compute=wl.mix_dtype)
-            O.box_backward_input(do, d["boxes"], wl.H, wl.W)
-            O.box_backward_params(x, do, d["boxes"])
-        return n * wl.C * wl.B * wl.H * wl.W
+            O.box_backward_input(do, d["boxes"], wl.H, wl.W, stride=stride)
+            O.box_backward_params(x, do, d["boxes"], stride=stride)
+        return n * wl.C * wl.B * Ho * Wo
 
     t0 = time.perf_counter()
     pb = run(1)
@@ -194,8 +199,11 @@ def main():
     backward = wl.backward and not args.inference
     if args.inference:
         flags |= bc.BC_FLAG_INTEGER_CORNERS
+    s_ = args.stride
     st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, wl.mix_dtype, wl.relu, x_dt, flags,
-               backward)
+               backward, stride=s_)
+    if grad is not None and s_ > 1:
+        grad = grad[..., ::s_, ::s_].contiguous()
     for plan in st.plans:
         plan.overlap = not args.serial
     stream = torch.cuda.current_stream()
@@ -222,8 +230,21 @@ def main():
         step()
     torch.cuda.synchronize()
 
+    # Each timed pass starts behind ~30 ms of device-side spinning, queued
+    # before its first event: the host enqueues the steps while the GPU is
+    # busy, so no host launch gap lands inside a timed call or step.
+    spin = torch.cuda._sleep
+    probe = 1 << 20
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record(stream)
+    spin(probe)
+    s1.record(stream)
+    torch.cuda.synchronize()
+    spin_cycles = int(probe * 30.0 / max(s0.elapsed_time(s1), 1e-3))
+
     # timed region: plain steps
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spin(spin_cycles)
     e0.record(stream)
     for _ in range(args.steps):
         step()
@@ -233,6 +254,7 @@ def main():
 
     # second timed pass with an event after every library call
     timing["on"] = True
+    spin(spin_cycles)
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
@@ -249,7 +271,7 @@ def main():
     calls = {}
     for label, ts in per.items():
         avg_ms = sum(ts) / len(ts)
-        c = call_cost(label, wl, o_bytes)
+        c = call_cost(label, wl, o_bytes, args.stride)
         ent = {"avg_us": round(avg_ms * 1e3, 2), "launches": len(ts) // args.steps, "bound": c["bound"],
                "share": round(sum(ts) / args.steps / serial_ms, 3)}
         if c["bound"] == "hbm":
@@ -272,13 +294,14 @@ def main():
         calls[label] = ent
     dom = max(calls, key=lambda k: calls[k]["avg_us"] * calls[k]["launches"])
     dc = calls[dom]
-    traffic = load_traffic(dom, wl.key + ("_inference" if args.inference else ""), src_hash)
+    traffic = load_traffic(dom, wl.key + ("_inference" if args.inference else "")
+                           + (f"_stride{args.stride}" if args.stride > 1 else ""), src_hash)
     roofline = {"bound": dc["bound"], "achieved": dc["achieved"], "peak": dc["peak"], "unit": dc["unit"],
                 "frac": dc["frac"], "traffic": traffic, "kernel": dom, "avg_us": dc["avg_us"],
                 "per_launch": ("algo_bytes=%d" % dc["algo_bytes"]) if dc["bound"] == "hbm"
                 else ("algo_flops=%d" % dc["algo_flops"])}
 
-    pix_box = wl.pixel_box * wl.layers
+    pix_box = wl.N * wl.C * wl.B * st.plans[0].Ho * st.plans[0].Wo * wl.layers
     value = pix_box / (ms * 1e-3) / 1e9
     box_ms = sum(calls[k]["avg_us"] * calls[k]["launches"] for k in calls if k.startswith("box")) / 1e3
     line = {
@@ -291,7 +314,7 @@ def main():
                    "mix": None if wl.mix_out is None else f"{wl.C * wl.B}->{wl.mix_out} {wl.mix_dtype}",
                    "layers": wl.layers, "relu": wl.relu, "mean_offset": wl.mean_offset,
                    "integer_corners": bool(args.inference), "backward": backward,
-                   "overlap_weight_grad": backward and not args.serial,
+                   "overlap_weight_grad": backward and not args.serial, "stride": args.stride,
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
         "roofline": roofline,
@@ -300,7 +323,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference)
+        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference, args.stride)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -183,6 +183,28 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * box_conv_fwd_strided / box_conv_bwd_strided -- the same layer with an
+ * integer stride (Section 3.1 assumes an integer stride: shifting a box by
+ * whole pixels leaves its interpolation weights unchanged).  Output pixel
+ * (i, j) is the box placed at input pixel (stride*i, stride*j):
+ *   y      : [N][C*B][Ho][Wo], Ho = ceil(H/stride), Wo = ceil(W/stride);
+ *   grad_y : the same shape; the gradients are those of the strided layer
+ *            (the backward tabulates grad_y placed at every stride-th pixel,
+ *            zeros elsewhere: the transpose of the sampling).
+ * stride : 1 .. 1024 (BC_ERR_SHAPE otherwise); stride 1 is box_conv_fwd /
+ *          box_conv_bwd.  Every other argument, flag and workspace size is
+ *          as for those calls (the workspace query takes the input size).
+ * ---------------------------------------------------------------------- */
+bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes,
+                               int N, int C, int H, int W, int B, int stride,
+                               void* y, bc_dtype y_dt, unsigned flags,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* grad_y,
+                               int N, int C, int H, int W, int B, int stride,
+                               float* grad_x, float* grad_boxes, unsigned flags,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pointwise_mix -- the 1x1 convolution over the C*B filtered maps
  * (Section 1, Section 3.2), per image n with P = H*W pixels, on MFMA:
  *   BC_MIX_FWD        : a = w [M][K], b = in [N][K][P]   -> out [N][M][P]

@@ -6,7 +6,8 @@ kernels.  The library is required: if it is not built, or a GPU is not
 present, the calls raise -- there is no fallback implementation.
 
 Entry points (same names as the C ABI): box_prep, sat_build, box_conv_fwd,
-box_conv_bwd, pointwise_mix, plus the workspace-size queries.
+box_conv_bwd, box_conv_fwd_strided, box_conv_bwd_strided, pointwise_mix, plus
+the workspace-size queries.
 """
 from __future__ import annotations
 
@@ -31,6 +32,8 @@ SIGNATURES = {
     "sat_build": (_i, [_vp, _i, _vp, _vp, _i, _i, _i, _i, _vp]),
     "box_conv_fwd": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
     "box_conv_bwd": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
+    "box_conv_fwd_strided": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
+    "box_conv_bwd_strided": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
     "pointwise_mix": (_i, [_i, _vp, _i, _vp, _i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
@@ -122,29 +125,59 @@ def sat_build(x: torch.Tensor, sat: torch.Tensor, mean: torch.Tensor | None = No
     return sat
 
 
+def _strided_shape(N, C, H, W, B, stride):
+    return (N, C * B, (H + stride - 1) // stride, (W + stride - 1) // stride)
+
+
 def box_conv_fwd(x: torch.Tensor, boxes: torch.Tensor, y: torch.Tensor, flags: int = 0,
-                 ws: torch.Tensor | None = None):
-    """x [N, C, H, W], boxes [C, B, 4] fp32 -> y [N, C*B, H, W] (int32, fp32 or bf16)."""
+                 ws: torch.Tensor | None = None, stride: int = 1):
+    """x [N, C, H, W], boxes [C, B, 4] fp32 -> y [N, C*B, ceil(H/stride), ceil(W/stride)]
+    (int32, fp32 or bf16); stride > 1 calls box_conv_fwd_strided."""
     N, C, H, W = x.shape
     B = boxes.shape[1]
+    if tuple(y.shape) != _strided_shape(N, C, H, W, B, stride):
+        raise BoxConvError(f"box_conv_fwd: y has shape {tuple(y.shape)}")
     if ws is None:
         ws = _workspace(box_workspace_bytes(0, N, C, H, W, B, flags), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load_library().box_conv_fwd(_ptr(x), dtype_code(x), _ptr(boxes), N, C, H, W, B, _ptr(y),
-                                       dtype_code(y), flags, _ptr(ws), nbytes, _stream()), "box_conv_fwd")
+    lib = load_library()
+    if stride == 1:
+        st = lib.box_conv_fwd(_ptr(x), dtype_code(x), _ptr(boxes), N, C, H, W, B, _ptr(y), dtype_code(y), flags,
+                              _ptr(ws), nbytes, _stream())
+    else:
+        st = lib.box_conv_fwd_strided(_ptr(x), dtype_code(x), _ptr(boxes), N, C, H, W, B, stride, _ptr(y),
+                                      dtype_code(y), flags, _ptr(ws), nbytes, _stream())
+    _check(st, "box_conv_fwd")
     return y
 
 
+def box_conv_fwd_strided(x, boxes, stride: int, y, flags: int = 0, ws=None):
+    return box_conv_fwd(x, boxes, y, flags, ws, stride)
+
+
 def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, grad_x: torch.Tensor | None,
-                 grad_boxes: torch.Tensor | None, flags: int = 0, ws: torch.Tensor | None = None):
+                 grad_boxes: torch.Tensor | None, flags: int = 0, ws: torch.Tensor | None = None, stride: int = 1):
+    """grad_y [N, C*B, ceil(H/stride), ceil(W/stride)]; stride > 1 calls box_conv_bwd_strided."""
     N, C, H, W = x.shape
     B = boxes.shape[1]
+    if tuple(grad_y.shape) != _strided_shape(N, C, H, W, B, stride):
+        raise BoxConvError(f"box_conv_bwd: grad_y has shape {tuple(grad_y.shape)}")
     if ws is None:
         ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load_library().box_conv_bwd(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, _ptr(grad_x),
-                                       _ptr(grad_boxes), flags, _ptr(ws), nbytes, _stream()), "box_conv_bwd")
+    lib = load_library()
+    if stride == 1:
+        st = lib.box_conv_bwd(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, _ptr(grad_x), _ptr(grad_boxes),
+                              flags, _ptr(ws), nbytes, _stream())
+    else:
+        st = lib.box_conv_bwd_strided(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, stride, _ptr(grad_x),
+                                      _ptr(grad_boxes), flags, _ptr(ws), nbytes, _stream())
+    _check(st, "box_conv_bwd")
     return grad_x, grad_boxes
+
+
+def box_conv_bwd_strided(x, boxes, grad_y, stride: int, grad_x, grad_boxes, flags: int = 0, ws=None):
+    return box_conv_bwd(x, boxes, grad_y, grad_x, grad_boxes, flags, ws, stride)
 
 
 def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):

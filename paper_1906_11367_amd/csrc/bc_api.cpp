@@ -10,6 +10,7 @@ namespace {
 
 constexpr size_t kAlign = 256;           // workspace sub-buffer alignment
 constexpr size_t kLdsBudget = 64 * 1024; // LDS per block for the table paths
+constexpr int kMaxStride = 1024;
 constexpr long kMaxDim = 1 << 16;
 
 inline size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
@@ -120,10 +121,11 @@ size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigne
   return 0;
 }
 
-bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
-                       void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
+                               int stride, void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
   if (!x || !boxes || !y) return BC_ERR_NULL;
-  if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  if (!dims_ok(N, C, H, W, B) || stride < 1 || stride > kMaxStride) return BC_ERR_SHAPE;
   if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM | BC_FLAG_INTEGER_CORNERS)) return BC_ERR_UNSUPPORTED;
   const bool is_int = x_dt == BC_I32;
   const bool rounded = (flags & BC_FLAG_INTEGER_CORNERS) != 0;
@@ -145,19 +147,24 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, 
   if (e != hipSuccess) return BC_ERR_HIP;
   if (!hbm)
     return hip_status(
-        bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, rounded, stream));
+        bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, rounded, stride, stream));
   float* means = offset ? reinterpret_cast<float*>(base + L.means) : nullptr;
   e = bc::launch_sat_build(x, is_int, base + L.sat, means, N * C, H, W, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  return hip_status(
-      bc::launch_box_fwd_gather(base + L.sat, is_int, means, taps, y, out_kind, N, C, H, W, B, rounded, stream));
+  return hip_status(bc::launch_box_fwd_gather(base + L.sat, is_int, means, taps, y, out_kind, N, C, H, W, B, rounded,
+                                              stride, stream));
 }
 
-bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,
-                       float* grad_x, float* grad_boxes, unsigned flags, void* ws, size_t ws_bytes,
-                       hipStream_t stream) {
+bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
+                       void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return box_conv_fwd_strided(x, x_dt, boxes, N, C, H, W, B, 1, y, y_dt, flags, ws, ws_bytes, stream);
+}
+
+bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W,
+                               int B, int stride, float* grad_x, float* grad_boxes, unsigned flags, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
   if (!x || !boxes || !grad_y) return BC_ERR_NULL;
-  if (!dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  if (!dims_ok(N, C, H, W, B) || stride < 1 || stride > kMaxStride) return BC_ERR_SHAPE;
   if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM | BC_FLAG_INTEGER_CORNERS)) return BC_ERR_UNSUPPORTED;
   const bool rounded = (flags & BC_FLAG_INTEGER_CORNERS) != 0;
   // rounding the corners is not differentiable: with rounded corners the
@@ -181,16 +188,23 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
   if (!hbm) {
-    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, stream);
+    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, stride, stream);
   } else {
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
-    e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
+    e = stride == 1 ? bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream)
+                    : bc::launch_sat_build_up(grad_y, sat_g, N * C * B, H, W, stride, stream);
     if (e == hipSuccess)
       e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, rounded, stream);
   }
   if (e != hipSuccess) return BC_ERR_HIP;
   if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);
   return hip_status(e);
+}
+
+bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,
+                       float* grad_x, float* grad_boxes, unsigned flags, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  return box_conv_bwd_strided(x, boxes, grad_y, N, C, H, W, B, 1, grad_x, grad_boxes, flags, ws, ws_bytes, stream);
 }
 
 bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream) {

@@ -90,6 +90,36 @@ __device__ __forceinline__ void table_row_pass(T* S, int H, int W, int pitch) {
   }
 }
 
+// Column pass (lanes own columns) and row pass of a padded LDS table whose
+// interior holds the map, each reading kScan elements ahead before it writes.
+template <typename T>
+__device__ __forceinline__ void table_scans(T* S, int H, int W, int pitch) {
+  constexpr int kScan = 16;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  T* R = S + kPad;
+  for (int v = tid + 1; v <= W; v += nt) {
+    T run = (T)0;
+    int u = 1;
+    for (; u + kScan - 1 <= H; u += kScan) {
+      T r[kScan];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) r[k] = R[(u + k) * pitch + v];
+#pragma unroll
+      for (int k = 0; k < kScan; ++k) {
+        run += r[k];
+        R[(u + k) * pitch + v] = run;
+      }
+    }
+    for (; u <= H; ++u) {
+      run += R[u * pitch + v];
+      R[u * pitch + v] = run;
+    }
+  }
+  __syncthreads();
+  table_row_pass(S, H, W, pitch);
+  __syncthreads();
+}
+
 // Exclusive table of one H x W map in LDS, padded (LdsTable): S(u, v) at
 // S[u * pitch + kPad + v].  The map is first copied into the table's interior
 // with every thread issuing 16-byte loads in batches (the loads of a batch are
@@ -100,7 +130,7 @@ __device__ __forceinline__ void table_row_pass(T* S, int H, int W, int pitch) {
 template <typename T>
 __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch, float mu, bool sub) {
   using V = typename Vec4<T>::type;
-  constexpr int kBatch = 8, kScan = 16;
+  constexpr int kBatch = 8;
   const int tid = threadIdx.x, nt = blockDim.x;
   T* R = S + kPad;
   table_zero_edges(S, H, pitch);
@@ -143,27 +173,25 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
     }
   }
   __syncthreads();
-  for (int v = tid + 1; v <= W; v += nt) {
-    T run = (T)0;
-    int u = 1;
-    for (; u + kScan - 1 <= H; u += kScan) {
-      T r[kScan];
-#pragma unroll
-      for (int k = 0; k < kScan; ++k) r[k] = R[(u + k) * pitch + v];
-#pragma unroll
-      for (int k = 0; k < kScan; ++k) {
-        run += r[k];
-        R[(u + k) * pitch + v] = run;
-      }
-    }
-    for (; u <= H; ++u) {
-      run += R[u * pitch + v];
-      R[u * pitch + v] = run;
-    }
+  table_scans(S, H, W, pitch);
+}
+
+// Table of a zero-upsampled fp32 map (the transpose of sampling every s-th
+// pixel): src (Ho x Wo) placed at (s*i, s*j) of an H x W map, zeros
+// elsewhere; s * (Ho - 1) < H and s * (Wo - 1) < W.
+__device__ void build_table_lds_up(const float* __restrict__ src, float* S, int H, int W, int pitch, int s, int Ho,
+                                   int Wo) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  float* R = S + kPad;
+  table_zero_edges(S, H, pitch);
+  for (int k = tid; k < H * pitch; k += nt) S[pitch + k] = 0.f;  // rows 1..H
+  __syncthreads();
+  for (int k = tid; k < Ho * Wo; k += nt) {
+    const int i = k / Wo, j = k - i * Wo;
+    R[(s * i + 1) * pitch + s * j + 1] = src[k];
   }
   __syncthreads();
-  table_row_pass(S, H, W, pitch);
-  __syncthreads();
+  table_scans(S, H, W, pitch);
 }
 
 // ---------------------------------------------------------------------------
@@ -259,6 +287,70 @@ __device__ __forceinline__ void box_walk_int(const Src& S, const Taps<T>& tp, in
     }
   }
 }
+
+// Strided forward walk of one item: output column j (input column x = s*j)
+// and output rows i0 .. i1-1 (input rows s*i).  Consecutive outputs are s
+// rows apart and share no table rows, so each output reads its own: two rows
+// per y edge (one with integer corners), runs of two columns (one) at both x
+// edges -- the 16 (4) samples of Eq. 2-3.  emit.put(k, o) for output row
+// i0 + k.  With kOffset the table holds the map minus mu, and mu * (clipped
+// area) is added back.
+template <int SEGS, typename T, bool kOffset, bool kInt, typename Src, typename Emit>
+__device__ __forceinline__ void box_walk_strided(const Src& S, const Taps<T>& tp, int H, int W, int x, int i0,
+                                                 int i1, int s, float mu, Emit& emit) {
+  const int ba = x + tp.ox[0], bb = x + tp.ox[2];
+  const typename Src::Cols cl = S.cols(ba, bb);
+  const int st = S.row_step();
+  float ex = 0.f;
+  if (kOffset) {
+    ex = kInt ? (float)(clampi(bb, 0, W) - clampi(ba, 0, W))
+              : (float)tp.wx[0] * (float)clampi(ba, 0, W) + (float)tp.wx[1] * (float)clampi(ba + 1, 0, W) +
+                    (float)tp.wx[2] * (float)clampi(bb, 0, W) + (float)tp.wx[3] * (float)clampi(bb + 1, 0, W);
+  }
+#pragma unroll
+  for (int k = 0; k < SEGS; ++k) {
+    const int i = i0 + k;
+    if (i < i1) {
+      const int y = s * i;
+      const int rc = S.row_coord(y + tp.oy[0]), rd = S.row_coord(y + tp.oy[2]);
+      T o;
+      if constexpr (kInt) {
+        T ca[1], cb[1], da[1], db[1];
+        S.template runs<1>(rc, cl, ca, cb);
+        S.template runs<1>(rd, cl, da, db);
+        o = (db[0] - da[0]) - (cb[0] - ca[0]);
+      } else {
+        T u[4];
+        const int rows[4] = {rc, rc + st, rd, rd + st};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          T sa[2], sb[2];
+          S.template runs<2>(rows[r], cl, sa, sb);
+          u[r] = tp.wx[0] * sa[0] + tp.wx[1] * sa[1] + tp.wx[2] * sb[0] + tp.wx[3] * sb[1];
+        }
+        o = tp.wy[0] * u[0] + tp.wy[1] * u[1] + tp.wy[2] * u[2] + tp.wy[3] * u[3];
+      }
+      if (kOffset) {
+        const float ey = kInt ? (float)(clampi(y + tp.oy[2], 0, H) - clampi(y + tp.oy[0], 0, H))
+                              : (float)tp.wy[0] * (float)clampi(y + tp.oy[0], 0, H) +
+                                    (float)tp.wy[1] * (float)clampi(y + tp.oy[1], 0, H) +
+                                    (float)tp.wy[2] * (float)clampi(y + tp.oy[2], 0, H) +
+                                    (float)tp.wy[3] * (float)clampi(y + tp.oy[3], 0, H);
+        o = o + (T)(mu * (ex * ey));
+      }
+      emit.put(k, o);
+    }
+  }
+}
+
+// Emitter of one strided output column: output row i0 + k at plane offset
+// off0 + k * Wo (off0 = i0 * Wo + j).
+template <typename OutT, typename T>
+struct StoreCol {
+  OutT* out;
+  int Wo, off0;
+  __device__ __forceinline__ void put(int k, T o) { out[(unsigned)(off0 + k * Wo)] = convert_out<OutT, T>(o); }
+};
 
 // Forward walk of one item: integer-corner or interpolated.
 template <int SEG, typename T, bool kOffset, bool kFull, bool kInt, typename Src, typename Emit>
@@ -406,14 +498,16 @@ __global__ void k_box_prep(const float* __restrict__ boxes, int CB, int rounded,
 constexpr int kStrip = 16;
 constexpr int kSatMaxK = 16;  // elements per lane in a row scan: W <= 1024
 
-template <typename T>
+// kUp: x is [maps][Ho][Wo] and the table is that of its zero-upsampled H x W
+// map (x[i][j] at (s*i, s*j)); mean must then be null.
+template <typename T, bool kUp>
 __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* __restrict__ sat,
-                                                   float* __restrict__ mean, int H, int W) {
+                                                   float* __restrict__ mean, int H, int W, int s, int Ho, int Wo) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);
   __shared__ float red[16];
   const int map = blockIdx.x;
-  const T* src = x + (size_t)map * H * W;
+  const T* src = x + (size_t)map * (kUp ? (size_t)Ho * Wo : (size_t)H * W);
   T* dst = sat + (size_t)map * (H + 1) * (W + 1);
   float mu = 0.f;
   const bool sub = mean != nullptr;
@@ -430,14 +524,18 @@ __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* _
   for (int r0 = 0; r0 < H; r0 += kStrip) {
     const int rows = min(kStrip, H - r0);
     for (int rr = wave; rr < rows; rr += nw) {
-      const T* row = src + (size_t)(r0 + rr) * W;
+      const int r = r0 + rr;
+      const T* row = kUp ? src + (size_t)(r / s) * Wo : src + (size_t)r * W;
+      const bool live = !kUp || r % s == 0;
       T v[kSatMaxK];
       T run = (T)0;
 #pragma unroll
       for (int k = 0; k < kSatMaxK; ++k) {
         if (k < K) {
           const int idx = lane * K + k;
-          T val = idx < W ? row[idx] : (T)0;
+          T val;
+          if constexpr (kUp) val = (live && idx < W && idx % s == 0) ? row[idx / s] : (T)0;
+          else val = idx < W ? row[idx] : (T)0;
           if (sub && idx < W) val = (T)((float)val - mu);
           run += val;
           v[k] = run;
@@ -542,6 +640,70 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   else walk_fwd<SEG, T, kOffset, false, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
 
+// Strided forward (stride s > 1) on a map's table in LDS, boxes b0 .. b0+nb-1
+// of channel c: items are (output column, segment of kSegS output rows),
+// column fastest; a box's items are padded to per_box_p (a multiple of 64)
+// so each wave serves one box.
+constexpr int kSegS = 8;
+template <typename T, typename OutT, bool kOffset, bool kInt>
+__device__ __forceinline__ void fwd_boxes_strided(const LdsTable<T>& tab, const int* __restrict__ taps,
+                                                  OutT* __restrict__ y, int map, int c, int b0, int nb, int H, int W,
+                                                  int B, int s, int Ho, int Wo, int per_box_p, float mu) {
+  const int per_box = Wo * ((Ho + kSegS - 1) / kSegS);
+  for (int it = threadIdx.x; it < nb * per_box_p; it += blockDim.x) {
+    const int bl = __builtin_amdgcn_readfirstlane(it / per_box_p);
+    const int r = it - bl * per_box_p;
+    if (r >= per_box) continue;
+    const int seg = r / Wo, j = r - seg * Wo;
+    const int b = b0 + bl;
+    const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
+    const int i0 = seg * kSegS;
+    StoreCol<OutT, T> em{y + ((size_t)map * B + b) * Ho * Wo, Wo, i0 * Wo + j};
+    box_walk_strided<kSegS, T, kOffset, kInt>(tab, tp, H, W, s * j, i0, min(i0 + kSegS, Ho), s, mu, em);
+  }
+}
+
+template <typename T, typename OutT, bool kOffset, bool kInt>
+__global__ __launch_bounds__(256) void k_box_fwd_lds_strided(const T* __restrict__ x, const int* __restrict__ taps,
+                                                             OutT* __restrict__ y, int C, int H, int W, int B, int s,
+                                                             int Ho, int Wo, int bpg, int per_box_p) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  T* S = reinterpret_cast<T*>(smem_raw);
+  __shared__ float red[16];
+  const int pitch = lds_pitch_dev(W);
+  const int ngrp = (B + bpg - 1) / bpg;
+  const int map = blockIdx.x / ngrp, grp = blockIdx.x - map * ngrp;
+  const T* src = x + (size_t)map * H * W;
+  float mu = 0.f;
+  if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
+  build_table_lds(src, S, H, W, pitch, mu, kOffset);
+  const int b0 = grp * bpg;
+  fwd_boxes_strided<T, OutT, kOffset, kInt>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0,
+                                            min(bpg, B - b0), H, W, B, s, Ho, Wo, per_box_p, mu);
+}
+
+// Strided forward, table in HBM: one block per (map, box, block of 256 items).
+template <typename T, typename OutT, bool kOffset, bool kInt>
+__global__ __launch_bounds__(256) void k_box_fwd_gather_strided(const T* __restrict__ sat,
+                                                                const float* __restrict__ means,
+                                                                const int* __restrict__ taps, OutT* __restrict__ y,
+                                                                int C, int H, int W, int B, int s, int Ho, int Wo,
+                                                                int nblk, int total) {
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= total) return;
+  const int blk = L % nblk, mb = L / nblk;
+  const int b = mb % B, map = mb / B, c = map % C;
+  const int it = blk * 256 + threadIdx.x;
+  if (it >= Wo * ((Ho + kSegS - 1) / kSegS)) return;
+  const int seg = it / Wo, j = it - seg * Wo;
+  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
+  const float mu = kOffset ? means[map] : 0.f;
+  const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
+  const int i0 = seg * kSegS;
+  StoreCol<OutT, T> em{y + ((size_t)map * B + b) * Ho * Wo, Wo, i0 * Wo + j};
+  box_walk_strided<kSegS, T, kOffset, kInt>(tab, tp, H, W, s * j, i0, min(i0 + kSegS, Ho), s, mu, em);
+}
+
 // Map values of one item, 0 outside the map (they then add nothing to the
 // parameter gradients).
 template <int SEG>
@@ -586,11 +748,14 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // the input gradient (in registers, summed over b) and the edge gradients;
 // each wave writes its edge-gradient sums to
 // partials[(n * nw + wave) * C*B + c*B + b][4].  kInt (boxes with integer
-// corners): the adjoint four-corner sums only, no edge gradients.
-template <int SEG, bool kInt>
+// corners): the adjoint four-corner sums only, no edge gradients.  kUp
+// (stride s > 1): grad_y is [maps][Ho][Wo] and is tabulated zero-upsampled,
+// which makes every gradient that of the strided layer.
+template <int SEG, bool kInt, bool kUp>
 __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
                                                      const float* __restrict__ gy, float* __restrict__ gx,
-                                                     float* __restrict__ partials, int C, int H, int W, int B) {
+                                                     float* __restrict__ partials, int C, int H, int W, int B,
+                                                     int s, int Ho, int Wo) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -603,7 +768,8 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
   const bool full = y0 + SEG <= H && x0 + kQ <= W;
   const size_t plane = (size_t)H * W;
-  const float* g0 = gy + (size_t)map * B * plane;
+  const size_t gplane = kUp ? (size_t)Ho * Wo : plane;
+  const float* g0 = gy + (size_t)map * B * gplane;
   float v[SEG][kQ], acc[SEG][kQ];
   if constexpr (!kInt) load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
 #pragma unroll
@@ -614,7 +780,8 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x
   const int* adj = taps + (size_t)C * B * 16;
   for (int b = 0; b < B; ++b) {
     __syncthreads();
-    build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
+    if constexpr (kUp) build_table_lds_up(g0 + b * gplane, SG, H, W, pitch, s, Ho, Wo);
+    else build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
     const Taps<float> tp = load_taps(adj + (size_t)(c * B + b) * 16, W, H);
     if constexpr (kInt) {  // integer corners: input gradient only
       AccRows<SEG> em{acc};
@@ -752,17 +919,26 @@ hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, 
                             hipStream_t s) {
   const size_t shm = (size_t)kStrip * W * 4;
   if (is_int)
-    hipLaunchKernelGGL(k_sat_build<int>, dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat, (float*)nullptr, H, W);
+    hipLaunchKernelGGL((k_sat_build<int, false>), dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat,
+                       (float*)nullptr, H, W, 1, H, W);
   else
-    hipLaunchKernelGGL(k_sat_build<float>, dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat, mean, H, W);
+    hipLaunchKernelGGL((k_sat_build<float, false>), dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat, mean,
+                       H, W, 1, H, W);
+  return last_error();
+}
+
+hipError_t launch_sat_build_up(const float* x, float* sat, int maps, int H, int W, int stride, hipStream_t s) {
+  const size_t shm = (size_t)kStrip * W * 4;
+  const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
+  hipLaunchKernelGGL((k_sat_build<float, true>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H, W, stride,
+                     Ho, Wo);
   return last_error();
 }
 
 // Forward launch geometry shared by both LDS kernels.
 struct FwdGeom { int per_box_p, bpg, ngrp, threads; };
-static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
+static FwdGeom fwd_geom_items(int N, int C, int B, int per_box) {
   FwdGeom g;
-  const int per_box = n_chunks(W) * n_segs(H, seg);
   g.per_box_p = ((per_box + 63) / 64) * 64;
   g.bpg = 256 / g.per_box_p;
   if (g.bpg < 1) g.bpg = 1;
@@ -773,70 +949,98 @@ static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
   g.threads = min(g.bpg * g.per_box_p, 256);
   return g;
 }
+static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
+  return fwd_geom_items(N, C, B, n_chunks(W) * n_segs(H, seg));
+}
 
 template <typename T, typename OutT, bool kOffset>
 static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int H, int W, int B, bool rounded,
-                      hipStream_t s) {
+                      int stride, hipStream_t s) {
   constexpr int SEG = 16;
-  const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
+  if (stride == 1) {
+    const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
+    with_flag(rounded, [&](auto ki) {
+      hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
+                         dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+    });
+    return;
+  }
+  const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
+  const FwdGeom g = fwd_geom_items(N, C, B, Wo * ((Ho + kSegS - 1) / kSegS));
   with_flag(rounded, [&](auto ki) {
-    hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
-                       dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+    hipLaunchKernelGGL((k_box_fwd_lds_strided<T, OutT, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
+                       dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, stride, Ho, Wo, g.bpg,
+                       g.per_box_p);
   });
 }
 
 hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void* y, int out_kind, int N, int C,
-                              int H, int W, int B, bool offset, bool rounded, hipStream_t s) {
+                              int H, int W, int B, bool offset, bool rounded, int stride, hipStream_t s) {
   if (is_int) {
-    fwd_lds_t<int, int, false>(x, taps, y, N, C, H, W, B, rounded, s);
+    fwd_lds_t<int, int, false>(x, taps, y, N, C, H, W, B, rounded, stride, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_lds_t<float, uint16_t, true>(x, taps, y, N, C, H, W, B, rounded, s);
-    else fwd_lds_t<float, uint16_t, false>(x, taps, y, N, C, H, W, B, rounded, s);
+    if (offset) fwd_lds_t<float, uint16_t, true>(x, taps, y, N, C, H, W, B, rounded, stride, s);
+    else fwd_lds_t<float, uint16_t, false>(x, taps, y, N, C, H, W, B, rounded, stride, s);
   } else {
-    if (offset) fwd_lds_t<float, float, true>(x, taps, y, N, C, H, W, B, rounded, s);
-    else fwd_lds_t<float, float, false>(x, taps, y, N, C, H, W, B, rounded, s);
+    if (offset) fwd_lds_t<float, float, true>(x, taps, y, N, C, H, W, B, rounded, stride, s);
+    else fwd_lds_t<float, float, false>(x, taps, y, N, C, H, W, B, rounded, stride, s);
   }
   return last_error();
 }
 
 template <typename T, typename OutT, bool kOffset>
 static void fwd_gather_t(const void* sat, const float* means, const int* taps, void* y, int N, int C, int H, int W,
-                         int B, bool rounded, hipStream_t s) {
+                         int B, bool rounded, int stride, hipStream_t s) {
   constexpr int SEG = 16;
-  const int items = n_chunks(W) * n_segs(H, SEG);
-  const int nblk = (items + 255) / 256;
+  if (stride == 1) {
+    const int items = n_chunks(W) * n_segs(H, SEG);
+    const int nblk = (items + 255) / 256;
+    const int total = N * C * B * nblk;
+    with_flag(rounded, [&](auto ki) {
+      hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(pad8(total)),
+                         dim3(256), 0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
+    });
+    return;
+  }
+  const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
+  const int nblk = (Wo * ((Ho + kSegS - 1) / kSegS) + 255) / 256;
   const int total = N * C * B * nblk;
   with_flag(rounded, [&](auto ki) {
-    hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(pad8(total)), dim3(256),
-                       0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
+    hipLaunchKernelGGL((k_box_fwd_gather_strided<T, OutT, kOffset, decltype(ki)::value>), dim3(pad8(total)),
+                       dim3(256), 0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, stride, Ho, Wo, nblk,
+                       total);
   });
 }
 
 hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const int* taps, void* y,
-                                 int out_kind, int N, int C, int H, int W, int B, bool rounded, hipStream_t s) {
+                                 int out_kind, int N, int C, int H, int W, int B, bool rounded, int stride,
+                                 hipStream_t s) {
   const bool offset = means != nullptr;
   if (is_int) {
-    fwd_gather_t<int, int, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
+    fwd_gather_t<int, int, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, stride, s);
   } else if (out_kind == 2) {
-    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, taps, y, N, C, H, W, B, rounded, s);
-    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
+    if (offset) fwd_gather_t<float, uint16_t, true>(sat, means, taps, y, N, C, H, W, B, rounded, stride, s);
+    else fwd_gather_t<float, uint16_t, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, stride, s);
   } else {
-    if (offset) fwd_gather_t<float, float, true>(sat, means, taps, y, N, C, H, W, B, rounded, s);
-    else fwd_gather_t<float, float, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, s);
+    if (offset) fwd_gather_t<float, float, true>(sat, means, taps, y, N, C, H, W, B, rounded, stride, s);
+    else fwd_gather_t<float, float, false>(sat, nullptr, taps, y, N, C, H, W, B, rounded, stride, s);
   }
   return last_error();
 }
 
 template <int SEG>
 static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N, int C,
-                      int H, int W, int B, bool rounded, hipStream_t s) {
+                      int H, int W, int B, bool rounded, int stride, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int threads = ((items + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
+  const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   with_flag(rounded, [&](auto ki) {
-    hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value>), dim3(N * C), dim3(threads), shm, s, x, taps, gy,
-                       gx, partials, C, H, W, B);
+    with_flag(stride > 1, [&](auto ku) {
+      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value>), dim3(N * C), dim3(threads),
+                         shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
+    });
   });
 }
 
@@ -854,10 +1058,10 @@ int box_bwd_lds_waves(int H, int W) {
 }
 
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N,
-                              int C, int H, int W, int B, bool rounded, hipStream_t s) {
+                              int C, int H, int W, int B, bool rounded, int stride, hipStream_t s) {
   const int seg = box_bwd_lds_seg(H, W);
-  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, s);
-  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, s);
+  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
   else return hipErrorInvalidValue;
   return last_error();
 }

@@ -24,24 +24,32 @@ inline size_t tap_table_bytes(int C, int B) { return (size_t)2 * C * B * 16 * 4;
 
 hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean,
                             int maps, int H, int W, hipStream_t s);
+// Tables of zero-upsampled maps: x [maps][ceil(H/stride)][ceil(W/stride)]
+// placed at every stride-th pixel of an H x W map (stride > 1).
+hipError_t launch_sat_build_up(const float* x, float* sat, int maps, int H, int W, int stride, hipStream_t s);
 
 // Forward, table in LDS.  out_kind: 0 = same type as x, 1 = fp32, 2 = bf16.
+// stride > 1: y is [N][C*B][ceil(H/stride)][ceil(W/stride)].
 hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void* y, int out_kind,
-                              int N, int C, int H, int W, int B, bool offset, bool rounded, hipStream_t s);
+                              int N, int C, int H, int W, int B, bool offset, bool rounded, int stride,
+                              hipStream_t s);
 // Forward, table read from HBM (built beforehand by sat_build into `sat`).
 hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* means, const int* taps,
                                  void* y, int out_kind, int N, int C, int H, int W, int B, bool rounded,
-                                 hipStream_t s);
+                                 int stride, hipStream_t s);
 
 // Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
 // LDS path: one block of box_bwd_lds_waves() waves per map, P = N * waves;
 // box_bwd_lds_seg() == 0 means the map has too many items for one block.
-// rounded: input gradient only (partials unused).
+// rounded: input gradient only (partials unused).  stride > 1: gy is
+// [N][C*B][ceil(H/stride)][ceil(W/stride)] (tabulated zero-upsampled).
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx,
-                              float* partials, int N, int C, int H, int W, int B, bool rounded, hipStream_t s);
+                              float* partials, int N, int C, int H, int W, int B, bool rounded, int stride,
+                              hipStream_t s);
 int box_bwd_lds_seg(int H, int W);
 int box_bwd_lds_waves(int H, int W);
-// HBM path: tables of every gradient map in sat_g (built by sat_build);
+// HBM path: tables of every gradient map in sat_g (built by sat_build, or
+// sat_build_up for stride > 1);
 // P = N * box_bwd_gather_blocks() * 4.
 int box_bwd_gather_blocks(int H, int W);
 hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx,

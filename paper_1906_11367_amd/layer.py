@@ -36,12 +36,15 @@ class LayerPlan:
     with_backward: bool = True
     device: str = "cuda"
     overlap: bool = True       # weight gradient on a second stream during the backward
+    stride: int = 1            # box filter stride: outputs ceil(H/stride) x ceil(W/stride)
 
     def __post_init__(self):
         dev = torch.device(self.device)
         N, C, H, W, B = self.N, self.C, self.H, self.W, self.B
+        Ho, Wo = (H + self.stride - 1) // self.stride, (W + self.stride - 1) // self.stride
+        self.Ho, self.Wo = Ho, Wo
         K = C * B
-        P = H * W
+        P = Ho * Wo
         self.K, self.P = K, P
         integer = self.x_dtype == torch.int32
         if integer:
@@ -50,11 +53,11 @@ class LayerPlan:
             o_dt = torch.bfloat16
         else:
             o_dt = torch.float32
-        self.o = torch.empty((N, K, H, W), dtype=o_dt, device=dev)
+        self.o = torch.empty((N, K, Ho, Wo), dtype=o_dt, device=dev)
         self.compute = bc.BC_BF16 if self.mix_dtype == "bf16" else bc.BC_F32
         self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
         if self.M is not None:
-            self.z = torch.empty((N, self.M, H, W), dtype=torch.int32 if integer else torch.float32, device=dev)
+            self.z = torch.empty((N, self.M, Ho, Wo), dtype=torch.int32 if integer else torch.float32, device=dev)
             # the mix's weights in its compute type, refreshed from w every forward
             self.w_c = (torch.empty((self.M, K), dtype=torch.bfloat16, device=dev)
                         if self.compute == bc.BC_BF16 else None)
@@ -63,7 +66,7 @@ class LayerPlan:
             self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
             self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
             if self.M is not None:
-                self.do = torch.empty((N, K, H, W), dtype=torch.float32, device=dev)
+                self.do = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=dev)
                 self.dw = torch.empty((self.M, K), dtype=torch.float32, device=dev)
                 self.ws_mixw = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, N, self.M, K, P,
                                                           self.compute), dev)
@@ -75,7 +78,7 @@ class LayerPlan:
         """tap(label), if given, is called after each library call (the benchmark
         records a stream event there)."""
         tap = tap or _no_tap
-        bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd)
+        bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd, stride=self.stride)
         tap("box_conv_fwd")
         if self.M is None:
             return self.o
@@ -121,11 +124,12 @@ class LayerPlan:
             tap("mix_bwd_data")
             do = self.do
             dw = self.dw
-        bc.box_conv_bwd(x, boxes, do, self.dx, self.dboxes, self.flags, self.ws_bwd)
+        grad_boxes = None if self.flags & bc.BC_FLAG_INTEGER_CORNERS else self.dboxes
+        bc.box_conv_bwd(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
         tap("box_conv_bwd")
         if self.M is not None and overlap:
             main.wait_event(self.ev_dw)         # dW (and the reuse of O, dZ) ordered after the side stream
-        return self.dx, self.dboxes, dw
+        return self.dx, grad_boxes, dw
 
 
 def _no_tap(label):
@@ -142,11 +146,11 @@ class Stack:
     """`layers` box-conv layers in sequence; layer l's mix output feeds layer l+1."""
 
     def __init__(self, N, C, H, W, B, M, layers, mix_dtype, relu, x_dtype=torch.float32, flags=0,
-                 backward=True, device="cuda"):
-        if layers > 1 and M != C:
-            raise ValueError("stacked layers need M == C")
-        self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device)
-                      for _ in range(layers)]
+                 backward=True, device="cuda", stride=1):
+        if layers > 1 and (M != C or stride != 1):
+            raise ValueError("stacked layers need M == C and stride 1")
+        self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device,
+                                stride=stride) for _ in range(layers)]
 
     def forward(self, x, params, tap=None):
         """params: list of (boxes, w) device tensors.  Returns the inputs of every

@@ -102,6 +102,19 @@ def test_bwd_argument_errors():
     assert lib.box_conv_bwd(*a) == 5
 
 
+def test_strided_argument_errors():
+    lib = bc.load_library()
+    fwd = [FAKE, bc.BC_F32, FAKE, 2, 3, 8, 8, 4, 2, FAKE, bc.BC_F32, 0, None, 0, None]
+    bwd = [FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, 2, FAKE, FAKE, 0, None, 0, None]
+    for args, fn in ((fwd, lib.box_conv_fwd_strided), (bwd, lib.box_conv_bwd_strided)):
+        assert fn(*args) == 5                  # valid stride: fails only for lack of a workspace
+        for bad in (0, -1, 1025):
+            a = list(args); a[8] = bad
+            assert fn(*a) == 2, bad
+        a = list(args); a[0] = None
+        assert fn(*a) == 1
+
+
 def test_mix_argument_errors():
     lib = bc.load_library()
     ok = [bc.BC_MIX_FWD, FAKE, bc.BC_F32, FAKE, bc.BC_F32, FAKE, bc.BC_F32, 2, 64, 512, 3072, bc.BC_F32,

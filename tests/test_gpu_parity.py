@@ -315,6 +315,126 @@ def test_integer_corners_box_grad_rejected():
 
 
 # ---------------------------------------------------------------------------
+# Integer stride: the box at every s-th pixel
+# ---------------------------------------------------------------------------
+def _fwd_s(x, bx, stride, y_dtype=torch.float32, flags=0):
+    N, C, H, W = x.shape
+    B = bx.shape[1]
+    y = torch.empty((N, C * B, O.strided_size(H, stride), O.strided_size(W, stride)), dtype=y_dtype, device="cuda")
+    bc.box_conv_fwd(dev(x), dev(bx), y, flags, stride=stride)
+    return host(y)
+
+
+@pytest.mark.parametrize("stride", [2, 3])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM, INT_CORNERS, INT_CORNERS | bc.BC_FLAG_FORCE_HBM])
+def test_fwd_strided_int_bit_exact(stride, flags):
+    say(f"fwd strided int32 stride={stride} flags={flags}")
+    wl = wlmod.WORKLOADS[1]
+    d = wlmod.make_inputs(wl)
+    bx = d["boxes"] if not flags & INT_CORNERS else rounding_boxes(np.random.default_rng(113), wl.C, wl.B)
+    got = _fwd_s(d["x"], bx, stride, torch.int32, flags)
+    want = O.box_forward(d["x"], bx, integer_corners=bool(flags & INT_CORNERS), stride=stride)
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("key,scale", [
+    (3, dict(N=2, C=8)),
+    (2, dict(N=1, C=3, H=37, W=29, B=5)),
+    (3, dict(N=1, C=2, H=17, W=100, B=3)),
+])
+@pytest.mark.parametrize("stride", [2, 3])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM, bc.BC_FLAG_MEAN_OFFSET, INT_CORNERS])
+def test_fwd_strided_f32(key, scale, stride, flags):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
+    d = wlmod.make_inputs(wl)
+    say(f"fwd strided {wl.key} {scale} stride={stride} flags={flags}")
+    got = _fwd_s(d["x"], d["boxes"], stride, torch.float32, flags)
+    want = O.box_forward(d["x"], d["boxes"], integer_corners=bool(flags & INT_CORNERS), stride=stride)
+    check(got, want, RTOL_F32, "O")
+
+
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_MEAN_OFFSET])
+def test_fwd_strided_large_maps(flags):
+    wl = wlmod.WORKLOADS[4].scaled(N=1, C=2)
+    d = wlmod.make_inputs(wl)
+    say(f"fwd strided {wl.key} reduced stride=2 flags={flags}")
+    got = _fwd_s(d["x"], d["boxes"], 2, torch.float32, flags)
+    check(got, O.box_forward(d["x"], d["boxes"], stride=2), RTOL_F32, "O")
+
+
+def test_strided_api_stride_one_is_plain():
+    wl = wlmod.WORKLOADS[2].scaled(N=1, C=3)
+    d = wlmod.make_inputs(wl)
+    N, C, H, W, B = wl.N, wl.C, wl.H, wl.W, wl.B
+    x, bx = dev(d["x"]), dev(d["boxes"])
+    y1 = torch.empty((N, C * B, H, W), device="cuda")
+    y2 = torch.empty_like(y1)
+    bc.box_conv_fwd(x, bx, y1)
+    lib = bc.load_library()
+    ws = bc._workspace(bc.box_workspace_bytes(0, N, C, H, W, B, 0), x.device)
+    st = lib.box_conv_fwd_strided(bc._ptr(x), bc.BC_F32, bc._ptr(bx), N, C, H, W, B, 1, bc._ptr(y2), bc.BC_F32, 0,
+                                  bc._ptr(ws), ws.numel(), bc._stream())
+    assert st == 0
+    np.testing.assert_array_equal(host(y1), host(y2))
+
+
+@pytest.mark.parametrize("key,scale", [
+    (3, dict(N=2, C=4)),
+    (2, dict(N=1, C=3, H=37, W=29, B=5)),
+    (3, dict(N=2, C=2, H=17, W=100, B=3)),
+    (4, dict(N=1, C=1, B=3)),
+])
+@pytest.mark.parametrize("stride", [2, 3])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_bwd_strided(key, scale, stride, flags):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
+    d = wlmod.make_inputs(wl)
+    Ho, Wo = O.strided_size(wl.H, stride), O.strided_size(wl.W, stride)
+    g = np.random.default_rng(114).standard_normal((wl.N, wl.C * wl.B, Ho, Wo)).astype(np.float32)
+    say(f"bwd strided {wl.key} {scale} stride={stride} flags={flags}")
+    gx = torch.empty((wl.N, wl.C, wl.H, wl.W), dtype=torch.float32, device="cuda")
+    gb = torch.empty((wl.C, wl.B, 4), dtype=torch.float32, device="cuda")
+    bc.box_conv_bwd(dev(d["x"]), dev(d["boxes"]), dev(g), gx, gb, flags, stride=stride)
+    check(host(gx), O.box_backward_input(g, d["boxes"], wl.H, wl.W, stride=stride), RTOL_F32, "dx")
+    check(host(gb), O.box_backward_params(d["x"], g, d["boxes"], stride=stride), RTOL_F32, "dboxes")
+
+
+@pytest.mark.parametrize("flags", [INT_CORNERS, INT_CORNERS | bc.BC_FLAG_FORCE_HBM])
+def test_bwd_strided_integer_corners(flags):
+    wl = wlmod.WORKLOADS[3].scaled(N=2, C=3, H=37, W=29)
+    d = wlmod.make_inputs(wl)
+    s = 2
+    Ho, Wo = O.strided_size(wl.H, s), O.strided_size(wl.W, s)
+    g = np.random.default_rng(115).standard_normal((wl.N, wl.C * wl.B, Ho, Wo)).astype(np.float32)
+    say(f"bwd strided integer corners flags={flags}")
+    gx = torch.empty((wl.N, wl.C, wl.H, wl.W), dtype=torch.float32, device="cuda")
+    bc.box_conv_bwd(dev(d["x"]), dev(d["boxes"]), dev(g), gx, None, flags, stride=s)
+    want = O.box_backward_input(g, d["boxes"], wl.H, wl.W, integer_corners=True, stride=s)
+    check(host(gx), want, RTOL_F32, "dx")
+
+
+def test_layer_strided_fp32():
+    """The whole layer at stride 2 (fp32 mix): every output against the
+    oracle's strided box filter composed with its mix."""
+    wl = wlmod.WORKLOADS[2].scaled(N=2, C=8)
+    d = wlmod.make_inputs(wl)
+    s = 2
+    Ho, Wo = O.strided_size(wl.H, s), O.strided_size(wl.W, s)
+    g = np.random.default_rng(116).standard_normal((wl.N, wl.mix_out, Ho, Wo)).astype(np.float32)
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, "f32", False, 0, True, stride=s)
+    xd, bd, wd = dev(d["x"]), dev(d["boxes"]), dev(d["w"])
+    z = plan.forward(xd, bd, wd)
+    dx, db, dw = plan.backward(xd, bd, wd, dev(g))
+    torch.cuda.synchronize()
+    o = O.box_forward(d["x"], d["boxes"], stride=s)
+    check(host(z), O.mix_forward(d["w"], o, compute="f32"), RTOL_F32, "Z")
+    do = O.mix_backward_data(d["w"], g, compute="f32")
+    check(host(dw), O.mix_backward_weight(g, o, compute="f32"), RTOL_F32, "dW")
+    check(host(dx), O.box_backward_input(do, d["boxes"], wl.H, wl.W, stride=s), RTOL_F32, "dx")
+    check(host(db), O.box_backward_params(d["x"], do, d["boxes"], stride=s), RTOL_F32, "dboxes")
+
+
+# ---------------------------------------------------------------------------
 # a7 / a8: backward of the box filter
 # ---------------------------------------------------------------------------
 def _bwd(x, bx, g, flags=0):
