@@ -178,17 +178,32 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
 
 // Table of a zero-upsampled fp32 map (the transpose of sampling every s-th
 // pixel): src (Ho x Wo) placed at (s*i, s*j) of an H x W map, zeros
-// elsewhere; s * (Ho - 1) < H and s * (Wo - 1) < W.
+// elsewhere; s * (Ho - 1) < H and s * (Wo - 1) < W.  Each source value
+// writes its whole s x s block of the interior (the value at the block's
+// corner, zeros elsewhere), so every interior element is written once; the
+// loads of a batch are in flight together.
 __device__ void build_table_lds_up(const float* __restrict__ src, float* S, int H, int W, int pitch, int s, int Ho,
                                    int Wo) {
-  const int tid = threadIdx.x, nt = blockDim.x;
+  constexpr int kB = 8;
+  const int tid = threadIdx.x, nt = blockDim.x, n = Ho * Wo;
   float* R = S + kPad;
   table_zero_edges(S, H, pitch);
-  for (int k = tid; k < H * pitch; k += nt) S[pitch + k] = 0.f;  // rows 1..H
-  __syncthreads();
-  for (int k = tid; k < Ho * Wo; k += nt) {
-    const int i = k / Wo, j = k - i * Wo;
-    R[(s * i + 1) * pitch + s * j + 1] = src[k];
+  for (int base = 0; base < n; base += nt * kB) {
+    float g[kB];
+#pragma unroll
+    for (int b = 0; b < kB; ++b) g[b] = src[min(base + b * nt + tid, n - 1)];
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      const int k = base + b * nt + tid;
+      if (k < n) {
+        const int i = k / Wo, j = k - i * Wo;
+        const int u1 = min(s * i + s, H), v1 = min(s * j + s, W);
+        for (int u = s * i; u < u1; ++u) {
+          float* row = R + (u + 1) * pitch + 1;
+          for (int v = s * j; v < v1; ++v) row[v] = (u == s * i && v == s * j) ? g[b] : 0.f;
+        }
+      }
+    }
   }
   __syncthreads();
   table_scans(S, H, W, pitch);
