@@ -48,6 +48,11 @@ R13 Integer stride s (Section 3.1 assumes an integer stride so that the
     interpolation weights stay fixed): output pixel (i, j) is the box placed
     at input pixel (s*i, s*j); the output is ceil(H/s) x ceil(W/s).  Stride 1
     is the plain layer.
+R14 Box-parameter reparameterisation (Section 3.2): the corners x_l, x_h,
+    y_l, y_h are kept as u in [-1, 1] relative to a maximum box size M (per
+    axis): x_l = u_xl * M_x / 2 and x_h = u_xh * M_x / 2 (so u = 0 is the
+    1x1 identity box), converted during the forward pass; after each update
+    u is clipped to [-1, 1] and a reversed pair (x_l > x_h) is swapped.
 R12 Integer corners for inference (Conclusions: once the boxes have
     converged, round the sampling points to integers so that no interpolation
     is needed): each edge a, b, c, d is rounded to the nearest integer, a tie
@@ -65,6 +70,7 @@ __all__ = [
     "box_param_grad_from_edges", "bf16_round", "mix_forward",
     "mix_backward_data", "mix_backward_weight", "relu", "layer_forward",
     "stack_forward", "stack_backward", "naive_box_forward_eq1", "strided_size", "zero_upsample",
+    "boxes_from_unit", "unit_grad_from_box_grad", "clip_unit_params",
     "naive_box_forward_overlap", "tolerance_ok", "rel_errors",
 ]
 
@@ -325,6 +331,45 @@ def box_backward_params(x, grad_y, boxes, stride=1):
     e = box_param_grad_from_edges(x, g, boxes)
     ga, gb, gc, gd = e[..., 0], e[..., 1], e[..., 2], e[..., 3]
     return np.stack([ga + gb, gc + gd, gb - ga, gd - gc], axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Box-parameter reparameterisation (Section 3.2; reading R14)
+# ---------------------------------------------------------------------------
+def boxes_from_unit(u, max_w, max_h):
+    """(cx, cy, rx, ry) fp32 [..., 4] of corners given as u = (u_xl, u_xh,
+    u_yl, u_yh) in [-1, 1]: x_l = u_xl * max_w / 2, x_h = u_xh * max_w / 2,
+    and the box covers [x + x_l, x + x_h + 1), i.e. cx = (x_l + x_h) / 2,
+    rx = (x_h - x_l + 1) / 2 (likewise y).  fp64, rounded once to fp32."""
+    u = np.asarray(u, dtype=np.float32).astype(np.float64)
+    mw, mh = float(np.float32(max_w)), float(np.float32(max_h))
+    xl, xh = u[..., 0] * mw / 2, u[..., 1] * mw / 2
+    yl, yh = u[..., 2] * mh / 2, u[..., 3] * mh / 2
+    return np.stack([(xl + xh) / 2, (yl + yh) / 2, (xh - xl + 1) / 2, (yh - yl + 1) / 2],
+                    axis=-1).astype(np.float32)
+
+
+def unit_grad_from_box_grad(grad_boxes, max_w, max_h):
+    """Chain rule through boxes_from_unit: dL/du from dL/d(cx, cy, rx, ry).
+    dL/du_xl = (dcx - drx) / 2 * max_w / 2, dL/du_xh = (dcx + drx) / 2 * max_w / 2
+    (likewise y).  fp64, rounded once to fp32."""
+    g = np.asarray(grad_boxes, dtype=np.float32).astype(np.float64)
+    mw, mh = float(np.float32(max_w)), float(np.float32(max_h))
+    dcx, dcy, drx, dry = g[..., 0], g[..., 1], g[..., 2], g[..., 3]
+    return np.stack([(dcx - drx) / 2 * mw / 2, (dcx + drx) / 2 * mw / 2,
+                     (dcy - dry) / 2 * mh / 2, (dcy + dry) / 2 * mh / 2], axis=-1).astype(np.float32)
+
+
+def clip_unit_params(u):
+    """After an update: each u clipped to [-1, 1], then a reversed pair
+    (u_xl > u_xh, or u_yl > u_yh) swapped, so that x_l <= x_h and y_l <= y_h."""
+    v = np.clip(np.asarray(u, dtype=np.float32), np.float32(-1), np.float32(1))
+    out = v.copy()
+    out[..., 0] = np.minimum(v[..., 0], v[..., 1])
+    out[..., 1] = np.maximum(v[..., 0], v[..., 1])
+    out[..., 2] = np.minimum(v[..., 2], v[..., 3])
+    out[..., 3] = np.maximum(v[..., 2], v[..., 3])
+    return out
 
 
 # ---------------------------------------------------------------------------

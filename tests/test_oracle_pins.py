@@ -400,6 +400,58 @@ def test_strided_param_grad_finite_difference_exact():
 
 
 # --------------------------------------------------------------------------
+# Box-parameter reparameterisation (reading R14)
+# --------------------------------------------------------------------------
+def test_unit_params_identity_and_corners():
+    np.testing.assert_array_equal(O.boxes_from_unit(np.zeros((2, 3, 4)), 64, 48),
+                                  np.broadcast_to(np.float32([0, 0, 0.5, 0.5]), (2, 3, 4)))
+    u = np.array([[[0.25, 0.5, -0.5, 0.75], [-1.0, 1.0, -0.125, -0.125]]], dtype=np.float32)
+    a, b, c, d = O.box_edges(O.boxes_from_unit(u, 64, 48))
+    # the corners of the definition: x_l = u_xl * 32, x_h = u_xh * 32, box [x_l, x_h + 1)
+    np.testing.assert_array_equal(a[0], [8, -32])
+    np.testing.assert_array_equal(b[0], [17, 33])
+    np.testing.assert_array_equal(c[0], [-12, -3])
+    np.testing.assert_array_equal(d[0], [19, -2])
+
+
+def test_unit_grad_finite_difference():
+    rng = np.random.default_rng(27)
+    N, C, B, H, W = 1, 2, 2, 12, 10
+    Mw, Mh = 16.0, 12.0
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    # corners whose edges sit away from pixel boundaries (one linear piece)
+    u = np.empty((C, B, 4), dtype=np.float32)
+    for c in range(C):
+        for b in range(B):
+            while True:
+                cand = np.sort(rng.uniform(-0.9, 0.9, size=2)).tolist() + np.sort(rng.uniform(-0.9, 0.9, size=2)).tolist()
+                cand = np.float32(cand)
+                e = np.array(O.box_edges(O.boxes_from_unit(cand[None], Mw, Mh))).ravel()
+                f = e - np.floor(e)
+                if np.all((f > 0.1) & (f < 0.9)):
+                    u[c, b] = cand
+                    break
+    bx = O.boxes_from_unit(u, Mw, Mh)
+    gu = O.unit_grad_from_box_grad(O.box_backward_params(x, g, bx), Mw, Mh)
+    L0 = np.sum(O.box_forward(x, bx) * g)
+    for c in range(C):
+        for b in range(B):
+            for k in range(4):
+                p = u.copy()
+                p[c, b, k] = np.float32(p[c, b, k] + np.float32(0.005))
+                h = float(p[c, b, k]) - float(u[c, b, k])
+                fd = (np.sum(O.box_forward(x, O.boxes_from_unit(p, Mw, Mh)) * g) - L0) / h
+                assert abs(fd - gu[c, b, k]) <= 1e-3 * (1 + abs(fd)), (c, b, k, fd, gu[c, b, k])
+
+
+def test_clip_unit_params_closed_form():
+    u = np.array([[0.5, -0.3, 2.0, -3.0], [-1.5, -2.0, 0.25, 0.25], [0.1, 0.2, 0.9, 1.2]], dtype=np.float32)
+    want = np.array([[-0.3, 0.5, -1.0, 1.0], [-1.0, -1.0, 0.25, 0.25], [0.1, 0.2, 0.9, 1.0]], dtype=np.float32)
+    np.testing.assert_array_equal(O.clip_unit_params(u), want)
+
+
+# --------------------------------------------------------------------------
 # Input gradient: adjoint of the forward map
 # --------------------------------------------------------------------------
 def test_input_grad_adjoint_and_mirrored_box():
@@ -732,7 +784,22 @@ def _mut_rounded_floor(boxes):
     return tuple(np.floor(e) for e in _OM.box_edges(boxes))
 
 
-_ORIG = {k: getattr(_OM, k) for k in ("overlap_matrix", "_edge_selector")}
+def _mut_unit_full_scale(u, max_w, max_h):
+    return _ORIG["boxes_from_unit"](u, 2 * max_w, 2 * max_h)
+
+
+def _mut_unit_grad_sign(grad_boxes, max_w, max_h):
+    g = np.asarray(grad_boxes, dtype=np.float32).copy()
+    g[..., 2:] = -g[..., 2:]
+    return _ORIG["unit_grad_from_box_grad"](g, max_w, max_h)
+
+
+def _mut_clip_no_swap(u):
+    return np.clip(np.asarray(u, dtype=np.float32), np.float32(-1), np.float32(1))
+
+
+_ORIG = {k: getattr(_OM, k) for k in ("overlap_matrix", "_edge_selector", "boxes_from_unit",
+                                      "unit_grad_from_box_grad")}
 
 _MUTATIONS = {
     "edges_sign": ("box_edges", _mut_edges_sign),
@@ -747,6 +814,9 @@ _MUTATIONS = {
     "rounded_half_even": ("rounded_edges", _mut_rounded_half_even),
     "rounded_floor": ("rounded_edges", _mut_rounded_floor),
     "upsample_offset": ("zero_upsample", _mut_upsample_offset),
+    "unit_full_scale": ("boxes_from_unit", _mut_unit_full_scale),
+    "unit_grad_sign": ("unit_grad_from_box_grad", _mut_unit_grad_sign),
+    "clip_no_swap": ("clip_unit_params", _mut_clip_no_swap),
 }
 
 _PINS = [
@@ -759,7 +829,8 @@ _PINS = [
     test_adjoint_taps_carry_param_gradient, test_rounded_edges_closed_form,
     lambda: test_integer_corners_forward_equals_eq1_loops("int"), test_integer_corners_backward_is_adjoint,
     lambda: test_strided_forward_equals_eq1_loops(2), test_strided_input_grad_is_adjoint,
-    test_strided_param_grad_finite_difference_exact,
+    test_strided_param_grad_finite_difference_exact, test_unit_params_identity_and_corners,
+    test_unit_grad_finite_difference, test_clip_unit_params_closed_form,
 ]
 
 
