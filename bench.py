@@ -49,6 +49,10 @@ def parse():
     p.add_argument("--stride", type=int, default=1,
                    help="box filter stride (outputs at every stride-th pixel; the 1x1 mix and the backward "
                         "run on the strided grid)")
+    p.add_argument("--unit-params", action="store_true",
+                   help="train the boxes as unit corners in [-1, 1] relative to a maximum box size equal to "
+                        "the map size (drawn U[-0.5, 0.5]); the step then also converts them, takes their "
+                        "gradient and clips them")
     p.add_argument("--serial", action="store_true",
                    help="run every call in order on one stream in the timed pass too (no overlapped "
                         "weight gradient): the configuration the per-kernel profiles are taken in")
@@ -77,6 +81,8 @@ def call_cost(label, wl, o_bytes, stride=1):
                    write Z; bwd_data: read dZ, write dO; bwd_weight: read dZ
                    and O), reported against the HBM peak
     """
+    if label.startswith("box_params"):        # read and write [C][B][4] fp32
+        return {"bound": "hbm", "bytes": 2 * wl.C * wl.B * 16}
     px = wl.N * wl.C * wl.H * wl.W
     Ho, Wo = (wl.H + stride - 1) // stride, (wl.W + stride - 1) // stride
     pb = wl.N * wl.C * wl.B * Ho * Wo          # output pixel*box
@@ -200,18 +206,21 @@ def main():
     if args.inference:
         flags |= bc.BC_FLAG_INTEGER_CORNERS
     s_ = args.stride
+    unit = (float(wl.W), float(wl.H)) if args.unit_params else None
     st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, wl.mix_dtype, wl.relu, x_dt, flags,
-               backward, stride=s_)
+               backward, stride=s_, unit_size=unit)
+    if unit is not None:
+        params = [(dev(wlmod.make_unit_corners(wl, li)), w) for li, (_, w) in enumerate(params)]
     if grad is not None and s_ > 1:
         grad = grad[..., ::s_, ::s_].contiguous()
     for plan in st.plans:
         plan.overlap = not args.serial
     stream = torch.cuda.current_stream()
-    timing = {"on": False, "events": []}
+    timing = {"on": False, "events": [], "pool": []}
 
     def tap(label):
         if timing["on"]:
-            e = torch.cuda.Event(enable_timing=True)
+            e = timing["pool"].pop()
             e.record(stream)
             timing["events"].append((label, e))
 
@@ -225,12 +234,17 @@ def main():
         inputs, out = st.forward(x, params, t)
         if backward:
             st.backward(inputs, params, grad, t)
+            if unit is not None:      # the per-update step on the unit corners
+                for plan, (u, _) in zip(st.plans, params):
+                    plan.clip(u)
+                if t:
+                    t("box_params_clip")
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # Each timed pass starts behind ~30 ms of device-side spinning, queued
+    # Each timed pass starts behind ~100 ms of device-side spinning, queued
     # before its first event: the host enqueues the steps while the GPU is
     # busy, so no host launch gap lands inside a timed call or step.
     spin = torch.cuda._sleep
@@ -240,7 +254,7 @@ def main():
     spin(probe)
     s1.record(stream)
     torch.cuda.synchronize()
-    spin_cycles = int(probe * 30.0 / max(s0.elapsed_time(s1), 1e-3))
+    spin_cycles = int(probe * 100.0 / max(s0.elapsed_time(s1), 1e-3))
 
     # timed region: plain steps
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -252,7 +266,9 @@ def main():
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
 
-    # second timed pass with an event after every library call
+    # second timed pass with an event after every library call (events made
+    # beforehand, so the pass itself only records them)
+    timing["pool"] = [torch.cuda.Event(enable_timing=True) for _ in range(16 * args.steps)]
     timing["on"] = True
     spin(spin_cycles)
     for _ in range(args.steps):
@@ -315,6 +331,7 @@ def main():
                    "layers": wl.layers, "relu": wl.relu, "mean_offset": wl.mean_offset,
                    "integer_corners": bool(args.inference), "backward": backward,
                    "overlap_weight_grad": backward and not args.serial, "stride": args.stride,
+                   "unit_params": bool(args.unit_params),
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
         "roofline": roofline,

@@ -205,6 +205,28 @@ bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* 
                                void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Box-parameter reparameterisation (Section 3.2): the corners x_l, x_h, y_l,
+ * y_h of each box are trained as u = (u_xl, u_xh, u_yl, u_yh) in [-1, 1],
+ * relative to a maximum box size (max_w, max_h pixels):
+ *   x_l = u_xl * max_w / 2, x_h = u_xh * max_w / 2 (likewise y), the box
+ *   covering [x + x_l, x + x_h + 1) -- u = 0 is the 1x1 identity box.
+ * u, boxes, grad_boxes, grad_u : device fp32 [C][B][4], 16-byte aligned.
+ * All arithmetic in fp64, each result rounded once to fp32.
+ *
+ * box_params_from_unit : boxes (cx, cy, rx, ry) for box_conv_* from u.
+ * box_params_unit_grad : grad_u = dL/du from grad_boxes = dL/d(cx, cy, rx, ry)
+ *                        (the chain rule of box_params_from_unit).
+ * box_params_clip      : after an update, in place: u clipped to [-1, 1] and
+ *                        a reversed pair (u_xl > u_xh or u_yl > u_yh) swapped.
+ * Errors: NULL pointers, C, B <= 0, max sizes not in (0, 1e6].
+ * ---------------------------------------------------------------------- */
+bc_status box_params_from_unit(const float* u, int C, int B, float max_w, float max_h,
+                               float* boxes, hipStream_t stream);
+bc_status box_params_unit_grad(const float* grad_boxes, int C, int B, float max_w, float max_h,
+                               float* grad_u, hipStream_t stream);
+bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * pointwise_mix -- the 1x1 convolution over the C*B filtered maps
  * (Section 1, Section 3.2), per image n with P = H*W pixels, on MFMA:
  *   BC_MIX_FWD        : a = w [M][K], b = in [N][K][P]   -> out [N][M][P]

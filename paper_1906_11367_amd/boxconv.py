@@ -6,8 +6,9 @@ kernels.  The library is required: if it is not built, or a GPU is not
 present, the calls raise -- there is no fallback implementation.
 
 Entry points (same names as the C ABI): box_prep, sat_build, box_conv_fwd,
-box_conv_bwd, box_conv_fwd_strided, box_conv_bwd_strided, pointwise_mix, plus
-the workspace-size queries.
+box_conv_bwd, box_conv_fwd_strided, box_conv_bwd_strided, pointwise_mix, the
+box-parameter reparameterisation (box_params_from_unit, box_params_unit_grad,
+box_params_clip), plus the workspace-size queries.
 """
 from __future__ import annotations
 
@@ -33,6 +34,9 @@ SIGNATURES = {
     "box_conv_fwd": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
     "box_conv_bwd": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
     "box_conv_fwd_strided": (_i, [_vp, _i, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _u, _vp, _sz, _vp]),
+    "box_params_from_unit": (_i, [_vp, _i, _i, _f, _f, _vp, _vp]),
+    "box_params_unit_grad": (_i, [_vp, _i, _i, _f, _f, _vp, _vp]),
+    "box_params_clip": (_i, [_vp, _i, _i, _vp]),
     "box_conv_bwd_strided": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
     "pointwise_mix": (_i, [_i, _vp, _i, _vp, _i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
@@ -178,6 +182,27 @@ def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, gra
 
 def box_conv_bwd_strided(x, boxes, grad_y, stride: int, grad_x, grad_boxes, flags: int = 0, ws=None):
     return box_conv_bwd(x, boxes, grad_y, grad_x, grad_boxes, flags, ws, stride)
+
+
+def box_params_from_unit(u: torch.Tensor, max_w: float, max_h: float, boxes: torch.Tensor):
+    """u [C, B, 4] unit corners -> boxes [C, B, 4] (cx, cy, rx, ry) in pixels."""
+    C, B = u.shape[0], u.shape[1]
+    _check(load_library().box_params_from_unit(_ptr(u), C, B, max_w, max_h, _ptr(boxes), _stream()),
+           "box_params_from_unit")
+    return boxes
+
+
+def box_params_unit_grad(grad_boxes: torch.Tensor, max_w: float, max_h: float, grad_u: torch.Tensor):
+    C, B = grad_boxes.shape[0], grad_boxes.shape[1]
+    _check(load_library().box_params_unit_grad(_ptr(grad_boxes), C, B, max_w, max_h, _ptr(grad_u), _stream()),
+           "box_params_unit_grad")
+    return grad_u
+
+
+def box_params_clip(u: torch.Tensor):
+    C, B = u.shape[0], u.shape[1]
+    _check(load_library().box_params_clip(_ptr(u), C, B, _stream()), "box_params_clip")
+    return u
 
 
 def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):

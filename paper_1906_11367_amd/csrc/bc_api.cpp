@@ -207,6 +207,33 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   return box_conv_bwd_strided(x, boxes, grad_y, N, C, H, W, B, 1, grad_x, grad_boxes, flags, ws, ws_bytes, stream);
 }
 
+static bool unit_args_ok(int C, int B, float mw, float mh) {
+  return C > 0 && B > 0 && (long)C * B <= (1L << 28) && mw > 0.f && mh > 0.f && mw <= 1e6f && mh <= 1e6f;
+}
+
+bc_status box_params_from_unit(const float* u, int C, int B, float max_w, float max_h, float* boxes,
+                               hipStream_t stream) {
+  if (!u || !boxes) return BC_ERR_NULL;
+  if (!unit_args_ok(C, B, max_w, max_h)) return BC_ERR_SHAPE;
+  if (!aligned16(u) || !aligned16(boxes)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_unit_params(0, u, C * B, max_w, max_h, boxes, stream));
+}
+
+bc_status box_params_unit_grad(const float* grad_boxes, int C, int B, float max_w, float max_h, float* grad_u,
+                               hipStream_t stream) {
+  if (!grad_boxes || !grad_u) return BC_ERR_NULL;
+  if (!unit_args_ok(C, B, max_w, max_h)) return BC_ERR_SHAPE;
+  if (!aligned16(grad_boxes) || !aligned16(grad_u)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_unit_params(1, grad_boxes, C * B, max_w, max_h, grad_u, stream));
+}
+
+bc_status box_params_clip(float* u, int C, int B, hipStream_t stream) {
+  if (!u) return BC_ERR_NULL;
+  if (!unit_args_ok(C, B, 1.f, 1.f)) return BC_ERR_SHAPE;
+  if (!aligned16(u)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_unit_params(2, nullptr, C * B, 1.f, 1.f, u, stream));
+}
+
 bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream) {
   if (!src || !dst) return BC_ERR_NULL;
   if (n == 0 || n > ((size_t)1 << 40)) return BC_ERR_SHAPE;

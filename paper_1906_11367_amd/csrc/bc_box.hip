@@ -505,6 +505,44 @@ __global__ void k_box_prep(const float* __restrict__ boxes, int CB, int rounded,
   for (int k = 0; k < 4; ++k) { f[4 + k] = t.wx[k]; f[8 + k] = t.wy[k]; r[12 + k] = 0; }
 }
 
+// Box-parameter reparameterisation (Section 3.2): corners kept as u in
+// [-1, 1] relative to a maximum box size M per axis, x_l = u_xl * M_x / 2,
+// x_h = u_xh * M_x / 2, box [x + x_l, x + x_h + 1).  fp64 arithmetic (exact
+// for these operands), rounded once to fp32.
+__global__ void k_boxes_from_unit(const float* __restrict__ u, int n, float mw, float mh,
+                                  float* __restrict__ boxes) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float* q = u + (size_t)i * 4;
+  const double xl = (double)q[0] * (double)mw / 2, xh = (double)q[1] * (double)mw / 2;
+  const double yl = (double)q[2] * (double)mh / 2, yh = (double)q[3] * (double)mh / 2;
+  *reinterpret_cast<float4*>(boxes + (size_t)i * 4) =
+      make_float4((float)((xl + xh) / 2), (float)((yl + yh) / 2), (float)((xh - xl + 1) / 2), (float)((yh - yl + 1) / 2));
+}
+
+// dL/du from dL/d(cx, cy, rx, ry) through the map above: x_l = a and
+// x_h = b - 1 with cx = (a + b - 1) / 2, rx = (b - a) / 2.
+__global__ void k_unit_grad(const float* __restrict__ g, int n, float mw, float mh, float* __restrict__ gu) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float4 q = *reinterpret_cast<const float4*>(g + (size_t)i * 4);
+  const double sx = (double)mw / 2, sy = (double)mh / 2;
+  *reinterpret_cast<float4*>(gu + (size_t)i * 4) =
+      make_float4((float)(((double)q.x - q.z) / 2 * sx), (float)(((double)q.x + q.z) / 2 * sx),
+                  (float)(((double)q.y - q.w) / 2 * sy), (float)(((double)q.y + q.w) / 2 * sy));
+}
+
+// After an update: clip u to [-1, 1] and swap a reversed corner pair.
+__global__ void k_clip_unit(float* __restrict__ u, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float4 q = *reinterpret_cast<float4*>(u + (size_t)i * 4);
+  q.x = fminf(fmaxf(q.x, -1.f), 1.f); q.y = fminf(fmaxf(q.y, -1.f), 1.f);
+  q.z = fminf(fmaxf(q.z, -1.f), 1.f); q.w = fminf(fmaxf(q.w, -1.f), 1.f);
+  *reinterpret_cast<float4*>(u + (size_t)i * 4) = make_float4(fminf(q.x, q.y), fmaxf(q.x, q.y), fminf(q.z, q.w),
+                                                              fmaxf(q.z, q.w));
+}
+
 // Standalone table in HBM, one block per map.  The map is processed in strips
 // of kStrip rows staged in LDS: each wave scans whole rows (every lane holds a
 // run of consecutive elements, scanned serially, then a wave-level scan of
@@ -920,6 +958,14 @@ static hipError_t last_error() { return hipGetLastError(); }
 hipError_t launch_box_prep(const float* boxes, int C, int B, bool rounded, void* table, hipStream_t s) {
   const int n = 2 * C * B;
   hipLaunchKernelGGL(k_box_prep, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, (int)rounded, (int*)table);
+  return last_error();
+}
+
+hipError_t launch_unit_params(int op, const float* in, int n, float mw, float mh, float* out, hipStream_t s) {
+  const dim3 grid((n + 255) / 256), block(256);
+  if (op == 0) hipLaunchKernelGGL(k_boxes_from_unit, grid, block, 0, s, in, n, mw, mh, out);
+  else if (op == 1) hipLaunchKernelGGL(k_unit_grad, grid, block, 0, s, in, n, mw, mh, out);
+  else hipLaunchKernelGGL(k_clip_unit, grid, block, 0, s, out, n);
   return last_error();
 }
 

@@ -54,6 +54,10 @@ int box_bwd_lds_waves(int H, int W);
 int box_bwd_gather_blocks(int H, int W);
 hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx,
                                  float* partials, int N, int C, int H, int W, int B, bool rounded, hipStream_t s);
+// Box-parameter reparameterisation over n = C*B boxes: op 0 = boxes from
+// unit corners (in -> out), 1 = unit gradient from box gradient (in -> out),
+// 2 = clip and order unit corners in place (out).
+hipError_t launch_unit_params(int op, const float* in, int n, float mw, float mh, float* out, hipStream_t s);
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 

@@ -37,6 +37,10 @@ class LayerPlan:
     device: str = "cuda"
     overlap: bool = True       # weight gradient on a second stream during the backward
     stride: int = 1            # box filter stride: outputs ceil(H/stride) x ceil(W/stride)
+    # (max_w, max_h): the boxes are given as unit corners u in [-1, 1] relative
+    # to that maximum box size (converted in the forward; the backward returns
+    # dL/du); None: the boxes are (cx, cy, rx, ry) in pixels
+    unit_size: tuple | None = None
 
     def __post_init__(self):
         dev = torch.device(self.device)
@@ -56,6 +60,8 @@ class LayerPlan:
         self.o = torch.empty((N, K, Ho, Wo), dtype=o_dt, device=dev)
         self.compute = bc.BC_BF16 if self.mix_dtype == "bf16" else bc.BC_F32
         self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
+        if self.unit_size is not None:
+            self.boxes_px = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
         if self.M is not None:
             self.z = torch.empty((N, self.M, Ho, Wo), dtype=torch.int32 if integer else torch.float32, device=dev)
             # the mix's weights in its compute type, refreshed from w every forward
@@ -65,6 +71,8 @@ class LayerPlan:
             self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
             self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
             self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
+            if self.unit_size is not None:
+                self.du = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
             if self.M is not None:
                 self.do = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=dev)
                 self.dw = torch.empty((self.M, K), dtype=torch.float32, device=dev)
@@ -78,6 +86,8 @@ class LayerPlan:
         """tap(label), if given, is called after each library call (the benchmark
         records a stream event there)."""
         tap = tap or _no_tap
+        if self.unit_size is not None:
+            boxes = bc.box_params_from_unit(boxes, *self.unit_size, self.boxes_px)
         bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd, stride=self.stride)
         tap("box_conv_fwd")
         if self.M is None:
@@ -100,6 +110,9 @@ class LayerPlan:
         each call alone."""
         overlap = tap is None and self.overlap
         tap = tap or _no_tap
+        u = None
+        if self.unit_size is not None:
+            u, boxes = boxes, self.boxes_px      # the forward's conversion of u
         if self.M is None:
             do = grad_out
             dw = None
@@ -127,9 +140,17 @@ class LayerPlan:
         grad_boxes = None if self.flags & bc.BC_FLAG_INTEGER_CORNERS else self.dboxes
         bc.box_conv_bwd(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
         tap("box_conv_bwd")
+        if u is not None and grad_boxes is not None:
+            grad_boxes = bc.box_params_unit_grad(grad_boxes, *self.unit_size, self.du)
+            tap("box_params")
         if self.M is not None and overlap:
             main.wait_event(self.ev_dw)         # dW (and the reuse of O, dZ) ordered after the side stream
         return self.dx, grad_boxes, dw
+
+
+    def clip(self, u: torch.Tensor):
+        """After an update of the unit corners: clip to [-1, 1], order each pair."""
+        return bc.box_params_clip(u)
 
 
 def _no_tap(label):
@@ -146,11 +167,11 @@ class Stack:
     """`layers` box-conv layers in sequence; layer l's mix output feeds layer l+1."""
 
     def __init__(self, N, C, H, W, B, M, layers, mix_dtype, relu, x_dtype=torch.float32, flags=0,
-                 backward=True, device="cuda", stride=1):
+                 backward=True, device="cuda", stride=1, unit_size=None):
         if layers > 1 and (M != C or stride != 1):
             raise ValueError("stacked layers need M == C and stride 1")
         self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device,
-                                stride=stride) for _ in range(layers)]
+                                stride=stride, unit_size=unit_size) for _ in range(layers)]
 
     def forward(self, x, params, tap=None):
         """params: list of (boxes, w) device tensors.  Returns the inputs of every

@@ -24,7 +24,7 @@ import os
 
 import numpy as np
 
-TAG_X, TAG_BOXES, TAG_W, TAG_GRAD = 0, 1, 2, 3
+TAG_X, TAG_BOXES, TAG_W, TAG_GRAD, TAG_UNIT = 0, 1, 2, 3, 4
 
 
 @dataclasses.dataclass(frozen=True)
@@ -122,6 +122,15 @@ def make_x(wl: Workload) -> np.ndarray:
 
     _per_image(wl.N, fill)
     return out
+
+
+def make_unit_corners(wl: Workload, layer: int = 0) -> np.ndarray:
+    """Box corners [C, B, 4] fp32 as unit coordinates (u_xl, u_xh, u_yl, u_yh)
+    drawn uniformly in [-0.5, 0.5] (the paper's initialisation, Section 3.2),
+    each pair in order (x_l <= x_h, y_l <= y_h)."""
+    g = _rng(wl.seed, TAG_UNIT, layer)
+    u = np.sort(g.uniform(-0.5, 0.5, size=(wl.C, wl.B, 2, 2)), axis=-1)
+    return u.reshape(wl.C, wl.B, 4).astype(np.float32)
 
 
 def make_boxes(wl: Workload, layer: int = 0) -> np.ndarray:

@@ -115,6 +115,18 @@ def test_strided_argument_errors():
         assert fn(*a) == 1
 
 
+def test_unit_params_argument_errors():
+    lib = bc.load_library()
+    assert lib.box_params_from_unit(None, 2, 4, 64.0, 48.0, FAKE, None) == 1
+    assert lib.box_params_from_unit(FAKE, 0, 4, 64.0, 48.0, FAKE, None) == 2
+    assert lib.box_params_from_unit(FAKE, 2, 4, 0.0, 48.0, FAKE, None) == 2
+    assert lib.box_params_from_unit(FAKE, 2, 4, 64.0, 48.0, FAKE_MISALIGNED, None) == 4
+    assert lib.box_params_unit_grad(FAKE, 2, 4, 64.0, -1.0, FAKE, None) == 2
+    assert lib.box_params_unit_grad(FAKE, 2, 4, 64.0, 48.0, None, None) == 1
+    assert lib.box_params_clip(None, 2, 4, None) == 1
+    assert lib.box_params_clip(FAKE_MISALIGNED, 2, 4, None) == 4
+
+
 def test_mix_argument_errors():
     lib = bc.load_library()
     ok = [bc.BC_MIX_FWD, FAKE, bc.BC_F32, FAKE, bc.BC_F32, FAKE, bc.BC_F32, 2, 64, 512, 3072, bc.BC_F32,

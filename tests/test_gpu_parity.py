@@ -435,6 +435,51 @@ def test_layer_strided_fp32():
 
 
 # ---------------------------------------------------------------------------
+# Box-parameter reparameterisation: bit-exact (fp64 arithmetic, one rounding)
+# ---------------------------------------------------------------------------
+def test_unit_params_bit_exact():
+    rng = np.random.default_rng(117)
+    C, B, Mw, Mh = 9, 5, 64.0, 48.0
+    u = rng.uniform(-1, 1, size=(C, B, 4)).astype(np.float32)
+    u[0, 0] = 0
+    boxes = torch.empty((C, B, 4), device="cuda")
+    bc.box_params_from_unit(dev(u), Mw, Mh, boxes)
+    np.testing.assert_array_equal(host(boxes), O.boxes_from_unit(u, Mw, Mh))
+    g = rng.standard_normal((C, B, 4)).astype(np.float32)
+    gu = torch.empty((C, B, 4), device="cuda")
+    bc.box_params_unit_grad(dev(g), Mw, Mh, gu)
+    np.testing.assert_array_equal(host(gu), O.unit_grad_from_box_grad(g, Mw, Mh))
+    v = (rng.standard_normal((C, B, 4)) * 1.5).astype(np.float32)
+    vd = dev(v)
+    bc.box_params_clip(vd)
+    np.testing.assert_array_equal(host(vd), O.clip_unit_params(v))
+
+
+def test_layer_unit_params_gradient():
+    """Layer trained through unit corners: box gradient in u equals the
+    oracle's chain rule of its parameter gradient."""
+    wl = wlmod.WORKLOADS[2].scaled(N=2, C=4)
+    d = wlmod.make_inputs(wl)
+    rng = np.random.default_rng(118)
+    Mw, Mh = 32.0, 32.0
+    u = O.clip_unit_params(rng.uniform(-0.5, 0.5, size=(wl.C, wl.B, 4)).astype(np.float32))
+    g = rng.standard_normal((wl.N, wl.mix_out, wl.H, wl.W)).astype(np.float32)
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, "f32", False, 0, True,
+                     unit_size=(Mw, Mh))
+    xd, ud, wd = dev(d["x"]), dev(u), dev(d["w"])
+    z = plan.forward(xd, ud, wd)
+    dx, du, dw = plan.backward(xd, ud, wd, dev(g))
+    torch.cuda.synchronize()
+    bx = O.boxes_from_unit(u, Mw, Mh)
+    o = O.box_forward(d["x"], bx)
+    check(host(z), O.mix_forward(d["w"], o, compute="f32"), RTOL_F32, "Z")
+    do = O.mix_backward_data(d["w"], g, compute="f32")
+    want = O.unit_grad_from_box_grad(O.box_backward_params(d["x"], do, bx), Mw, Mh)
+    check(host(du), want, RTOL_F32, "du")
+    check(host(dx), O.box_backward_input(do, bx, wl.H, wl.W), RTOL_F32, "dx")
+
+
+# ---------------------------------------------------------------------------
 # a7 / a8: backward of the box filter
 # ---------------------------------------------------------------------------
 def _bwd(x, bx, g, flags=0):
