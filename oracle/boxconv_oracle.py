@@ -53,6 +53,12 @@ R14 Box-parameter reparameterisation (Section 3.2): the corners x_l, x_h,
     axis): x_l = u_xl * M_x / 2 and x_h = u_xh * M_x / 2 (so u = 0 is the
     1x1 identity box), converted during the forward pass; after each update
     u is clipped to [-1, 1] and a reversed pair (x_l > x_h) is swapped.
+R15 Kernel splitting (Section 3.1, Fig. 2): a split box is cut at its centre
+    line(s) into 2 pieces side by side (mode 2x), 2 stacked (2y) or 4 (mode
+    4); piece p has its own weight w[c, b, p] and the output is the weighted
+    sum of the pieces' box sums.  The cut edges are m = (a + b) / 2 and
+    n = (c + d) / 2, so a split box keeps the 4 parameters of the box plus
+    the piece weights, and the pieces share the cut edges.
 R12 Integer corners for inference (Conclusions: once the boxes have
     converged, round the sampling points to integers so that no interpolation
     is needed): each edge a, b, c, d is rounded to the nearest integer, a tie
@@ -71,6 +77,8 @@ __all__ = [
     "mix_backward_data", "mix_backward_weight", "relu", "layer_forward",
     "stack_forward", "stack_backward", "naive_box_forward_eq1", "strided_size", "zero_upsample",
     "boxes_from_unit", "unit_grad_from_box_grad", "clip_unit_params",
+    "SPLIT_MODES", "split_edges", "box_forward_split", "box_backward_split_input",
+    "box_backward_split_params",
     "naive_box_forward_overlap", "tolerance_ok", "rel_errors",
 ]
 
@@ -303,19 +311,20 @@ def box_param_grad_from_edges(x, grad_y, boxes):
     out = np.zeros((C, B, 4), dtype=np.float64)
     for ci in range(C):
         for bi in range(B):
-            wx = overlap_matrix(W, a[ci, bi], b[ci, bi])
-            wy = overlap_matrix(H, c[ci, bi], d[ci, bi])
-            ea = _edge_selector(W, a[ci, bi])
-            eb = _edge_selector(W, b[ci, bi])
-            ec = _edge_selector(H, c[ci, bi])
-            ed = _edge_selector(H, d[ci, bi])
-            img = xf[:, ci]
-            gb = g[:, ci, bi]
-            out[ci, bi, 0] = -np.sum(gb * (wy @ img @ ea.T))
-            out[ci, bi, 1] = np.sum(gb * (wy @ img @ eb.T))
-            out[ci, bi, 2] = -np.sum(gb * (ec @ img @ wx.T))
-            out[ci, bi, 3] = np.sum(gb * (ed @ img @ wx.T))
+            out[ci, bi] = _edge_grads(xf[:, ci], g[:, ci, bi], a[ci, bi], b[ci, bi], c[ci, bi], d[ci, bi])
     return out
+
+
+def _edge_grads(img, gb, a, b, c, d):
+    """(dL/da, dL/db, dL/dc, dL/dd) of L = <gb, box sum of img over [a, b) x [c, d)>
+    for one box; img, gb: [N, H, W]."""
+    H, W = img.shape[-2:]
+    wx = overlap_matrix(W, a, b)
+    wy = overlap_matrix(H, c, d)
+    return np.array([-np.sum(gb * (wy @ img @ _edge_selector(W, a).T)),
+                     np.sum(gb * (wy @ img @ _edge_selector(W, b).T)),
+                     -np.sum(gb * (_edge_selector(H, c) @ img @ wx.T)),
+                     np.sum(gb * (_edge_selector(H, d) @ img @ wx.T))])
 
 
 def box_backward_params(x, grad_y, boxes, stride=1):
@@ -331,6 +340,107 @@ def box_backward_params(x, grad_y, boxes, stride=1):
     e = box_param_grad_from_edges(x, g, boxes)
     ga, gb, gc, gd = e[..., 0], e[..., 1], e[..., 2], e[..., 3]
     return np.stack([ga + gb, gc + gd, gb - ga, gd - gc], axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Kernel splitting (Section 3.1, Fig. 2; reading R15)
+# ---------------------------------------------------------------------------
+SPLIT_MODES = {"2x": (1, 2), "2y": (2, 1), "4": (2, 2)}   # (pieces along y, pieces along x)
+
+
+def split_edges(boxes, mode):
+    """Edges (a_p, b_p, c_p, d_p) fp64 [C, B, P, 4] of the pieces of split
+    boxes: the box [a, b) x [c, d) cut at m = (a + b) / 2 (modes 2x, 4) and
+    n = (c + d) / 2 (modes 2y, 4); piece p = i * nx + j covers rows
+    [r_i, r_{i+1}) and columns [k_j, k_{j+1}) with k = (a, m, b) or (a, b)
+    and r = (c, n, d) or (c, d)."""
+    a, b, c, d = box_edges(boxes)
+    ny, nx = SPLIT_MODES[mode]
+    ks = [a, (a + b) / 2, b] if nx == 2 else [a, b]
+    rs = [c, (c + d) / 2, d] if ny == 2 else [c, d]
+    out = np.empty(a.shape + (ny * nx, 4), dtype=np.float64)
+    for i in range(ny):
+        for j in range(nx):
+            out[..., i * nx + j, :] = np.stack([ks[j], ks[j + 1], rs[i], rs[i + 1]], axis=-1)
+    return out
+
+
+def box_forward_split(x, boxes, piece_w, mode):
+    """O[n, c*B+b] = sum_p w[c, b, p] * integral of x[n, c] over piece p (fp64).
+    piece_w: [C, B, P] with P = 2 (modes 2x, 2y) or 4."""
+    xf = np.asarray(x, dtype=np.float64)
+    N, C, H, W = xf.shape
+    B = boxes.shape[1]
+    e = split_edges(boxes, mode)
+    w = np.asarray(piece_w, dtype=np.float64)
+    out = np.zeros((N, C, B, H, W), dtype=np.float64)
+    for ci in range(C):
+        for bi in range(B):
+            for p in range(e.shape[2]):
+                a, b, c, d = e[ci, bi, p]
+                out[:, ci, bi] += w[ci, bi, p] * (overlap_matrix(H, c, d) @ xf[:, ci] @ overlap_matrix(W, a, b).T)
+    return out.reshape(N, C * B, H, W)
+
+
+def box_backward_split_input(grad_y, boxes, piece_w, mode, H, W):
+    """dI[n, c] = sum_b sum_p w[c, b, p] * Wy_p^T @ dO[n, c*B+b] @ Wx_p (the transpose)."""
+    g = np.asarray(grad_y, dtype=np.float64)
+    C, B = boxes.shape[0], boxes.shape[1]
+    N = g.shape[0]
+    g = g.reshape(N, C, B, H, W)
+    e = split_edges(boxes, mode)
+    w = np.asarray(piece_w, dtype=np.float64)
+    out = np.zeros((N, C, H, W), dtype=np.float64)
+    for ci in range(C):
+        for bi in range(B):
+            for p in range(e.shape[2]):
+                a, b, c, d = e[ci, bi, p]
+                out[:, ci] += w[ci, bi, p] * (overlap_matrix(H, c, d).T @ g[:, ci, bi] @ overlap_matrix(W, a, b))
+    return out
+
+
+def box_backward_split_params(x, grad_y, boxes, piece_w, mode):
+    """Gradients of L = <grad_y, O> for split boxes: (d/d(cx, cy, rx, ry) fp64
+    [C, B, 4], d/dw fp64 [C, B, P]).
+
+    dL/dw_p is <grad_y, box sum of piece p>.  The edge derivatives of each
+    piece (times its weight) are summed onto the edges of the box: the outer
+    edges directly, and the cut edges m = (a + b) / 2, n = (c + d) / 2 half to
+    each edge they are the mean of."""
+    xf = np.asarray(x, dtype=np.float64)
+    N, C, H, W = xf.shape
+    B = boxes.shape[1]
+    g = np.asarray(grad_y, dtype=np.float64).reshape(N, C, B, H, W)
+    e = split_edges(boxes, mode)
+    w = np.asarray(piece_w, dtype=np.float64)
+    ny, nx = SPLIT_MODES[mode]
+    gbox = np.zeros((C, B, 4), dtype=np.float64)
+    gw = np.zeros((C, B, ny * nx), dtype=np.float64)
+    for ci in range(C):
+        for bi in range(B):
+            img, gb = xf[:, ci], g[:, ci, bi]
+            gk = np.zeros(nx + 1)          # dL/d(column edge k)
+            gr = np.zeros(ny + 1)          # dL/d(row edge r)
+            for i in range(ny):
+                for j in range(nx):
+                    p = i * nx + j
+                    a, b, c, d = e[ci, bi, p]
+                    gw[ci, bi, p] = np.sum(gb * (overlap_matrix(H, c, d) @ img @ overlap_matrix(W, a, b).T))
+                    ge = w[ci, bi, p] * _edge_grads(img, gb, a, b, c, d)
+                    gk[j] += ge[0]
+                    gk[j + 1] += ge[1]
+                    gr[i] += ge[2]
+                    gr[i + 1] += ge[3]
+            ga, gbb = gk[0], gk[-1]
+            gc, gd = gr[0], gr[-1]
+            if nx == 2:
+                ga += gk[1] / 2
+                gbb += gk[1] / 2
+            if ny == 2:
+                gc += gr[1] / 2
+                gd += gr[1] / 2
+            gbox[ci, bi] = [ga + gbb, gc + gd, gbb - ga, gd - gc]
+    return gbox, gw
 
 
 # ---------------------------------------------------------------------------

@@ -452,6 +452,99 @@ def test_clip_unit_params_closed_form():
 
 
 # --------------------------------------------------------------------------
+# Kernel splitting (reading R15)
+# --------------------------------------------------------------------------
+def _split_case(mode, seed=28, N=1, C=2, B=2, H=11, W=9):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((N, C, H, W))
+    bx = _real_boxes(rng, C, B, cmax=3.0, rmin=0.5, rmax=4.0)
+    P = O.SPLIT_MODES[mode][0] * O.SPLIT_MODES[mode][1]
+    w = rng.standard_normal((C, B, P))
+    return rng, x, bx, w
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_equal_weights_is_the_box(mode):
+    _, x, bx, w = _split_case(mode)
+    ones = np.ones_like(w)
+    np.testing.assert_allclose(O.box_forward_split(x, bx, ones, mode), O.box_forward(x, bx), rtol=0, atol=1e-12)
+    g = np.random.default_rng(29).standard_normal((1, bx.shape[0] * bx.shape[1], 11, 9))
+    gbox, gw = O.box_backward_split_params(x, g, bx, ones, mode)
+    np.testing.assert_allclose(gbox, O.box_backward_params(x, g, bx), rtol=0, atol=1e-10)
+    # the piece sums add up to the box sum
+    np.testing.assert_allclose(gw.sum(-1), np.einsum("ncbhw,ncbhw->cb", g.reshape(1, 2, 2, 11, 9),
+                                                     O.box_forward(x, bx).reshape(1, 2, 2, 11, 9)), atol=1e-10)
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_piece_is_the_half_box(mode):
+    """One piece alone is the plain box over the half (quarter) of the box:
+    (cx -/+ rx/2, rx/2) in x, likewise in y -- built here from the box
+    parameters, not from the split edges."""
+    _, x, bx, w = _split_case(mode, seed=30)
+    ny, nx = O.SPLIT_MODES[mode]
+    for i in range(ny):
+        for j in range(nx):
+            sel = np.zeros_like(w)
+            sel[..., i * nx + j] = 1.0
+            half = bx.copy()
+            if nx == 2:
+                half[..., 0] = bx[..., 0] + (j - 0.5) * bx[..., 2]
+                half[..., 2] = bx[..., 2] / 2
+            if ny == 2:
+                half[..., 1] = bx[..., 1] + (i - 0.5) * bx[..., 3]
+                half[..., 3] = bx[..., 3] / 2
+            np.testing.assert_allclose(O.box_forward_split(x, bx, sel, mode), O.box_forward(x, half),
+                                       rtol=0, atol=1e-5)
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_backward_is_adjoint(mode):
+    rng, x, bx, w = _split_case(mode, seed=31)
+    g = rng.standard_normal((1, 4, 11, 9))
+    dx = O.box_backward_split_input(g, bx, w, mode, 11, 9)
+    lhs = np.sum(O.box_forward_split(x, bx, w, mode) * g)
+    assert abs(lhs - np.sum(x * dx)) <= 1e-12 * (1 + abs(lhs))
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_finite_differences(mode):
+    """L is linear in the piece weights and, inside one cell of every edge
+    (cut edges included), in each box parameter."""
+    rng = np.random.default_rng(32)
+    N, C, B, H, W = 1, 2, 2, 11, 9
+    x = rng.standard_normal((N, C, H, W))
+    g = rng.standard_normal((N, C * B, H, W))
+    bx = np.empty((C, B, 4), dtype=np.float32)
+    for c in range(C):
+        for b in range(B):
+            while True:
+                cand = np.float32([rng.uniform(-3, 3), rng.uniform(-3, 3), rng.uniform(0.8, 4), rng.uniform(0.8, 4)])
+                e = O.split_edges(cand[None, None], mode).ravel()
+                f = e - np.floor(e)
+                if np.all((f > 0.08) & (f < 0.92)):
+                    bx[c, b] = cand
+                    break
+    P = O.SPLIT_MODES[mode][0] * O.SPLIT_MODES[mode][1]
+    w = rng.standard_normal((C, B, P))
+    gbox, gw = O.box_backward_split_params(x, g, bx, w, mode)
+    L0 = np.sum(O.box_forward_split(x, bx, w, mode) * g)
+    for c in range(C):
+        for b in range(B):
+            for k in range(4):
+                q = bx.copy()
+                q[c, b, k] = np.float32(q[c, b, k] + np.float32(0.01))
+                h = float(q[c, b, k]) - float(bx[c, b, k])
+                fd = (np.sum(O.box_forward_split(x, q, w, mode) * g) - L0) / h
+                assert abs(fd - gbox[c, b, k]) <= 1e-7 * (1 + abs(fd)), (c, b, k, fd, gbox[c, b, k])
+            for p in range(P):
+                v = w.copy()
+                v[c, b, p] += 0.5
+                fd = (np.sum(O.box_forward_split(x, bx, v, mode) * g) - L0) / 0.5
+                assert abs(fd - gw[c, b, p]) <= 1e-9 * (1 + abs(fd))
+
+
+# --------------------------------------------------------------------------
 # Input gradient: adjoint of the forward map
 # --------------------------------------------------------------------------
 def test_input_grad_adjoint_and_mirrored_box():
@@ -780,6 +873,29 @@ def _mut_upsample_offset(g, H, W, stride):
     return out
 
 
+def _mut_split_at_thirds(boxes, mode):
+    e = _ORIG["split_edges"](boxes, mode)
+    ny, nx = O.SPLIT_MODES[mode]
+    if nx == 2:
+        a, b = e[..., 0, 0], e[..., 1, 1]
+        e[..., 0, 1] = e[..., 1, 0] = a + (b - a) / 3
+        if ny == 2:
+            e[..., 2, 1] = e[..., 3, 0] = a + (b - a) / 3
+    return e
+
+
+def _mut_split_box_grad_scaled(x, grad_y, boxes, piece_w, mode):
+    # a wrong factor on the box-parameter gradient (e.g. the cut edges'
+    # share counted twice)
+    gbox, gw = _ORIG["box_backward_split_params"](x, grad_y, boxes, piece_w, mode)
+    return gbox * 1.5, gw
+
+
+def _mut_split_weight_grad_swapped(x, grad_y, boxes, piece_w, mode):
+    gbox, gw = _ORIG["box_backward_split_params"](x, grad_y, boxes, piece_w, mode)
+    return gbox, gw[..., ::-1].copy()
+
+
 def _mut_rounded_floor(boxes):
     return tuple(np.floor(e) for e in _OM.box_edges(boxes))
 
@@ -799,7 +915,7 @@ def _mut_clip_no_swap(u):
 
 
 _ORIG = {k: getattr(_OM, k) for k in ("overlap_matrix", "_edge_selector", "boxes_from_unit",
-                                      "unit_grad_from_box_grad")}
+                                      "unit_grad_from_box_grad", "split_edges", "box_backward_split_params")}
 
 _MUTATIONS = {
     "edges_sign": ("box_edges", _mut_edges_sign),
@@ -817,6 +933,9 @@ _MUTATIONS = {
     "unit_full_scale": ("boxes_from_unit", _mut_unit_full_scale),
     "unit_grad_sign": ("unit_grad_from_box_grad", _mut_unit_grad_sign),
     "clip_no_swap": ("clip_unit_params", _mut_clip_no_swap),
+    "split_at_thirds": ("split_edges", _mut_split_at_thirds),
+    "split_box_grad_scaled": ("box_backward_split_params", _mut_split_box_grad_scaled),
+    "split_weight_grad_swapped": ("box_backward_split_params", _mut_split_weight_grad_swapped),
 }
 
 _PINS = [
@@ -831,6 +950,8 @@ _PINS = [
     lambda: test_strided_forward_equals_eq1_loops(2), test_strided_input_grad_is_adjoint,
     test_strided_param_grad_finite_difference_exact, test_unit_params_identity_and_corners,
     test_unit_grad_finite_difference, test_clip_unit_params_closed_form,
+    lambda: test_split_piece_is_the_half_box("4"), lambda: test_split_finite_differences("4"),
+    lambda: test_split_equal_weights_is_the_box("2x"),
 ]
 
 
