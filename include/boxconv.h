@@ -227,6 +227,47 @@ bc_status box_params_unit_grad(const float* grad_boxes, int C, int B, float max_
 bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Kernel splitting (Section 3.1, Fig. 2): each box is cut at its centre
+ * line(s), m = (a + b) / 2 and/or n = (c + d) / 2, into P pieces with their
+ * own learnable weights; the output is the weighted sum of the pieces' box
+ * integrals (each piece is a box of its own: 16 taps, same interpolation):
+ *   y[n][c*B+b] = sum_p piece_w[c][b][p] * (integral of x[n][c] over piece p).
+ * mode : BC_SPLIT_2X (P = 2: left, right halves), BC_SPLIT_2Y (P = 2: top,
+ *        bottom), BC_SPLIT_4 (P = 4: quadrants); piece p = i * nx + j covers
+ *        columns [k_j, k_{j+1}) of k = (a, m, b) (or (a, b)) and rows
+ *        [r_i, r_{i+1}) of r = (c, n, d) (or (c, d)); edges in fp64.
+ *        Other values: BC_ERR_UNSUPPORTED.
+ * x, boxes, grad_y, grad_x, grad_boxes : as box_conv_fwd / box_conv_bwd,
+ *        fp32 maps, stride 1, no flags.
+ * piece_w : device fp32 [C][B][P].
+ * y      : device [N][C*B][H][W], BC_F32 or BC_BF16.
+ * box_conv_split_bwd : gradients of L = <grad_y, y> (any of grad_x,
+ *        grad_boxes, grad_w may be NULL; all NULL is a no-op).  grad_boxes:
+ *        each piece's edge derivatives (Eq. 4) times its weight, summed onto
+ *        the box's edges, a cut edge contributing half to each of the two
+ *        edges it is the mean of; grad_w [C][B][P] = <grad_y, piece sum>.
+ *        Sums over n are fixed-order (deterministic).
+ * Limits : the map's table must fit in LDS (the tables of the HBM path are
+ *        not offered here): (H + 1) * ((W + 7) | 1) * 4 <= 64 KiB, and for
+ *        the backward at most 256 work items per map; BC_ERR_UNSUPPORTED
+ *        otherwise.  C * B <= 2^24.
+ * ws     : >= bc_split_workspace_bytes(op, ...) (op 0 = forward: the pieces'
+ *        tap records, 2*C*B*P*64 bytes; op 1 = backward: those plus per-wave
+ *        gradient partials).  The query returns 0 for an unsupported request.
+ * ---------------------------------------------------------------------- */
+#define BC_SPLIT_2X 1
+#define BC_SPLIT_2Y 2
+#define BC_SPLIT_4 3
+bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* piece_w,
+                             int N, int C, int H, int W, int B, int mode,
+                             void* y, bc_dtype y_dt, void* ws, size_t ws_bytes, hipStream_t stream);
+bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* piece_w,
+                             const float* grad_y, int N, int C, int H, int W, int B, int mode,
+                             float* grad_x, float* grad_boxes, float* grad_w,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int mode);
+
+/* ------------------------------------------------------------------------
  * pointwise_mix -- the 1x1 convolution over the C*B filtered maps
  * (Section 1, Section 3.2), per image n with P = H*W pixels, on MFMA:
  *   BC_MIX_FWD        : a = w [M][K], b = in [N][K][P]   -> out [N][M][P]

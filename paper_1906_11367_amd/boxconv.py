@@ -8,7 +8,8 @@ present, the calls raise -- there is no fallback implementation.
 Entry points (same names as the C ABI): box_prep, sat_build, box_conv_fwd,
 box_conv_bwd, box_conv_fwd_strided, box_conv_bwd_strided, pointwise_mix, the
 box-parameter reparameterisation (box_params_from_unit, box_params_unit_grad,
-box_params_clip), plus the workspace-size queries.
+box_params_clip), kernel splitting (box_conv_split_fwd, box_conv_split_bwd),
+plus the workspace-size queries.
 """
 from __future__ import annotations
 
@@ -23,6 +24,7 @@ LIB_PATH = os.path.join(_HERE, "libboxconv.so")
 BC_I32, BC_F32, BC_BF16 = 0, 1, 2
 BC_MIX_FWD, BC_MIX_BWD_DATA, BC_MIX_BWD_WEIGHT = 0, 1, 2
 BC_FLAG_MEAN_OFFSET, BC_FLAG_FORCE_HBM, BC_FLAG_INTEGER_CORNERS = 1, 2, 4
+BC_SPLIT_2X, BC_SPLIT_2Y, BC_SPLIT_4 = 1, 2, 3
 STATUS = {0: "BC_OK", 1: "BC_ERR_NULL", 2: "BC_ERR_SHAPE", 3: "BC_ERR_DTYPE", 4: "BC_ERR_ALIGN",
           5: "BC_ERR_WORKSPACE", 6: "BC_ERR_HIP", 7: "BC_ERR_UNSUPPORTED"}
 
@@ -39,6 +41,9 @@ SIGNATURES = {
     "box_params_clip": (_i, [_vp, _i, _i, _vp]),
     "box_conv_bwd_strided": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
     "pointwise_mix": (_i, [_i, _vp, _i, _vp, _i, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
+    "box_conv_split_fwd": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp, _sz, _vp]),
+    "box_conv_split_bwd": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bc_split_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
@@ -203,6 +208,55 @@ def box_params_clip(u: torch.Tensor):
     C, B = u.shape[0], u.shape[1]
     _check(load_library().box_params_clip(_ptr(u), C, B, _stream()), "box_params_clip")
     return u
+
+
+SPLIT_MODES = {"2x": BC_SPLIT_2X, "2y": BC_SPLIT_2Y, "4": BC_SPLIT_4}
+SPLIT_PIECES = {BC_SPLIT_2X: 2, BC_SPLIT_2Y: 2, BC_SPLIT_4: 4}
+
+
+def _split_mode(mode) -> int:
+    m = SPLIT_MODES.get(mode, mode)
+    if m not in SPLIT_PIECES:
+        raise BoxConvError(f"unknown split mode {mode!r}")
+    return m
+
+
+def split_workspace_bytes(op: int, N, C, H, W, B, mode) -> int:
+    return int(load_library().bc_split_workspace_bytes(op, N, C, H, W, B, _split_mode(mode)))
+
+
+def box_conv_split_fwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tensor, mode, y: torch.Tensor,
+                       ws: torch.Tensor | None = None):
+    """x [N, C, H, W] fp32, boxes [C, B, 4], piece_w [C, B, P] -> y [N, C*B, H, W] (fp32 or bf16).
+    mode: "2x", "2y", "4" or a BC_SPLIT_* code."""
+    m = _split_mode(mode)
+    N, C, H, W = x.shape
+    B = boxes.shape[1]
+    if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(y.shape) != (N, C * B, H, W):
+        raise BoxConvError("box_conv_split_fwd: piece_w or y has the wrong shape")
+    if ws is None:
+        ws = _workspace(split_workspace_bytes(0, N, C, H, W, B, m), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().box_conv_split_fwd(_ptr(x), _ptr(boxes), _ptr(piece_w), N, C, H, W, B, m, _ptr(y),
+                                             dtype_code(y), _ptr(ws), nbytes, _stream()), "box_conv_split_fwd")
+    return y
+
+
+def box_conv_split_bwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tensor, mode, grad_y: torch.Tensor,
+                       grad_x: torch.Tensor | None, grad_boxes: torch.Tensor | None,
+                       grad_w: torch.Tensor | None, ws: torch.Tensor | None = None):
+    m = _split_mode(mode)
+    N, C, H, W = x.shape
+    B = boxes.shape[1]
+    if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(grad_y.shape) != (N, C * B, H, W):
+        raise BoxConvError("box_conv_split_bwd: piece_w or grad_y has the wrong shape")
+    if ws is None:
+        ws = _workspace(split_workspace_bytes(1, N, C, H, W, B, m), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().box_conv_split_bwd(_ptr(x), _ptr(boxes), _ptr(piece_w), _ptr(grad_y), N, C, H, W, B, m,
+                                             _ptr(grad_x), _ptr(grad_boxes), _ptr(grad_w), _ptr(ws), nbytes,
+                                             _stream()), "box_conv_split_bwd")
+    return grad_x, grad_boxes, grad_w
 
 
 def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):

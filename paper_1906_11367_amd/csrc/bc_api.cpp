@@ -207,6 +207,84 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   return box_conv_bwd_strided(x, boxes, grad_y, N, C, H, W, B, 1, grad_x, grad_boxes, flags, ws, ws_bytes, stream);
 }
 
+// Kernel splitting: pieces per box along x and y of a split mode, or 0.
+static int split_pieces(int mode, int& nx, int& ny) {
+  switch (mode) {
+    case BC_SPLIT_2X: nx = 2; ny = 1; return 2;
+    case BC_SPLIT_2Y: nx = 1; ny = 2; return 2;
+    case BC_SPLIT_4: nx = 2; ny = 2; return 4;
+  }
+  return 0;
+}
+
+// Split workspaces: the pieces' tap records at offset 0, then (backward) the
+// per-wave partials of 8 words (4 edge and 4 piece-weight gradients).
+static size_t split_taps_bytes(int C, int B, int P) { return align_up((size_t)2 * C * B * P * 16 * 4); }
+static int split_partial_rows(int N, int H, int W) { return N * bc::box_bwd_lds_waves(H, W); }
+
+static bool split_dims_ok(int N, int C, int H, int W, int B) {
+  return dims_ok(N, C, H, W, B) && (long)C * B <= (1L << 24);
+}
+
+size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int mode) {
+  int nx, ny;
+  const int P = split_pieces(mode, nx, ny);
+  if (P == 0 || !split_dims_ok(N, C, H, W, B)) return 0;
+  if (op == 0) return split_taps_bytes(C, B, P);
+  if (op == 1) {
+    if (!bwd_lds_fits(H, W)) return 0;
+    return split_taps_bytes(C, B, P) + align_up((size_t)split_partial_rows(N, H, W) * C * B * 8 * 4);
+  }
+  return 0;
+}
+
+bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* piece_w, int N, int C, int H, int W,
+                             int B, int mode, void* y, bc_dtype y_dt, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  if (!x || !boxes || !piece_w || !y) return BC_ERR_NULL;
+  if (!split_dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  int nx, ny;
+  const int P = split_pieces(mode, nx, ny);
+  if (P == 0) return BC_ERR_UNSUPPORTED;
+  if (y_dt != BC_F32 && y_dt != BC_BF16) return BC_ERR_DTYPE;
+  if (!fwd_lds_fits(H, W)) return BC_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(y)) return BC_ERR_ALIGN;
+  if (!ws || ws_bytes < split_taps_bytes(C, B, P)) return BC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BC_ERR_ALIGN;
+  hipError_t e = bc::launch_box_prep_split(boxes, C, B, nx, ny, ws, stream);
+  if (e != hipSuccess) return BC_ERR_HIP;
+  return hip_status(bc::launch_box_fwd_lds_split(x, static_cast<const int*>(ws), piece_w, y, y_dt == BC_BF16, N, C,
+                                                 H, W, B, P, stream));
+}
+
+bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* piece_w, const float* grad_y, int N,
+                             int C, int H, int W, int B, int mode, float* grad_x, float* grad_boxes, float* grad_w,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!x || !boxes || !piece_w || !grad_y) return BC_ERR_NULL;
+  if (!split_dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
+  int nx, ny;
+  const int P = split_pieces(mode, nx, ny);
+  if (P == 0) return BC_ERR_UNSUPPORTED;
+  if (!bwd_lds_fits(H, W)) return BC_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(grad_y) ||
+      (grad_x && !aligned16(grad_x)) || (grad_boxes && !aligned16(grad_boxes)) || (grad_w && !aligned16(grad_w)))
+    return BC_ERR_ALIGN;
+  if (!grad_x && !grad_boxes && !grad_w) return BC_OK;
+  const size_t taps = split_taps_bytes(C, B, P);
+  const int rows = split_partial_rows(N, H, W);
+  if (!ws || ws_bytes < taps + align_up((size_t)rows * C * B * 8 * 4)) return BC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BC_ERR_ALIGN;
+  char* base = static_cast<char*>(ws);
+  float* partials = reinterpret_cast<float*>(base + taps);
+  hipError_t e = bc::launch_box_prep_split(boxes, C, B, nx, ny, base, stream);
+  if (e == hipSuccess)
+    e = bc::launch_box_bwd_lds_split(x, reinterpret_cast<const int*>(base), piece_w, grad_y, grad_x, partials, N, C,
+                                     H, W, B, nx, ny, stream);
+  if (e == hipSuccess && (grad_boxes || grad_w))
+    e = bc::launch_split_grad_reduce(partials, rows, C * B, P, grad_boxes, grad_w, stream);
+  return hip_status(e);
+}
+
 static bool unit_args_ok(int C, int B, float mw, float mh) {
   return C > 0 && B > 0 && (long)C * B <= (1L << 28) && mw > 0.f && mh > 0.f && mw <= 1e6f && mh <= 1e6f;
 }

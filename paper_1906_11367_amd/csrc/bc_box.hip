@@ -951,6 +951,208 @@ __global__ __launch_bounds__(256) void k_box_grad_reduce(const float* __restrict
 }
 
 // ---------------------------------------------------------------------------
+// Kernel splitting (Section 3.1, Fig. 2): a box cut at its centre line(s)
+// m = (a + b) / 2, n = (c + d) / 2 into nx * ny pieces with their own
+// weights; the output is the weighted sum of the pieces' box sums.
+// ---------------------------------------------------------------------------
+// Records of the pieces: [2][C*B][P] of 16 words (the pieces' forward taps,
+// then their adjoint taps); piece p = i * nx + j of a box covers columns
+// [k_j, k_{j+1}) and rows [r_i, r_{i+1}) of k = (a, m, b) or (a, b) and
+// r = (c, n, d) or (c, d), all in fp64.
+__global__ void k_box_prep_split(const float* __restrict__ boxes, int CB, int nx, int ny, int* __restrict__ table) {
+  const int P = nx * ny;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 2 * CB * P) return;
+  const bool adj = i >= CB * P;
+  const int k = adj ? i - CB * P : i;
+  const int box = k / P, pc = k - box * P;
+  const int pi = pc / nx, pj = pc - pi * nx;
+  const float* q = boxes + (size_t)box * 4;
+  const double cx = q[0], cy = q[1], rx = q[2], ry = q[3];
+  const double a = 0.5 + cx - rx, b = 0.5 + cx + rx, c = 0.5 + cy - ry, d = 0.5 + cy + ry;
+  const double m = (a + b) / 2, n = (c + d) / 2;
+  const double ka = (nx == 2 && pj == 1) ? m : a, kb = (nx == 2 && pj == 0) ? m : b;
+  const double rc = (ny == 2 && pi == 1) ? n : c, rd = (ny == 2 && pi == 0) ? n : d;
+  const Taps<float> t = taps_from_edges(ka, kb, rc, rd, adj, 1 << 20, 1 << 20);
+  int* r = table + (size_t)i * 16;
+  float* f = reinterpret_cast<float*>(r);
+  r[0] = t.ox[0]; r[1] = t.ox[2]; r[2] = t.oy[0]; r[3] = t.oy[2];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) { f[4 + e] = t.wx[e]; f[8 + e] = t.wy[e]; r[12 + e] = 0; }
+}
+
+// Forward of split boxes on a map's table in LDS: as k_box_fwd_lds (a wave
+// per box), each item summing its pieces in registers -- each piece is one
+// walk with its weight folded into the y taps -- then storing once.
+template <typename OutT, int SEG>
+__global__ __launch_bounds__(256) void k_box_fwd_lds_split(const float* __restrict__ x, const int* __restrict__ taps,
+                                                           const float* __restrict__ piece_w, OutT* __restrict__ y,
+                                                           int C, int H, int W, int B, int P, int bpg,
+                                                           int per_box_p) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  float* S = reinterpret_cast<float*>(smem_raw);
+  const int pitch = lds_pitch_dev(W);
+  const int ngrp = (B + bpg - 1) / bpg;
+  const int map = blockIdx.x / ngrp, grp = blockIdx.x - map * ngrp, c = map % C;
+  build_table_lds(x + (size_t)map * H * W, S, H, W, pitch, 0.f, false);
+  const LdsTable<float> tab{S, pitch, W, H};
+  const int b0 = grp * bpg, nb = min(bpg, B - b0);
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
+  for (int it = threadIdx.x; it < nb * per_box_p; it += blockDim.x) {
+    const int bl = __builtin_amdgcn_readfirstlane(it / per_box_p);
+    const int r = it - bl * per_box_p;
+    if (r >= per_box) continue;
+    const int seg = r / nch, ch = r - seg * nch;
+    const int b = b0 + bl, cb = c * B + b;
+    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+    const bool full = y0 + SEG <= H && x0 + kQ <= W;
+    float acc[SEG][kQ];
+#pragma unroll
+    for (int s = 0; s < SEG; ++s)
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+    AccRows<SEG> em{acc};
+    for (int pc = 0; pc < P; ++pc) {
+      Taps<float> tp = load_taps(taps + ((size_t)cb * P + pc) * 16, W, H);
+      const float w = piece_w[(size_t)cb * P + pc];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) tp.wy[k] *= w;
+      if (full) box_walk<SEG, float, false, true>(tab, tp, H, W, x0, y0, y1, 0.f, em);
+      else box_walk<SEG, float, false, false>(tab, tp, H, W, x0, y0, y1, 0.f, em);
+    }
+    OutT* out = y + ((size_t)map * B + b) * H * W;
+#pragma unroll
+    for (int s = 0; s < SEG; ++s) {
+      if (y0 + s < H) {
+#pragma unroll
+        for (int q = 0; q < kQ; ++q)
+          if (x0 + q < W) out[(size_t)(y0 + s) * W + x0 + q] = convert_out<OutT, float>(acc[s][q]);
+      }
+    }
+  }
+}
+
+// Backward of split boxes, table in LDS: as k_box_bwd_lds, each box's
+// gradient table walked once per piece with the piece's adjoint taps (its
+// weight folded into the y taps for the input gradient).  Per piece the
+// walk's per-tap-row sums give the piece's edge gradients (edge_grads, times
+// its weight) and the weight gradient sum_r wy_r * P[8 + r] (the adjoint
+// piece sums weighted by x).  The pieces' edge gradients are summed onto the
+// box edges, a cut edge half to each edge it is the mean of.  Each wave
+// writes (dL/da, dL/db, dL/dc, dL/dd, dL/dw_0 .. dL/dw_3) to
+// partials[(n * nw + wave) * C*B + c*B + b][8].
+template <int SEG>
+__global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ taps,
+                                                           const float* __restrict__ piece_w,
+                                                           const float* __restrict__ gy, float* __restrict__ gx,
+                                                           float* __restrict__ partials, int C, int H, int W, int B,
+                                                           int nx, int ny) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int pitch = lds_pitch_dev(W);
+  float* SG = reinterpret_cast<float*>(smem_raw);
+  const int map = blockIdx.x, n = map / C, c = map - n * C;
+  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = threadIdx.x;
+  const bool active = it < nch * nseg;
+  const int seg = it / nch, ch = it - seg * nch;
+  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+  const bool full = y0 + SEG <= H && x0 + kQ <= W;
+  const size_t plane = (size_t)H * W;
+  const float* g0 = gy + (size_t)map * B * plane;
+  const int P = nx * ny;
+  float v[SEG][kQ], acc[SEG][kQ];
+  load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  const LdsTable<float> tg{SG, pitch, W, H};
+  const int* adj = taps + (size_t)C * B * P * 16;
+  for (int b = 0; b < B; ++b) {
+    __syncthreads();
+    build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
+    const int cb = c * B + b;
+    float gk[3] = {0.f, 0.f, 0.f}, gr[3] = {0.f, 0.f, 0.f}, gw[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int pc = 0; pc < P; ++pc) {
+      const Taps<float> tp = load_taps(adj + ((size_t)cb * P + pc) * 16, W, H);
+      const float w = piece_w[(size_t)cb * P + pc];
+      Taps<float> tw = tp;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) tw.wy[k] *= w;
+      float Ps[12];
+#pragma unroll
+      for (int k = 0; k < 12; ++k) Ps[k] = 0.f;
+      if (active) {
+        if (full) adjoint_walk<SEG, true>(tg, tw, x0, y0, y1, v, acc, Ps);
+        else adjoint_walk<SEG, false>(tg, tw, x0, y0, y1, v, acc, Ps);
+      }
+      float g4[4];
+      edge_grads(tp, Ps, g4);
+      const int pi = pc / nx, pj = pc - pi * nx;
+      gk[pj] += w * g4[0];
+      gk[pj + 1] += w * g4[1];
+      gr[pi] += w * g4[2];
+      gr[pi + 1] += w * g4[3];
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) s = fmaf(tp.wy[k], Ps[8 + k], s);
+      gw[pc] = s;
+    }
+    float g8[8];
+    g8[0] = gk[0] + (nx == 2 ? 0.5f * gk[1] : 0.f);
+    g8[1] = gk[nx] + (nx == 2 ? 0.5f * gk[1] : 0.f);
+    g8[2] = gr[0] + (ny == 2 ? 0.5f * gr[1] : 0.f);
+    g8[3] = gr[ny] + (ny == 2 ? 0.5f * gr[1] : 0.f);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) g8[4 + k] = gw[k];
+    float* pp = partials + (((size_t)n * nw + wave) * C * B + cb) * 8;
+    store_wave_partial(g8, pp);
+    store_wave_partial(g8 + 4, pp + 4);
+  }
+  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * plane, H, W, x0, y0, acc);
+}
+
+// Fixed-tree sum of the split partials [Pn][CB][8] (as k_box_grad_reduce) and
+// the change of variables of the box edges; the weight gradients as summed.
+__global__ __launch_bounds__(256) void k_split_grad_reduce(const float* __restrict__ partials, int Pn, int CB,
+                                                           int P, float* __restrict__ grad_boxes,
+                                                           float* __restrict__ grad_w) {
+  __shared__ float4 red[4][kReduceBoxes][2];
+  const int j = threadIdx.x % kReduceBoxes, q = threadIdx.x / kReduceBoxes;
+  const int i = blockIdx.x * kReduceBoxes + j;
+  float4 s0 = make_float4(0.f, 0.f, 0.f, 0.f), s1 = s0;
+  if (i < CB)
+    for (int p = q; p < Pn; p += 256 / kReduceBoxes) {
+      const float4* v = reinterpret_cast<const float4*>(partials + ((size_t)p * CB + i) * 8);
+      const float4 a = v[0], b = v[1];
+      s0.x += a.x; s0.y += a.y; s0.z += a.z; s0.w += a.w;
+      s1.x += b.x; s1.y += b.y; s1.z += b.z; s1.w += b.w;
+    }
+#pragma unroll
+  for (int m = 16; m < 64; m <<= 1) {
+    s0.x += __shfl_xor(s0.x, m); s0.y += __shfl_xor(s0.y, m); s0.z += __shfl_xor(s0.z, m); s0.w += __shfl_xor(s0.w, m);
+    s1.x += __shfl_xor(s1.x, m); s1.y += __shfl_xor(s1.y, m); s1.z += __shfl_xor(s1.z, m); s1.w += __shfl_xor(s1.w, m);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) < kReduceBoxes) { red[wave][j][0] = s0; red[wave][j][1] = s1; }
+  __syncthreads();
+  if (threadIdx.x < kReduceBoxes && i < CB) {
+    float t[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float4 a = red[w][j][0], b = red[w][j][1];
+      t[0] += a.x; t[1] += a.y; t[2] += a.z; t[3] += a.w;
+      t[4] += b.x; t[5] += b.y; t[6] += b.z; t[7] += b.w;
+    }
+    if (grad_boxes)
+      *reinterpret_cast<float4*>(grad_boxes + (size_t)i * 4) = make_float4(t[0] + t[1], t[2] + t[3], t[1] - t[0], t[3] - t[2]);
+    if (grad_w)
+      for (int k = 0; k < P; ++k) grad_w[(size_t)i * P + k] = t[4 + k];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 static hipError_t last_error() { return hipGetLastError(); }
@@ -1145,6 +1347,50 @@ hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* 
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes, hipStream_t s) {
   hipLaunchKernelGGL(k_box_grad_reduce, dim3((CB + kReduceBoxes - 1) / kReduceBoxes), dim3(256), 0, s, partials, P, CB,
                      grad_boxes);
+  return last_error();
+}
+
+hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int ny, void* table, hipStream_t s) {
+  const int n = 2 * C * B * nx * ny;
+  hipLaunchKernelGGL(k_box_prep_split, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, nx, ny, (int*)table);
+  return last_error();
+}
+
+hipError_t launch_box_fwd_lds_split(const float* x, const int* taps, const float* piece_w, void* y, bool bf16_out,
+                                    int N, int C, int H, int W, int B, int P, hipStream_t s) {
+  constexpr int SEG = 16;
+  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
+  const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
+  if (bf16_out)
+    hipLaunchKernelGGL((k_box_fwd_lds_split<uint16_t, SEG>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s, x, taps,
+                       piece_w, (uint16_t*)y, C, H, W, B, P, g.bpg, g.per_box_p);
+  else
+    hipLaunchKernelGGL((k_box_fwd_lds_split<float, SEG>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s, x, taps,
+                       piece_w, (float*)y, C, H, W, B, P, g.bpg, g.per_box_p);
+  return last_error();
+}
+
+hipError_t launch_box_bwd_lds_split(const float* x, const int* taps, const float* piece_w, const float* gy, float* gx,
+                                    float* partials, int N, int C, int H, int W, int B, int nx, int ny,
+                                    hipStream_t s) {
+  const int seg = box_bwd_lds_seg(H, W);
+  if (seg == 0) return hipErrorInvalidValue;
+  const int items = n_chunks(W) * n_segs(H, seg);
+  const int threads = ((items + 63) / 64) * 64;
+  const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
+  if (seg == 8)
+    hipLaunchKernelGGL((k_box_bwd_lds_split<8>), dim3(N * C), dim3(threads), shm, s, x, taps, piece_w, gy, gx,
+                       partials, C, H, W, B, nx, ny);
+  else
+    hipLaunchKernelGGL((k_box_bwd_lds_split<4>), dim3(N * C), dim3(threads), shm, s, x, taps, piece_w, gy, gx,
+                       partials, C, H, W, B, nx, ny);
+  return last_error();
+}
+
+hipError_t launch_split_grad_reduce(const float* partials, int Pn, int CB, int P, float* grad_boxes, float* grad_w,
+                                    hipStream_t s) {
+  hipLaunchKernelGGL(k_split_grad_reduce, dim3((CB + kReduceBoxes - 1) / kReduceBoxes), dim3(256), 0, s, partials,
+                     Pn, CB, P, grad_boxes, grad_w);
   return last_error();
 }
 

@@ -61,6 +61,19 @@ hipError_t launch_unit_params(int op, const float* in, int n, float mw, float mh
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 
+// Kernel splitting (nx x ny pieces per box, fp32 maps, tables in LDS): piece
+// tap records [2][C*B][nx*ny][16], the forward, the backward (partials
+// [N * waves][C*B][8]) and the reduce to grad_boxes [C*B][4] and the piece
+// weights' gradient [C*B][nx*ny].
+hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int ny, void* table, hipStream_t s);
+hipError_t launch_box_fwd_lds_split(const float* x, const int* taps, const float* piece_w, void* y, bool bf16_out,
+                                    int N, int C, int H, int W, int B, int P, hipStream_t s);
+hipError_t launch_box_bwd_lds_split(const float* x, const int* taps, const float* piece_w, const float* gy, float* gx,
+                                    float* partials, int N, int C, int H, int W, int B, int nx, int ny,
+                                    hipStream_t s);
+hipError_t launch_split_grad_reduce(const float* partials, int Pn, int CB, int P, float* grad_boxes, float* grad_w,
+                                    hipStream_t s);
+
 // 1x1 mix GEMMs.
 hipError_t launch_mix(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out,
                       int out_dt, int N, int M, int K, int P, int compute_dt, int relu,

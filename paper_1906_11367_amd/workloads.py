@@ -24,7 +24,7 @@ import os
 
 import numpy as np
 
-TAG_X, TAG_BOXES, TAG_W, TAG_GRAD, TAG_UNIT = 0, 1, 2, 3, 4
+TAG_X, TAG_BOXES, TAG_W, TAG_GRAD, TAG_UNIT, TAG_PIECE = 0, 1, 2, 3, 4, 5
 
 
 @dataclasses.dataclass(frozen=True)
@@ -131,6 +131,13 @@ def make_unit_corners(wl: Workload, layer: int = 0) -> np.ndarray:
     g = _rng(wl.seed, TAG_UNIT, layer)
     u = np.sort(g.uniform(-0.5, 0.5, size=(wl.C, wl.B, 2, 2)), axis=-1)
     return u.reshape(wl.C, wl.B, 4).astype(np.float32)
+
+
+def make_piece_weights(wl: Workload, pieces: int, layer: int = 0) -> np.ndarray:
+    """Weights [C, B, pieces] fp32 of the pieces of split boxes, uniform in
+    [-1, 1] (learnable parameters; any sign)."""
+    g = _rng(wl.seed, TAG_PIECE, layer)
+    return g.uniform(-1.0, 1.0, size=(wl.C, wl.B, pieces)).astype(np.float32)
 
 
 def make_boxes(wl: Workload, layer: int = 0) -> np.ndarray:

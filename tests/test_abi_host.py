@@ -26,7 +26,8 @@ def declared_functions():
 def test_header_declares_the_four_entry_points():
     names = declared_functions()
     for n in ("sat_build", "box_conv_fwd", "box_conv_bwd", "pointwise_mix", "box_prep",
-              "bc_box_workspace_bytes", "bc_mix_workspace_bytes", "bc_status_string", "bc_abi_version"):
+              "bc_box_workspace_bytes", "bc_mix_workspace_bytes", "bc_status_string", "bc_abi_version",
+              "box_conv_split_fwd", "box_conv_split_bwd", "bc_split_workspace_bytes"):
         assert n in names, n
 
 
@@ -125,6 +126,43 @@ def test_unit_params_argument_errors():
     assert lib.box_params_unit_grad(FAKE, 2, 4, 64.0, 48.0, None, None) == 1
     assert lib.box_params_clip(None, 2, 4, None) == 1
     assert lib.box_params_clip(FAKE_MISALIGNED, 2, 4, None) == 4
+
+
+def test_split_argument_errors():
+    lib = bc.load_library()
+    fwd = [FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, bc.BC_SPLIT_4, FAKE, bc.BC_F32, None, 0, None]
+    assert lib.box_conv_split_fwd(*fwd) == 5                 # valid: fails only for lack of a workspace
+    a = list(fwd); a[2] = None
+    assert lib.box_conv_split_fwd(*a) == 1                   # piece weights are required
+    for bad in (0, 4, -1):
+        a = list(fwd); a[8] = bad
+        assert lib.box_conv_split_fwd(*a) == 7, bad
+    a = list(fwd); a[10] = bc.BC_I32
+    assert lib.box_conv_split_fwd(*a) == 3
+    a = list(fwd); a[5] = 256; a[6] = 256                  # table does not fit LDS: not offered
+    assert lib.box_conv_split_fwd(*a) == 7
+    a = list(fwd); a[2] = FAKE_MISALIGNED
+    assert lib.box_conv_split_fwd(*a) == 4
+    a = list(fwd); a[11] = FAKE; a[12] = lib.bc_split_workspace_bytes(0, 2, 3, 8, 8, 4, bc.BC_SPLIT_4) - 1
+    assert lib.box_conv_split_fwd(*a) == 5
+    bwd = [FAKE, FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, bc.BC_SPLIT_2X, FAKE, FAKE, FAKE, None, 0, None]
+    assert lib.box_conv_split_bwd(*bwd) == 5
+    a = list(bwd); a[10] = None; a[11] = None; a[12] = None  # nothing requested: no-op
+    assert lib.box_conv_split_bwd(*a) == 0
+    a = list(bwd); a[12] = FAKE_MISALIGNED
+    assert lib.box_conv_split_bwd(*a) == 4
+    a = list(bwd); a[9] = 9
+    assert lib.box_conv_split_bwd(*a) == 7
+    a = list(bwd); a[6] = 256; a[7] = 256
+    assert lib.box_conv_split_bwd(*a) == 7
+    # workspace: the pieces' records (2 * C*B * P * 64 bytes), and for the
+    # backward the 8-word partials of every wave of every image
+    assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) == 2 * 256 * 4 * 4 * 64
+    assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_2Y) == 2 * 256 * 4 * 2 * 64
+    assert lib.bc_split_workspace_bytes(1, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) >= \
+        2 * 256 * 4 * 4 * 64 + 32 * 256 * 4 * 32
+    assert lib.bc_split_workspace_bytes(1, 4, 8, 256, 256, 4, bc.BC_SPLIT_4) == 0
+    assert lib.bc_split_workspace_bytes(0, 4, 8, 64, 48, 4, 0) == 0
 
 
 def test_mix_argument_errors():

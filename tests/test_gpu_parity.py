@@ -482,6 +482,141 @@ def test_layer_unit_params_gradient():
 # ---------------------------------------------------------------------------
 # a7 / a8: backward of the box filter
 # ---------------------------------------------------------------------------
+# ---------------------------------------------------------------------------
+# f2: kernel splitting (pieces with their own weights)
+# ---------------------------------------------------------------------------
+SPLIT_CASES = [
+    (2, dict(N=2, C=3)),
+    (3, dict(N=3, C=2)),
+    (2, dict(N=1, C=3, H=37, W=29, B=5)),
+    (3, dict(N=2, C=2, H=17, W=100, B=3)),
+    (3, dict(N=1, C=1, H=1, W=1, B=2)),
+]
+
+
+def _split(x, bx, w, mode, g=None, y_dtype=torch.float32):
+    N, C, H, W = x.shape
+    B = bx.shape[1]
+    xd, bd, wd = dev(x), dev(bx), dev(w)
+    y = torch.empty((N, C * B, H, W), dtype=y_dtype, device="cuda")
+    bc.box_conv_split_fwd(xd, bd, wd, mode, y)
+    if g is None:
+        return host(y)
+    gx = torch.empty((N, C, H, W), dtype=torch.float32, device="cuda")
+    gb = torch.empty((C, B, 4), dtype=torch.float32, device="cuda")
+    gw = torch.empty_like(wd)
+    bc.box_conv_split_bwd(xd, bd, wd, mode, dev(g), gx, gb, gw)
+    return host(y), host(gx), host(gb), host(gw)
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+@pytest.mark.parametrize("key,scale", SPLIT_CASES)
+def test_split_fwd_bwd(mode, key, scale):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
+    d = wlmod.make_inputs(wl)
+    P = bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]]
+    w = wlmod.make_piece_weights(wl, P)
+    g = np.random.default_rng(120).standard_normal((wl.N, wl.C * wl.B, wl.H, wl.W)).astype(np.float32)
+    say(f"split {mode} {wl.key} {scale}")
+    y, gx, gb, gw = _split(d["x"], d["boxes"], w, mode, g)
+    check(y, O.box_forward_split(d["x"], d["boxes"], w, mode), RTOL_F32, "y")
+    check(gx, O.box_backward_split_input(g, d["boxes"], w, mode, wl.H, wl.W), RTOL_F32, "dx")
+    want_b, want_w = O.box_backward_split_params(d["x"], g, d["boxes"], w, mode)
+    check(gb, want_b, RTOL_F32, "dboxes")
+    check(gw, want_w, RTOL_F32, "dw")
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_cut_on_pixel_boundaries(mode):
+    """Boxes of even integer size: both the outer edges and the cut lie on
+    pixel boundaries, where every edge derivative is one-sided."""
+    rng = np.random.default_rng(121)
+    N, C, B, H, W = 2, 2, 4, 23, 19
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    g = rng.standard_normal((N, C * B, H, W)).astype(np.float32)
+    bx = np.empty((C, B, 4), dtype=np.float32)
+    for ax in range(2):
+        size = 2 * rng.integers(1, 6, size=(C, B))
+        lo = rng.integers(-8, 8, size=(C, B))
+        bx[..., ax] = lo + (size - 1) / 2.0
+        bx[..., 2 + ax] = size / 2.0
+    e = O.split_edges(bx, mode)
+    assert np.all(e == np.floor(e))
+    w = rng.uniform(-1, 1, size=(C, B, bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]])).astype(np.float32)
+    say(f"split {mode} integer cuts")
+    y, gx, gb, gw = _split(x, bx, w, mode, g)
+    check(y, O.box_forward_split(x, bx, w, mode), RTOL_F32, "y")
+    check(gx, O.box_backward_split_input(g, bx, w, mode, H, W), RTOL_F32, "dx")
+    want_b, want_w = O.box_backward_split_params(x, g, bx, w, mode)
+    check(gb, want_b, RTOL_F32, "dboxes")
+    check(gw, want_w, RTOL_F32, "dw")
+
+
+def test_split_bf16_output_is_rounded_fp32():
+    wl = wlmod.WORKLOADS[3].scaled(N=2, C=4)
+    d = wlmod.make_inputs(wl)
+    w = wlmod.make_piece_weights(wl, 4)
+    say("split 4 bf16 output")
+    got = _split(d["x"], d["boxes"], w, "4", y_dtype=torch.bfloat16)
+    ref = O.box_forward_split(d["x"], d["boxes"], w, "4")
+    # as for the unsplit forward: the fp32 value the kernel rounds is within
+    # the fp32 error bound of the oracle's, so its bf16 code is reachable
+    # from [r - e, r + e]
+    e = bb.scale_err(ref, bb.E_F32)
+    assert np.all(np.abs(got - O.bf16_round(ref)) <= bb.bf16_band(ref, e))
+    assert np.mean(got == O.bf16_round(ref)) > 0.9
+
+
+def test_split_unit_weights_equal_the_box_layer():
+    """All piece weights 1: the pieces tile the box, so the split layer is the
+    plain layer (same values up to rounding; the parameter gradients agree)."""
+    wl = wlmod.WORKLOADS[2].scaled(N=2, C=3)
+    d = wlmod.make_inputs(wl)
+    g = np.random.default_rng(122).standard_normal((wl.N, wl.C * wl.B, wl.H, wl.W)).astype(np.float32)
+    y0 = _fwd(d["x"], d["boxes"])
+    gx0, gb0 = _bwd(d["x"], d["boxes"], g)
+    for mode in ("2x", "2y", "4"):
+        ones = np.ones((wl.C, wl.B, bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]]), dtype=np.float32)
+        say(f"split {mode} unit weights vs plain layer")
+        y, gx, gb, _ = _split(d["x"], d["boxes"], ones, mode, g)
+        check(y, y0, RTOL_F32, "y")
+        check(gx, gx0, RTOL_F32, "dx")
+        check(gb, gb0, RTOL_F32, "dboxes")
+
+
+def test_split_deterministic():
+    wl = wlmod.WORKLOADS[3].scaled(N=2, C=4)
+    d = wlmod.make_inputs(wl)
+    w = wlmod.make_piece_weights(wl, 4)
+    g = np.random.default_rng(123).standard_normal((2, 16, 64, 48)).astype(np.float32)
+    a = _split(d["x"], d["boxes"], w, "4", g)
+    b = _split(d["x"], d["boxes"], w, "4", g)
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)
+
+
+def test_split_full_size_sampled():
+    """The pose-layer shape (32 x 256 maps of 64 x 48, 4 boxes each), split in
+    four: outputs and gradients of sampled channels against the oracle."""
+    wl = wlmod.WORKLOADS[3]
+    d = wlmod.make_inputs(wl)
+    w = wlmod.make_piece_weights(wl, 4)
+    N, C, H, W, B = wl.N, wl.C, wl.H, wl.W, wl.B
+    g = np.random.default_rng(124).standard_normal((N, C * B, H, W), dtype=np.float32)
+    say(f"split 4 full size {wl.key}")
+    y, gx, gb, gw = _split(d["x"], d["boxes"], w, "4", g)
+    rng = np.random.default_rng(125)
+    for c in rng.choice(C, size=3, replace=False):
+        ns = rng.choice(N, size=2, replace=False)
+        xs, bs, ws = d["x"][ns][:, [c]], d["boxes"][[c]], w[[c]]
+        gs = g[ns][:, c * B:(c + 1) * B]
+        check(y[ns][:, c * B:(c + 1) * B], O.box_forward_split(xs, bs, ws, "4"), RTOL_F32, f"y c={c}")
+        check(gx[ns][:, [c]], O.box_backward_split_input(gs, bs, ws, "4", H, W), RTOL_F32, f"dx c={c}")
+        want_b, want_w = O.box_backward_split_params(d["x"][:, [c]], g[:, c * B:(c + 1) * B], bs, ws, "4")
+        check(gb[[c]], want_b, RTOL_F32, f"dboxes c={c}")
+        check(gw[[c]], want_w, RTOL_F32, f"dw c={c}")
+
+
 def _bwd(x, bx, g, flags=0):
     N, C, H, W = x.shape
     B = bx.shape[1]
