@@ -53,6 +53,9 @@ def parse():
                    help="train the boxes as unit corners in [-1, 1] relative to a maximum box size equal to "
                         "the map size (drawn U[-0.5, 0.5]); the step then also converts them, takes their "
                         "gradient and clips them")
+    p.add_argument("--split", choices=["2x", "2y", "4"], default=None,
+                   help="kernel splitting: every box cut into 2 (along x or y) or 4 pieces with their own "
+                        "weights (fp32 maps, stride 1; the table-offset flag is not used)")
     p.add_argument("--serial", action="store_true",
                    help="run every call in order on one stream in the timed pass too (no overlapped "
                         "weight gradient): the configuration the per-kernel profiles are taken in")
@@ -86,9 +89,9 @@ def call_cost(label, wl, o_bytes, stride=1):
     px = wl.N * wl.C * wl.H * wl.W
     Ho, Wo = (wl.H + stride - 1) // stride, (wl.W + stride - 1) // stride
     pb = wl.N * wl.C * wl.B * Ho * Wo          # output pixel*box
-    if label == "box_conv_fwd":
+    if label in ("box_conv_fwd", "box_conv_split_fwd"):
         return {"bound": "hbm", "bytes": 4 * px + o_bytes * pb}
-    if label == "box_conv_bwd":
+    if label in ("box_conv_bwd", "box_conv_split_bwd"):
         return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 4 * px}
     flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * Ho * Wo
     z = 4 * wl.N * wl.mix_out * Ho * Wo
@@ -113,7 +116,7 @@ def load_traffic(label, wl_key, src_hash):
         return None
 
 
-def cpu_baseline(wl, d, budget_s, inference=False, stride=1):
+def cpu_baseline(wl, d, budget_s, inference=False, stride=1, split=None, piece_w=None):
     """Times the CPU oracle (fwd + bwd of the layer; with `inference`, the
     integer-corner forward only) on a sample of images.
 
@@ -141,6 +144,17 @@ def cpu_baseline(wl, d, budget_s, inference=False, stride=1):
             if wl.mix_out is not None:
                 O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
             return n * wl.C * wl.B * Ho * Wo
+        if split is not None:
+            o = O.box_forward_split(x, d["boxes"], piece_w, split)
+            if wl.mix_out is not None:
+                O.mix_forward(d["w"], o, compute=wl.mix_dtype, apply_relu=wl.relu)
+                if g is not None:
+                    O.mix_backward_weight(g, o, compute=wl.mix_dtype)
+                    g = O.mix_backward_data(d["w"], g, compute=wl.mix_dtype)
+            if g is not None:
+                O.box_backward_split_input(g, d["boxes"], piece_w, split, wl.H, wl.W)
+                O.box_backward_split_params(x, g, d["boxes"], piece_w, split)
+            return n * wl.C * wl.B * Ho * Wo
         o = O.box_forward(x, d["boxes"], stride=stride)
         if wl.mix_out is None:
             if g is not None:
@@ -164,6 +178,8 @@ def cpu_baseline(wl, d, budget_s, inference=False, stride=1):
         pb = run(n)
         t1 = time.perf_counter() - t0
     what = "integer-corner fwd" if inference else "fwd+bwd"
+    if split is not None:
+        what += f", boxes split {split}"
     return {"value": pb / t1 / 1e9, "unit": "Gpix·box/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} of {wl.N} images, all {wl.C} channels x {wl.B} boxes, one layer, "
                       f"{what}, fp64 NumPy, {t1:.1f} s"}
@@ -202,15 +218,24 @@ def main():
     grad = dev(d["grad"]) if d["grad"] is not None else None
     x_dt = torch.int32 if wl.x_kind == "int8range" else torch.float32
     flags = bc.BC_FLAG_MEAN_OFFSET if wl.mean_offset else 0
+    if args.split is not None:
+        if args.inference or args.stride != 1 or wl.x_kind == "int8range" or wl.layers > 1:
+            print("--split takes a one-layer fp32 workload with backward, stride 1", file=sys.stderr)
+            return 2
+        flags = 0
     backward = wl.backward and not args.inference
     if args.inference:
         flags |= bc.BC_FLAG_INTEGER_CORNERS
     s_ = args.stride
     unit = (float(wl.W), float(wl.H)) if args.unit_params else None
     st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, wl.mix_dtype, wl.relu, x_dt, flags,
-               backward, stride=s_, unit_size=unit)
+               backward, stride=s_, unit_size=unit, split=args.split)
     if unit is not None:
         params = [(dev(wlmod.make_unit_corners(wl, li)), w) for li, (_, w) in enumerate(params)]
+    piece_w = None
+    if args.split is not None:
+        piece_w = wlmod.make_piece_weights(wl, bc.SPLIT_PIECES[bc.SPLIT_MODES[args.split]])
+        params = [((b, dev(piece_w)), w) for b, w in params]
     if grad is not None and s_ > 1:
         grad = grad[..., ::s_, ::s_].contiguous()
     for plan in st.plans:
@@ -236,7 +261,7 @@ def main():
             st.backward(inputs, params, grad, t)
             if unit is not None:      # the per-update step on the unit corners
                 for plan, (u, _) in zip(st.plans, params):
-                    plan.clip(u)
+                    plan.clip(u[0] if args.split is not None else u)
                 if t:
                     t("box_params_clip")
 
@@ -311,7 +336,8 @@ def main():
     dom = max(calls, key=lambda k: calls[k]["avg_us"] * calls[k]["launches"])
     dc = calls[dom]
     traffic = load_traffic(dom, wl.key + ("_inference" if args.inference else "")
-                           + (f"_stride{args.stride}" if args.stride > 1 else ""), src_hash)
+                           + (f"_stride{args.stride}" if args.stride > 1 else "")
+                           + (f"_split{args.split}" if args.split else ""), src_hash)
     roofline = {"bound": dc["bound"], "achieved": dc["achieved"], "peak": dc["peak"], "unit": dc["unit"],
                 "frac": dc["frac"], "traffic": traffic, "kernel": dom, "avg_us": dc["avg_us"],
                 "per_launch": ("algo_bytes=%d" % dc["algo_bytes"]) if dc["bound"] == "hbm"
@@ -328,10 +354,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.key, "N": wl.N, "C": wl.C, "H": wl.H, "W": wl.W, "B": wl.B,
                    "mix": None if wl.mix_out is None else f"{wl.C * wl.B}->{wl.mix_out} {wl.mix_dtype}",
-                   "layers": wl.layers, "relu": wl.relu, "mean_offset": wl.mean_offset,
+                   "layers": wl.layers, "relu": wl.relu, "mean_offset": bool(flags & bc.BC_FLAG_MEAN_OFFSET),
                    "integer_corners": bool(args.inference), "backward": backward,
                    "overlap_weight_grad": backward and not args.serial, "stride": args.stride,
-                   "unit_params": bool(args.unit_params),
+                   "unit_params": bool(args.unit_params), "split": args.split,
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
         "roofline": roofline,
@@ -340,7 +366,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference, args.stride)
+        line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference, args.stride,
+                                            args.split, piece_w)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -5,6 +5,9 @@ Forward:  O = box_conv_fwd(x)            (bf16 copy when the mix runs in bf16)
 Backward: dW = pointwise_mix(BWD_WEIGHT, dZ, O)
           dO = pointwise_mix(BWD_DATA, w, dZ)
           dx, dboxes = box_conv_bwd(x, dO)
+With kernel splitting (`split` = "2x", "2y" or "4") the box filter is
+box_conv_split_fwd / box_conv_split_bwd: the boxes argument is then the pair
+(boxes, piece weights) and the backward returns the pair of their gradients.
 The weight gradient depends on neither of the other two backward calls; it
 runs on a second stream (default priority) alongside them, and the caller's
 stream waits for it before the backward returns.
@@ -41,6 +44,7 @@ class LayerPlan:
     # to that maximum box size (converted in the forward; the backward returns
     # dL/du); None: the boxes are (cx, cy, rx, ry) in pixels
     unit_size: tuple | None = None
+    split: str | None = None   # kernel splitting mode: None, "2x", "2y" or "4"
 
     def __post_init__(self):
         dev = torch.device(self.device)
@@ -59,7 +63,13 @@ class LayerPlan:
             o_dt = torch.float32
         self.o = torch.empty((N, K, Ho, Wo), dtype=o_dt, device=dev)
         self.compute = bc.BC_BF16 if self.mix_dtype == "bf16" else bc.BC_F32
-        self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
+        if self.split is not None:
+            if integer or self.stride != 1 or self.flags:
+                raise ValueError("kernel splitting takes fp32 maps, stride 1 and no box flags")
+            self.pieces = bc.SPLIT_PIECES[bc.SPLIT_MODES[self.split]]
+            self.ws_fwd = _ws(bc.split_workspace_bytes(0, N, C, H, W, B, self.split), dev)
+        else:
+            self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
         if self.unit_size is not None:
             self.boxes_px = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
         if self.M is not None:
@@ -68,7 +78,11 @@ class LayerPlan:
             self.w_c = (torch.empty((self.M, K), dtype=torch.bfloat16, device=dev)
                         if self.compute == bc.BC_BF16 else None)
         if self.with_backward:
-            self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
+            if self.split is not None:
+                self.ws_bwd = _ws(bc.split_workspace_bytes(1, N, C, H, W, B, self.split), dev)
+                self.dpiece = torch.empty((C, B, self.pieces), dtype=torch.float32, device=dev)
+            else:
+                self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
             self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
             self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
             if self.unit_size is not None:
@@ -86,10 +100,17 @@ class LayerPlan:
         """tap(label), if given, is called after each library call (the benchmark
         records a stream event there)."""
         tap = tap or _no_tap
+        piece_w = None
+        if self.split is not None:
+            boxes, piece_w = boxes
         if self.unit_size is not None:
             boxes = bc.box_params_from_unit(boxes, *self.unit_size, self.boxes_px)
-        bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd, stride=self.stride)
-        tap("box_conv_fwd")
+        if piece_w is not None:
+            bc.box_conv_split_fwd(x, boxes, piece_w, self.split, self.o, self.ws_fwd)
+            tap("box_conv_split_fwd")
+        else:
+            bc.box_conv_fwd(x, boxes, self.o, self.flags, self.ws_fwd, stride=self.stride)
+            tap("box_conv_fwd")
         if self.M is None:
             return self.o
         if self.w_c is not None:
@@ -111,6 +132,9 @@ class LayerPlan:
         overlap = tap is None and self.overlap
         tap = tap or _no_tap
         u = None
+        piece_w = None
+        if self.split is not None:
+            boxes, piece_w = boxes
         if self.unit_size is not None:
             u, boxes = boxes, self.boxes_px      # the forward's conversion of u
         if self.M is None:
@@ -138,11 +162,17 @@ class LayerPlan:
             do = self.do
             dw = self.dw
         grad_boxes = None if self.flags & bc.BC_FLAG_INTEGER_CORNERS else self.dboxes
-        bc.box_conv_bwd(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
-        tap("box_conv_bwd")
+        if piece_w is not None:
+            bc.box_conv_split_bwd(x, boxes, piece_w, self.split, do, self.dx, grad_boxes, self.dpiece, self.ws_bwd)
+            tap("box_conv_split_bwd")
+        else:
+            bc.box_conv_bwd(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
+            tap("box_conv_bwd")
         if u is not None and grad_boxes is not None:
             grad_boxes = bc.box_params_unit_grad(grad_boxes, *self.unit_size, self.du)
             tap("box_params")
+        if piece_w is not None:
+            grad_boxes = (grad_boxes, self.dpiece)
         if self.M is not None and overlap:
             main.wait_event(self.ev_dw)         # dW (and the reuse of O, dZ) ordered after the side stream
         return self.dx, grad_boxes, dw
@@ -167,11 +197,11 @@ class Stack:
     """`layers` box-conv layers in sequence; layer l's mix output feeds layer l+1."""
 
     def __init__(self, N, C, H, W, B, M, layers, mix_dtype, relu, x_dtype=torch.float32, flags=0,
-                 backward=True, device="cuda", stride=1, unit_size=None):
+                 backward=True, device="cuda", stride=1, unit_size=None, split=None):
         if layers > 1 and (M != C or stride != 1):
             raise ValueError("stacked layers need M == C and stride 1")
         self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device,
-                                stride=stride, unit_size=unit_size) for _ in range(layers)]
+                                stride=stride, unit_size=unit_size, split=split) for _ in range(layers)]
 
     def forward(self, x, params, tap=None):
         """params: list of (boxes, w) device tensors.  Returns the inputs of every

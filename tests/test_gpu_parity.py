@@ -584,6 +584,35 @@ def test_split_unit_weights_equal_the_box_layer():
         check(gb, gb0, RTOL_F32, "dboxes")
 
 
+@pytest.mark.parametrize("relu", [False, True])
+def test_layer_split_fp32(relu):
+    """The whole layer with boxes split in four (fp32 mix, overlapped weight
+    gradient): outputs and every gradient against the oracle's split box
+    filter composed with its mix."""
+    wl = wlmod.WORKLOADS[2].scaled(N=2, C=8)
+    d = wlmod.make_inputs(wl)
+    pw = wlmod.make_piece_weights(wl, 4)
+    g = np.random.default_rng(126).standard_normal((wl.N, wl.mix_out, wl.H, wl.W)).astype(np.float32)
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, "f32", relu, 0, True, split="4")
+    xd, wd = dev(d["x"]), dev(d["w"])
+    params = (dev(d["boxes"]), dev(pw))
+    say(f"layer split 4 relu={relu}")
+    z = plan.forward(xd, params, wd)
+    dx, (db, dpw), dw = plan.backward(xd, params, wd, dev(g))
+    torch.cuda.synchronize()
+    o = O.box_forward_split(d["x"], d["boxes"], pw, "4")
+    zr = O.mix_forward(d["w"], o, compute="f32", apply_relu=relu)
+    check(host(z), zr, RTOL_F32, "Z")
+    # the ReLU mask is taken from the layer's fp32 output on both sides
+    mask = host(z) if relu else None
+    do = O.mix_backward_data(d["w"], g, compute="f32", relu_out=mask)
+    check(host(dw), O.mix_backward_weight(g, o, compute="f32", relu_out=mask), RTOL_F32, "dW")
+    check(host(dx), O.box_backward_split_input(do, d["boxes"], pw, "4", wl.H, wl.W), RTOL_F32, "dx")
+    want_b, want_w = O.box_backward_split_params(d["x"], do, d["boxes"], pw, "4")
+    check(host(db), want_b, RTOL_F32, "dboxes")
+    check(host(dpw), want_w, RTOL_F32, "dpiece_w")
+
+
 def test_split_deterministic():
     wl = wlmod.WORKLOADS[3].scaled(N=2, C=4)
     d = wlmod.make_inputs(wl)
