@@ -217,8 +217,10 @@ static int split_pieces(int mode, int& nx, int& ny) {
   return 0;
 }
 
-// Split workspaces: the pieces' tap records at offset 0, then (backward) the
-// per-wave partials of 8 words (4 edge and 4 piece-weight gradients).
+// Split workspaces: forward, the boxes' corner records (32 words per box);
+// backward, the pieces' tap records at offset 0, then the per-wave partials
+// of 8 words (4 edge and 4 piece-weight gradients).
+static size_t split_corner_bytes(int C, int B) { return align_up((size_t)C * B * 32 * 4); }
 static size_t split_taps_bytes(int C, int B, int P) { return align_up((size_t)2 * C * B * P * 16 * 4); }
 static int split_partial_rows(int N, int H, int W) { return N * bc::box_bwd_lds_waves(H, W); }
 
@@ -230,7 +232,7 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
   int nx, ny;
   const int P = split_pieces(mode, nx, ny);
   if (P == 0 || !split_dims_ok(N, C, H, W, B)) return 0;
-  if (op == 0) return split_taps_bytes(C, B, P);
+  if (op == 0) return split_corner_bytes(C, B);
   if (op == 1) {
     if (!bwd_lds_fits(H, W)) return 0;
     return split_taps_bytes(C, B, P) + align_up((size_t)split_partial_rows(N, H, W) * C * B * 8 * 4);
@@ -249,12 +251,12 @@ bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* pi
   if (y_dt != BC_F32 && y_dt != BC_BF16) return BC_ERR_DTYPE;
   if (!fwd_lds_fits(H, W)) return BC_ERR_UNSUPPORTED;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(y)) return BC_ERR_ALIGN;
-  if (!ws || ws_bytes < split_taps_bytes(C, B, P)) return BC_ERR_WORKSPACE;
+  if (!ws || ws_bytes < split_corner_bytes(C, B)) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
-  hipError_t e = bc::launch_box_prep_split(boxes, C, B, nx, ny, ws, stream);
+  hipError_t e = bc::launch_box_prep_corners(boxes, piece_w, C, B, nx, ny, ws, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  return hip_status(bc::launch_box_fwd_lds_split(x, static_cast<const int*>(ws), piece_w, y, y_dt == BC_BF16, N, C,
-                                                 H, W, B, P, stream));
+  return hip_status(bc::launch_box_fwd_lds_split(x, static_cast<const int*>(ws), y, y_dt == BC_BF16, N, C, H, W, B,
+                                                 nx, ny, stream));
 }
 
 bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* piece_w, const float* grad_y, int N,

@@ -981,13 +981,127 @@ __global__ void k_box_prep_split(const float* __restrict__ boxes, int CB, int nx
   for (int e = 0; e < 4; ++e) { f[4 + e] = t.wx[e]; f[8 + e] = t.wy[e]; r[12 + e] = 0; }
 }
 
-// Forward of split boxes on a map's table in LDS: as k_box_fwd_lds (a wave
-// per box), each item summing its pieces in registers -- each piece is one
-// walk with its weight folded into the y taps -- then storing once.
-template <typename OutT, int SEG>
-__global__ __launch_bounds__(256) void k_box_fwd_lds_split(const float* __restrict__ x, const int* __restrict__ taps,
-                                                           const float* __restrict__ piece_w, OutT* __restrict__ y,
-                                                           int C, int H, int W, int B, int P, int bpg,
+// Corner records of split boxes for the forward, 32 words per box: a split
+// box is sum_{i,j} w_ij * (box sum over [k_j, k_{j+1}) x [r_i, r_{i+1})), and
+// each piece's box sum is the four-corner difference of the interpolated
+// table, so the whole box is sum over the (nx+1) x (ny+1) shared corners of
+// coef(ri, kj) * T(r_ri, k_kj) with
+//   coef(ri, kj) = w(ri-1, kj-1) - w(ri-1, kj) - w(ri, kj-1) + w(ri, kj)
+// (w = 0 outside the pieces): 9 interpolated corners for 4 pieces instead of
+// 16.  Words: 0..2 column-corner floors, 3..5 row-corner floors, 6..11 row
+// weights (1 - beta, beta) per row corner, 12..29 column weights
+// coef * (1 - alpha), coef * alpha per (row corner, column corner); fp64
+// edges and products, each weight rounded once.
+__global__ void k_box_prep_corners(const float* __restrict__ boxes, const float* __restrict__ piece_w, int CB,
+                                   int nx, int ny, int* __restrict__ table) {
+  const int box = blockIdx.x * blockDim.x + threadIdx.x;
+  if (box >= CB) return;
+  const float* q = boxes + (size_t)box * 4;
+  const double cx = q[0], cy = q[1], rx = q[2], ry = q[3];
+  const double a = 0.5 + cx - rx, b = 0.5 + cx + rx, c = 0.5 + cy - ry, d = 0.5 + cy + ry;
+  const double ke[3] = {a, nx == 2 ? (a + b) / 2 : b, b};
+  const double re[3] = {c, ny == 2 ? (c + d) / 2 : d, d};
+  const float* wp = piece_w + (size_t)box * nx * ny;
+  auto w = [&](int i, int j) -> double {
+    return (i < 0 || j < 0 || i >= ny || j >= nx) ? 0.0 : (double)wp[i * nx + j];
+  };
+  int* r = table + (size_t)box * 32;
+  float* f = reinterpret_cast<float*>(r);
+  double alpha[3];
+  for (int k = 0; k <= nx; ++k) {
+    int fl;
+    edge_split(ke[k], 1 << 20, fl, alpha[k]);
+    r[k] = fl;
+  }
+  for (int i = 0; i <= ny; ++i) {
+    int fl;
+    double beta;
+    edge_split(re[i], 1 << 20, fl, beta);
+    r[3 + i] = fl;
+    f[6 + 2 * i] = (float)(1.0 - beta);
+    f[7 + 2 * i] = (float)beta;
+    for (int k = 0; k <= nx; ++k) {
+      const double cf = w(i - 1, k - 1) - w(i - 1, k) - w(i, k - 1) + w(i, k);
+      f[12 + (i * 3 + k) * 2] = (float)(cf * (1.0 - alpha[k]));
+      f[13 + (i * 3 + k) * 2] = (float)(cf * alpha[k]);
+    }
+  }
+  for (int k = 30; k < 32; ++k) r[k] = 0;
+}
+
+// Forward walk of a split box over its shared corners (record above), on a
+// map's table in LDS: per table row v and row corner ri the column-weighted
+// row R_ri(v)[q] = sum_kj cw0 * S(v, x+f_kj) + cw1 * S(v, x+f_kj+1), and the
+// output of row y is sum_ri (1-beta) R_ri(y+f_ri) + beta R_ri(y+f_ri+1).
+// Each step reads one new table row per row corner (NXC runs of kQ+1 words)
+// and reuses the one from the step before.
+template <int SEG, int NXC, int NYC, bool kFull, typename Emit>
+__device__ __forceinline__ void corner_walk(const LdsTable<float>& S, const int* __restrict__ rec, int x0, int y0,
+                                            int y1, Emit& emit) {
+  const float* f = reinterpret_cast<const float*>(rec);
+  const int W = S.W, H = S.H;
+  const char* base = reinterpret_cast<const char*>(S.p + kPad);
+  const char* col[NXC];
+  float cw[NYC][NXC][2], wy[NYC][2];
+  int rc[NYC];
+  const int st = S.row_step();
+#pragma unroll
+  for (int k = 0; k < NXC; ++k) col[k] = base + clampi(x0 + clampi(rec[k], -(W + 1), W + 1), -kPad, W) * 4;
+#pragma unroll
+  for (int i = 0; i < NYC; ++i) {
+    rc[i] = (y0 + clampi(rec[3 + i], -(H + 1), H + 1)) * st;
+    wy[i][0] = f[6 + 2 * i];
+    wy[i][1] = f[7 + 2 * i];
+#pragma unroll
+    for (int k = 0; k < NXC; ++k) {
+      cw[i][k][0] = f[12 + (i * 3 + k) * 2];
+      cw[i][k][1] = f[13 + (i * 3 + k) * 2];
+    }
+  }
+  const int hi = H * st;
+  auto row = [&](int i, int coord, float* R) {
+    const int off = med3_i32(coord, hi);
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) R[q] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NXC; ++k) {
+      const float* sa = reinterpret_cast<const float*>(col[k] + off);
+      float v[kQ + 1];
+#pragma unroll
+      for (int t = 0; t <= kQ; ++t) v[t] = sa[t];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) R[q] = fmaf(cw[i][k][0], v[q], fmaf(cw[i][k][1], v[q + 1], R[q]));
+    }
+  };
+  float Rc[NYC][kQ];
+#pragma unroll
+  for (int i = 0; i < NYC; ++i) row(i, rc[i], Rc[i]);
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    if (kFull || y0 + s < y1) {
+      float o[kQ];
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) o[q] = 0.f;
+#pragma unroll
+      for (int i = 0; i < NYC; ++i) {
+        float Rn[kQ];
+        row(i, rc[i] + (s + 1) * st, Rn);
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+          o[q] = fmaf(wy[i][0], Rc[i][q], fmaf(wy[i][1], Rn[q], o[q]));
+          Rc[i][q] = Rn[q];
+        }
+      }
+      emit.template put<kFull>(s, o);
+    }
+  }
+}
+
+// Forward of split boxes, table in LDS: as k_box_fwd_lds (a wave per box,
+// items of 3 columns x SEG rows), each item walking its box's shared corners.
+template <typename OutT, int SEG, int NXC, int NYC>
+__global__ __launch_bounds__(256) void k_box_fwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
+                                                           OutT* __restrict__ y, int C, int H, int W, int B, int bpg,
                                                            int per_box_p) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   float* S = reinterpret_cast<float*>(smem_raw);
@@ -1003,32 +1117,13 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds_split(const float* __restri
     const int r = it - bl * per_box_p;
     if (r >= per_box) continue;
     const int seg = r / nch, ch = r - seg * nch;
-    const int b = b0 + bl, cb = c * B + b;
-    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-    const bool full = y0 + SEG <= H && x0 + kQ <= W;
-    float acc[SEG][kQ];
-#pragma unroll
-    for (int s = 0; s < SEG; ++s)
-#pragma unroll
-      for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
-    AccRows<SEG> em{acc};
-    for (int pc = 0; pc < P; ++pc) {
-      Taps<float> tp = load_taps(taps + ((size_t)cb * P + pc) * 16, W, H);
-      const float w = piece_w[(size_t)cb * P + pc];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) tp.wy[k] *= w;
-      if (full) box_walk<SEG, float, false, true>(tab, tp, H, W, x0, y0, y1, 0.f, em);
-      else box_walk<SEG, float, false, false>(tab, tp, H, W, x0, y0, y1, 0.f, em);
-    }
+    const int b = b0 + bl;
+    const int* rb = rec + (size_t)(c * B + b) * 32;
     OutT* out = y + ((size_t)map * B + b) * H * W;
-#pragma unroll
-    for (int s = 0; s < SEG; ++s) {
-      if (y0 + s < H) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q)
-          if (x0 + q < W) out[(size_t)(y0 + s) * W + x0 + q] = convert_out<OutT, float>(acc[s][q]);
-      }
-    }
+    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+    StoreRows<OutT, float> em{out, W, x0, y0 * W + x0};
+    if (y0 + SEG <= H && x0 + kQ <= W) corner_walk<SEG, NXC, NYC, true>(tab, rb, x0, y0, y1, em);
+    else corner_walk<SEG, NXC, NYC, false>(tab, rb, x0, y0, y1, em);
   }
 }
 
@@ -1356,17 +1451,35 @@ hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int n
   return last_error();
 }
 
-hipError_t launch_box_fwd_lds_split(const float* x, const int* taps, const float* piece_w, void* y, bool bf16_out,
-                                    int N, int C, int H, int W, int B, int P, hipStream_t s) {
+hipError_t launch_box_prep_corners(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
+                                   void* table, hipStream_t s) {
+  const int n = C * B;
+  hipLaunchKernelGGL(k_box_prep_corners, dim3((n + 255) / 256), dim3(256), 0, s, boxes, piece_w, n, nx, ny,
+                     (int*)table);
+  return last_error();
+}
+
+template <typename OutT, int NXC, int NYC>
+static void fwd_split_t(const float* x, const int* rec, void* y, int N, int C, int H, int W, int B, hipStream_t s) {
   constexpr int SEG = 16;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
   const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
-  if (bf16_out)
-    hipLaunchKernelGGL((k_box_fwd_lds_split<uint16_t, SEG>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s, x, taps,
-                       piece_w, (uint16_t*)y, C, H, W, B, P, g.bpg, g.per_box_p);
-  else
-    hipLaunchKernelGGL((k_box_fwd_lds_split<float, SEG>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s, x, taps,
-                       piece_w, (float*)y, C, H, W, B, P, g.bpg, g.per_box_p);
+  hipLaunchKernelGGL((k_box_fwd_lds_split<OutT, SEG, NXC, NYC>), dim3(N * C * g.ngrp), dim3(g.threads), shm, s, x,
+                     rec, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+}
+
+template <typename OutT>
+static void fwd_split_mode(const float* x, const int* rec, void* y, int N, int C, int H, int W, int B, int nx, int ny,
+                           hipStream_t s) {
+  if (nx == 2 && ny == 2) fwd_split_t<OutT, 3, 3>(x, rec, y, N, C, H, W, B, s);
+  else if (nx == 2) fwd_split_t<OutT, 3, 2>(x, rec, y, N, C, H, W, B, s);
+  else fwd_split_t<OutT, 2, 3>(x, rec, y, N, C, H, W, B, s);
+}
+
+hipError_t launch_box_fwd_lds_split(const float* x, const int* rec, void* y, bool bf16_out, int N, int C, int H, int W,
+                                    int B, int nx, int ny, hipStream_t s) {
+  if (bf16_out) fwd_split_mode<uint16_t>(x, rec, y, N, C, H, W, B, nx, ny, s);
+  else fwd_split_mode<float>(x, rec, y, N, C, H, W, B, nx, ny, s);
   return last_error();
 }
 

@@ -61,13 +61,17 @@ hipError_t launch_unit_params(int op, const float* in, int n, float mw, float mh
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 
-// Kernel splitting (nx x ny pieces per box, fp32 maps, tables in LDS): piece
-// tap records [2][C*B][nx*ny][16], the forward, the backward (partials
+// Kernel splitting (nx x ny pieces per box, fp32 maps, tables in LDS).
+// Backward: piece tap records [2][C*B][nx*ny][16], the backward (partials
 // [N * waves][C*B][8]) and the reduce to grad_boxes [C*B][4] and the piece
 // weights' gradient [C*B][nx*ny].
 hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int ny, void* table, hipStream_t s);
-hipError_t launch_box_fwd_lds_split(const float* x, const int* taps, const float* piece_w, void* y, bool bf16_out,
-                                    int N, int C, int H, int W, int B, int P, hipStream_t s);
+// Forward: corner records [C*B][32] (the pieces' shared corners with the
+// piece weights folded into per-corner coefficients).
+hipError_t launch_box_prep_corners(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
+                                   void* table, hipStream_t s);
+hipError_t launch_box_fwd_lds_split(const float* x, const int* rec, void* y, bool bf16_out, int N, int C, int H, int W,
+                                    int B, int nx, int ny, hipStream_t s);
 hipError_t launch_box_bwd_lds_split(const float* x, const int* taps, const float* piece_w, const float* gy, float* gx,
                                     float* partials, int N, int C, int H, int W, int B, int nx, int ny,
                                     hipStream_t s);
