@@ -253,9 +253,9 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
  *        otherwise.  C * B <= 2^24.
  * ws     : >= bc_split_workspace_bytes(op, ...) (op 0 = forward: one record
  *        of 128 bytes per box, its shared corners with the piece weights
- *        folded in; op 1 = backward: the pieces' tap records, 2*C*B*P*64
- *        bytes, plus per-wave gradient partials).  The query returns 0 for an
- *        unsupported request.
+ *        folded in; op 1 = backward: the same for the mirrored boxes, plus
+ *        per-wave gradient partials).  The query returns 0 for an unsupported
+ *        request.
  * ---------------------------------------------------------------------- */
 #define BC_SPLIT_2X 1
 #define BC_SPLIT_2Y 2

@@ -217,11 +217,10 @@ static int split_pieces(int mode, int& nx, int& ny) {
   return 0;
 }
 
-// Split workspaces: forward, the boxes' corner records (32 words per box);
-// backward, the pieces' tap records at offset 0, then the per-wave partials
-// of 8 words (4 edge and 4 piece-weight gradients).
+// Split workspaces: the boxes' corner records (32 words per box; the
+// backward's are those of the mirrored boxes) at offset 0, then (backward)
+// the per-wave partials of 8 words (4 edge and 4 piece-weight gradients).
 static size_t split_corner_bytes(int C, int B) { return align_up((size_t)C * B * 32 * 4); }
-static size_t split_taps_bytes(int C, int B, int P) { return align_up((size_t)2 * C * B * P * 16 * 4); }
 static int split_partial_rows(int N, int H, int W) { return N * bc::box_bwd_lds_waves(H, W); }
 
 static bool split_dims_ok(int N, int C, int H, int W, int B) {
@@ -235,7 +234,7 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
   if (op == 0) return split_corner_bytes(C, B);
   if (op == 1) {
     if (!bwd_lds_fits(H, W)) return 0;
-    return split_taps_bytes(C, B, P) + align_up((size_t)split_partial_rows(N, H, W) * C * B * 8 * 4);
+    return split_corner_bytes(C, B) + align_up((size_t)split_partial_rows(N, H, W) * C * B * 8 * 4);
   }
   return 0;
 }
@@ -272,16 +271,16 @@ bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* pi
       (grad_x && !aligned16(grad_x)) || (grad_boxes && !aligned16(grad_boxes)) || (grad_w && !aligned16(grad_w)))
     return BC_ERR_ALIGN;
   if (!grad_x && !grad_boxes && !grad_w) return BC_OK;
-  const size_t taps = split_taps_bytes(C, B, P);
+  const size_t taps = split_corner_bytes(C, B);
   const int rows = split_partial_rows(N, H, W);
   if (!ws || ws_bytes < taps + align_up((size_t)rows * C * B * 8 * 4)) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
   char* base = static_cast<char*>(ws);
   float* partials = reinterpret_cast<float*>(base + taps);
-  hipError_t e = bc::launch_box_prep_split(boxes, C, B, nx, ny, base, stream);
+  hipError_t e = bc::launch_box_prep_corners_adj(boxes, piece_w, C, B, nx, ny, base, stream);
   if (e == hipSuccess)
-    e = bc::launch_box_bwd_lds_split(x, reinterpret_cast<const int*>(base), piece_w, grad_y, grad_x, partials, N, C,
-                                     H, W, B, nx, ny, stream);
+    e = bc::launch_box_bwd_lds_split(x, reinterpret_cast<const int*>(base), grad_y, grad_x, partials, N, C, H, W, B,
+                                     nx, ny, stream);
   if (e == hipSuccess && (grad_boxes || grad_w))
     e = bc::launch_split_grad_reduce(partials, rows, C * B, P, grad_boxes, grad_w, stream);
   return hip_status(e);

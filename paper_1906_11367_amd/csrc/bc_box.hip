@@ -955,32 +955,6 @@ __global__ __launch_bounds__(256) void k_box_grad_reduce(const float* __restrict
 // m = (a + b) / 2, n = (c + d) / 2 into nx * ny pieces with their own
 // weights; the output is the weighted sum of the pieces' box sums.
 // ---------------------------------------------------------------------------
-// Records of the pieces: [2][C*B][P] of 16 words (the pieces' forward taps,
-// then their adjoint taps); piece p = i * nx + j of a box covers columns
-// [k_j, k_{j+1}) and rows [r_i, r_{i+1}) of k = (a, m, b) or (a, b) and
-// r = (c, n, d) or (c, d), all in fp64.
-__global__ void k_box_prep_split(const float* __restrict__ boxes, int CB, int nx, int ny, int* __restrict__ table) {
-  const int P = nx * ny;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 2 * CB * P) return;
-  const bool adj = i >= CB * P;
-  const int k = adj ? i - CB * P : i;
-  const int box = k / P, pc = k - box * P;
-  const int pi = pc / nx, pj = pc - pi * nx;
-  const float* q = boxes + (size_t)box * 4;
-  const double cx = q[0], cy = q[1], rx = q[2], ry = q[3];
-  const double a = 0.5 + cx - rx, b = 0.5 + cx + rx, c = 0.5 + cy - ry, d = 0.5 + cy + ry;
-  const double m = (a + b) / 2, n = (c + d) / 2;
-  const double ka = (nx == 2 && pj == 1) ? m : a, kb = (nx == 2 && pj == 0) ? m : b;
-  const double rc = (ny == 2 && pi == 1) ? n : c, rd = (ny == 2 && pi == 0) ? n : d;
-  const Taps<float> t = taps_from_edges(ka, kb, rc, rd, adj, 1 << 20, 1 << 20);
-  int* r = table + (size_t)i * 16;
-  float* f = reinterpret_cast<float*>(r);
-  r[0] = t.ox[0]; r[1] = t.ox[2]; r[2] = t.oy[0]; r[3] = t.oy[2];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) { f[4 + e] = t.wx[e]; f[8 + e] = t.wy[e]; r[12 + e] = 0; }
-}
-
 // Corner records of split boxes for the forward, 32 words per box: a split
 // box is sum_{i,j} w_ij * (box sum over [k_j, k_{j+1}) x [r_i, r_{i+1})), and
 // each piece's box sum is the four-corner difference of the interpolated
@@ -1127,21 +1101,136 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds_split(const float* __restri
   }
 }
 
-// Backward of split boxes, table in LDS: as k_box_bwd_lds, each box's
-// gradient table walked once per piece with the piece's adjoint taps (its
-// weight folded into the y taps for the input gradient).  Per piece the
-// walk's per-tap-row sums give the piece's edge gradients (edge_grads, times
-// its weight) and the weight gradient sum_r wy_r * P[8 + r] (the adjoint
-// piece sums weighted by x).  The pieces' edge gradients are summed onto the
-// box edges, a cut edge half to each edge it is the mean of.  Each wave
-// writes (dL/da, dL/db, dL/dc, dL/dd, dL/dw_0 .. dL/dw_3) to
+// Adjoint corner records of split boxes for the backward, 32 words per box.
+// The transpose of a split box's correlation is the mirrored split box: column
+// corners k' = 1 - (b, m, a), row corners r' = 1 - (d, n, c) (ascending), and
+// mirrored piece (i', j') carries w(ny-1-i', nx-1-j').  Each mirrored corner
+// is split as e = f + alpha with alpha in (0, 1] (f = ceil(e) - 1), so that
+// the column (row) difference across a corner is the one-sided derivative the
+// box gradient takes.  Words: 0..2 column floors, 3..5 row floors, 6..8
+// alpha, 9..11 beta, 12..20 coef'(ri, kj) of the mirrored pieces (as in the
+// forward corner record); fp64 edges, each word rounded once.
+__global__ void k_box_prep_corners_adj(const float* __restrict__ boxes, const float* __restrict__ piece_w, int CB,
+                                       int nx, int ny, int* __restrict__ table) {
+  const int box = blockIdx.x * blockDim.x + threadIdx.x;
+  if (box >= CB) return;
+  const float* q = boxes + (size_t)box * 4;
+  const double cx = q[0], cy = q[1], rx = q[2], ry = q[3];
+  const double a = 0.5 + cx - rx, b = 0.5 + cx + rx, c = 0.5 + cy - ry, d = 0.5 + cy + ry;
+  const double ke[3] = {1.0 - b, nx == 2 ? 1.0 - (a + b) / 2 : 1.0 - a, 1.0 - a};
+  const double re[3] = {1.0 - d, ny == 2 ? 1.0 - (c + d) / 2 : 1.0 - c, 1.0 - c};
+  const float* wp = piece_w + (size_t)box * nx * ny;
+  auto w = [&](int i, int j) -> double {  // weight of mirrored piece (i, j)
+    return (i < 0 || j < 0 || i >= ny || j >= nx) ? 0.0 : (double)wp[(ny - 1 - i) * nx + (nx - 1 - j)];
+  };
+  int* r = table + (size_t)box * 32;
+  float* f = reinterpret_cast<float*>(r);
+  for (int k = 0; k <= nx; ++k) {
+    int fl;
+    double al;
+    edge_split_upper(ke[k], 1 << 20, fl, al);
+    r[k] = fl;
+    f[6 + k] = (float)al;
+  }
+  for (int i = 0; i <= ny; ++i) {
+    int fl;
+    double be;
+    edge_split_upper(re[i], 1 << 20, fl, be);
+    r[3 + i] = fl;
+    f[9 + i] = (float)be;
+    for (int k = 0; k <= nx; ++k) f[12 + i * 3 + k] = (float)(w(i - 1, k - 1) - w(i - 1, k) - w(i, k - 1) + w(i, k));
+  }
+  for (int k = 21; k < 32; ++k) r[k] = 0;
+}
+
+// Backward walk of one split box over its mirrored corners on the table of
+// an upstream-gradient map (record above).  For a table row R read at step s
+// for row corner ri (R = y0 + s + f_ri + 1; R = y0 + f_ri at the start) and
+// column corner kj, with D = S(R, x+f_kj+1) - S(R, x+f_kj) and X = S(R,
+// x+f_kj) + alpha_kj * D (the row interpolated at the corner):
+//   input gradient: acc[s'][q] += coef(ri, kj) * wy * X for the output rows
+//     s' that read R (wy = beta for the row below the corner, 1 - beta for
+//     the row above);
+//   per-tap-row sums for the parameter gradient, with the input values v:
+//     PX[ri][t][kj] += v[s'] * X and PD[ri][t][kj] += v[s'] * D, t = 1 for
+//     the output row s' = s (R = its row f + 1), t = 0 for s' = s + 1.
+template <int SEG, int NXC, int NYC>
+__device__ __forceinline__ void corner_adjoint_walk(const LdsTable<float>& S, const int* __restrict__ rec, int x0,
+                                                    int y0, const float (&v)[SEG][kQ], float (&acc)[SEG][kQ],
+                                                    float (&PX)[NYC][2][NXC], float (&PD)[NYC][2][NXC]) {
+  const float* f = reinterpret_cast<const float*>(rec);
+  const int W = S.W, H = S.H;
+  const char* base = reinterpret_cast<const char*>(S.p + kPad);
+  const int st = S.row_step(), hi = H * st;
+  const char* col[NXC];
+  float al[NXC];
+#pragma unroll
+  for (int k = 0; k < NXC; ++k) {
+    col[k] = base + clampi(x0 + clampi(rec[k], -(W + 1), W + 1), -kPad, W) * 4;
+    al[k] = f[6 + k];
+  }
+#pragma unroll
+  for (int i = 0; i < NYC; ++i) {
+    const int r0 = (y0 + clampi(rec[3 + i], -(H + 1), H + 1)) * st;
+    const float be = f[9 + i], wy0 = 1.f - be;
+    float cf[NXC];
+#pragma unroll
+    for (int k = 0; k < NXC; ++k) cf[k] = f[12 + i * 3 + k];
+    // step s = -1 reads row y0 + f (the upper row of output row 0); step s
+    // reads row y0 + s + f + 1 (lower row of output s, upper row of s + 1)
+#pragma unroll
+    for (int s = -1; s < SEG; ++s) {
+      const int off = med3_i32(r0 + (s + 1) * st, hi);
+      float R[kQ] = {0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < NXC; ++k) {
+        const float* sa = reinterpret_cast<const float*>(col[k] + off);
+        float t[kQ + 1];
+#pragma unroll
+        for (int u = 0; u <= kQ; ++u) t[u] = sa[u];
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+          const float D = t[q + 1] - t[q];
+          const float X = fmaf(al[k], D, t[q]);
+          R[q] = fmaf(cf[k], X, R[q]);
+          if (s >= 0) {
+            PX[i][1][k] = fmaf(v[s][q], X, PX[i][1][k]);
+            PD[i][1][k] = fmaf(v[s][q], D, PD[i][1][k]);
+          }
+          if (s + 1 < SEG) {
+            PX[i][0][k] = fmaf(v[s + 1][q], X, PX[i][0][k]);
+            PD[i][0][k] = fmaf(v[s + 1][q], D, PD[i][0][k]);
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        if (s >= 0) acc[s][q] = fmaf(be, R[q], acc[s][q]);
+        if (s + 1 < SEG) acc[s + 1][q] = fmaf(wy0, R[q], acc[s + 1][q]);
+      }
+    }
+  }
+}
+
+// Backward of split boxes, table in LDS: as k_box_bwd_lds (one block per map,
+// one item of 3 columns x SEG rows per thread, input values in registers), one
+// walk over each box's mirrored corners.  From the per-tap-row sums, per
+// mirrored corner (ri, kj): Q = (1-beta) PX0 + beta PX1 (the corner's
+// lookup, weighted by x), QX = (1-beta) PD0 + beta PD1 (its x derivative),
+// QY = PX1 - PX0 (its y derivative); then
+//   dL/dk'_kj = sum_ri coef(ri, kj) QX,  dL/dr'_ri = sum_kj coef(ri, kj) QY,
+//   dL/dw'(i, j) = Q(i+1, j+1) - Q(i+1, j) - Q(i, j+1) + Q(i, j)
+// (the mirrored piece's adjoint sum weighted by x).  Mirroring back:
+// dL/dk_j = -dL/dk'_{nx-j}, a cut edge (the mean of the outer two) gives half
+// to each, and dL/dw(i, j) = dL/dw'(ny-1-i, nx-1-j).  Each wave writes
+// (dL/da, dL/db, dL/dc, dL/dd, dL/dw_0 .. dL/dw_3) to
 // partials[(n * nw + wave) * C*B + c*B + b][8].
-template <int SEG>
-__global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ taps,
-                                                           const float* __restrict__ piece_w,
+template <int SEG, int NXC, int NYC>
+__global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
                                                            const float* __restrict__ gy, float* __restrict__ gx,
-                                                           float* __restrict__ partials, int C, int H, int W, int B,
-                                                           int nx, int ny) {
+                                                           float* __restrict__ partials, int C, int H, int W,
+                                                           int B) {
+  constexpr int nx = NXC - 1, ny = NYC - 1;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -1151,11 +1240,9 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restri
   const int it = threadIdx.x;
   const bool active = it < nch * nseg;
   const int seg = it / nch, ch = it - seg * nch;
-  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  const bool full = y0 + SEG <= H && x0 + kQ <= W;
+  const int x0 = ch * kQ, y0 = seg * SEG;
   const size_t plane = (size_t)H * W;
   const float* g0 = gy + (size_t)map * B * plane;
-  const int P = nx * ny;
   float v[SEG][kQ], acc[SEG][kQ];
   load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
 #pragma unroll
@@ -1163,44 +1250,48 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restri
 #pragma unroll
     for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
   const LdsTable<float> tg{SG, pitch, W, H};
-  const int* adj = taps + (size_t)C * B * P * 16;
   for (int b = 0; b < B; ++b) {
     __syncthreads();
     build_table_lds(g0 + b * plane, SG, H, W, pitch, 0.f, false);
     const int cb = c * B + b;
-    float gk[3] = {0.f, 0.f, 0.f}, gr[3] = {0.f, 0.f, 0.f}, gw[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int pc = 0; pc < P; ++pc) {
-      const Taps<float> tp = load_taps(adj + ((size_t)cb * P + pc) * 16, W, H);
-      const float w = piece_w[(size_t)cb * P + pc];
-      Taps<float> tw = tp;
+    const int* rb = rec + (size_t)cb * 32;
+    float PX[NYC][2][NXC], PD[NYC][2][NXC];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) tw.wy[k] *= w;
-      float Ps[12];
+    for (int i = 0; i < NYC; ++i)
 #pragma unroll
-      for (int k = 0; k < 12; ++k) Ps[k] = 0.f;
-      if (active) {
-        if (full) adjoint_walk<SEG, true>(tg, tw, x0, y0, y1, v, acc, Ps);
-        else adjoint_walk<SEG, false>(tg, tw, x0, y0, y1, v, acc, Ps);
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int k = 0; k < NXC; ++k) { PX[i][t][k] = 0.f; PD[i][t][k] = 0.f; }
+    if (active) corner_adjoint_walk<SEG, NXC, NYC>(tg, rb, x0, y0, v, acc, PX, PD);
+    const float* f = reinterpret_cast<const float*>(rb);
+    float Q[NYC][NXC], gk[NXC], gr[NYC];
+#pragma unroll
+    for (int k = 0; k < NXC; ++k) gk[k] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NYC; ++i) {
+      const float be = f[9 + i], wy0 = 1.f - be;
+      gr[i] = 0.f;
+#pragma unroll
+      for (int k = 0; k < NXC; ++k) {
+        const float cf = f[12 + i * 3 + k];
+        Q[i][k] = fmaf(wy0, PX[i][0][k], be * PX[i][1][k]);
+        gk[k] = fmaf(cf, fmaf(wy0, PD[i][0][k], be * PD[i][1][k]), gk[k]);
+        gr[i] = fmaf(cf, PX[i][1][k] - PX[i][0][k], gr[i]);
       }
-      float g4[4];
-      edge_grads(tp, Ps, g4);
-      const int pi = pc / nx, pj = pc - pi * nx;
-      gk[pj] += w * g4[0];
-      gk[pj + 1] += w * g4[1];
-      gr[pi] += w * g4[2];
-      gr[pi + 1] += w * g4[3];
-      float s = 0.f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) s = fmaf(tp.wy[k], Ps[8 + k], s);
-      gw[pc] = s;
     }
+    // mirrored corner kj is original corner nx - kj, with the sign flipped
     float g8[8];
-    g8[0] = gk[0] + (nx == 2 ? 0.5f * gk[1] : 0.f);
-    g8[1] = gk[nx] + (nx == 2 ? 0.5f * gk[1] : 0.f);
-    g8[2] = gr[0] + (ny == 2 ? 0.5f * gr[1] : 0.f);
-    g8[3] = gr[ny] + (ny == 2 ? 0.5f * gr[1] : 0.f);
+    g8[0] = -gk[nx] - (nx == 2 ? 0.5f * gk[1] : 0.f);
+    g8[1] = -gk[0] - (nx == 2 ? 0.5f * gk[1] : 0.f);
+    g8[2] = -gr[ny] - (ny == 2 ? 0.5f * gr[1] : 0.f);
+    g8[3] = -gr[0] - (ny == 2 ? 0.5f * gr[1] : 0.f);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) g8[4 + k] = gw[k];
+    for (int k = 4; k < 8; ++k) g8[k] = 0.f;
+#pragma unroll
+    for (int i = 0; i < ny; ++i)
+#pragma unroll
+      for (int j = 0; j < nx; ++j)
+        g8[4 + (ny - 1 - i) * nx + (nx - 1 - j)] = (Q[i + 1][j + 1] - Q[i + 1][j]) - (Q[i][j + 1] - Q[i][j]);
     float* pp = partials + (((size_t)n * nw + wave) * C * B + cb) * 8;
     store_wave_partial(g8, pp);
     store_wave_partial(g8 + 4, pp + 4);
@@ -1445,12 +1536,6 @@ hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* g
   return last_error();
 }
 
-hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int ny, void* table, hipStream_t s) {
-  const int n = 2 * C * B * nx * ny;
-  hipLaunchKernelGGL(k_box_prep_split, dim3((n + 255) / 256), dim3(256), 0, s, boxes, C * B, nx, ny, (int*)table);
-  return last_error();
-}
-
 hipError_t launch_box_prep_corners(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
                                    void* table, hipStream_t s) {
   const int n = C * B;
@@ -1483,20 +1568,37 @@ hipError_t launch_box_fwd_lds_split(const float* x, const int* rec, void* y, boo
   return last_error();
 }
 
-hipError_t launch_box_bwd_lds_split(const float* x, const int* taps, const float* piece_w, const float* gy, float* gx,
-                                    float* partials, int N, int C, int H, int W, int B, int nx, int ny,
-                                    hipStream_t s) {
-  const int seg = box_bwd_lds_seg(H, W);
-  if (seg == 0) return hipErrorInvalidValue;
-  const int items = n_chunks(W) * n_segs(H, seg);
-  const int threads = ((items + 63) / 64) * 64;
+hipError_t launch_box_prep_corners_adj(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
+                                       void* table, hipStream_t s) {
+  const int n = C * B;
+  hipLaunchKernelGGL(k_box_prep_corners_adj, dim3((n + 255) / 256), dim3(256), 0, s, boxes, piece_w, n, nx, ny,
+                     (int*)table);
+  return last_error();
+}
+
+template <int SEG, int NXC, int NYC>
+static void bwd_split_t(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N, int C,
+                        int H, int W, int B, hipStream_t s) {
+  const int threads = ((n_chunks(W) * n_segs(H, SEG) + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
-  if (seg == 8)
-    hipLaunchKernelGGL((k_box_bwd_lds_split<8>), dim3(N * C), dim3(threads), shm, s, x, taps, piece_w, gy, gx,
-                       partials, C, H, W, B, nx, ny);
-  else
-    hipLaunchKernelGGL((k_box_bwd_lds_split<4>), dim3(N * C), dim3(threads), shm, s, x, taps, piece_w, gy, gx,
-                       partials, C, H, W, B, nx, ny);
+  hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC>), dim3(N * C), dim3(threads), shm, s, x, rec, gy, gx,
+                     partials, C, H, W, B);
+}
+
+template <int SEG>
+static void bwd_split_mode(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N, int C,
+                           int H, int W, int B, int nx, int ny, hipStream_t s) {
+  if (nx == 2 && ny == 2) bwd_split_t<SEG, 3, 3>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+  else if (nx == 2) bwd_split_t<SEG, 3, 2>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+  else bwd_split_t<SEG, 2, 3>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+}
+
+hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N,
+                                    int C, int H, int W, int B, int nx, int ny, hipStream_t s) {
+  const int seg = box_bwd_lds_seg(H, W);
+  if (seg == 8) bwd_split_mode<8>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
+  else if (seg == 4) bwd_split_mode<4>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
+  else return hipErrorInvalidValue;
   return last_error();
 }
 

@@ -105,39 +105,6 @@ __device__ __forceinline__ Taps<float> make_taps_adjoint(const float* p, int lim
   return t;
 }
 
-// Taps of the box [a, b) x [c, d) given by its fp64 edges (a piece of a split
-// box): the forward split (floor) or, with `adjoint`, the mirrored box
-// [1-b, 1-a) x [1-d, 1-c) with the upper split (ceil - 1), as
-// make_taps_f32 / make_taps_adjoint build them from (cx, cy, rx, ry).
-__device__ __forceinline__ Taps<float> taps_from_edges(double a, double b, double c, double d, bool adjoint,
-                                                       int limx, int limy) {
-  if (adjoint) {
-    const double a2 = 1.0 - b, b2 = 1.0 - a, c2 = 1.0 - d, d2 = 1.0 - c;
-    a = a2; b = b2; c = c2; d = d2;
-  }
-  int fa, fb, fc, fd;
-  double aa, ab, ac, ad;
-  if (adjoint) {
-    edge_split_upper(a, limx, fa, aa);
-    edge_split_upper(b, limx, fb, ab);
-    edge_split_upper(c, limy, fc, ac);
-    edge_split_upper(d, limy, fd, ad);
-  } else {
-    edge_split(a, limx, fa, aa);
-    edge_split(b, limx, fb, ab);
-    edge_split(c, limy, fc, ac);
-    edge_split(d, limy, fd, ad);
-  }
-  Taps<float> t;
-  t.ox[0] = fa; t.ox[1] = fa + 1; t.ox[2] = fb; t.ox[3] = fb + 1;
-  t.oy[0] = fc; t.oy[1] = fc + 1; t.oy[2] = fd; t.oy[3] = fd + 1;
-  t.wx[0] = (float)(aa - 1.0); t.wx[1] = (float)(-aa);
-  t.wx[2] = (float)(1.0 - ab); t.wx[3] = (float)ab;
-  t.wy[0] = (float)(ac - 1.0); t.wy[1] = (float)(-ac);
-  t.wy[2] = (float)(1.0 - ad); t.wy[3] = (float)ad;
-  return t;
-}
-
 // Taps of a box whose corners are rounded to integers (the inference form of
 // the Conclusions: once the boxes have converged the sampling points are
 // rounded, and each corner is one table sample).  Each edge e (fp64) is

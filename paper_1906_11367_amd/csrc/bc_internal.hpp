@@ -62,19 +62,19 @@ hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* g
                                   hipStream_t s);
 
 // Kernel splitting (nx x ny pieces per box, fp32 maps, tables in LDS).
-// Backward: piece tap records [2][C*B][nx*ny][16], the backward (partials
-// [N * waves][C*B][8]) and the reduce to grad_boxes [C*B][4] and the piece
-// weights' gradient [C*B][nx*ny].
-hipError_t launch_box_prep_split(const float* boxes, int C, int B, int nx, int ny, void* table, hipStream_t s);
 // Forward: corner records [C*B][32] (the pieces' shared corners with the
-// piece weights folded into per-corner coefficients).
+// piece weights folded into per-corner coefficients).  Backward: adjoint
+// corner records [C*B][32] (the mirrored split box), partials
+// [N * waves][C*B][8], and the reduce to grad_boxes [C*B][4] and the piece
+// weights' gradient [C*B][nx*ny].
 hipError_t launch_box_prep_corners(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
                                    void* table, hipStream_t s);
 hipError_t launch_box_fwd_lds_split(const float* x, const int* rec, void* y, bool bf16_out, int N, int C, int H, int W,
                                     int B, int nx, int ny, hipStream_t s);
-hipError_t launch_box_bwd_lds_split(const float* x, const int* taps, const float* piece_w, const float* gy, float* gx,
-                                    float* partials, int N, int C, int H, int W, int B, int nx, int ny,
-                                    hipStream_t s);
+hipError_t launch_box_prep_corners_adj(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
+                                       void* table, hipStream_t s);
+hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N,
+                                    int C, int H, int W, int B, int nx, int ny, hipStream_t s);
 hipError_t launch_split_grad_reduce(const float* partials, int Pn, int CB, int P, float* grad_boxes, float* grad_w,
                                     hipStream_t s);
 

@@ -155,13 +155,12 @@ def test_split_argument_errors():
     assert lib.box_conv_split_bwd(*a) == 7
     a = list(bwd); a[6] = 256; a[7] = 256
     assert lib.box_conv_split_bwd(*a) == 7
-    # workspace: forward, one 128-byte corner record per box; backward, the
-    # pieces' records (2 * C*B * P * 64 bytes) and the 8-word partials of
-    # every wave of every image
+    # workspace: one 128-byte corner record per box, and for the backward the
+    # 8-word partials of every wave of every image
     assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) == 256 * 4 * 128
     assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_2Y) == 256 * 4 * 128
     assert lib.bc_split_workspace_bytes(1, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) >= \
-        2 * 256 * 4 * 4 * 64 + 32 * 256 * 4 * 32
+        256 * 4 * 128 + 32 * 256 * 4 * 32
     assert lib.bc_split_workspace_bytes(1, 4, 8, 256, 256, 4, bc.BC_SPLIT_4) == 0
     assert lib.bc_split_workspace_bytes(0, 4, 8, 64, 48, 4, 0) == 0
 
