@@ -293,7 +293,8 @@ def main():
 
     # second timed pass with an event after every library call (events made
     # beforehand, so the pass itself only records them)
-    timing["pool"] = [torch.cuda.Event(enable_timing=True) for _ in range(16 * args.steps)]
+    # at most 8 calls per layer and step, plus the step's start and clip
+    timing["pool"] = [torch.cuda.Event(enable_timing=True) for _ in range((8 * wl.layers + 2) * args.steps)]
     timing["on"] = True
     spin(spin_cycles)
     for _ in range(args.steps):
