@@ -550,10 +550,13 @@ __global__ void k_clip_unit(float* __restrict__ u, int n) {
 // strip, writing finished table rows coalesced.
 constexpr int kStrip = 16;
 constexpr int kSatMaxK = 16;  // elements per lane in a row scan: W <= 1024
+constexpr int kSatRowsPerWave = 4;  // rows of a strip each wave loads before scanning them
 
 // kUp: x is [maps][Ho][Wo] and the table is that of its zero-upsampled H x W
 // map (x[i][j] at (s*i, s*j)); mean must then be null.
-template <typename T, bool kUp>
+// KM: elements per lane in a row scan, K = ceil(W / 64) <= KM (4 for
+// W <= 256, else 16).
+template <typename T, bool kUp, int KM>
 __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* __restrict__ sat,
                                                    float* __restrict__ mean, int H, int W, int s, int Ho, int Wo) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -571,39 +574,56 @@ __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* _
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int K = (W + 63) >> 6;
   for (int v = tid; v <= W; v += blockDim.x) dst[v] = (T)0;
-  T carry[kSatMaxK / 4];
+  T carry[KM / 4];
 #pragma unroll
-  for (int j = 0; j < kSatMaxK / 4; ++j) carry[j] = (T)0;
+  for (int j = 0; j < KM / 4; ++j) carry[j] = (T)0;
   for (int r0 = 0; r0 < H; r0 += kStrip) {
     const int rows = min(kStrip, H - r0);
-    for (int rr = wave; rr < rows; rr += nw) {
-      const int r = r0 + rr;
-      const T* row = kUp ? src + (size_t)(r / s) * Wo : src + (size_t)r * W;
-      const bool live = !kUp || r % s == 0;
-      T v[kSatMaxK];
-      T run = (T)0;
+    // rows rr = wave + i * nw of the strip: all of a wave's loads are issued
+    // before its first scan
+    for (int rb = wave; rb < rows; rb += kSatRowsPerWave * nw) {
+      T v[kSatRowsPerWave][KM];
 #pragma unroll
-      for (int k = 0; k < kSatMaxK; ++k) {
-        if (k < K) {
-          const int idx = lane * K + k;
-          T val;
-          if constexpr (kUp) val = (live && idx < W && idx % s == 0) ? row[idx / s] : (T)0;
-          else val = idx < W ? row[idx] : (T)0;
-          if (sub && idx < W) val = (T)((float)val - mu);
-          run += val;
-          v[k] = run;
+      for (int i = 0; i < kSatRowsPerWave; ++i) {
+        const int rr = rb + i * nw, r = r0 + rr;
+        const T* row = kUp ? src + (size_t)(r / s) * Wo : src + (size_t)r * W;
+        const bool live = rr < rows && (!kUp || r % s == 0);
+#pragma unroll
+        for (int k = 0; k < KM; ++k) {
+          if (k < K) {
+            const int idx = lane * K + k;
+            T val;
+            if constexpr (kUp) val = (live && idx < W && idx % s == 0) ? row[idx / s] : (T)0;
+            else val = (live && idx < W) ? row[idx] : (T)0;
+            if (sub && idx < W) val = (T)((float)val - mu);
+            v[i][k] = val;
+          }
         }
       }
-      const T excl = wave_incl_scan(run, lane) - run;
 #pragma unroll
-      for (int k = 0; k < kSatMaxK; ++k) {
-        const int idx = lane * K + k;
-        if (k < K && idx < W) tile[rr * W + idx] = v[k] + excl;
+      for (int i = 0; i < kSatRowsPerWave; ++i) {
+        const int rr = rb + i * nw;
+        T run = (T)0;
+#pragma unroll
+        for (int k = 0; k < KM; ++k) {
+          if (k < K) {
+            run += v[i][k];
+            v[i][k] = run;
+          }
+        }
+        const T excl = wave_incl_scan(run, lane) - run;
+        if (rr < rows) {
+#pragma unroll
+          for (int k = 0; k < KM; ++k) {
+            const int idx = lane * K + k;
+            if (k < K && idx < W) tile[rr * W + idx] = v[i][k] + excl;
+          }
+        }
       }
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kSatMaxK / 4; ++j) {
+    for (int j = 0; j < KM / 4; ++j) {
       const int v = tid + j * 256;
       if (v < W) {
         T cs = carry[j];
@@ -1364,23 +1384,33 @@ static void with_flag(bool v, F&& f) {
   else f(std::integral_constant<bool, false>{});
 }
 
-hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W,
-                            hipStream_t s) {
+template <int KM>
+static void sat_build_t(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W, hipStream_t s) {
   const size_t shm = (size_t)kStrip * W * 4;
   if (is_int)
-    hipLaunchKernelGGL((k_sat_build<int, false>), dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat,
+    hipLaunchKernelGGL((k_sat_build<int, false, KM>), dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat,
                        (float*)nullptr, H, W, 1, H, W);
   else
-    hipLaunchKernelGGL((k_sat_build<float, false>), dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat, mean,
-                       H, W, 1, H, W);
+    hipLaunchKernelGGL((k_sat_build<float, false, KM>), dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat,
+                       mean, H, W, 1, H, W);
+}
+
+hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W,
+                            hipStream_t s) {
+  if (W <= 256) sat_build_t<4>(x, is_int, sat, mean, maps, H, W, s);
+  else sat_build_t<kSatMaxK>(x, is_int, sat, mean, maps, H, W, s);
   return last_error();
 }
 
 hipError_t launch_sat_build_up(const float* x, float* sat, int maps, int H, int W, int stride, hipStream_t s) {
   const size_t shm = (size_t)kStrip * W * 4;
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
-  hipLaunchKernelGGL((k_sat_build<float, true>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H, W, stride,
-                     Ho, Wo);
+  if (W <= 256)
+    hipLaunchKernelGGL((k_sat_build<float, true, 4>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H, W,
+                       stride, Ho, Wo);
+  else
+    hipLaunchKernelGGL((k_sat_build<float, true, kSatMaxK>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H,
+                       W, stride, Ho, Wo);
   return last_error();
 }
 
