@@ -55,7 +55,7 @@ typedef enum {
   BC_ERR_ALIGN = 4,       /* a tensor pointer is not 16-byte aligned */
   BC_ERR_WORKSPACE = 5,   /* workspace missing or smaller than required */
   BC_ERR_HIP = 6,         /* the HIP runtime reported an error at launch */
-  BC_ERR_UNSUPPORTED = 7  /* valid request this build does not implement */
+  BC_ERR_UNSUPPORTED = 7  /* valid request the library does not implement */
 } bc_status;
 
 typedef enum { BC_I32 = 0, BC_F32 = 1, BC_BF16 = 2 } bc_dtype;
