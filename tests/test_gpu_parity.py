@@ -697,6 +697,81 @@ def test_bwd_integer_edges(flags):
     check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
 
 
+# ---------------------------------------------------------------------------
+# Edges of the path selection: widest maps, the LDS-table limit, the
+# backward's 256-item LDS limit, and degenerate boxes in the backward
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("H,W", [(5, 1024), (3, 1021)])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_widest_maps(H, W, flags):
+    """W up to 1024 (the row-scan limit): the forward's table fits LDS, the
+    backward has more than 256 items and takes the HBM tables."""
+    rng = np.random.default_rng(130)
+    x = rng.standard_normal((1, 2, H, W)).astype(np.float32)
+    g = rng.standard_normal((1, 6, H, W)).astype(np.float32)
+    bx = real_boxes(rng, 2, 3, 40.0, 0.5, 300.0)
+    say(f"widest maps {H}x{W} flags={flags}")
+    check(_fwd(x, bx, flags=flags), O.box_forward(x, bx), RTOL_F32, "O")
+    gx, gb = _bwd(x, bx, g, flags)
+    check(gx, O.box_backward_input(g, bx, H, W), RTOL_F32, "dx")
+    check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
+
+
+@pytest.mark.parametrize("H,W", [(120, 120), (128, 128), (128, 48), (136, 48)])
+def test_lds_limits(H, W):
+    """Maps on both sides of the LDS limits: 120x120 is the largest square
+    table the forward keeps in LDS (128x128 is not), 128x48 the largest map
+    the backward walks in one block (136x48 is not)."""
+    rng = np.random.default_rng(131)
+    x = rng.standard_normal((2, 2, H, W)).astype(np.float32)
+    g = rng.standard_normal((2, 4, H, W)).astype(np.float32)
+    bx = real_boxes(rng, 2, 2, 30.0, 0.5, 40.0)
+    say(f"lds limits {H}x{W}")
+    check(_fwd(x, bx), O.box_forward(x, bx), RTOL_F32, "O")
+    gx, gb = _bwd(x, bx, g)
+    check(gx, O.box_backward_input(g, bx, H, W), RTOL_F32, "dx")
+    check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
+
+
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_bwd_degenerate_boxes(flags):
+    """Boxes covering everything, entirely outside the map, of zero size, or
+    thin: the gradients against the oracle (zero where the box reads nothing)."""
+    rng = np.random.default_rng(132)
+    x = rng.standard_normal((2, 2, 9, 7)).astype(np.float32)
+    g = rng.standard_normal((2, 8, 9, 7)).astype(np.float32)
+    bx = np.array([[[0, 0, 1000, 1000], [500, 0, 3, 3], [0, 0, 0, 0], [0.3, 0.2, 0.1, 0.05]],
+                   [[-20, 30, 2, 2], [0, 0, 4.5, 0.5], [2.2, -1.1, 0.5, 6], [0, 0, 0.5, 0.5]]],
+                  dtype=np.float32)
+    say(f"bwd degenerate boxes flags={flags}")
+    gx, gb = _bwd(x, bx, g, flags)
+    check(gx, O.box_backward_input(g, bx, 9, 7), RTOL_F32, "dx")
+    want = O.box_backward_params(x, g, bx)
+    check(gb, want, RTOL_F32, "dboxes")
+    # a box entirely outside the map reads nothing: no gradient at all
+    assert np.all(gb[0, 1] == 0) and np.all(gb[1, 0] == 0)
+
+
+@pytest.mark.parametrize("mode", ["2x", "2y", "4"])
+def test_split_degenerate_boxes(mode):
+    """Split boxes with zero-width pieces (rx = 0 or ry = 0), boxes outside
+    the map and boxes covering everything."""
+    rng = np.random.default_rng(133)
+    x = rng.standard_normal((2, 2, 9, 7)).astype(np.float32)
+    g = rng.standard_normal((2, 8, 9, 7)).astype(np.float32)
+    bx = np.array([[[0, 0, 1000, 1000], [500, 0, 3, 3], [0, 0, 0, 0], [0.3, 0.2, 0.0, 2.5]],
+                   [[-20, 30, 2, 2], [0, 0, 4.5, 0.0], [2.2, -1.1, 0.5, 6], [0, 0, 0.5, 0.5]]],
+                  dtype=np.float32)
+    w = rng.uniform(-1, 1, size=(2, 4, bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]])).astype(np.float32)
+    say(f"split {mode} degenerate boxes")
+    y, gx, gb, gw = _split(x, bx, w, mode, g)
+    check(y, O.box_forward_split(x, bx, w, mode), RTOL_F32, "y")
+    check(gx, O.box_backward_split_input(g, bx, w, mode, 9, 7), RTOL_F32, "dx")
+    want_b, want_w = O.box_backward_split_params(x, g, bx, w, mode)
+    check(gb, want_b, RTOL_F32, "dboxes")
+    check(gw, want_w, RTOL_F32, "dw")
+
+
 def test_bwd_deterministic():
     wl = wlmod.WORKLOADS[3].scaled(N=2, C=4)
     d = wlmod.make_inputs(wl)
