@@ -8,6 +8,8 @@ can compute one image, one map or one box at a time.
 * large maps (256x256, mean-offset table): sampled maps of O and dx, sampled
   boxes' parameter gradients over every image.
 * 6-layer stack: image 0's output and input gradient (normwise).
+* pose layer, inference (integer corners, forward only) and stride 2: the
+  configurations bench.py --inference / --stride 2 time, sampled likewise.
 """
 import sys
 
@@ -162,3 +164,77 @@ def test_stack6_full_size_image0():
         pw, nw = O.rel_errors(host(got), ref)
         say(f"  {name}: normwise {nw:.3e}  pointwise {pw:.3e}  (bar {bar})")
         assert nw <= bar
+
+
+def _sampled_mix_checks(wl, d, o_fn, dw_got, db_got, stride, ks):
+    """dW columns and box-parameter gradients of sampled boxes k = c*B + b,
+    summed over every image (bf16 mix operands, bounds as in bf16_bounds)."""
+    B = wl.B
+    wb = O.bf16_round(d["w"])
+    g = d["grad"][..., ::stride, ::stride]
+    gb = O.bf16_round(g).reshape(wl.N, wl.mix_out, -1)
+    Ho, Wo = g.shape[-2:]
+    for k in ks:
+        c, b = divmod(k, B)
+        bx = d["boxes"][c:c + 1, b:b + 1]
+        o_k = o_fn(d["x"][:, c:c + 1], bx)[:, 0]
+        D_k = bb.bf16_band(o_k, bb.scale_err(o_k, bb.E_F32))
+        ob = O.bf16_round(o_k).reshape(wl.N, -1)
+        dw_ref = np.einsum("nmp,np->m", gb, ob)
+        dw_bnd = np.einsum("nmp,np->m", np.abs(gb), D_k.reshape(wl.N, -1))
+        check_bounded(dw_got[:, k], dw_ref, dw_bnd, RTOL_BF16, f"dW[:, {k}]")
+        if db_got is not None:
+            do_k = np.einsum("m,nmp->np", wb[:, k], gb).reshape(wl.N, 1, Ho, Wo)
+            db_ref = O.box_backward_params(d["x"][:, c:c + 1], do_k, bx, stride=stride)[0, 0]
+            pw = np.abs(db_got[c, b] - db_ref) / (np.abs(db_ref) + np.sqrt(np.mean(db_ref ** 2)))
+            say(f"  dboxes[{c},{b}]: {pw.max():.3e}")
+            assert pw.max() <= RTOL_BF16
+
+
+def test_pose_layer_inference_full_size_sampled():
+    """The inference forward bench.py --inference times: boxes with integer
+    corners, bf16 filtered maps, bf16 mix; images 0 and N-1 of O and Z."""
+    wl = wlmod.WORKLOADS[3]
+    d = wlmod.make_inputs(wl)
+    say(f"{wl.key} inference full size")
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, wl.mix_dtype, wl.relu,
+                     bc.BC_FLAG_INTEGER_CORNERS, False)
+    z = plan.forward(dev(d["x"]), dev(d["boxes"]), dev(d["w"]))
+    torch.cuda.synchronize()
+    wb = O.bf16_round(d["w"])
+    for n in (0, wl.N - 1):
+        o = O.box_forward(d["x"][n:n + 1], d["boxes"], integer_corners=True)
+        D = bb.bf16_band(o, bb.scale_err(o, bb.E_F32))
+        check_bounded(host(plan.o[n:n + 1]), O.bf16_round(o), D, RTOL_BF16, f"O[{n}] (bf16)")
+        zr = O.mix_forward(d["w"], o, compute="bf16")
+        ez = np.einsum("mk,nkhw->nmhw", np.abs(wb), D, optimize=True)
+        check_bounded(host(z[n:n + 1]), zr, ez, RTOL_BF16, f"Z[{n}]")
+
+
+def test_pose_layer_stride2_full_size_sampled():
+    """The strided layer bench.py --stride 2 times: images 0 and N-1 of O, Z,
+    dO and dx; dW columns and box-parameter gradients of sampled boxes."""
+    wl = wlmod.WORKLOADS[3]
+    d = wlmod.make_inputs(wl)
+    s = 2
+    say(f"{wl.key} stride {s} full size")
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, wl.mix_dtype, wl.relu, 0, True,
+                     stride=s)
+    xd, bd, wd = dev(d["x"]), dev(d["boxes"]), dev(d["w"])
+    g = np.ascontiguousarray(d["grad"][..., ::s, ::s])
+    z = plan.forward(xd, bd, wd)
+    dx, db, dw = plan.backward(xd, bd, wd, dev(g))
+    torch.cuda.synchronize()
+    wb = O.bf16_round(d["w"])
+    for n in (0, wl.N - 1):
+        o = O.box_forward(d["x"][n:n + 1], d["boxes"], stride=s)
+        D = bb.bf16_band(o, bb.scale_err(o, bb.E_F32))
+        check_bounded(host(plan.o[n:n + 1]), O.bf16_round(o), D, RTOL_BF16, f"O[{n}] (bf16)")
+        zr = O.mix_forward(d["w"], o, compute="bf16")
+        ez = np.einsum("mk,nkhw->nmhw", np.abs(wb), D, optimize=True)
+        check_bounded(host(z[n:n + 1]), zr, ez, RTOL_BF16, f"Z[{n}]")
+        do = O.mix_backward_data(d["w"], g[n:n + 1], compute="bf16")
+        check(host(plan.do[n:n + 1]), do, RTOL_BF16, f"dO[{n}]")
+        check(host(dx[n:n + 1]), O.box_backward_input(do, d["boxes"], wl.H, wl.W, stride=s), RTOL_BF16, f"dx[{n}]")
+    ks = sorted(np.random.default_rng(8).choice(wl.C * wl.B, size=8, replace=False).tolist())
+    _sampled_mix_checks(wl, d, lambda x, bx: O.box_forward(x, bx, stride=s), host(dw), host(db), s, ks)

@@ -613,6 +613,34 @@ def test_layer_split_fp32(relu):
     check(host(dpw), want_w, RTOL_F32, "dpiece_w")
 
 
+def test_layer_split_unit_params():
+    """Split boxes trained as unit corners: the layer converts u to pixels,
+    runs the split filter and returns dL/du and the piece weights' gradient."""
+    wl = wlmod.WORKLOADS[2].scaled(N=2, C=4)
+    d = wlmod.make_inputs(wl)
+    u = wlmod.make_unit_corners(wl)
+    pw = wlmod.make_piece_weights(wl, 2)
+    g = np.random.default_rng(127).standard_normal((wl.N, wl.mix_out, wl.H, wl.W)).astype(np.float32)
+    mw, mh = float(wl.W), float(wl.H)
+    plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, "f32", False, 0, True,
+                     split="2x", unit_size=(mw, mh))
+    xd, wd = dev(d["x"]), dev(d["w"])
+    params = (dev(u), dev(pw))
+    say("layer split 2x with unit corners")
+    z = plan.forward(xd, params, wd)
+    dx, (du, dpw), dw = plan.backward(xd, params, wd, dev(g))
+    torch.cuda.synchronize()
+    bx = O.boxes_from_unit(u, mw, mh).astype(np.float32)
+    o = O.box_forward_split(d["x"], bx, pw, "2x")
+    check(host(z), O.mix_forward(d["w"], o, compute="f32"), RTOL_F32, "Z")
+    do = O.mix_backward_data(d["w"], g, compute="f32")
+    check(host(dx), O.box_backward_split_input(do, bx, pw, "2x", wl.H, wl.W), RTOL_F32, "dx")
+    gbox, gw = O.box_backward_split_params(d["x"], do, bx, pw, "2x")
+    check(host(du), O.unit_grad_from_box_grad(gbox, mw, mh), RTOL_F32, "du")
+    check(host(dpw), gw, RTOL_F32, "dpiece_w")
+    check(host(dw), O.mix_backward_weight(g, o, compute="f32"), RTOL_F32, "dW")
+
+
 def test_split_deterministic():
     wl = wlmod.WORKLOADS[3].scaled(N=2, C=4)
     d = wlmod.make_inputs(wl)
