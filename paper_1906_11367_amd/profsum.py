@@ -14,6 +14,14 @@
 --copy-*  passes over a plain elementwise kernel that reads and writes a known
           number of bytes: FETCH_SIZE / WRITE_SIZE of the kernels above are
           scaled by (known bytes / counted bytes) of that kernel.
+--derived utilisation per kernel from SQ counters (MI355X: 8 XCDs, 1024
+          SIMDs; GRBM_GUI_ACTIVE sums the XCDs' active cycles):
+            cycles     = GRBM_GUI_ACTIVE / 8
+            VALU busy  = 4 * SQ_ACTIVE_INST_VALU / (1024 * cycles)
+                         (a wave64 VALU instruction occupies its SIMD 4 cycles)
+            MFMA busy  = SQ_VALU_MFMA_BUSY_CYCLES / (1024 * cycles)
+            wait share = SQ_WAIT_ANY / SQ_WAVE_CYCLES (wave cycles spent waiting)
+            LDS conflict = SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS
 Prints a Markdown table per kernel (average duration, calls, counters per
 dispatch); --json writes the HBM bytes per launch of the kernels whose name
 contains --kernel.
@@ -28,6 +36,7 @@ import json
 import os
 
 COPY_BYTES = 256 << 20      # the calibration kernel reads and writes 256 MiB
+XCDS, SIMDS = 8, 1024       # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
 
 def _csv(dir_, suffix):
@@ -88,6 +97,7 @@ def main():
     ap.add_argument("--source-hash")
     ap.add_argument("--warmup", type=int, default=0)
     ap.add_argument("--steps", type=int, default=0)
+    ap.add_argument("--derived", action="store_true")
     a = ap.parse_args()
     fetch_f = write_f = None
     if a.copy_fetch:
@@ -122,6 +132,22 @@ def main():
             if a.kernel and a.kernel in n:
                 result[n] = rd + wr
         print(f"| {n[:70]} | {s.get('calls', '')} | {s.get('avg_us', 0):.2f} | {s.get('pct', 0):.1f} | {extra} |")
+    if a.derived:
+        print()
+        print("| kernel | VALU instr / wave | VALU busy | MFMA busy | LDS instr / wave | LDS conflict | wait share |")
+        print("|---|---|---|---|---|---|---|")
+        for n in names:
+            c = merged.get(n, {})
+            if not c.get("SQ_WAVES") or not c.get("GRBM_GUI_ACTIVE") or n.startswith("at::"):
+                continue
+            cyc = c["GRBM_GUI_ACTIVE"] / XCDS
+            w = c["SQ_WAVES"]
+            valu = 4 * c.get("SQ_ACTIVE_INST_VALU", 0) / (SIMDS * cyc)
+            mfma = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) / (SIMDS * cyc)
+            lds_c = c.get("SQ_LDS_BANK_CONFLICT", 0) / max(c.get("SQ_ACTIVE_INST_LDS", 0), 1)
+            wait = c.get("SQ_WAIT_ANY", 0) / max(c.get("SQ_WAVE_CYCLES", 0), 1)
+            print(f"| {n[:70]} | {c.get('SQ_INSTS_VALU', 0) / w:.0f} | {100 * valu:.1f} % | {100 * mfma:.1f} % | "
+                  f"{c.get('SQ_INSTS_LDS', 0) / w:.0f} | {lds_c:.2f} | {100 * wait:.1f} % |")
     if a.json and result:
         with open(a.json, "w") as f:
             json.dump({"source_hash": a.source_hash, "kernels": {k: v for k, v in result.items()},
