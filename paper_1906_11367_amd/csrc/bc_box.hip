@@ -703,7 +703,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   const int it = blk * 256 + threadIdx.x;
   if (it >= nch * nseg) return;
   const int seg = it / nch, ch = it - seg * nch;
-  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
+  const GlobalTable<T, true> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
   const float mu = kOffset ? means[map] : 0.f;
   const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
   OutT* out = y + ((size_t)map * B + b) * H * W;
@@ -769,7 +769,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather_strided(const T* __restr
   const int it = blk * 256 + threadIdx.x;
   if (it >= Wo * ((Ho + kSegS - 1) / kSegS)) return;
   const int seg = it / Wo, j = it - seg * Wo;
-  const GlobalTable<T> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
+  const GlobalTable<T, true> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
   const float mu = kOffset ? means[map] : 0.f;
   const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
   const int i0 = seg * kSegS;

@@ -187,7 +187,7 @@ struct LdsTable {
 
 // Table in HBM, (H+1) x (W+1), unpadded: row coordinates are row indices and
 // every index is clamped.
-template <typename T>
+template <typename T, bool kVec = false>
 struct GlobalTable {
   const T* __restrict__ p;
   int pitch, W, H;
@@ -198,8 +198,24 @@ struct GlobalTable {
   template <int N = kQ + 1>
   __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
     const T* r = p + (size_t)clampi(coord, 0, H) * pitch;
+    run<N>(r, c.a, sa);
+    run<N>(r, c.b, sb);
+  }
+  // N consecutive words of row r from column j, clamped to [0, W]; with
+  // kVec, one 16-byte load (4-byte aligned) when the whole run of 4 is
+  // inside the row (the backward gather keeps the scalar loads: the wider
+  // path would cost it registers it does not have).
+  template <int N>
+  __device__ __forceinline__ void run(const T* r, int j, T* s) const {
+    typedef T vec4u __attribute__((ext_vector_type(4))) __attribute__((aligned(sizeof(T))));
+    if (kVec && N == 4 && j >= 0 && j + 3 <= W) {
+      const vec4u q = *reinterpret_cast<const vec4u*>(r + j);
+      s[0] = q.x; s[1] = q.y; s[2] = q.z;
+      if constexpr (N == 4) s[3] = q.w;
+    } else {
 #pragma unroll
-    for (int k = 0; k < N; ++k) { sa[k] = r[clampi(c.a + k, 0, W)]; sb[k] = r[clampi(c.b + k, 0, W)]; }
+      for (int k = 0; k < N; ++k) s[k] = r[clampi(j + k, 0, W)];
+    }
   }
 };
 
