@@ -236,7 +236,9 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
  *        bottom), BC_SPLIT_4 (P = 4: quadrants); piece p = i * nx + j covers
  *        columns [k_j, k_{j+1}) of k = (a, m, b) (or (a, b)) and rows
  *        [r_i, r_{i+1}) of r = (c, n, d) (or (c, d)); edges in fp64.
- *        Other values: BC_ERR_UNSUPPORTED.
+ *        OR-ed with BC_SPLIT_FORCE_HBM: take the HBM-table kernels even
+ *        where the map's table fits in LDS (same results up to fp32
+ *        rounding order).  Other values: BC_ERR_UNSUPPORTED.
  * x, boxes, grad_y, grad_x, grad_boxes : as box_conv_fwd / box_conv_bwd,
  *        fp32 maps, stride 1, no flags.
  * piece_w : device fp32 [C][B][P].
@@ -247,19 +249,23 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
  *        the box's edges, a cut edge contributing half to each of the two
  *        edges it is the mean of; grad_w [C][B][P] = <grad_y, piece sum>.
  *        Sums over n are fixed-order (deterministic).
- * Limits : the map's table must fit in LDS (the tables of the HBM path are
- *        not offered here): (H + 1) * ((W + 7) | 1) * 4 <= 64 KiB, and for
- *        the backward at most 256 work items per map; BC_ERR_UNSUPPORTED
- *        otherwise.  C * B <= 2^24.
+ * Paths : as box_conv_fwd / box_conv_bwd: the map's table in LDS when
+ *        (H + 1) * ((W + 7) | 1) * 4 <= 64 KiB (and, for the backward, the
+ *        map has at most 256 work items), else tables in HBM built into the
+ *        workspace, which needs W <= 1024 (BC_ERR_SHAPE otherwise).
+ *        C * B <= 2^24.
  * ws     : >= bc_split_workspace_bytes(op, ...) (op 0 = forward: one record
  *        of 128 bytes per box, its shared corners with the piece weights
- *        folded in; op 1 = backward: the same for the mirrored boxes, plus
- *        per-wave gradient partials).  The query returns 0 for an unsupported
- *        request.
+ *        folded in, plus the HBM path's tables of the N*C input maps; op 1 =
+ *        backward: the same records for the mirrored boxes, the HBM path's
+ *        tables of the N*C*B upstream-gradient maps, and per-wave gradient
+ *        partials).  The query takes the same mode (with its
+ *        BC_SPLIT_FORCE_HBM bit) and returns 0 for an unsupported request.
  * ---------------------------------------------------------------------- */
 #define BC_SPLIT_2X 1
 #define BC_SPLIT_2Y 2
 #define BC_SPLIT_4 3
+#define BC_SPLIT_FORCE_HBM 0x100
 bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* piece_w,
                              int N, int C, int H, int W, int B, int mode,
                              void* y, bc_dtype y_dt, void* ws, size_t ws_bytes, hipStream_t stream);

@@ -25,6 +25,7 @@ BC_I32, BC_F32, BC_BF16 = 0, 1, 2
 BC_MIX_FWD, BC_MIX_BWD_DATA, BC_MIX_BWD_WEIGHT = 0, 1, 2
 BC_FLAG_MEAN_OFFSET, BC_FLAG_FORCE_HBM, BC_FLAG_INTEGER_CORNERS = 1, 2, 4
 BC_SPLIT_2X, BC_SPLIT_2Y, BC_SPLIT_4 = 1, 2, 3
+BC_SPLIT_FORCE_HBM = 0x100
 STATUS = {0: "BC_OK", 1: "BC_ERR_NULL", 2: "BC_ERR_SHAPE", 3: "BC_ERR_DTYPE", 4: "BC_ERR_ALIGN",
           5: "BC_ERR_WORKSPACE", 6: "BC_ERR_HIP", 7: "BC_ERR_UNSUPPORTED"}
 
@@ -221,39 +222,43 @@ def _split_mode(mode) -> int:
     return m
 
 
-def split_workspace_bytes(op: int, N, C, H, W, B, mode) -> int:
-    return int(load_library().bc_split_workspace_bytes(op, N, C, H, W, B, _split_mode(mode)))
+def split_workspace_bytes(op: int, N, C, H, W, B, mode, force_hbm: bool = False) -> int:
+    code = _split_mode(mode) | (BC_SPLIT_FORCE_HBM if force_hbm else 0)
+    return int(load_library().bc_split_workspace_bytes(op, N, C, H, W, B, code))
 
 
 def box_conv_split_fwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tensor, mode, y: torch.Tensor,
-                       ws: torch.Tensor | None = None):
+                       ws: torch.Tensor | None = None, force_hbm: bool = False):
     """x [N, C, H, W] fp32, boxes [C, B, 4], piece_w [C, B, P] -> y [N, C*B, H, W] (fp32 or bf16).
-    mode: "2x", "2y", "4" or a BC_SPLIT_* code."""
+    mode: "2x", "2y", "4" or a BC_SPLIT_* code; force_hbm: take the HBM-table
+    kernels even where the map's table fits in LDS."""
     m = _split_mode(mode)
+    code = m | (BC_SPLIT_FORCE_HBM if force_hbm else 0)
     N, C, H, W = x.shape
     B = boxes.shape[1]
     if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(y.shape) != (N, C * B, H, W):
         raise BoxConvError("box_conv_split_fwd: piece_w or y has the wrong shape")
     if ws is None:
-        ws = _workspace(split_workspace_bytes(0, N, C, H, W, B, m), x.device)
+        ws = _workspace(split_workspace_bytes(0, N, C, H, W, B, m, force_hbm), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load_library().box_conv_split_fwd(_ptr(x), _ptr(boxes), _ptr(piece_w), N, C, H, W, B, m, _ptr(y),
+    _check(load_library().box_conv_split_fwd(_ptr(x), _ptr(boxes), _ptr(piece_w), N, C, H, W, B, code, _ptr(y),
                                              dtype_code(y), _ptr(ws), nbytes, _stream()), "box_conv_split_fwd")
     return y
 
 
 def box_conv_split_bwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tensor, mode, grad_y: torch.Tensor,
                        grad_x: torch.Tensor | None, grad_boxes: torch.Tensor | None,
-                       grad_w: torch.Tensor | None, ws: torch.Tensor | None = None):
+                       grad_w: torch.Tensor | None, ws: torch.Tensor | None = None, force_hbm: bool = False):
     m = _split_mode(mode)
+    code = m | (BC_SPLIT_FORCE_HBM if force_hbm else 0)
     N, C, H, W = x.shape
     B = boxes.shape[1]
     if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(grad_y.shape) != (N, C * B, H, W):
         raise BoxConvError("box_conv_split_bwd: piece_w or grad_y has the wrong shape")
     if ws is None:
-        ws = _workspace(split_workspace_bytes(1, N, C, H, W, B, m), x.device)
+        ws = _workspace(split_workspace_bytes(1, N, C, H, W, B, m, force_hbm), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load_library().box_conv_split_bwd(_ptr(x), _ptr(boxes), _ptr(piece_w), _ptr(grad_y), N, C, H, W, B, m,
+    _check(load_library().box_conv_split_bwd(_ptr(x), _ptr(boxes), _ptr(piece_w), _ptr(grad_y), N, C, H, W, B, code,
                                              _ptr(grad_x), _ptr(grad_boxes), _ptr(grad_w), _ptr(ws), nbytes,
                                              _stream()), "box_conv_split_bwd")
     return grad_x, grad_boxes, grad_w

@@ -207,9 +207,10 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, 
   return box_conv_bwd_strided(x, boxes, grad_y, N, C, H, W, B, 1, grad_x, grad_boxes, flags, ws, ws_bytes, stream);
 }
 
-// Kernel splitting: pieces per box along x and y of a split mode, or 0.
+// Kernel splitting: pieces per box along x and y of a split mode, or 0 (the
+// BC_SPLIT_FORCE_HBM bit is ignored here).
 static int split_pieces(int mode, int& nx, int& ny) {
-  switch (mode) {
+  switch (mode & ~BC_SPLIT_FORCE_HBM) {
     case BC_SPLIT_2X: nx = 2; ny = 1; return 2;
     case BC_SPLIT_2Y: nx = 1; ny = 2; return 2;
     case BC_SPLIT_4: nx = 2; ny = 2; return 4;
@@ -218,10 +219,27 @@ static int split_pieces(int mode, int& nx, int& ny) {
 }
 
 // Split workspaces: the boxes' corner records (32 words per box; the
-// backward's are those of the mirrored boxes) at offset 0, then (backward)
-// the per-wave partials of 8 words (4 edge and 4 piece-weight gradients).
+// backward's are those of the mirrored boxes) at offset 0; on the HBM path
+// the tables next (one per input map in the forward, one per upstream-gradient
+// map in the backward); then (backward) the per-wave partials of 8 words
+// (4 edge and 4 piece-weight gradients).
 static size_t split_corner_bytes(int C, int B) { return align_up((size_t)C * B * 32 * 4); }
-static int split_partial_rows(int N, int H, int W) { return N * bc::box_bwd_lds_waves(H, W); }
+
+struct SplitWs { size_t sat, partials, total; int rows; };
+static SplitWs split_fwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+  SplitWs w{};
+  w.sat = split_corner_bytes(C, B);
+  w.total = w.sat + (hbm ? align_up((size_t)N * C * table_elems(H, W) * 4) : 0);
+  return w;
+}
+static SplitWs split_bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+  SplitWs w{};
+  w.sat = split_corner_bytes(C, B);
+  w.partials = w.sat + (hbm ? align_up((size_t)N * C * B * table_elems(H, W) * 4) : 0);
+  w.rows = hbm ? N * bc::box_bwd_gather_blocks(H, W) * 4 : N * bc::box_bwd_lds_waves(H, W);
+  w.total = w.partials + align_up((size_t)w.rows * C * B * 8 * 4);
+  return w;
+}
 
 static bool split_dims_ok(int N, int C, int H, int W, int B) {
   return dims_ok(N, C, H, W, B) && (long)C * B <= (1L << 24);
@@ -231,10 +249,14 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
   int nx, ny;
   const int P = split_pieces(mode, nx, ny);
   if (P == 0 || !split_dims_ok(N, C, H, W, B)) return 0;
-  if (op == 0) return split_corner_bytes(C, B);
+  const bool force = (mode & BC_SPLIT_FORCE_HBM) != 0;
+  if (op == 0) {
+    const bool hbm = force || !fwd_lds_fits(H, W);
+    return hbm && W > 1024 ? 0 : split_fwd_ws(N, C, H, W, B, hbm).total;
+  }
   if (op == 1) {
-    if (!bwd_lds_fits(H, W)) return 0;
-    return split_corner_bytes(C, B) + align_up((size_t)split_partial_rows(N, H, W) * C * B * 8 * 4);
+    const bool hbm = force || !bwd_lds_fits(H, W);
+    return hbm && W > 1024 ? 0 : split_bwd_ws(N, C, H, W, B, hbm).total;
   }
   return 0;
 }
@@ -248,14 +270,22 @@ bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* pi
   const int P = split_pieces(mode, nx, ny);
   if (P == 0) return BC_ERR_UNSUPPORTED;
   if (y_dt != BC_F32 && y_dt != BC_BF16) return BC_ERR_DTYPE;
-  if (!fwd_lds_fits(H, W)) return BC_ERR_UNSUPPORTED;
+  const bool hbm = (mode & BC_SPLIT_FORCE_HBM) || !fwd_lds_fits(H, W);
+  if (hbm && W > 1024) return BC_ERR_SHAPE;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(y)) return BC_ERR_ALIGN;
-  if (!ws || ws_bytes < split_corner_bytes(C, B)) return BC_ERR_WORKSPACE;
+  const SplitWs L = split_fwd_ws(N, C, H, W, B, hbm);
+  if (!ws || ws_bytes < L.total) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
-  hipError_t e = bc::launch_box_prep_corners(boxes, piece_w, C, B, nx, ny, ws, stream);
+  char* base = static_cast<char*>(ws);
+  const int* rec = reinterpret_cast<const int*>(base);
+  hipError_t e = bc::launch_box_prep_corners(boxes, piece_w, C, B, nx, ny, base, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  return hip_status(bc::launch_box_fwd_lds_split(x, static_cast<const int*>(ws), y, y_dt == BC_BF16, N, C, H, W, B,
-                                                 nx, ny, stream));
+  if (!hbm)
+    return hip_status(bc::launch_box_fwd_lds_split(x, rec, y, y_dt == BC_BF16, N, C, H, W, B, nx, ny, stream));
+  float* sat = reinterpret_cast<float*>(base + L.sat);
+  e = bc::launch_sat_build(x, false, sat, nullptr, N * C, H, W, stream);
+  if (e != hipSuccess) return BC_ERR_HIP;
+  return hip_status(bc::launch_box_fwd_gather_split(sat, rec, y, y_dt == BC_BF16, N, C, H, W, B, nx, ny, stream));
 }
 
 bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* piece_w, const float* grad_y, int N,
@@ -266,23 +296,29 @@ bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* pi
   int nx, ny;
   const int P = split_pieces(mode, nx, ny);
   if (P == 0) return BC_ERR_UNSUPPORTED;
-  if (!bwd_lds_fits(H, W)) return BC_ERR_UNSUPPORTED;
+  const bool hbm = (mode & BC_SPLIT_FORCE_HBM) || !bwd_lds_fits(H, W);
+  if (hbm && W > 1024) return BC_ERR_SHAPE;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(grad_y) ||
       (grad_x && !aligned16(grad_x)) || (grad_boxes && !aligned16(grad_boxes)) || (grad_w && !aligned16(grad_w)))
     return BC_ERR_ALIGN;
   if (!grad_x && !grad_boxes && !grad_w) return BC_OK;
-  const size_t taps = split_corner_bytes(C, B);
-  const int rows = split_partial_rows(N, H, W);
-  if (!ws || ws_bytes < taps + align_up((size_t)rows * C * B * 8 * 4)) return BC_ERR_WORKSPACE;
+  const SplitWs L = split_bwd_ws(N, C, H, W, B, hbm);
+  if (!ws || ws_bytes < L.total) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
   char* base = static_cast<char*>(ws);
-  float* partials = reinterpret_cast<float*>(base + taps);
+  const int* rec = reinterpret_cast<const int*>(base);
+  float* partials = reinterpret_cast<float*>(base + L.partials);
   hipError_t e = bc::launch_box_prep_corners_adj(boxes, piece_w, C, B, nx, ny, base, stream);
-  if (e == hipSuccess)
-    e = bc::launch_box_bwd_lds_split(x, reinterpret_cast<const int*>(base), grad_y, grad_x, partials, N, C, H, W, B,
-                                     nx, ny, stream);
+  if (e == hipSuccess && !hbm)
+    e = bc::launch_box_bwd_lds_split(x, rec, grad_y, grad_x, partials, N, C, H, W, B, nx, ny, stream);
+  if (e == hipSuccess && hbm) {
+    float* sat_g = reinterpret_cast<float*>(base + L.sat);
+    e = bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream);
+    if (e == hipSuccess)
+      e = bc::launch_box_bwd_gather_split(x, sat_g, rec, grad_x, partials, N, C, H, W, B, nx, ny, stream);
+  }
   if (e == hipSuccess && (grad_boxes || grad_w))
-    e = bc::launch_split_grad_reduce(partials, rows, C * B, P, grad_boxes, grad_w, stream);
+    e = bc::launch_split_grad_reduce(partials, L.rows, C * B, P, grad_boxes, grad_w, stream);
   return hip_status(e);
 }
 

@@ -1029,21 +1029,20 @@ __global__ void k_box_prep_corners(const float* __restrict__ boxes, const float*
 // output of row y is sum_ri (1-beta) R_ri(y+f_ri) + beta R_ri(y+f_ri+1).
 // Each step reads one new table row per row corner (NXC runs of kQ+1 words)
 // and reuses the one from the step before.
-template <int SEG, int NXC, int NYC, bool kFull, typename Emit>
-__device__ __forceinline__ void corner_walk(const LdsTable<float>& S, const int* __restrict__ rec, int x0, int y0,
-                                            int y1, Emit& emit) {
+template <int SEG, int NXC, int NYC, bool kFull, typename Src, typename Emit>
+__device__ __forceinline__ void corner_walk(const Src& S, const int* __restrict__ rec, int x0, int y0, int y1,
+                                            Emit& emit) {
   const float* f = reinterpret_cast<const float*>(rec);
   const int W = S.W, H = S.H;
-  const char* base = reinterpret_cast<const char*>(S.p + kPad);
-  const char* col[NXC];
+  typename Src::Col col[NXC];
   float cw[NYC][NXC][2], wy[NYC][2];
   int rc[NYC];
   const int st = S.row_step();
 #pragma unroll
-  for (int k = 0; k < NXC; ++k) col[k] = base + clampi(x0 + clampi(rec[k], -(W + 1), W + 1), -kPad, W) * 4;
+  for (int k = 0; k < NXC; ++k) col[k] = S.col(x0 + clampi(rec[k], -(W + 1), W + 1));
 #pragma unroll
   for (int i = 0; i < NYC; ++i) {
-    rc[i] = (y0 + clampi(rec[3 + i], -(H + 1), H + 1)) * st;
+    rc[i] = S.row_coord(y0 + clampi(rec[3 + i], -(H + 1), H + 1));
     wy[i][0] = f[6 + 2 * i];
     wy[i][1] = f[7 + 2 * i];
 #pragma unroll
@@ -1052,17 +1051,14 @@ __device__ __forceinline__ void corner_walk(const LdsTable<float>& S, const int*
       cw[i][k][1] = f[13 + (i * 3 + k) * 2];
     }
   }
-  const int hi = H * st;
   auto row = [&](int i, int coord, float* R) {
-    const int off = med3_i32(coord, hi);
+    const typename Src::Row rr = S.row(coord);
 #pragma unroll
     for (int q = 0; q < kQ; ++q) R[q] = 0.f;
 #pragma unroll
     for (int k = 0; k < NXC; ++k) {
-      const float* sa = reinterpret_cast<const float*>(col[k] + off);
       float v[kQ + 1];
-#pragma unroll
-      for (int t = 0; t <= kQ; ++t) v[t] = sa[t];
+      S.run4(rr, col[k], v);
 #pragma unroll
       for (int q = 0; q < kQ; ++q) R[q] = fmaf(cw[i][k][0], v[q], fmaf(cw[i][k][1], v[q + 1], R[q]));
     }
@@ -1174,24 +1170,23 @@ __global__ void k_box_prep_corners_adj(const float* __restrict__ boxes, const fl
 //   per-tap-row sums for the parameter gradient, with the input values v:
 //     PX[ri][t][kj] += v[s'] * X and PD[ri][t][kj] += v[s'] * D, t = 1 for
 //     the output row s' = s (R = its row f + 1), t = 0 for s' = s + 1.
-template <int SEG, int NXC, int NYC>
-__device__ __forceinline__ void corner_adjoint_walk(const LdsTable<float>& S, const int* __restrict__ rec, int x0,
-                                                    int y0, const float (&v)[SEG][kQ], float (&acc)[SEG][kQ],
+template <int SEG, int NXC, int NYC, typename Src>
+__device__ __forceinline__ void corner_adjoint_walk(const Src& S, const int* __restrict__ rec, int x0, int y0,
+                                                    const float (&v)[SEG][kQ], float (&acc)[SEG][kQ],
                                                     float (&PX)[NYC][2][NXC], float (&PD)[NYC][2][NXC]) {
   const float* f = reinterpret_cast<const float*>(rec);
   const int W = S.W, H = S.H;
-  const char* base = reinterpret_cast<const char*>(S.p + kPad);
-  const int st = S.row_step(), hi = H * st;
-  const char* col[NXC];
+  const int st = S.row_step();
+  typename Src::Col col[NXC];
   float al[NXC];
 #pragma unroll
   for (int k = 0; k < NXC; ++k) {
-    col[k] = base + clampi(x0 + clampi(rec[k], -(W + 1), W + 1), -kPad, W) * 4;
+    col[k] = S.col(x0 + clampi(rec[k], -(W + 1), W + 1));
     al[k] = f[6 + k];
   }
 #pragma unroll
   for (int i = 0; i < NYC; ++i) {
-    const int r0 = (y0 + clampi(rec[3 + i], -(H + 1), H + 1)) * st;
+    const int r0 = S.row_coord(y0 + clampi(rec[3 + i], -(H + 1), H + 1));
     const float be = f[9 + i], wy0 = 1.f - be;
     float cf[NXC];
 #pragma unroll
@@ -1200,14 +1195,12 @@ __device__ __forceinline__ void corner_adjoint_walk(const LdsTable<float>& S, co
     // reads row y0 + s + f + 1 (lower row of output s, upper row of s + 1)
 #pragma unroll
     for (int s = -1; s < SEG; ++s) {
-      const int off = med3_i32(r0 + (s + 1) * st, hi);
+      const typename Src::Row rr = S.row(r0 + (s + 1) * st);
       float R[kQ] = {0.f, 0.f, 0.f};
 #pragma unroll
       for (int k = 0; k < NXC; ++k) {
-        const float* sa = reinterpret_cast<const float*>(col[k] + off);
         float t[kQ + 1];
-#pragma unroll
-        for (int u = 0; u <= kQ; ++u) t[u] = sa[u];
+        S.run4(rr, col[k], t);
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
           const float D = t[q + 1] - t[q];
@@ -1232,25 +1225,59 @@ __device__ __forceinline__ void corner_adjoint_walk(const LdsTable<float>& S, co
   }
 }
 
-// Backward of split boxes, table in LDS: as k_box_bwd_lds (one block per map,
-// one item of 3 columns x SEG rows per thread, input values in registers), one
-// walk over each box's mirrored corners.  From the per-tap-row sums, per
-// mirrored corner (ri, kj): Q = (1-beta) PX0 + beta PX1 (the corner's
-// lookup, weighted by x), QX = (1-beta) PD0 + beta PD1 (its x derivative),
-// QY = PX1 - PX0 (its y derivative); then
+// One item's share of a split box's gradients from its per-tap-row sums
+// (adjoint corner record f): per mirrored corner (ri, kj),
+// Q = (1-beta) PX0 + beta PX1 (the corner's lookup, weighted by x),
+// QX = (1-beta) PD0 + beta PD1 (its x derivative), QY = PX1 - PX0 (its y
+// derivative); then
 //   dL/dk'_kj = sum_ri coef(ri, kj) QX,  dL/dr'_ri = sum_kj coef(ri, kj) QY,
 //   dL/dw'(i, j) = Q(i+1, j+1) - Q(i+1, j) - Q(i, j+1) + Q(i, j)
 // (the mirrored piece's adjoint sum weighted by x).  Mirroring back:
 // dL/dk_j = -dL/dk'_{nx-j}, a cut edge (the mean of the outer two) gives half
-// to each, and dL/dw(i, j) = dL/dw'(ny-1-i, nx-1-j).  Each wave writes
-// (dL/da, dL/db, dL/dc, dL/dd, dL/dw_0 .. dL/dw_3) to
-// partials[(n * nw + wave) * C*B + c*B + b][8].
+// to each, and dL/dw(i, j) = dL/dw'(ny-1-i, nx-1-j).  g8 = (dL/da, dL/db,
+// dL/dc, dL/dd, dL/dw_0 .. dL/dw_3), unused weight slots 0.
+template <int NXC, int NYC>
+__device__ __forceinline__ void split_box_grads(const float* __restrict__ f, const float (&PX)[NYC][2][NXC],
+                                                const float (&PD)[NYC][2][NXC], float (&g8)[8]) {
+  constexpr int nx = NXC - 1, ny = NYC - 1;
+  float Q[NYC][NXC], gk[NXC], gr[NYC];
+#pragma unroll
+  for (int k = 0; k < NXC; ++k) gk[k] = 0.f;
+#pragma unroll
+  for (int i = 0; i < NYC; ++i) {
+    const float be = f[9 + i], wy0 = 1.f - be;
+    gr[i] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NXC; ++k) {
+      const float cf = f[12 + i * 3 + k];
+      Q[i][k] = fmaf(wy0, PX[i][0][k], be * PX[i][1][k]);
+      gk[k] = fmaf(cf, fmaf(wy0, PD[i][0][k], be * PD[i][1][k]), gk[k]);
+      gr[i] = fmaf(cf, PX[i][1][k] - PX[i][0][k], gr[i]);
+    }
+  }
+  // mirrored corner kj is original corner nx - kj, with the sign flipped
+  g8[0] = -gk[nx] - (nx == 2 ? 0.5f * gk[1] : 0.f);
+  g8[1] = -gk[0] - (nx == 2 ? 0.5f * gk[1] : 0.f);
+  g8[2] = -gr[ny] - (ny == 2 ? 0.5f * gr[1] : 0.f);
+  g8[3] = -gr[0] - (ny == 2 ? 0.5f * gr[1] : 0.f);
+#pragma unroll
+  for (int k = 4; k < 8; ++k) g8[k] = 0.f;
+#pragma unroll
+  for (int i = 0; i < ny; ++i)
+#pragma unroll
+    for (int j = 0; j < nx; ++j)
+      g8[4 + (ny - 1 - i) * nx + (nx - 1 - j)] = (Q[i + 1][j + 1] - Q[i + 1][j]) - (Q[i][j + 1] - Q[i][j]);
+}
+
+// Backward of split boxes, table in LDS: as k_box_bwd_lds (one block per map,
+// one item of 3 columns x SEG rows per thread, input values in registers), one
+// walk over each box's mirrored corners.  Each wave writes its split_box_grads
+// sums to partials[(n * nw + wave) * C*B + c*B + b][8].
 template <int SEG, int NXC, int NYC>
 __global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
                                                            const float* __restrict__ gy, float* __restrict__ gx,
                                                            float* __restrict__ partials, int C, int H, int W,
                                                            int B) {
-  constexpr int nx = NXC - 1, ny = NYC - 1;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -1283,40 +1310,82 @@ __global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restri
 #pragma unroll
         for (int k = 0; k < NXC; ++k) { PX[i][t][k] = 0.f; PD[i][t][k] = 0.f; }
     if (active) corner_adjoint_walk<SEG, NXC, NYC>(tg, rb, x0, y0, v, acc, PX, PD);
-    const float* f = reinterpret_cast<const float*>(rb);
-    float Q[NYC][NXC], gk[NXC], gr[NYC];
-#pragma unroll
-    for (int k = 0; k < NXC; ++k) gk[k] = 0.f;
-#pragma unroll
-    for (int i = 0; i < NYC; ++i) {
-      const float be = f[9 + i], wy0 = 1.f - be;
-      gr[i] = 0.f;
-#pragma unroll
-      for (int k = 0; k < NXC; ++k) {
-        const float cf = f[12 + i * 3 + k];
-        Q[i][k] = fmaf(wy0, PX[i][0][k], be * PX[i][1][k]);
-        gk[k] = fmaf(cf, fmaf(wy0, PD[i][0][k], be * PD[i][1][k]), gk[k]);
-        gr[i] = fmaf(cf, PX[i][1][k] - PX[i][0][k], gr[i]);
-      }
-    }
-    // mirrored corner kj is original corner nx - kj, with the sign flipped
     float g8[8];
-    g8[0] = -gk[nx] - (nx == 2 ? 0.5f * gk[1] : 0.f);
-    g8[1] = -gk[0] - (nx == 2 ? 0.5f * gk[1] : 0.f);
-    g8[2] = -gr[ny] - (ny == 2 ? 0.5f * gr[1] : 0.f);
-    g8[3] = -gr[0] - (ny == 2 ? 0.5f * gr[1] : 0.f);
-#pragma unroll
-    for (int k = 4; k < 8; ++k) g8[k] = 0.f;
-#pragma unroll
-    for (int i = 0; i < ny; ++i)
-#pragma unroll
-      for (int j = 0; j < nx; ++j)
-        g8[4 + (ny - 1 - i) * nx + (nx - 1 - j)] = (Q[i + 1][j + 1] - Q[i + 1][j]) - (Q[i][j + 1] - Q[i][j]);
+    split_box_grads<NXC, NYC>(reinterpret_cast<const float*>(rb), PX, PD, g8);
     float* pp = partials + (((size_t)n * nw + wave) * C * B + cb) * 8;
     store_wave_partial(g8, pp);
     store_wave_partial(g8 + 4, pp + 4);
   }
   if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * plane, H, W, x0, y0, acc);
+}
+
+// Forward of split boxes, table in HBM: as k_box_fwd_gather (one block per
+// (map, box, block of 256 items), one map's blocks on one XCD).
+template <typename OutT, int SEG, int NXC, int NYC>
+__global__ __launch_bounds__(256) void k_box_fwd_gather_split(const float* __restrict__ sat,
+                                                              const int* __restrict__ rec, OutT* __restrict__ y,
+                                                              int C, int H, int W, int B, int nblk, int total) {
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= total) return;
+  const int blk = L % nblk, mb = L / nblk;
+  const int b = mb % B, map = mb / B, c = map % C;
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = blk * 256 + threadIdx.x;
+  if (it >= nch * nseg) return;
+  const int seg = it / nch, ch = it - seg * nch;
+  const GlobalTable<float, true> tab{sat + (size_t)map * (H + 1) * (W + 1), W + 1, W, H};
+  const int* rb = rec + (size_t)(c * B + b) * 32;
+  OutT* out = y + ((size_t)map * B + b) * H * W;
+  const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+  StoreRows<OutT, float> em{out, W, x0, y0 * W + x0};
+  if (y0 + SEG <= H && x0 + kQ <= W) corner_walk<SEG, NXC, NYC, true>(tab, rb, x0, y0, y1, em);
+  else corner_walk<SEG, NXC, NYC, false>(tab, rb, x0, y0, y1, em);
+}
+
+// Backward of split boxes, tables of the upstream-gradient maps in HBM: as
+// k_box_bwd_gather (one block per (map, block of 256 items), looping over the
+// boxes).  Each wave writes its split_box_grads sums to
+// partials[((n * nblk + blk) * 4 + wave) * C*B + c*B + b][8].
+template <int SEG, int NXC, int NYC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_box_bwd_gather_split(
+    const float* __restrict__ x, const float* __restrict__ sat_g, const int* __restrict__ rec,
+    float* __restrict__ gx, float* __restrict__ partials, int C, int H, int W, int B, int nblk, int total) {
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= total) return;
+  const int blk = L % nblk, map = L / nblk;
+  const int n = map / C, c = map - n * C;
+  const int wave = threadIdx.x >> 6;
+  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG;
+  const int it = blk * 256 + threadIdx.x;
+  const bool active = it < nch * nseg;
+  const int seg = it / nch, ch = it - seg * nch;
+  const int x0 = ch * kQ, y0 = seg * SEG;
+  const size_t tsz = (size_t)(H + 1) * (W + 1);
+  float v[SEG][kQ], acc[SEG][kQ];
+  load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) acc[s][q] = 0.f;
+  for (int b = 0; b < B; ++b) {
+    const GlobalTable<float> tg{sat_g + ((size_t)map * B + b) * tsz, W + 1, W, H};
+    const int cb = c * B + b;
+    const int* rb = rec + (size_t)cb * 32;
+    float PX[NYC][2][NXC], PD[NYC][2][NXC];
+#pragma unroll
+    for (int i = 0; i < NYC; ++i)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int k = 0; k < NXC; ++k) { PX[i][t][k] = 0.f; PD[i][t][k] = 0.f; }
+    if (active) corner_adjoint_walk<SEG, NXC, NYC>(tg, rb, x0, y0, v, acc, PX, PD);
+    float g8[8];
+    split_box_grads<NXC, NYC>(reinterpret_cast<const float*>(rb), PX, PD, g8);
+    float* pp = partials + ((((size_t)n * nblk + blk) * 4 + wave) * C * B + cb) * 8;
+    store_wave_partial(g8, pp);
+    store_wave_partial(g8 + 4, pp + 4);
+  }
+  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
 }
 
 // Fixed-tree sum of the split partials [Pn][CB][8] (as k_box_grad_reduce) and
@@ -1629,6 +1698,48 @@ hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float*
   if (seg == 8) bwd_split_mode<8>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
   else if (seg == 4) bwd_split_mode<4>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
   else return hipErrorInvalidValue;
+  return last_error();
+}
+
+template <typename OutT, int NXC, int NYC>
+static void fwd_gather_split_t(const float* sat, const int* rec, void* y, int N, int C, int H, int W, int B,
+                               hipStream_t s) {
+  constexpr int SEG = 16;
+  const int nblk = (n_chunks(W) * n_segs(H, SEG) + 255) / 256;
+  const int total = N * C * B * nblk;
+  hipLaunchKernelGGL((k_box_fwd_gather_split<OutT, SEG, NXC, NYC>), dim3(pad8(total)), dim3(256), 0, s, sat, rec,
+                     (OutT*)y, C, H, W, B, nblk, total);
+}
+
+template <typename OutT>
+static void fwd_gather_split_mode(const float* sat, const int* rec, void* y, int N, int C, int H, int W, int B, int nx,
+                                  int ny, hipStream_t s) {
+  if (nx == 2 && ny == 2) fwd_gather_split_t<OutT, 3, 3>(sat, rec, y, N, C, H, W, B, s);
+  else if (nx == 2) fwd_gather_split_t<OutT, 3, 2>(sat, rec, y, N, C, H, W, B, s);
+  else fwd_gather_split_t<OutT, 2, 3>(sat, rec, y, N, C, H, W, B, s);
+}
+
+hipError_t launch_box_fwd_gather_split(const float* sat, const int* rec, void* y, bool bf16_out, int N, int C, int H,
+                                       int W, int B, int nx, int ny, hipStream_t s) {
+  if (bf16_out) fwd_gather_split_mode<uint16_t>(sat, rec, y, N, C, H, W, B, nx, ny, s);
+  else fwd_gather_split_mode<float>(sat, rec, y, N, C, H, W, B, nx, ny, s);
+  return last_error();
+}
+
+template <int NXC, int NYC>
+static void bwd_gather_split_t(const float* x, const float* sat_g, const int* rec, float* gx, float* partials, int N,
+                               int C, int H, int W, int B, hipStream_t s) {
+  const int nblk = box_bwd_gather_blocks(H, W);
+  const int total = N * C * nblk;
+  hipLaunchKernelGGL((k_box_bwd_gather_split<kBwdGatherSeg, NXC, NYC>), dim3(pad8(total)), dim3(256), 0, s, x, sat_g,
+                     rec, gx, partials, C, H, W, B, nblk, total);
+}
+
+hipError_t launch_box_bwd_gather_split(const float* x, const float* sat_g, const int* rec, float* gx, float* partials,
+                                       int N, int C, int H, int W, int B, int nx, int ny, hipStream_t s) {
+  if (nx == 2 && ny == 2) bwd_gather_split_t<3, 3>(x, sat_g, rec, gx, partials, N, C, H, W, B, s);
+  else if (nx == 2) bwd_gather_split_t<3, 2>(x, sat_g, rec, gx, partials, N, C, H, W, B, s);
+  else bwd_gather_split_t<2, 3>(x, sat_g, rec, gx, partials, N, C, H, W, B, s);
   return last_error();
 }
 

@@ -175,6 +175,19 @@ struct LdsTable {
   }
   __device__ __forceinline__ int row_step() const { return pitch * (int)sizeof(T); }
   __device__ __forceinline__ int row_coord(int v) const { return v * row_step(); }
+  // One column run at a time (the split-box corner walks): col(x) a clamped
+  // column, row(coord) a clamped row, run4 the 4 words from there.
+  using Col = const char*;
+  using Row = int;
+  __device__ __forceinline__ Col col(int x) const {
+    return reinterpret_cast<const char*>(p + kPad) + clampi(x, -kPad, W) * (int)sizeof(T);
+  }
+  __device__ __forceinline__ Row row(int coord) const { return med3_i32(coord, H * row_step()); }
+  __device__ __forceinline__ void run4(Row r, Col c, T* v) const {
+    const T* s = reinterpret_cast<const T*>(c + r);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = s[k];
+  }
   template <int N = kQ + 1>
   __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
     const int row = med3_i32(coord, H * row_step());
@@ -195,6 +208,11 @@ struct GlobalTable {
   __device__ __forceinline__ Cols cols(int ba, int bb) const { return {ba, bb}; }
   __device__ __forceinline__ int row_step() const { return 1; }
   __device__ __forceinline__ int row_coord(int v) const { return v; }
+  using Col = int;
+  using Row = const T*;
+  __device__ __forceinline__ Col col(int x) const { return x; }
+  __device__ __forceinline__ Row row(int coord) const { return p + (size_t)clampi(coord, 0, H) * pitch; }
+  __device__ __forceinline__ void run4(Row r, Col c, T* v) const { run<4>(r, c, v); }
   template <int N = kQ + 1>
   __device__ __forceinline__ void runs(int coord, const Cols& c, T* sa, T* sb) const {
     const T* r = p + (size_t)clampi(coord, 0, H) * pitch;

@@ -61,12 +61,14 @@ hipError_t launch_unit_params(int op, const float* in, int n, float mw, float mh
 hipError_t launch_box_grad_reduce(const float* partials, int P, int CB, float* grad_boxes,
                                   hipStream_t s);
 
-// Kernel splitting (nx x ny pieces per box, fp32 maps, tables in LDS).
-// Forward: corner records [C*B][32] (the pieces' shared corners with the
-// piece weights folded into per-corner coefficients).  Backward: adjoint
-// corner records [C*B][32] (the mirrored split box), partials
-// [N * waves][C*B][8], and the reduce to grad_boxes [C*B][4] and the piece
-// weights' gradient [C*B][nx*ny].
+// Kernel splitting (nx x ny pieces per box, fp32 maps).  Forward: corner
+// records [C*B][32] (the pieces' shared corners with the piece weights folded
+// into per-corner coefficients).  Backward: adjoint corner records [C*B][32]
+// (the mirrored split box), partials [rows][C*B][8] (rows = N * waves per map
+// on the LDS path, N * box_bwd_gather_blocks * 4 on the HBM path), and the
+// reduce to grad_boxes [C*B][4] and the piece weights' gradient [C*B][nx*ny].
+// The *_gather_split launchers read the tables sat_build wrote: one per input
+// map (forward), one per upstream-gradient map (backward).
 hipError_t launch_box_prep_corners(const float* boxes, const float* piece_w, int C, int B, int nx, int ny,
                                    void* table, hipStream_t s);
 hipError_t launch_box_fwd_lds_split(const float* x, const int* rec, void* y, bool bf16_out, int N, int C, int H, int W,
@@ -75,6 +77,10 @@ hipError_t launch_box_prep_corners_adj(const float* boxes, const float* piece_w,
                                        void* table, hipStream_t s);
 hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N,
                                     int C, int H, int W, int B, int nx, int ny, hipStream_t s);
+hipError_t launch_box_fwd_gather_split(const float* sat, const int* rec, void* y, bool bf16_out, int N, int C, int H,
+                                       int W, int B, int nx, int ny, hipStream_t s);
+hipError_t launch_box_bwd_gather_split(const float* x, const float* sat_g, const int* rec, float* gx, float* partials,
+                                       int N, int C, int H, int W, int B, int nx, int ny, hipStream_t s);
 hipError_t launch_split_grad_reduce(const float* partials, int Pn, int CB, int P, float* grad_boxes, float* grad_w,
                                     hipStream_t s);
 

@@ -134,13 +134,19 @@ def test_split_argument_errors():
     assert lib.box_conv_split_fwd(*fwd) == 5                 # valid: fails only for lack of a workspace
     a = list(fwd); a[2] = None
     assert lib.box_conv_split_fwd(*a) == 1                   # piece weights are required
-    for bad in (0, 4, -1):
+    for bad in (0, 4, -1, bc.BC_SPLIT_FORCE_HBM, bc.BC_SPLIT_4 | 0x200):
         a = list(fwd); a[8] = bad
         assert lib.box_conv_split_fwd(*a) == 7, bad
+    a = list(fwd); a[8] = bc.BC_SPLIT_4 | bc.BC_SPLIT_FORCE_HBM
+    assert lib.box_conv_split_fwd(*a) == 5
     a = list(fwd); a[10] = bc.BC_I32
     assert lib.box_conv_split_fwd(*a) == 3
-    a = list(fwd); a[5] = 256; a[6] = 256                  # table does not fit LDS: not offered
-    assert lib.box_conv_split_fwd(*a) == 7
+    a = list(fwd); a[5] = 256; a[6] = 256                  # table does not fit LDS: HBM path
+    assert lib.box_conv_split_fwd(*a) == 5
+    a = list(fwd); a[5] = 4; a[6] = 1025                   # fits LDS: no width limit
+    assert lib.box_conv_split_fwd(*a) == 5
+    a[8] = bc.BC_SPLIT_4 | bc.BC_SPLIT_FORCE_HBM            # HBM path: W up to 1024
+    assert lib.box_conv_split_fwd(*a) == 2
     a = list(fwd); a[2] = FAKE_MISALIGNED
     assert lib.box_conv_split_fwd(*a) == 4
     a = list(fwd); a[11] = FAKE; a[12] = lib.bc_split_workspace_bytes(0, 2, 3, 8, 8, 4, bc.BC_SPLIT_4) - 1
@@ -154,15 +160,25 @@ def test_split_argument_errors():
     a = list(bwd); a[9] = 9
     assert lib.box_conv_split_bwd(*a) == 7
     a = list(bwd); a[6] = 256; a[7] = 256
-    assert lib.box_conv_split_bwd(*a) == 7
+    assert lib.box_conv_split_bwd(*a) == 5
+    a = list(bwd); a[6] = 4; a[7] = 1025
+    assert lib.box_conv_split_bwd(*a) == 2
     # workspace: one 128-byte corner record per box, and for the backward the
     # 8-word partials of every wave of every image
     assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) == 256 * 4 * 128
     assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, bc.BC_SPLIT_2Y) == 256 * 4 * 128
     assert lib.bc_split_workspace_bytes(1, 32, 256, 64, 48, 4, bc.BC_SPLIT_4) >= \
         256 * 4 * 128 + 32 * 256 * 4 * 32
-    assert lib.bc_split_workspace_bytes(1, 4, 8, 256, 256, 4, bc.BC_SPLIT_4) == 0
     assert lib.bc_split_workspace_bytes(0, 4, 8, 64, 48, 4, 0) == 0
+    # HBM path (table too large, or forced): the tables come first after the
+    # records; the backward's are those of the N*C*B upstream-gradient maps
+    tab = 257 * 257 * 4
+    assert lib.bc_split_workspace_bytes(0, 4, 8, 256, 256, 4, bc.BC_SPLIT_4) >= 8 * 4 * 128 + 4 * 8 * tab
+    assert lib.bc_split_workspace_bytes(1, 4, 8, 256, 256, 4, bc.BC_SPLIT_4) >= 8 * 4 * 128 + 4 * 8 * 4 * tab
+    forced = bc.BC_SPLIT_4 | bc.BC_SPLIT_FORCE_HBM
+    assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, forced) >= 256 * 4 * 128 + 32 * 256 * 65 * 49 * 4
+    assert lib.bc_split_workspace_bytes(0, 4, 8, 4, 1025, 4, forced) == 0
+    assert lib.bc_split_workspace_bytes(1, 4, 8, 4, 1025, 4, bc.BC_SPLIT_4) == 0
 
 
 def test_mix_argument_errors():

@@ -494,31 +494,32 @@ SPLIT_CASES = [
 ]
 
 
-def _split(x, bx, w, mode, g=None, y_dtype=torch.float32):
+def _split(x, bx, w, mode, g=None, y_dtype=torch.float32, hbm=False):
     N, C, H, W = x.shape
     B = bx.shape[1]
     xd, bd, wd = dev(x), dev(bx), dev(w)
     y = torch.empty((N, C * B, H, W), dtype=y_dtype, device="cuda")
-    bc.box_conv_split_fwd(xd, bd, wd, mode, y)
+    bc.box_conv_split_fwd(xd, bd, wd, mode, y, force_hbm=hbm)
     if g is None:
         return host(y)
     gx = torch.empty((N, C, H, W), dtype=torch.float32, device="cuda")
     gb = torch.empty((C, B, 4), dtype=torch.float32, device="cuda")
     gw = torch.empty_like(wd)
-    bc.box_conv_split_bwd(xd, bd, wd, mode, dev(g), gx, gb, gw)
+    bc.box_conv_split_bwd(xd, bd, wd, mode, dev(g), gx, gb, gw, force_hbm=hbm)
     return host(y), host(gx), host(gb), host(gw)
 
 
+@pytest.mark.parametrize("hbm", [False, True])
 @pytest.mark.parametrize("mode", ["2x", "2y", "4"])
 @pytest.mark.parametrize("key,scale", SPLIT_CASES)
-def test_split_fwd_bwd(mode, key, scale):
+def test_split_fwd_bwd(mode, key, scale, hbm):
     wl = wlmod.WORKLOADS[key].scaled(**scale)
     d = wlmod.make_inputs(wl)
     P = bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]]
     w = wlmod.make_piece_weights(wl, P)
     g = np.random.default_rng(120).standard_normal((wl.N, wl.C * wl.B, wl.H, wl.W)).astype(np.float32)
-    say(f"split {mode} {wl.key} {scale}")
-    y, gx, gb, gw = _split(d["x"], d["boxes"], w, mode, g)
+    say(f"split {mode} {wl.key} {scale} hbm={hbm}")
+    y, gx, gb, gw = _split(d["x"], d["boxes"], w, mode, g, hbm=hbm)
     check(y, O.box_forward_split(d["x"], d["boxes"], w, mode), RTOL_F32, "y")
     check(gx, O.box_backward_split_input(g, d["boxes"], w, mode, wl.H, wl.W), RTOL_F32, "dx")
     want_b, want_w = O.box_backward_split_params(d["x"], g, d["boxes"], w, mode)
@@ -780,8 +781,9 @@ def test_bwd_degenerate_boxes(flags):
     assert np.all(gb[0, 1] == 0) and np.all(gb[1, 0] == 0)
 
 
+@pytest.mark.parametrize("hbm", [False, True])
 @pytest.mark.parametrize("mode", ["2x", "2y", "4"])
-def test_split_degenerate_boxes(mode):
+def test_split_degenerate_boxes(mode, hbm):
     """Split boxes with zero-width pieces (rx = 0 or ry = 0), boxes outside
     the map and boxes covering everything."""
     rng = np.random.default_rng(133)
@@ -791,10 +793,30 @@ def test_split_degenerate_boxes(mode):
                    [[-20, 30, 2, 2], [0, 0, 4.5, 0.0], [2.2, -1.1, 0.5, 6], [0, 0, 0.5, 0.5]]],
                   dtype=np.float32)
     w = rng.uniform(-1, 1, size=(2, 4, bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]])).astype(np.float32)
-    say(f"split {mode} degenerate boxes")
-    y, gx, gb, gw = _split(x, bx, w, mode, g)
+    say(f"split {mode} degenerate boxes hbm={hbm}")
+    y, gx, gb, gw = _split(x, bx, w, mode, g, hbm=hbm)
     check(y, O.box_forward_split(x, bx, w, mode), RTOL_F32, "y")
     check(gx, O.box_backward_split_input(g, bx, w, mode, 9, 7), RTOL_F32, "dx")
+    want_b, want_w = O.box_backward_split_params(x, g, bx, w, mode)
+    check(gb, want_b, RTOL_F32, "dboxes")
+    check(gw, want_w, RTOL_F32, "dw")
+
+
+@pytest.mark.parametrize("mode", ["2x", "4"])
+@pytest.mark.parametrize("H,W", [(70, 100), (131, 133)])
+def test_split_large_maps(H, W, mode):
+    """Maps past the LDS limits, which take the HBM tables by themselves:
+    70x100 has a forward table in LDS but too many backward items for one
+    block; 131x133 has neither (ragged in both directions)."""
+    rng = np.random.default_rng(134)
+    x = rng.standard_normal((1, 2, H, W)).astype(np.float32)
+    g = rng.standard_normal((1, 6, H, W)).astype(np.float32)
+    bx = real_boxes(rng, 2, 3, 35.0, 0.5, 45.0)
+    w = rng.uniform(-1, 1, size=(2, 3, bc.SPLIT_PIECES[bc.SPLIT_MODES[mode]])).astype(np.float32)
+    say(f"split {mode} large maps {H}x{W}")
+    y, gx, gb, gw = _split(x, bx, w, mode, g)
+    check(y, O.box_forward_split(x, bx, w, mode), RTOL_F32, "y")
+    check(gx, O.box_backward_split_input(g, bx, w, mode, H, W), RTOL_F32, "dx")
     want_b, want_w = O.box_backward_split_params(x, g, bx, w, mode)
     check(gb, want_b, RTOL_F32, "dboxes")
     check(gw, want_w, RTOL_F32, "dw")
