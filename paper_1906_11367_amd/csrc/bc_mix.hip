@@ -355,8 +355,8 @@ struct Stager {
 
 // Stores the 2 x 2 accumulator tiles of one wave.  OK: 0 = fp32, 1 = int32
 // (exact integer values), 3 = fp32 accumulate, 4 = fp32 with ReLU.  `full`
-// (block-uniform) skips the bounds checks.
-template <int OK>
+// (block-uniform) skips the bounds checks.  NT: non-temporal stores (0, 1, 4).
+template <int OK, bool NT>
 __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[2][2], char* cbase, int ib, int jb, int rows,
                                          int cols, long ldc, bool full) {
 #pragma unroll
@@ -370,10 +370,16 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[2][2], char* cbas
         if (full || (i < rows && j < cols)) {
           const float v = acc[x][y][r];
           const size_t o = (size_t)i * ldc + j;
-          if constexpr (OK == 1) reinterpret_cast<int*>(cbase)[o] = (int)v;
-          else if constexpr (OK == 3) reinterpret_cast<float*>(cbase)[o] += v;
-          else if constexpr (OK == 4) reinterpret_cast<float*>(cbase)[o] = fmaxf(v, 0.f);
-          else reinterpret_cast<float*>(cbase)[o] = v;
+          if constexpr (OK == 3) {
+            reinterpret_cast<float*>(cbase)[o] += v;
+          } else if constexpr (OK == 1) {
+            if constexpr (NT) __builtin_nontemporal_store((int)v, reinterpret_cast<int*>(cbase) + o);
+            else reinterpret_cast<int*>(cbase)[o] = (int)v;
+          } else {
+            const float u = OK == 4 ? fmaxf(v, 0.f) : v;
+            if constexpr (NT) __builtin_nontemporal_store(u, reinterpret_cast<float*>(cbase) + o);
+            else reinterpret_cast<float*>(cbase)[o] = u;
+          }
         }
       }
 }
@@ -394,7 +400,10 @@ constexpr int mix_waves() {
 }
 
 // out-kind: 0 = store fp32 (relu optional), 1 = store int32 (exact integers),
-// 2 = store fp32 partial (BWD_WEIGHT split), 3 = fp32 with accumulate.
+// 2 = store fp32 partial (BWD_WEIGHT split), 3 = fp32 with accumulate; plus
+// kOutNT for non-temporal stores of 0 and 1.
+constexpr int kOutNT = 8;
+
 template <bool BF16, int ADT, bool AKC, bool AMASK, int BDT, bool BKC, bool BMASK>
 __global__ __launch_bounds__(kMixThreads)
 __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BMASK>(), 8))) void k_mix_gemm(
@@ -508,11 +517,16 @@ __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BM
   const bool full = i0 + kBM <= rows && j0 + kBN <= cols;
   const int ib = i0 + wm * 64 + 4 * (lane >> 5), jb = j0 + wn * 64 + (lane & 31);
   switch (out_kind) {
-    case 1: epilogue<1>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
-    case 3: epilogue<3>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    case 1: epilogue<1, false>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    case 1 | kOutNT: epilogue<1, true>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    case 3: epilogue<3, false>(acc, cbase, ib, jb, rows, cols, ldc, full); break;
+    case kOutNT:
+      if (relu) epilogue<4, true>(acc, cbase, ib, jb, rows, cols, ldc, full);
+      else epilogue<0, true>(acc, cbase, ib, jb, rows, cols, ldc, full);
+      break;
     default:
-      if (relu) epilogue<4>(acc, cbase, ib, jb, rows, cols, ldc, full);
-      else epilogue<0>(acc, cbase, ib, jb, rows, cols, ldc, full);
+      if (relu) epilogue<4, false>(acc, cbase, ib, jb, rows, cols, ldc, full);
+      else epilogue<0, false>(acc, cbase, ib, jb, rows, cols, ldc, full);
   }
 }
 
@@ -595,17 +609,29 @@ static void with_dt(int dt, F&& f) {
   }
 }
 
+// Non-temporal stores of the final outputs, per mode: they are read once, by
+// a later call, and are larger than the caches; keeping them out leaves the
+// caches to the operands the other calls re-read.  Measured on the whole
+// layer step (each alone on one GEMM gains less): pose layer 0.657 ->
+// 0.638 ms, six stacked layers with ReLU 4.64 -> 4.47 ms.  Run back to back
+// with warm caches the GEMMs gain far more (BWD_DATA 171 -> 119 us), and
+// after a cache flush they lose (165 -> 186 us): the step is what counts.
+constexpr bool kNtFwd = true;
+constexpr bool kNtBwdData = true;
+
 template <bool BF16>
 static hipError_t launch_mix_t(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out, int out_dt,
                                int N, int M, int K, int P, int relu, const float* aux, int accumulate, void* ws,
                                hipStream_t s) {
   const int out_kind_plain = out_dt == 0 ? 1 : 0;
+  const int ok_fwd = out_kind_plain | (kNtFwd ? kOutNT : 0);
+  const int ok_bwd_data = out_kind_plain | (kNtBwdData ? kOutNT : 0);
   if (mode == 0) {
     // C = out[n] (M x P): A = w (row-major M x K), B(l=k, j=p) = in[n][k][p]
     with_dt<BF16>(a_dt, [&](auto ad) {
       with_dt<BF16>(b_dt, [&](auto bd) {
         gemm_launch<BF16, decltype(ad)::value, true, false, decltype(bd)::value, false, false>(
-            a, b, nullptr, out, M, P, K, K, P, P, 0, (long)K * P, (long)M * P, N, 0, 0, out_kind_plain, relu, s);
+            a, b, nullptr, out, M, P, K, K, P, P, 0, (long)K * P, (long)M * P, N, 0, 0, ok_fwd, relu, s);
       });
     });
     return hipGetLastError();
@@ -616,10 +642,10 @@ static hipError_t launch_mix_t(int mode, const void* a, int a_dt, const void* b,
       with_dt<BF16>(b_dt, [&](auto bd) {
         if (relu)
           gemm_launch<BF16, decltype(ad)::value, false, false, decltype(bd)::value, false, true>(
-              a, b, aux, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, out_kind_plain, 0, s);
+              a, b, aux, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, ok_bwd_data, 0, s);
         else
           gemm_launch<BF16, decltype(ad)::value, false, false, decltype(bd)::value, false, false>(
-              a, b, nullptr, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, out_kind_plain, 0, s);
+              a, b, nullptr, out, K, P, M, K, P, P, 0, (long)M * P, (long)K * P, N, 0, 0, ok_bwd_data, 0, s);
       });
     });
     return hipGetLastError();
