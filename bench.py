@@ -82,7 +82,9 @@ def call_cost(label, wl, o_bytes, stride=1):
     mix_*        : 2*N*M*K*P FLOPs (one GEMM), reported against the MFMA
                    peak; also the operand bytes it must move (fwd: read O,
                    write Z; bwd_data: read dZ, write dO; bwd_weight: read dZ
-                   and O), reported against the HBM peak
+                   and O), reported against the HBM peak; dZ is 2 bytes per
+                   element after relu_grad (ReLU after a bf16 mix), else 4
+    relu_grad    : read dZ and Z (fp32), write the masked dZ (bf16)
     """
     if label.startswith("box_params"):        # read and write [C][B][4] fp32
         return {"bound": "hbm", "bytes": 2 * wl.C * wl.B * 16}
@@ -94,8 +96,12 @@ def call_cost(label, wl, o_bytes, stride=1):
     if label in ("box_conv_bwd", "box_conv_split_bwd"):
         return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 4 * px}
     flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * Ho * Wo
-    z = 4 * wl.N * wl.mix_out * Ho * Wo
-    mix_bytes = {"mix_fwd": o_bytes * pb + z, "mix_bwd_data": z + 4 * pb, "mix_bwd_weight": z + o_bytes * pb}
+    nz = wl.N * wl.mix_out * Ho * Wo
+    z = 4 * nz
+    if label == "relu_grad":
+        return {"bound": "hbm", "bytes": 10 * nz}
+    dz = 2 * nz if (wl.relu and wl.mix_dtype == "bf16") else z
+    mix_bytes = {"mix_fwd": o_bytes * pb + z, "mix_bwd_data": dz + 4 * pb, "mix_bwd_weight": dz + o_bytes * pb}
     return {"bound": "mfma", "flops": flops, "bytes": mix_bytes.get(label)}
 
 

@@ -310,6 +310,21 @@ bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt,
  * ---------------------------------------------------------------------- */
 bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * bc_relu_grad_bf16 -- the backward of a ReLU after the mix (a layer whose
+ * mix output is rectified, as in the stacked blocks of the dense prediction
+ * network, Section 3.3):
+ *   dst[i] = bf16(out[i] > 0 ? grad[i] : 0), round to nearest even.
+ * grad: device fp32 [n], dL/d(rectified output); out: device fp32 [n], the
+ * rectified forward output; dst: device bf16 codes [n].  These are exactly
+ * the operand values pointwise_mix(BC_BF16, relu = 1, aux = out) forms from
+ * grad on load, so BWD_DATA and BWD_WEIGHT with relu = 0 on dst (BC_BF16
+ * storage) return bitwise the same results, reading 2 bytes per element
+ * instead of 8 in each GEMM.  Errors: BC_ERR_NULL, BC_ERR_SHAPE (n = 0),
+ * BC_ERR_ALIGN (pointers not 16-byte aligned).
+ * ---------------------------------------------------------------------- */
+bc_status bc_relu_grad_bf16(const float* grad, const float* out, void* dst, size_t n, hipStream_t stream);
+
 /* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd. */
 size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags);
 size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt);

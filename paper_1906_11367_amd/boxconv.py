@@ -9,7 +9,8 @@ Entry points (same names as the C ABI): box_prep, sat_build, box_conv_fwd,
 box_conv_bwd, box_conv_fwd_strided, box_conv_bwd_strided, pointwise_mix, the
 box-parameter reparameterisation (box_params_from_unit, box_params_unit_grad,
 box_params_clip), kernel splitting (box_conv_split_fwd, box_conv_split_bwd),
-plus the workspace-size queries.
+the bf16 helpers (bc_cast_bf16, bc_relu_grad_bf16), plus the workspace-size
+queries.
 """
 from __future__ import annotations
 
@@ -48,6 +49,7 @@ SIGNATURES = {
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
+    "bc_relu_grad_bf16": (_i, [_vp, _vp, _vp, _sz, _vp]),
     "bc_status_string": (ctypes.c_char_p, [_i]),
     "bc_abi_version": (_i, []),
 }
@@ -269,6 +271,17 @@ def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):
     if src.numel() != dst.numel():
         raise BoxConvError("bc_cast_bf16: size mismatch")
     _check(load_library().bc_cast_bf16(_ptr(src), _ptr(dst), src.numel(), _stream()), "bc_cast_bf16")
+    return dst
+
+
+def relu_grad_bf16(grad: torch.Tensor, out: torch.Tensor, dst: torch.Tensor):
+    """dst (bf16) = bf16(out > 0 ? grad : 0): the ReLU backward in the mix's compute type."""
+    if not (grad.numel() == out.numel() == dst.numel()):
+        raise BoxConvError("bc_relu_grad_bf16: size mismatch")
+    if grad.dtype != torch.float32 or out.dtype != torch.float32 or dst.dtype != torch.bfloat16:
+        raise BoxConvError("bc_relu_grad_bf16: grad and out fp32, dst bf16")
+    _check(load_library().bc_relu_grad_bf16(_ptr(grad), _ptr(out), _ptr(dst), grad.numel(), _stream()),
+           "bc_relu_grad_bf16")
     return dst
 
 

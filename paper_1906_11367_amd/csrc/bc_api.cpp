@@ -356,6 +356,13 @@ bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream
   return hip_status(bc::launch_cast_bf16(src, dst, n, stream));
 }
 
+bc_status bc_relu_grad_bf16(const float* grad, const float* out, void* dst, size_t n, hipStream_t stream) {
+  if (!grad || !out || !dst) return BC_ERR_NULL;
+  if (n == 0 || n > ((size_t)1 << 40)) return BC_ERR_SHAPE;
+  if (!aligned16(grad) || !aligned16(out) || !aligned16(dst)) return BC_ERR_ALIGN;
+  return hip_status(bc::launch_relu_cast_bf16(grad, out, dst, n, stream));
+}
+
 size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt) {
   if (N <= 0 || M <= 0 || K <= 0 || P <= 0) return 0;
   return bc::mix_workspace_bytes((int)mode, N, M, K, P, (int)compute_dt);

@@ -90,5 +90,6 @@ hipError_t launch_mix(int mode, const void* a, int a_dt, const void* b, int b_dt
                       const float* aux, int accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 size_t mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt);
 hipError_t launch_cast_bf16(const float* src, void* dst, size_t n, hipStream_t s);
+hipError_t launch_relu_cast_bf16(const float* g, const float* aux, void* dst, size_t n, hipStream_t s);
 
 }  // namespace bc

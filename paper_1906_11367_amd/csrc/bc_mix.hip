@@ -551,6 +551,37 @@ hipError_t launch_cast_bf16(const float* src, void* dst, size_t n, hipStream_t s
   return hipGetLastError();
 }
 
+// ReLU backward of the mix in its compute type: dst[i] = bf16(aux[i] > 0 ?
+// g[i] : 0), round to nearest even, 8 elements per thread.  These are the
+// operand bits a masked bf16 GEMM (MASK) forms from g and aux on load, so
+// the unmasked GEMMs on dst compute exactly the same sums.
+__global__ void k_relu_cast_bf16(const float* __restrict__ g, const float* __restrict__ aux,
+                                 uint16_t* __restrict__ dst, size_t n) {
+  const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (i >= n) return;
+  if (i + 8 <= n) {
+    const float4 a0 = *reinterpret_cast<const float4*>(g + i);
+    const float4 a1 = *reinterpret_cast<const float4*>(g + i + 4);
+    const float4 m0 = *reinterpret_cast<const float4*>(aux + i);
+    const float4 m1 = *reinterpret_cast<const float4*>(aux + i + 4);
+    uint4 q;
+    q.x = pack2_bf16(m0.x > 0.f ? a0.x : 0.f, m0.y > 0.f ? a0.y : 0.f);
+    q.y = pack2_bf16(m0.z > 0.f ? a0.z : 0.f, m0.w > 0.f ? a0.w : 0.f);
+    q.z = pack2_bf16(m1.x > 0.f ? a1.x : 0.f, m1.y > 0.f ? a1.y : 0.f);
+    q.w = pack2_bf16(m1.z > 0.f ? a1.z : 0.f, m1.w > 0.f ? a1.w : 0.f);
+    *reinterpret_cast<uint4*>(dst + i) = q;
+  } else {
+    for (size_t k = i; k < n; ++k) dst[k] = (uint16_t)(pack2_bf16(aux[k] > 0.f ? g[k] : 0.f, 0.f) & 0xffffu);
+  }
+}
+
+hipError_t launch_relu_cast_bf16(const float* g, const float* aux, void* dst, size_t n, hipStream_t s) {
+  const size_t threads = (n + 7) / 8;
+  hipLaunchKernelGGL(k_relu_cast_bf16, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, g, aux,
+                     (uint16_t*)dst, n);
+  return hipGetLastError();
+}
+
 // Fixed-order sum of split-K partials: out = (accumulate ? out : 0) + sum_s part[s].
 __global__ void k_mix_reduce(const float* __restrict__ part, int S, size_t n, float* __restrict__ out, int accumulate) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;

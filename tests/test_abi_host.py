@@ -128,6 +128,15 @@ def test_unit_params_argument_errors():
     assert lib.box_params_clip(FAKE_MISALIGNED, 2, 4, None) == 4
 
 
+def test_relu_grad_argument_errors():
+    lib = bc.load_library()
+    assert lib.bc_relu_grad_bf16(None, FAKE, FAKE, 8, None) == 1
+    assert lib.bc_relu_grad_bf16(FAKE, None, FAKE, 8, None) == 1
+    assert lib.bc_relu_grad_bf16(FAKE, FAKE, None, 8, None) == 1
+    assert lib.bc_relu_grad_bf16(FAKE, FAKE, FAKE, 0, None) == 2
+    assert lib.bc_relu_grad_bf16(FAKE, FAKE_MISALIGNED, FAKE, 8, None) == 4
+
+
 def test_split_argument_errors():
     lib = bc.load_library()
     fwd = [FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, bc.BC_SPLIT_4, FAKE, bc.BC_F32, None, 0, None]

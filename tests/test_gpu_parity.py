@@ -886,6 +886,59 @@ def test_cast_bf16_bit_exact():
     np.testing.assert_array_equal(host(dst), O.bf16_round(v))
 
 
+def test_relu_grad_bf16_bit_exact():
+    """The ReLU backward in the mix's compute type, bf16(z > 0 ? g : 0),
+    against the oracle's rounding of the same selection: exact ties, zeros of
+    either sign and NaN in the mask (all mask out), n not a multiple of 8."""
+    rng = np.random.default_rng(111)
+    n = 100005
+    g = (rng.standard_normal(n) * 7).astype(np.float32)
+    z = rng.standard_normal(n).astype(np.float32)
+    z[:64] = 0.0
+    z[64:128] = -0.0
+    z[128:136] = np.nan
+    z[136:144] = np.inf
+    g[200:456] = ((np.arange(256, dtype=np.uint32) << 16) | 0x3F808000).view(np.float32)
+    z[200:456] = 1.0
+    dst = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    bc.relu_grad_bf16(dev(g), dev(z), dst)
+    with np.errstate(invalid="ignore"):
+        want = O.bf16_round(np.where(z > 0, g, np.float32(0.0)))
+    np.testing.assert_array_equal(host(dst), want)
+
+
+@pytest.mark.parametrize("dims", [(2, 64, 192, 160), (1, 40, 72, 77)])
+def test_relu_grad_prepass_matches_masked_gemms(dims):
+    """BWD_DATA and BWD_WEIGHT on the pre-masked bf16 gradient return bitwise
+    what the masked GEMMs return from the fp32 gradient and the forward
+    output (the layer's ReLU path relies on it)."""
+    N, M, K, P = dims
+    rng = np.random.default_rng(112)
+    gz = rng.standard_normal((N, M, P)).astype(np.float32)
+    zf = rng.standard_normal((N, M, P)).astype(np.float32)
+    w = (rng.standard_normal((M, K)) / np.sqrt(K)).astype(np.float32)
+    o = rng.standard_normal((N, K, P)).astype(np.float32)
+    cd = bc.BC_BF16
+    wd, od, gd, zd = dev(w), dev(o), dev(gz), dev(zf)
+    say(f"relu pre-pass vs masked GEMMs {dims}")
+    gm = torch.empty((N, M, P), dtype=torch.bfloat16, device="cuda")
+    bc.relu_grad_bf16(gd, zd, gm)
+    do_a = torch.empty((N, K, P), dtype=torch.float32, device="cuda")
+    do_b = torch.empty_like(do_a)
+    bc.pointwise_mix(bc.BC_MIX_BWD_DATA, wd, gd, do_a, N, M, K, P, cd, relu=1, aux=zd)
+    bc.pointwise_mix(bc.BC_MIX_BWD_DATA, wd, gm, do_b, N, M, K, P, cd)
+    assert torch.equal(do_a, do_b)
+    dw_a = torch.empty((M, K), dtype=torch.float32, device="cuda")
+    dw_b = torch.empty_like(dw_a)
+    bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, gd, od, dw_a, N, M, K, P, cd, relu=1, aux=zd)
+    bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, gm, od, dw_b, N, M, K, P, cd)
+    assert torch.equal(dw_a, dw_b)
+    # and both against the oracle's masked backward
+    zr = zf.reshape(N, M, P, 1)
+    check(host(do_b), O.mix_backward_data(w, gz.reshape(N, M, P, 1), compute="bf16", relu_out=zr).reshape(N, K, P),
+          RTOL_BF16_MIX, "dO")
+
+
 def test_mix_integer_exact():
     wl = wlmod.WORKLOADS[1]
     d = wlmod.make_inputs(wl)
