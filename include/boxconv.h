@@ -145,7 +145,8 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
  *          four-sample sum of Eq. 2, exact int32 for BC_I32 maps).
  * ws     : >= bc_box_workspace_bytes(0, ...) bytes: the tap records of
  *          box_prep (2*C*B*64 bytes), plus the maps' tables when a table does
- *          not fit in LDS or BC_FLAG_FORCE_HBM is set.
+ *          not fit in LDS ((H + 1) * ((W + 7) | 1) * 4 > 80 KiB) or
+ *          BC_FLAG_FORCE_HBM is set.
  * ---------------------------------------------------------------------- */
 bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
                        int N, int C, int H, int W, int B,
@@ -250,7 +251,7 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
  *        edges it is the mean of; grad_w [C][B][P] = <grad_y, piece sum>.
  *        Sums over n are fixed-order (deterministic).
  * Paths : as box_conv_fwd / box_conv_bwd: the map's table in LDS when
- *        (H + 1) * ((W + 7) | 1) * 4 <= 64 KiB (and, for the backward, the
+ *        (H + 1) * ((W + 7) | 1) * 4 <= 80 KiB (and, for the backward, the
  *        map has at most 256 work items), else tables in HBM built into the
  *        workspace, which needs W <= 1024 (BC_ERR_SHAPE otherwise).
  *        C * B <= 2^24.

@@ -746,10 +746,10 @@ def test_widest_maps(H, W, flags):
     check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
 
 
-@pytest.mark.parametrize("H,W", [(120, 120), (128, 128), (128, 48), (136, 48)])
+@pytest.mark.parametrize("H,W", [(128, 128), (138, 138), (140, 140), (128, 48), (136, 48)])
 def test_lds_limits(H, W):
-    """Maps on both sides of the LDS limits: 120x120 is the largest square
-    table the forward keeps in LDS (128x128 is not), 128x48 the largest map
+    """Maps on both sides of the LDS limits: 138x138 is the largest square
+    table the forward keeps in LDS (140x140 is not), 128x48 the largest map
     the backward walks in one block (136x48 is not)."""
     rng = np.random.default_rng(131)
     x = rng.standard_normal((2, 2, H, W)).astype(np.float32)
