@@ -837,8 +837,8 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // corners): the adjoint four-corner sums only, no edge gradients.  kUp
 // (stride s > 1): grad_y is [maps][Ho][Wo] and is tabulated zero-upsampled,
 // which makes every gradient that of the strided layer.
-template <int SEG, bool kInt, bool kUp>
-__global__ __launch_bounds__(256) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
+template <int SEG, bool kInt, bool kUp, int kMaxT>
+__global__ __launch_bounds__(kMaxT) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
                                                      const float* __restrict__ gy, float* __restrict__ gx,
                                                      float* __restrict__ partials, int C, int H, int W, int B,
                                                      int s, int Ho, int Wo) {
@@ -1590,7 +1590,7 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
   return last_error();
 }
 
-template <int SEG>
+template <int SEG, int kMaxT>
 static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N, int C,
                       int H, int W, int B, bool rounded, int stride, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
@@ -1599,30 +1599,34 @@ static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* g
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   with_flag(rounded, [&](auto ki) {
     with_flag(stride > 1, [&](auto ku) {
-      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value>), dim3(N * C), dim3(threads),
-                         shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
+      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT>), dim3(N * C),
+                         dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
     });
   });
 }
 
 // Segment length of the LDS backward: 8 rows when the map's items fit one
-// 256-thread block, else 4; 0 = the map needs more than 256 items.
-int box_bwd_lds_seg(int H, int W) {
+// 256-thread block, else 4 while they fit max_items threads; 0 = too many.
+// The 4-row walk fits 128 VGPRs, so its blocks may take up to 1024 threads
+// (maps up to 128x96 or 256x48): one block per CU, 16 waves.
+int box_bwd_lds_seg(int H, int W, int max_items) {
   if (n_chunks(W) * n_segs(H, 8) <= 256) return 8;
-  if (n_chunks(W) * n_segs(H, 4) <= 256) return 4;
+  if (n_chunks(W) * n_segs(H, 4) <= max_items) return 4;
   return 0;
 }
 
-int box_bwd_lds_waves(int H, int W) {
-  const int seg = box_bwd_lds_seg(H, W);
+int box_bwd_lds_waves(int H, int W, int max_items) {
+  const int seg = box_bwd_lds_seg(H, W, max_items);
   return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
 }
 
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N,
                               int C, int H, int W, int B, bool rounded, int stride, hipStream_t s) {
-  const int seg = box_bwd_lds_seg(H, W);
-  if (seg == 8) bwd_lds_t<8>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
-  else if (seg == 4) bwd_lds_t<4>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+  const int seg = box_bwd_lds_seg(H, W, kBwdLdsItems);
+  if (seg == 8) bwd_lds_t<8, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+  else if (seg == 4 && n_chunks(W) * n_segs(H, 4) <= 256)
+    bwd_lds_t<4, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+  else if (seg == 4) bwd_lds_t<4, kBwdLdsItems>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
   else return hipErrorInvalidValue;
   return last_error();
 }
@@ -1707,7 +1711,7 @@ static void bwd_split_mode(const float* x, const int* rec, const float* gy, floa
 
 hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N,
                                     int C, int H, int W, int B, int nx, int ny, hipStream_t s) {
-  const int seg = box_bwd_lds_seg(H, W);
+  const int seg = box_bwd_lds_seg(H, W, 256);
   if (seg == 8) bwd_split_mode<8>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
   else if (seg == 4) bwd_split_mode<4>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
   else return hipErrorInvalidValue;

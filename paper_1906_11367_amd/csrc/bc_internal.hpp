@@ -40,14 +40,16 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
 
 // Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
 // LDS path: one block of box_bwd_lds_waves() waves per map, P = N * waves;
-// box_bwd_lds_seg() == 0 means the map has too many items for one block.
+// box_bwd_lds_seg() == 0 means the map has too many items for one block
+// (max_items: kBwdLdsItems for the whole-box backward, 256 for the split one).
 // rounded: input gradient only (partials unused).  stride > 1: gy is
 // [N][C*B][ceil(H/stride)][ceil(W/stride)] (tabulated zero-upsampled).
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx,
                               float* partials, int N, int C, int H, int W, int B, bool rounded, int stride,
                               hipStream_t s);
-int box_bwd_lds_seg(int H, int W);
-int box_bwd_lds_waves(int H, int W);
+constexpr int kBwdLdsItems = 1024;
+int box_bwd_lds_seg(int H, int W, int max_items);
+int box_bwd_lds_waves(int H, int W, int max_items);
 // HBM path: tables of every gradient map in sat_g (built by sat_build, or
 // sat_build_up for stride > 1);
 // P = N * box_bwd_gather_blocks() * 4.

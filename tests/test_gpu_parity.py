@@ -746,11 +746,13 @@ def test_widest_maps(H, W, flags):
     check(gb, O.box_backward_params(x, g, bx), RTOL_F32, "dboxes")
 
 
-@pytest.mark.parametrize("H,W", [(128, 128), (138, 138), (140, 140), (128, 48), (136, 48)])
+@pytest.mark.parametrize("H,W", [(128, 128), (138, 138), (140, 140), (128, 48), (136, 48), (96, 96), (256, 48),
+                                 (260, 48)])
 def test_lds_limits(H, W):
     """Maps on both sides of the LDS limits: 138x138 is the largest square
-    table the forward keeps in LDS (140x140 is not), 128x48 the largest map
-    the backward walks in one block (136x48 is not)."""
+    table the forward keeps in LDS (140x140 is not); the backward walks a map
+    in one block of up to 256 threads to 128x48, of up to 1024 threads from
+    136x48 (and 96x96) to 256x48, and takes the HBM tables from 260x48."""
     rng = np.random.default_rng(131)
     x = rng.standard_normal((2, 2, H, W)).astype(np.float32)
     g = rng.standard_normal((2, 4, H, W)).astype(np.float32)
