@@ -37,10 +37,6 @@ bool fwd_lds_fits(int H, int W) {
 bool bwd_lds_fits(int H, int W) {
   return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(H, W, bc::kBwdLdsItems) > 0;
 }
-// The split backward's blocks take at most 256 threads.
-bool split_bwd_lds_fits(int H, int W) {
-  return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(H, W, 256) > 0;
-}
 
 // Workspace layouts.  Every box entry point first writes the tap records of
 // all boxes (box_prep) at offset 0; the HBM paths add their tables after it.
@@ -244,7 +240,7 @@ static SplitWs split_bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
   SplitWs w{};
   w.sat = split_corner_bytes(C, B);
   w.partials = w.sat + (hbm ? align_up((size_t)N * C * B * table_elems(H, W) * 4) : 0);
-  w.rows = hbm ? N * bc::box_bwd_gather_blocks(H, W) * 4 : N * bc::box_bwd_lds_waves(H, W, 256);
+  w.rows = hbm ? N * bc::box_bwd_gather_blocks(H, W) * 4 : N * bc::box_bwd_lds_waves(H, W, bc::kBwdLdsItems);
   w.total = w.partials + align_up((size_t)w.rows * C * B * 8 * 4);
   return w;
 }
@@ -263,7 +259,7 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
     return hbm && W > 1024 ? 0 : split_fwd_ws(N, C, H, W, B, hbm).total;
   }
   if (op == 1) {
-    const bool hbm = force || !split_bwd_lds_fits(H, W);
+    const bool hbm = force || !bwd_lds_fits(H, W);
     return hbm && W > 1024 ? 0 : split_bwd_ws(N, C, H, W, B, hbm).total;
   }
   return 0;
@@ -304,7 +300,7 @@ bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* pi
   int nx, ny;
   const int P = split_pieces(mode, nx, ny);
   if (P == 0) return BC_ERR_UNSUPPORTED;
-  const bool hbm = (mode & BC_SPLIT_FORCE_HBM) || !split_bwd_lds_fits(H, W);
+  const bool hbm = (mode & BC_SPLIT_FORCE_HBM) || !bwd_lds_fits(H, W);
   if (hbm && W > 1024) return BC_ERR_SHAPE;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(piece_w) || !aligned16(grad_y) ||
       (grad_x && !aligned16(grad_x)) || (grad_boxes && !aligned16(grad_boxes)) || (grad_w && !aligned16(grad_w)))

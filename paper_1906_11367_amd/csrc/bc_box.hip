@@ -1286,8 +1286,8 @@ __device__ __forceinline__ void split_box_grads(const float* __restrict__ f, con
 // one item of 3 columns x SEG rows per thread, input values in registers), one
 // walk over each box's mirrored corners.  Each wave writes its split_box_grads
 // sums to partials[(n * nw + wave) * C*B + c*B + b][8].
-template <int SEG, int NXC, int NYC>
-__global__ __launch_bounds__(256) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
+template <int SEG, int NXC, int NYC, int kMaxT>
+__global__ __launch_bounds__(kMaxT) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
                                                            const float* __restrict__ gy, float* __restrict__ gx,
                                                            float* __restrict__ partials, int C, int H, int W,
                                                            int B) {
@@ -1692,28 +1692,32 @@ hipError_t launch_box_prep_corners_adj(const float* boxes, const float* piece_w,
   return last_error();
 }
 
-template <int SEG, int NXC, int NYC>
+template <int SEG, int NXC, int NYC, int kMaxT>
 static void bwd_split_t(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N, int C,
                         int H, int W, int B, hipStream_t s) {
   const int threads = ((n_chunks(W) * n_segs(H, SEG) + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
-  hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC>), dim3(N * C), dim3(threads), shm, s, x, rec, gy, gx,
-                     partials, C, H, W, B);
+  hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC, kMaxT>), dim3(N * C), dim3(threads), shm, s, x, rec, gy,
+                     gx, partials, C, H, W, B);
 }
 
-template <int SEG>
+template <int SEG, int kMaxT>
 static void bwd_split_mode(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N, int C,
                            int H, int W, int B, int nx, int ny, hipStream_t s) {
-  if (nx == 2 && ny == 2) bwd_split_t<SEG, 3, 3>(x, rec, gy, gx, partials, N, C, H, W, B, s);
-  else if (nx == 2) bwd_split_t<SEG, 3, 2>(x, rec, gy, gx, partials, N, C, H, W, B, s);
-  else bwd_split_t<SEG, 2, 3>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+  if (nx == 2 && ny == 2) bwd_split_t<SEG, 3, 3, kMaxT>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+  else if (nx == 2) bwd_split_t<SEG, 3, 2, kMaxT>(x, rec, gy, gx, partials, N, C, H, W, B, s);
+  else bwd_split_t<SEG, 2, 3, kMaxT>(x, rec, gy, gx, partials, N, C, H, W, B, s);
 }
 
+// As the whole-box backward: 8-row items in blocks of up to 256 threads, else
+// 4-row items (at most 107 VGPRs) in blocks of up to kBwdLdsItems threads.
 hipError_t launch_box_bwd_lds_split(const float* x, const int* rec, const float* gy, float* gx, float* partials, int N,
                                     int C, int H, int W, int B, int nx, int ny, hipStream_t s) {
-  const int seg = box_bwd_lds_seg(H, W, 256);
-  if (seg == 8) bwd_split_mode<8>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
-  else if (seg == 4) bwd_split_mode<4>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
+  const int seg = box_bwd_lds_seg(H, W, kBwdLdsItems);
+  if (seg == 8) bwd_split_mode<8, 256>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
+  else if (seg == 4 && n_chunks(W) * n_segs(H, 4) <= 256)
+    bwd_split_mode<4, 256>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
+  else if (seg == 4) bwd_split_mode<4, kBwdLdsItems>(x, rec, gy, gx, partials, N, C, H, W, B, nx, ny, s);
   else return hipErrorInvalidValue;
   return last_error();
 }

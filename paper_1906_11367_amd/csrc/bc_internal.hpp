@@ -41,7 +41,8 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
 // Backward (fp32).  partials: [P][C*B][4] edge gradients (a, b, c, d).
 // LDS path: one block of box_bwd_lds_waves() waves per map, P = N * waves;
 // box_bwd_lds_seg() == 0 means the map has too many items for one block
-// (max_items: kBwdLdsItems for the whole-box backward, 256 for the split one).
+// (max_items: kBwdLdsItems; blocks of more than 256 threads run the 4-row
+// walk, which fits the 128 VGPRs such a block allows).
 // rounded: input gradient only (partials unused).  stride > 1: gy is
 // [N][C*B][ceil(H/stride)][ceil(W/stride)] (tabulated zero-upsampled).
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx,

@@ -170,7 +170,9 @@ def test_split_argument_errors():
     assert lib.box_conv_split_bwd(*a) == 7
     a = list(bwd); a[6] = 256; a[7] = 256
     assert lib.box_conv_split_bwd(*a) == 5
-    a = list(bwd); a[6] = 4; a[7] = 1025
+    a = list(bwd); a[6] = 4; a[7] = 1025                   # 342 items: one LDS block, no width limit
+    assert lib.box_conv_split_bwd(*a) == 5
+    a[9] = bc.BC_SPLIT_2X | bc.BC_SPLIT_FORCE_HBM          # HBM path: W up to 1024
     assert lib.box_conv_split_bwd(*a) == 2
     # workspace: one 128-byte corner record per box, and for the backward the
     # 8-word partials of every wave of every image
@@ -187,7 +189,8 @@ def test_split_argument_errors():
     forced = bc.BC_SPLIT_4 | bc.BC_SPLIT_FORCE_HBM
     assert lib.bc_split_workspace_bytes(0, 32, 256, 64, 48, 4, forced) >= 256 * 4 * 128 + 32 * 256 * 65 * 49 * 4
     assert lib.bc_split_workspace_bytes(0, 4, 8, 4, 1025, 4, forced) == 0
-    assert lib.bc_split_workspace_bytes(1, 4, 8, 4, 1025, 4, bc.BC_SPLIT_4) == 0
+    assert lib.bc_split_workspace_bytes(1, 4, 8, 4, 1025, 4, forced) == 0
+    assert lib.bc_split_workspace_bytes(1, 4, 8, 4, 1025, 4, bc.BC_SPLIT_4) > 0
 
 
 def test_mix_argument_errors():

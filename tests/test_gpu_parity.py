@@ -733,8 +733,9 @@ def test_bwd_integer_edges(flags):
 @pytest.mark.parametrize("H,W", [(5, 1024), (3, 1021)])
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
 def test_widest_maps(H, W, flags):
-    """W up to 1024 (the row-scan limit): the forward's table fits LDS, the
-    backward has more than 256 items and takes the HBM tables."""
+    """W up to 1024 (the HBM row-scan limit): the tables fit LDS and the
+    backward's 684 (342) items one block of up to 1024 threads; with
+    BC_FLAG_FORCE_HBM both take the HBM tables."""
     rng = np.random.default_rng(130)
     x = rng.standard_normal((1, 2, H, W)).astype(np.float32)
     g = rng.standard_normal((1, 6, H, W)).astype(np.float32)
@@ -805,11 +806,12 @@ def test_split_degenerate_boxes(mode, hbm):
 
 
 @pytest.mark.parametrize("mode", ["2x", "4"])
-@pytest.mark.parametrize("H,W", [(70, 100), (131, 133)])
+@pytest.mark.parametrize("H,W", [(70, 100), (131, 133), (150, 151)])
 def test_split_large_maps(H, W, mode):
-    """Maps past the LDS limits, which take the HBM tables by themselves:
-    70x100 has a forward table in LDS but too many backward items for one
-    block; 131x133 has neither (ragged in both directions)."""
+    """Maps at and past the LDS limits, each taking its path by itself:
+    70x100 walks its 612 backward items in one block of 640 threads; 131x133
+    keeps its forward table in LDS (74 KiB) but has too many backward items
+    for one block; 150x151 has neither in LDS (ragged in both directions)."""
     rng = np.random.default_rng(134)
     x = rng.standard_normal((1, 2, H, W)).astype(np.float32)
     g = rng.standard_normal((1, 6, H, W)).astype(np.float32)
