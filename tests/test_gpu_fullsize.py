@@ -120,12 +120,15 @@ def test_pose_layer_full_size_sampled():
         assert pw.max() <= RTOL_BF16
 
 
-# The large-map workload builds its tables from (map - mean): bar 1e-4.  The
-# plain fp32 table is the reported comparison: its edge integrals are
-# differences of table values ~ 3e4 (0.5-mean maps of 65536 pixels), so the
-# box-parameter gradient carries ~1e-4 of cancellation; bar 2e-4 there.
-@pytest.mark.parametrize("offset,rtol_params", [(True, 1e-4), (False, 2e-4)])
-def test_large_maps_full_size_sampled(offset, rtol_params):
+# The large-map workload builds its forward tables from (map - mean); the
+# plain fp32 table is the reported comparison.  Its values reach ~3e4
+# (0.5-mean maps of 65536 pixels), so each four-corner difference loses about
+# 1e-6 of relative precision (measured: outputs 1.8e-6 plain, 1.7e-7 with the
+# offset).  The backward tabulates only the upstream gradient, so its results
+# do not depend on the offset.  Bar 1e-4 for all.
+@pytest.mark.parametrize("offset", [True, False])
+def test_large_maps_full_size_sampled(offset):
+    rtol_params = 1e-4
     wl = wlmod.WORKLOADS[4].scaled(mean_offset=offset)
     d = wlmod.make_inputs(wl)
     say(f"{wl.key} full size, mean offset {offset}")
