@@ -484,7 +484,9 @@ __device__ __forceinline__ void edge_grads(const Taps<float>& tp, const float (&
 
 // Emitter of forward outputs: the kQ outputs of row y0 + s at plane offset
 // off0 + s * W (elements; off0 = y0 * W + x0).
-template <typename OutT, typename T>
+// kNT: non-temporal stores (the HBM-table forwards with outputs larger than
+// the last-level cache, see kStreamOutBytes).
+template <typename OutT, typename T, bool kNT = false>
 struct StoreRows {
   OutT* out;
   int W, x0, off0;
@@ -493,7 +495,10 @@ struct StoreRows {
     OutT* row = out + (unsigned)(off0 + s * W);
 #pragma unroll
     for (int q = 0; q < kQ; ++q)
-      if (kFull || x0 + q < W) row[q] = convert_out<OutT, T>(o[q]);
+      if (kFull || x0 + q < W) {
+        if constexpr (kNT) __builtin_nontemporal_store(convert_out<OutT, T>(o[q]), row + q);
+        else row[q] = convert_out<OutT, T>(o[q]);
+      }
   }
 };
 
@@ -704,7 +709,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
 
 // Forward, table in HBM: one block per (map, box, block of 256 items), mapped
 // so that one map's blocks run on one XCD.
-template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt, bool kNT>
 __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sat, const float* __restrict__ means,
                                                         const int* __restrict__ taps, OutT* __restrict__ y,
                                                         int C, int H, int W, int B, int nblk, int total) {
@@ -721,7 +726,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather(const T* __restrict__ sa
   const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
   OutT* out = y + ((size_t)map * B + b) * H * W;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
+  StoreRows<OutT, T, kNT> em{out, W, x0, y0 * W + x0};
   if (y0 + SEG <= H && x0 + kQ <= W) walk_fwd<SEG, T, kOffset, true, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
   else walk_fwd<SEG, T, kOffset, false, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
 }
@@ -1334,7 +1339,7 @@ __global__ __launch_bounds__(kMaxT) void k_box_bwd_lds_split(const float* __rest
 
 // Forward of split boxes, table in HBM: as k_box_fwd_gather (one block per
 // (map, box, block of 256 items), one map's blocks on one XCD).
-template <typename OutT, int SEG, int NXC, int NYC>
+template <typename OutT, int SEG, int NXC, int NYC, bool kNT>
 __global__ __launch_bounds__(256) void k_box_fwd_gather_split(const float* __restrict__ sat,
                                                               const int* __restrict__ rec, OutT* __restrict__ y,
                                                               int C, int H, int W, int B, int nblk, int total) {
@@ -1350,7 +1355,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_gather_split(const float* __res
   const int* rb = rec + (size_t)(c * B + b) * 32;
   OutT* out = y + ((size_t)map * B + b) * H * W;
   const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-  StoreRows<OutT, float> em{out, W, x0, y0 * W + x0};
+  StoreRows<OutT, float, kNT> em{out, W, x0, y0 * W + x0};
   if (y0 + SEG <= H && x0 + kQ <= W) corner_walk<SEG, NXC, NYC, true>(tab, rb, x0, y0, y1, em);
   else corner_walk<SEG, NXC, NYC, false>(tab, rb, x0, y0, y1, em);
 }
@@ -1550,6 +1555,15 @@ hipError_t launch_box_fwd_lds(const void* x, bool is_int, const int* taps, void*
   return last_error();
 }
 
+// The HBM-table forwards re-read their tables through the caches; an output
+// larger than the last-level cache (256 MiB) cannot stay there for the next
+// call anyway, so 4-byte outputs that large are stored non-temporally and
+// leave the caches to the tables (4 x 128 maps of 256x256, 8 boxes, fp32
+// out: 893 -> 776 us).  Narrower outputs keep ordinary stores: 2-byte
+// non-temporal stores were slower.
+constexpr size_t kStreamOutBytes = (size_t)256 << 20;
+static bool stream_out(size_t elems, size_t bytes_per) { return bytes_per == 4 && elems * bytes_per > kStreamOutBytes; }
+
 template <typename T, typename OutT, bool kOffset>
 static void fwd_gather_t(const void* sat, const float* means, const int* taps, void* y, int N, int C, int H, int W,
                          int B, bool rounded, int stride, hipStream_t s) {
@@ -1558,9 +1572,13 @@ static void fwd_gather_t(const void* sat, const float* means, const int* taps, v
     const int items = n_chunks(W) * n_segs(H, SEG);
     const int nblk = (items + 255) / 256;
     const int total = N * C * B * nblk;
+    const bool nt = stream_out((size_t)N * C * B * H * W, sizeof(OutT));
     with_flag(rounded, [&](auto ki) {
-      hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(pad8(total)),
-                         dim3(256), 0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk, total);
+      with_flag(nt, [&](auto kn) {
+        hipLaunchKernelGGL((k_box_fwd_gather<T, OutT, SEG, kOffset, decltype(ki)::value, decltype(kn)::value>),
+                           dim3(pad8(total)), dim3(256), 0, s, (const T*)sat, means, taps, (OutT*)y, C, H, W, B, nblk,
+                           total);
+      });
     });
     return;
   }
@@ -1728,8 +1746,10 @@ static void fwd_gather_split_t(const float* sat, const int* rec, void* y, int N,
   constexpr int SEG = 16;
   const int nblk = (n_chunks(W) * n_segs(H, SEG) + 255) / 256;
   const int total = N * C * B * nblk;
-  hipLaunchKernelGGL((k_box_fwd_gather_split<OutT, SEG, NXC, NYC>), dim3(pad8(total)), dim3(256), 0, s, sat, rec,
-                     (OutT*)y, C, H, W, B, nblk, total);
+  with_flag(stream_out((size_t)N * C * B * H * W, sizeof(OutT)), [&](auto kn) {
+    hipLaunchKernelGGL((k_box_fwd_gather_split<OutT, SEG, NXC, NYC, decltype(kn)::value>), dim3(pad8(total)),
+                       dim3(256), 0, s, sat, rec, (OutT*)y, C, H, W, B, nblk, total);
+  });
 }
 
 template <typename OutT>
