@@ -290,6 +290,7 @@ def test_fwd_integer_corners_bf16_output():
     (3, dict(N=3, C=4)),
     (2, dict(N=1, C=3, H=37, W=29, B=5)),
     (3, dict(N=2, C=2, H=17, W=100, B=3)),
+    (3, dict(N=1, C=2, H=96, W=97, B=3)),       # 792 items: one block of 832 threads
     (4, dict(N=1, C=1, B=3)),
 ])
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
@@ -382,6 +383,7 @@ def test_strided_api_stride_one_is_plain():
     (3, dict(N=2, C=4)),
     (2, dict(N=1, C=3, H=37, W=29, B=5)),
     (3, dict(N=2, C=2, H=17, W=100, B=3)),
+    (3, dict(N=1, C=2, H=96, W=97, B=3)),       # 792 items of the full-size map: one wide block
     (4, dict(N=1, C=1, B=3)),
 ])
 @pytest.mark.parametrize("stride", [2, 3])
