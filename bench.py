@@ -78,7 +78,8 @@ def call_cost(label, wl, o_bytes, stride=1):
     """Algorithmic bytes and FLOPs of one launch of a library call (one layer).
 
     box_conv_fwd : read x (4 B/pixel) + write O (o_bytes per output pixel*box)
-    box_conv_bwd : read x + read dO (4 B/output pixel*box) + write dx (4 B/pixel)
+    box_conv_bwd : read x + read dO (4 B/output pixel*box) + write dx (4 B/pixel;
+                   2 B for box_conv_bwd_relu_bf16)
     mix_*        : 2*N*M*K*P FLOPs (one GEMM), reported against the MFMA
                    peak; also the operand bytes it must move (fwd: read O,
                    write Z; bwd_data: read dZ, write dO; bwd_weight: read dZ
@@ -95,6 +96,8 @@ def call_cost(label, wl, o_bytes, stride=1):
         return {"bound": "hbm", "bytes": 4 * px + o_bytes * pb}
     if label in ("box_conv_bwd", "box_conv_split_bwd"):
         return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 4 * px}
+    if label == "box_conv_bwd_relu_bf16":                  # dx written in bf16
+        return {"bound": "hbm", "bytes": 4 * px + 4 * pb + 2 * px}
     flops = 2 * wl.N * wl.mix_out * wl.C * wl.B * Ho * Wo
     nz = wl.N * wl.mix_out * Ho * Wo
     z = 4 * nz

@@ -184,6 +184,24 @@ bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * box_conv_bwd_relu_bf16 -- box_conv_bwd_strided for a layer whose input x
+ * is the rectified output of a bf16 mix before it (stacked blocks of the
+ * dense prediction network, Section 3.3): the input gradient is written as
+ * that mix's backward operand,
+ *   grad_x_bf16[i] = bf16(x[i] > 0 ? dL/dx[i] : 0), round to nearest even,
+ * which is bc_relu_grad_bf16(dL/dx, x) bit for bit for every finite value
+ * and infinity (x > 0 is the ReLU's mask; a NaN stays a NaN), without
+ * writing the fp32 gradient or reading it back.
+ * grad_x_bf16 : device bf16 codes [N][C][H][W] or NULL (skip).
+ * Every other argument, flag and workspace size is as for
+ * box_conv_bwd_strided; BC_FLAG_INTEGER_CORNERS is BC_ERR_UNSUPPORTED.
+ * ---------------------------------------------------------------------- */
+bc_status box_conv_bwd_relu_bf16(const float* x, const float* boxes, const float* grad_y,
+                                 int N, int C, int H, int W, int B, int stride,
+                                 void* grad_x_bf16, float* grad_boxes, unsigned flags,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * box_conv_fwd_strided / box_conv_bwd_strided -- the same layer with an
  * integer stride (Section 3.1 assumes an integer stride: shifting a box by
  * whole pixels leaves its interpolation weights unchanged).  Output pixel

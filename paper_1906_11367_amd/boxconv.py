@@ -50,6 +50,7 @@ SIGNATURES = {
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
     "bc_relu_grad_bf16": (_i, [_vp, _vp, _vp, _sz, _vp]),
+    "box_conv_bwd_relu_bf16": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
     "bc_status_string": (ctypes.c_char_p, [_i]),
     "bc_abi_version": (_i, []),
 }
@@ -186,6 +187,26 @@ def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, gra
                                       _ptr(grad_boxes), flags, _ptr(ws), nbytes, _stream())
     _check(st, "box_conv_bwd")
     return grad_x, grad_boxes
+
+
+def box_conv_bwd_relu_bf16(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor,
+                           grad_x_bf16: torch.Tensor | None, grad_boxes: torch.Tensor | None, flags: int = 0,
+                           ws: torch.Tensor | None = None, stride: int = 1):
+    """As box_conv_bwd, with the input gradient written as bf16(x > 0 ? dL/dx : 0)
+    (x: the rectified output of a bf16 mix before this layer)."""
+    N, C, H, W = x.shape
+    B = boxes.shape[1]
+    if tuple(grad_y.shape) != _strided_shape(N, C, H, W, B, stride):
+        raise BoxConvError(f"box_conv_bwd_relu_bf16: grad_y has shape {tuple(grad_y.shape)}")
+    if grad_x_bf16 is not None and (grad_x_bf16.dtype != torch.bfloat16 or tuple(grad_x_bf16.shape) != (N, C, H, W)):
+        raise BoxConvError("box_conv_bwd_relu_bf16: grad_x must be bf16 [N, C, H, W]")
+    if ws is None:
+        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().box_conv_bwd_relu_bf16(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, stride,
+                                                 _ptr(grad_x_bf16), _ptr(grad_boxes), flags, _ptr(ws), nbytes,
+                                                 _stream()), "box_conv_bwd_relu_bf16")
+    return grad_x_bf16, grad_boxes
 
 
 def box_conv_bwd_strided(x, boxes, grad_y, stride: int, grad_x, grad_boxes, flags: int = 0, ws=None):

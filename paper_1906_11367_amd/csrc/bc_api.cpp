@@ -164,9 +164,10 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, 
   return box_conv_fwd_strided(x, x_dt, boxes, N, C, H, W, B, 1, y, y_dt, flags, ws, ws_bytes, stream);
 }
 
-bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W,
-                               int B, int stride, float* grad_x, float* grad_boxes, unsigned flags, void* ws,
-                               size_t ws_bytes, hipStream_t stream) {
+// Both backward entry points: grad_x fp32, or (relu_bf16) bf16(x > 0 ? dx : 0).
+static bc_status box_bwd_impl(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W,
+                              int B, int stride, void* grad_x, bool relu_bf16, float* grad_boxes, unsigned flags,
+                              void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!x || !boxes || !grad_y) return BC_ERR_NULL;
   if (!dims_ok(N, C, H, W, B) || stride < 1 || stride > kMaxStride) return BC_ERR_SHAPE;
   if (flags & ~(BC_FLAG_MEAN_OFFSET | BC_FLAG_FORCE_HBM | BC_FLAG_INTEGER_CORNERS)) return BC_ERR_UNSUPPORTED;
@@ -174,6 +175,7 @@ bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* 
   // rounding the corners is not differentiable: with rounded corners the
   // boxes are frozen and only the input gradient is defined
   if (rounded && grad_boxes) return BC_ERR_UNSUPPORTED;
+  if (rounded && relu_bf16) return BC_ERR_UNSUPPORTED;
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(grad_y) || (grad_x && !aligned16(grad_x)) ||
       (grad_boxes && !aligned16(grad_boxes)))
     return BC_ERR_ALIGN;
@@ -192,17 +194,31 @@ bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* 
   hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
   if (!hbm) {
-    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, stride, stream);
+    e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, relu_bf16, stride, stream);
   } else {
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);
     e = stride == 1 ? bc::launch_sat_build(grad_y, false, sat_g, nullptr, N * C * B, H, W, stream)
                     : bc::launch_sat_build_up(grad_y, sat_g, N * C * B, H, W, stride, stream);
     if (e == hipSuccess)
-      e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, rounded, stream);
+      e = bc::launch_box_bwd_gather(x, sat_g, taps, grad_x, partials, N, C, H, W, B, rounded, relu_bf16, stream);
   }
   if (e != hipSuccess) return BC_ERR_HIP;
   if (grad_boxes) e = bc::launch_box_grad_reduce(partials, L.P, C * B, grad_boxes, stream);
   return hip_status(e);
+}
+
+bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W,
+                               int B, int stride, float* grad_x, float* grad_boxes, unsigned flags, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  return box_bwd_impl(x, boxes, grad_y, N, C, H, W, B, stride, grad_x, false, grad_boxes, flags, ws, ws_bytes,
+                      stream);
+}
+
+bc_status box_conv_bwd_relu_bf16(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W,
+                                 int B, int stride, void* grad_x_bf16, float* grad_boxes, unsigned flags, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  return box_bwd_impl(x, boxes, grad_y, N, C, H, W, B, stride, grad_x_bf16, true, grad_boxes, flags, ws, ws_bytes,
+                      stream);
 }
 
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y, int N, int C, int H, int W, int B,

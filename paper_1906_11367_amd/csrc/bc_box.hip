@@ -823,6 +823,47 @@ __device__ __forceinline__ void store_item(float* __restrict__ out, int H, int W
   }
 }
 
+// The input gradient of a layer whose input x is a ReLU output, in the
+// compute type of the bf16 mix before it: bf16(x > 0 ? dx : 0), round to
+// nearest even.  x > 0 is the ReLU's own mask, so these are the operand bits
+// that mix's backward forms.  The mask is taken from the item's input values
+// once, as one bit per output (relu_mask), so they need not stay live.
+template <int SEG>
+__device__ __forceinline__ uint32_t relu_mask(const float (&v)[SEG][kQ]) {
+  static_assert(SEG * kQ <= 32, "one bit per output");
+  uint32_t m = 0;
+#pragma unroll
+  for (int s = 0; s < SEG; ++s)
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) m |= (v[s][q] > 0.f ? 1u : 0u) << (s * kQ + q);
+  return m;
+}
+
+// fp32 -> bf16 bits, round to nearest even, in integer arithmetic: the same
+// bits as the conversion instruction for every finite value and infinity (a
+// NaN stays a quiet NaN).  Here the instruction's form made the backward's
+// register allocation grow from 144 to 224 VGPRs; this one does not.
+__device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
+  const uint32_t b = __float_as_uint(f);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);
+  return (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
+}
+
+template <int SEG>
+__device__ __forceinline__ void store_item_relu_bf16(uint16_t* __restrict__ out, int H, int W, int x0, int y0,
+                                                     const float (&acc)[SEG][kQ], uint32_t mask) {
+#pragma unroll
+  for (int s = 0; s < SEG; ++s) {
+    const int yy = y0 + s;
+    if (yy < H) {
+#pragma unroll
+      for (int q = 0; q < kQ; ++q)
+        if (x0 + q < W)
+          out[(size_t)yy * W + x0 + q] = bf16_rne_bits(((mask >> (s * kQ + q)) & 1u) ? acc[s][q] : 0.f);
+    }
+  }
+}
+
 // The wave's sums of the four edge gradients, written by lane 0 to pp[0..3].
 __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict__ pp) {
 #pragma unroll
@@ -841,12 +882,14 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // partials[(n * nw + wave) * C*B + c*B + b][4].  kInt (boxes with integer
 // corners): the adjoint four-corner sums only, no edge gradients.  kUp
 // (stride s > 1): grad_y is [maps][Ho][Wo] and is tabulated zero-upsampled,
-// which makes every gradient that of the strided layer.
-template <int SEG, bool kInt, bool kUp, int kMaxT>
+// which makes every gradient that of the strided layer.  kRelu: gx is bf16,
+// store_item_relu_bf16 (not with kInt, which does not read x).
+template <int SEG, bool kInt, bool kUp, int kMaxT, bool kRelu>
 __global__ __launch_bounds__(kMaxT) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
-                                                     const float* __restrict__ gy, float* __restrict__ gx,
+                                                     const float* __restrict__ gy, void* __restrict__ gx,
                                                      float* __restrict__ partials, int C, int H, int W, int B,
                                                      int s, int Ho, int Wo) {
+  static_assert(!(kInt && kRelu), "the ReLU mask needs x");
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -863,6 +906,8 @@ __global__ __launch_bounds__(kMaxT) void k_box_bwd_lds(const float* __restrict__
   const float* g0 = gy + (size_t)map * B * gplane;
   float v[SEG][kQ], acc[SEG][kQ];
   if constexpr (!kInt) load_item<SEG>(x + (size_t)map * plane, H, W, x0, y0, active, v);
+  uint32_t rmask = 0;
+  if constexpr (kRelu) rmask = relu_mask<SEG>(v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
@@ -893,16 +938,19 @@ __global__ __launch_bounds__(kMaxT) void k_box_bwd_lds(const float* __restrict__
     edge_grads(tp, P, g4);
     store_wave_partial(g4, partials + (((size_t)n * nw + wave) * C * B + (size_t)c * B + b) * 4);
   }
-  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * plane, H, W, x0, y0, acc);
+  if (active && gx != nullptr) {
+    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * plane, H, W, x0, y0, acc, rmask);
+    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * plane, H, W, x0, y0, acc);
+  }
 }
 
 // Backward, tables in HBM (one table per gradient map, built beforehand).
 // One 256-thread block per (map, block of 256 items); loops over boxes.
 // partials: [((n * nblk + blk) * 4 + wave) * C*B + c*B + b][4]; kInt as in
 // k_box_bwd_lds.
-template <int SEG, bool kInt>
+template <int SEG, bool kInt, bool kRelu>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_box_bwd_gather(const float* __restrict__ x, const float* __restrict__ sat_g,
-                                                        const int* __restrict__ taps, float* __restrict__ gx,
+                                                        const int* __restrict__ taps, void* __restrict__ gx,
                                                         float* __restrict__ partials, int C, int H, int W, int B,
                                                         int nblk, int total) {
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -919,6 +967,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
   const size_t tsz = (size_t)(H + 1) * (W + 1);
   float v[SEG][kQ], acc[SEG][kQ];
   if constexpr (!kInt) load_item<SEG>(x + (size_t)map * H * W, H, W, x0, y0, active, v);
+  uint32_t rmask = 0;
+  if constexpr (kRelu) rmask = relu_mask<SEG>(v);
 #pragma unroll
   for (int s = 0; s < SEG; ++s)
 #pragma unroll
@@ -946,7 +996,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
     edge_grads(tp, P, g4);
     store_wave_partial(g4, partials + ((((size_t)n * nblk + blk) * 4 + wave) * C * B + (size_t)c * B + b) * 4);
   }
-  if (active && gx != nullptr) store_item<SEG>(gx + (size_t)map * H * W, H, W, x0, y0, acc);
+  if (active && gx != nullptr) {
+    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * H * W, H, W, x0, y0, acc, rmask);
+    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * H * W, H, W, x0, y0, acc);
+  }
 }
 
 // Second stage of the box-parameter gradient: fixed-order sum of the partial
@@ -1609,17 +1662,19 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
 }
 
 template <int SEG, int kMaxT>
-static void bwd_lds_t(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N, int C,
-                      int H, int W, int B, bool rounded, int stride, hipStream_t s) {
+static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N, int C,
+                      int H, int W, int B, bool rounded, bool relu_bf16, int stride, hipStream_t s) {
   const int items = n_chunks(W) * n_segs(H, SEG);
   const int threads = ((items + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
-  with_flag(rounded, [&](auto ki) {
-    with_flag(stride > 1, [&](auto ku) {
-      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT>), dim3(N * C),
-                         dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
-    });
+  auto go = [&](auto ki, auto ku, auto kr) {
+    hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT, decltype(kr)::value>),
+                       dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
+  };
+  with_flag(stride > 1, [&](auto ku) {
+    if (rounded) go(std::true_type{}, ku, std::false_type{});
+    else with_flag(relu_bf16, [&](auto kr) { go(std::false_type{}, ku, kr); });
   });
 }
 
@@ -1638,13 +1693,15 @@ int box_bwd_lds_waves(int H, int W, int max_items) {
   return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
 }
 
-hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx, float* partials, int N,
-                              int C, int H, int W, int B, bool rounded, int stride, hipStream_t s) {
+hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N,
+                              int C, int H, int W, int B, bool rounded, bool relu_bf16, int stride, hipStream_t s) {
+  if (rounded && relu_bf16) return hipErrorInvalidValue;
   const int seg = box_bwd_lds_seg(H, W, kBwdLdsItems);
-  if (seg == 8) bwd_lds_t<8, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+  if (seg == 8) bwd_lds_t<8, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, relu_bf16, stride, s);
   else if (seg == 4 && n_chunks(W) * n_segs(H, 4) <= 256)
-    bwd_lds_t<4, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
-  else if (seg == 4) bwd_lds_t<4, kBwdLdsItems>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, stride, s);
+    bwd_lds_t<4, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, relu_bf16, stride, s);
+  else if (seg == 4)
+    bwd_lds_t<4, kBwdLdsItems>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, relu_bf16, stride, s);
   else return hipErrorInvalidValue;
   return last_error();
 }
@@ -1653,14 +1710,17 @@ constexpr int kBwdGatherSeg = 8;
 
 int box_bwd_gather_blocks(int H, int W) { return (n_chunks(W) * n_segs(H, kBwdGatherSeg) + 255) / 256; }
 
-hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx, float* partials,
-                                 int N, int C, int H, int W, int B, bool rounded, hipStream_t s) {
+hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, void* gx, float* partials,
+                                 int N, int C, int H, int W, int B, bool rounded, bool relu_bf16, hipStream_t s) {
+  if (rounded && relu_bf16) return hipErrorInvalidValue;
   const int nblk = box_bwd_gather_blocks(H, W);
   const int total = N * C * nblk;
-  with_flag(rounded, [&](auto ki) {
-    hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg, decltype(ki)::value>), dim3(pad8(total)), dim3(256), 0, s, x,
-                       sat_g, taps, gx, partials, C, H, W, B, nblk, total);
-  });
+  auto go = [&](auto ki, auto kr) {
+    hipLaunchKernelGGL((k_box_bwd_gather<kBwdGatherSeg, decltype(ki)::value, decltype(kr)::value>), dim3(pad8(total)),
+                       dim3(256), 0, s, x, sat_g, taps, gx, partials, C, H, W, B, nblk, total);
+  };
+  if (rounded) go(std::true_type{}, std::false_type{});
+  else with_flag(relu_bf16, [&](auto kr) { go(std::false_type{}, kr); });
   return last_error();
 }
 

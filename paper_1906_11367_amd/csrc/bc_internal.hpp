@@ -45,9 +45,10 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
 // walk, which fits the 128 VGPRs such a block allows).
 // rounded: input gradient only (partials unused).  stride > 1: gy is
 // [N][C*B][ceil(H/stride)][ceil(W/stride)] (tabulated zero-upsampled).
-hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, float* gx,
-                              float* partials, int N, int C, int H, int W, int B, bool rounded, int stride,
-                              hipStream_t s);
+// relu_bf16: gx is bf16 [N][C][H][W], bf16(x > 0 ? dx : 0) (not with rounded).
+hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, void* gx,
+                              float* partials, int N, int C, int H, int W, int B, bool rounded, bool relu_bf16,
+                              int stride, hipStream_t s);
 constexpr int kBwdLdsItems = 1024;
 int box_bwd_lds_seg(int H, int W, int max_items);
 int box_bwd_lds_waves(int H, int W, int max_items);
@@ -55,8 +56,9 @@ int box_bwd_lds_waves(int H, int W, int max_items);
 // sat_build_up for stride > 1);
 // P = N * box_bwd_gather_blocks() * 4.
 int box_bwd_gather_blocks(int H, int W);
-hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, float* gx,
-                                 float* partials, int N, int C, int H, int W, int B, bool rounded, hipStream_t s);
+hipError_t launch_box_bwd_gather(const float* x, const float* sat_g, const int* taps, void* gx,
+                                 float* partials, int N, int C, int H, int W, int B, bool rounded, bool relu_bf16,
+                                 hipStream_t s);
 // Box-parameter reparameterisation over n = C*B boxes: op 0 = boxes from
 // unit corners (in -> out), 1 = unit gradient from box gradient (in -> out),
 // 2 = clip and order unit corners in place (out).

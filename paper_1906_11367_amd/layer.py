@@ -10,7 +10,10 @@ With a ReLU after a bf16 mix, dZ is first masked and rounded once
 same operand bits the masked GEMMs would form from the fp32 gradient, so the
 results are bitwise the same (six stacked pose layers: 4.47 -> 3.71 ms per
 step).  Without the ReLU a plain cast of dZ gains nothing on the step (the
-cast costs what the GEMMs save), so the GEMMs round dZ on load.
+cast costs what the GEMMs save), so the GEMMs round dZ on load.  In a stack
+the masked operand of layer l comes straight from the box backward of layer
+l + 1 (box_conv_bwd_relu_bf16: its input is layer l's rectified output, so
+x > 0 is the mask), with no fp32 gradient written or read back.
 With kernel splitting (`split` = "2x", "2y" or "4") the box filter is
 box_conv_split_fwd / box_conv_split_bwd: the boxes argument is then the pair
 (boxes, piece weights) and the backward returns the pair of their gradients.
@@ -51,6 +54,10 @@ class LayerPlan:
     # dL/du); None: the boxes are (cx, cy, rx, ry) in pixels
     unit_size: tuple | None = None
     split: str | None = None   # kernel splitting mode: None, "2x", "2y" or "4"
+    # dx written as bf16(x > 0 ? dx : 0) for the ReLU + bf16 mix below this layer
+    dx_relu_bf16: bool = False
+    # grad_out arrives as that masked bf16 operand (from the layer above)
+    grad_premasked: bool = False
 
     def __post_init__(self):
         dev = torch.device(self.device)
@@ -69,6 +76,10 @@ class LayerPlan:
             o_dt = torch.float32
         self.o = torch.empty((N, K, Ho, Wo), dtype=o_dt, device=dev)
         self.compute = bc.BC_BF16 if self.mix_dtype == "bf16" else bc.BC_F32
+        if self.dx_relu_bf16 and (integer or self.split is not None or self.flags & bc.BC_FLAG_INTEGER_CORNERS):
+            raise ValueError("a bf16 masked input gradient needs fp32 maps, whole boxes and real corners")
+        if self.grad_premasked and not (self.relu and self.M is not None and self.compute == bc.BC_BF16):
+            raise ValueError("a pre-masked incoming gradient needs a ReLU after a bf16 mix")
         if self.split is not None:
             if integer or self.stride != 1 or self.flags:
                 raise ValueError("kernel splitting takes fp32 maps, stride 1 and no box flags")
@@ -89,7 +100,8 @@ class LayerPlan:
                 self.dpiece = torch.empty((C, B, self.pieces), dtype=torch.float32, device=dev)
             else:
                 self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
-            self.dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
+            self.dx = torch.empty((N, C, H, W), dtype=torch.bfloat16 if self.dx_relu_bf16 else torch.float32,
+                                  device=dev)
             self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
             if self.unit_size is not None:
                 self.du = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
@@ -100,7 +112,7 @@ class LayerPlan:
                                                           self.compute), dev)
                 # the masked incoming gradient in bf16 (ReLU after a bf16 mix)
                 self.dz_bf16 = (torch.empty((N, self.M, Ho, Wo), dtype=torch.bfloat16, device=dev)
-                                if self.relu and self.compute == bc.BC_BF16 else None)
+                                if self.relu and self.compute == bc.BC_BF16 and not self.grad_premasked else None)
                 self.side = torch.cuda.Stream(device=dev)   # default priority
                 self.ev_in = torch.cuda.Event()
                 self.ev_dw = torch.cuda.Event()
@@ -152,7 +164,11 @@ class LayerPlan:
         else:
             aux = self.z if self.relu else None
             relu = int(self.relu)
-            if self.dz_bf16 is not None:
+            if self.grad_premasked:
+                if grad_out.dtype != torch.bfloat16:
+                    raise ValueError("grad_out must be the masked bf16 operand")
+                aux, relu = None, 0
+            elif self.dz_bf16 is not None:
                 grad_out = bc.relu_grad_bf16(grad_out, self.z, self.dz_bf16)
                 tap("relu_grad")
                 aux, relu = None, 0
@@ -179,6 +195,9 @@ class LayerPlan:
         if piece_w is not None:
             bc.box_conv_split_bwd(x, boxes, piece_w, self.split, do, self.dx, grad_boxes, self.dpiece, self.ws_bwd)
             tap("box_conv_split_bwd")
+        elif self.dx_relu_bf16:
+            bc.box_conv_bwd_relu_bf16(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
+            tap("box_conv_bwd_relu_bf16")
         else:
             bc.box_conv_bwd(x, boxes, do, self.dx, grad_boxes, self.flags, self.ws_bwd, stride=self.stride)
             tap("box_conv_bwd")
@@ -214,8 +233,14 @@ class Stack:
                  backward=True, device="cuda", stride=1, unit_size=None, split=None):
         if layers > 1 and (M != C or stride != 1):
             raise ValueError("stacked layers need M == C and stride 1")
+        # a ReLU after a bf16 mix below: the layer above writes its input
+        # gradient as that mix's masked bf16 operand
+        chain = (layers > 1 and backward and relu and mix_dtype == "bf16" and M is not None and split is None
+                 and x_dtype == torch.float32 and not flags & bc.BC_FLAG_INTEGER_CORNERS)
         self.plans = [LayerPlan(N, C, H, W, B, M, x_dtype, mix_dtype, relu, flags, backward, device,
-                                stride=stride, unit_size=unit_size, split=split) for _ in range(layers)]
+                                stride=stride, unit_size=unit_size, split=split,
+                                dx_relu_bf16=chain and l > 0, grad_premasked=chain and l < layers - 1)
+                      for l in range(layers)]
 
     def forward(self, x, params, tap=None):
         """params: list of (boxes, w) device tensors.  Returns the inputs of every

@@ -128,6 +128,22 @@ def test_unit_params_argument_errors():
     assert lib.box_params_clip(FAKE_MISALIGNED, 2, 4, None) == 4
 
 
+def test_bwd_relu_bf16_argument_errors():
+    lib = bc.load_library()
+    ok = [FAKE, FAKE, FAKE, 2, 3, 8, 8, 4, 1, FAKE, FAKE, 0, None, 0, None]
+    assert lib.box_conv_bwd_relu_bf16(*ok) == 5                        # valid: workspace missing
+    a = list(ok); a[0] = None
+    assert lib.box_conv_bwd_relu_bf16(*a) == 1
+    a = list(ok); a[8] = 0
+    assert lib.box_conv_bwd_relu_bf16(*a) == 2                         # stride
+    a = list(ok); a[10] = None; a[11] = bc.BC_FLAG_INTEGER_CORNERS     # the mask needs x: not with rounded corners
+    assert lib.box_conv_bwd_relu_bf16(*a) == 7
+    a = list(ok); a[9] = FAKE_MISALIGNED
+    assert lib.box_conv_bwd_relu_bf16(*a) == 4
+    a = list(ok); a[9] = None; a[10] = None                            # nothing requested: no-op
+    assert lib.box_conv_bwd_relu_bf16(*a) == 0
+
+
 def test_relu_grad_argument_errors():
     lib = bc.load_library()
     assert lib.bc_relu_grad_bf16(None, FAKE, FAKE, 8, None) == 1

@@ -945,6 +945,34 @@ def test_relu_grad_prepass_matches_masked_gemms(dims):
           RTOL_BF16_MIX, "dO")
 
 
+@pytest.mark.parametrize("H,W,stride,flags", [(64, 48, 1, 0), (37, 29, 1, 0), (96, 97, 1, 0), (64, 48, 1, 2),
+                                                (64, 48, 2, 0), (150, 151, 1, 0)])
+def test_bwd_relu_bf16_matches_relu_grad(H, W, stride, flags):
+    """box_conv_bwd_relu_bf16 writes bf16(x > 0 ? dx : 0) bit for bit as
+    bc_relu_grad_bf16 forms it from box_conv_bwd's fp32 dx and x, and the same
+    box gradient, on every backward path (LDS, wide LDS block, HBM tables,
+    strided).  x is a rectified map (zeros where the ReLU cut)."""
+    rng = np.random.default_rng(135)
+    N, C, B = 2, 3, 4
+    x = np.maximum(rng.standard_normal((N, C, H, W)), 0).astype(np.float32)
+    Ho, Wo = O.strided_size(H, stride), O.strided_size(W, stride)
+    g = rng.standard_normal((N, C * B, Ho, Wo)).astype(np.float32)
+    bx = real_boxes(rng, C, B, 20.0, 0.5, 24.0)
+    say(f"bwd relu bf16 {H}x{W} stride={stride} flags={flags}")
+    xd, bd, gd = dev(x), dev(bx), dev(g)
+    gx = torch.empty((N, C, H, W), dtype=torch.float32, device="cuda")
+    gb = torch.empty((C, B, 4), dtype=torch.float32, device="cuda")
+    bc.box_conv_bwd(xd, bd, gd, gx, gb, flags, stride=stride)
+    want = torch.empty((N, C, H, W), dtype=torch.bfloat16, device="cuda")
+    bc.relu_grad_bf16(gx, xd, want)
+    got = torch.empty_like(want)
+    gb2 = torch.empty_like(gb)
+    bc.box_conv_bwd_relu_bf16(xd, bd, gd, got, gb2, flags, stride=stride)
+    torch.cuda.synchronize()
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+    assert torch.equal(gb2, gb)
+
+
 def test_mix_integer_exact():
     wl = wlmod.WORKLOADS[1]
     d = wlmod.make_inputs(wl)
