@@ -176,7 +176,11 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
  *              fixed-order (deterministic) reduction.
  * ws         : >= bc_box_workspace_bytes(1, ...) bytes: the tap records,
  *              the per-wave partial edge gradients, and with the HBM path
- *              the tables of all N*C*B gradient maps.
+ *              the tables of all N*C*B gradient maps.  The HBM path is taken
+ *              with BC_FLAG_FORCE_HBM, or when a map's table exceeds 80 KiB
+ *              ((H + 1) * ((W + 7) | 1) * 4 bytes) or the map has more than
+ *              1024 work items of 3 columns x 4 rows (one block per map in
+ *              LDS otherwise); it needs W <= 1024 (BC_ERR_SHAPE otherwise).
  * ---------------------------------------------------------------------- */
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
                        int N, int C, int H, int W, int B,
@@ -270,8 +274,9 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
  *        Sums over n are fixed-order (deterministic).
  * Paths : as box_conv_fwd / box_conv_bwd: the map's table in LDS when
  *        (H + 1) * ((W + 7) | 1) * 4 <= 80 KiB (and, for the backward, the
- *        map has at most 256 work items), else tables in HBM built into the
- *        workspace, which needs W <= 1024 (BC_ERR_SHAPE otherwise).
+ *        map has at most 1024 work items of 3 columns x 4 rows: one block
+ *        per map), else tables in HBM built into the workspace, which needs
+ *        W <= 1024 (BC_ERR_SHAPE otherwise).
  *        C * B <= 2^24.
  * ws     : >= bc_split_workspace_bytes(op, ...) (op 0 = forward: one record
  *        of 128 bytes per box, its shared corners with the piece weights
