@@ -57,6 +57,17 @@ static int check(void) {
   EXPECT(sat_build(fake, BC_F32, fake, NULL, 1, 1, 8, 2000, NULL) == BC_ERR_SHAPE);
   EXPECT(box_conv_split_fwd(fake, fake, fake, 1, 1, 8, 8, 1, 9, fake, BC_F32, NULL, 0, NULL) ==
          BC_ERR_UNSUPPORTED);
+  EXPECT(box_conv_split_fwd(fake, fake, fake, 1, 1, 8, 8, 1, BC_SPLIT_4 | BC_SPLIT_FORCE_HBM, fake, BC_F32, NULL, 0,
+                            NULL) == BC_ERR_WORKSPACE);
+  /* the masked bf16 input gradient: nothing requested is a no-op; rounded
+     corners are refused (the mask needs x) */
+  EXPECT(box_conv_bwd_relu_bf16(fake, fake, fake, 1, 1, 8, 8, 1, 1, NULL, NULL, 0, NULL, 0, NULL) == BC_OK);
+  EXPECT(box_conv_bwd_relu_bf16(fake, fake, fake, 1, 1, 8, 8, 1, 1, fake, NULL, BC_FLAG_INTEGER_CORNERS, NULL, 0,
+                                NULL) == BC_ERR_UNSUPPORTED);
+  EXPECT(box_conv_bwd_relu_bf16(fake, fake, fake, 1, 1, 8, 8, 1, 1, fake, NULL, 0, NULL, 0, NULL) ==
+         BC_ERR_WORKSPACE);
+  EXPECT(bc_relu_grad_bf16(fake, fake, fake, 0, NULL) == BC_ERR_SHAPE);
+  EXPECT(bc_relu_grad_bf16(fake, fake_mis, fake, 8, NULL) == BC_ERR_ALIGN);
   EXPECT(box_params_clip(NULL, 1, 1, NULL) == BC_ERR_NULL);
   EXPECT(pointwise_mix((bc_mix_mode)9, fake, BC_F32, fake, BC_F32, fake, BC_F32, 1, 8, 8, 8, BC_F32, 0, NULL, 0,
                        NULL, 0, NULL) == BC_ERR_UNSUPPORTED);
