@@ -573,13 +573,20 @@ constexpr int kSatRowsPerWave = 4;  // rows of a strip each wave loads before sc
 // kUp: x is [maps][Ho][Wo] and the table is that of its zero-upsampled H x W
 // map (x[i][j] at (s*i, s*j)); mean must then be null.
 // KM: elements per lane in a row scan, K = ceil(W / 64) <= KM (4 for
-// W <= 256, else 16).
-template <typename T, bool kUp, int KM>
-__global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* __restrict__ sat,
-                                                   float* __restrict__ mean, int H, int W, int s, int Ho, int Wo) {
+// W <= 256, else 16).  kGroups > 1 (W <= 256, few maps): blocks of
+// 256 * kGroups threads take strips of kStrip * kGroups rows, and the column
+// pass runs kGroups row groups of kStrip rows in parallel, each starting from
+// the carried sums plus the totals of the groups above it.
+template <typename T, bool kUp, int KM, int kGroups>
+__global__ __launch_bounds__(256 * kGroups) void k_sat_build(const T* __restrict__ x, T* __restrict__ sat,
+                                                             float* __restrict__ mean, int H, int W, int s, int Ho,
+                                                             int Wo) {
+  static_assert(kGroups == 1 || KM == 4, "row groups need W <= 256");
+  constexpr int kRowsStrip = kStrip * kGroups;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);
   __shared__ float red[16];
+  __shared__ T part[kGroups > 1 ? kGroups * 256 : 1];
   const int map = blockIdx.x;
   const T* src = x + (size_t)map * (kUp ? (size_t)Ho * Wo : (size_t)H * W);
   T* dst = sat + (size_t)map * (H + 1) * (W + 1);
@@ -595,8 +602,8 @@ __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* _
   T carry[KM / 4];
 #pragma unroll
   for (int j = 0; j < KM / 4; ++j) carry[j] = (T)0;
-  for (int r0 = 0; r0 < H; r0 += kStrip) {
-    const int rows = min(kStrip, H - r0);
+  for (int r0 = 0; r0 < H; r0 += kRowsStrip) {
+    const int rows = min(kRowsStrip, H - r0);
     // rows rr = wave + i * nw of the strip: all of a wave's loads are issued
     // before its first scan
     for (int rb = wave; rb < rows; rb += kSatRowsPerWave * nw) {
@@ -640,16 +647,41 @@ __global__ __launch_bounds__(256) void k_sat_build(const T* __restrict__ x, T* _
       }
     }
     __syncthreads();
+    if constexpr (kGroups == 1) {
 #pragma unroll
-    for (int j = 0; j < KM / 4; ++j) {
-      const int v = tid + j * 256;
+      for (int j = 0; j < KM / 4; ++j) {
+        const int v = tid + j * 256;
+        if (v < W) {
+          T cs = carry[j];
+          for (int rr = 0; rr < rows; ++rr) {
+            cs += tile[rr * W + v];
+            dst[(size_t)(r0 + rr + 1) * (W + 1) + v + 1] = cs;
+          }
+          carry[j] = cs;
+        }
+      }
+    } else {
+      // column v, row group g: rows [g * kStrip, (g + 1) * kStrip) of the strip
+      const int v = tid & 255, g = tid >> 8;
+      const int ra = g * kStrip, rz = min(ra + kStrip, rows);
+      T ps = (T)0;
+      if (v < W)
+        for (int rr = ra; rr < rz; ++rr) ps += tile[rr * W + v];
+      part[g * 256 + v] = ps;
+      __syncthreads();
       if (v < W) {
-        T cs = carry[j];
-        for (int rr = 0; rr < rows; ++rr) {
+        T cs = carry[0], tot = (T)0;
+#pragma unroll
+        for (int h = 0; h < kGroups; ++h) {
+          const T p = part[h * 256 + v];
+          if (h < g) cs += p;
+          tot += p;
+        }
+        for (int rr = ra; rr < rz; ++rr) {
           cs += tile[rr * W + v];
           dst[(size_t)(r0 + rr + 1) * (W + 1) + v + 1] = cs;
         }
-        carry[j] = cs;
+        carry[0] += tot;
       }
     }
     if (tid < rows) dst[(size_t)(r0 + tid + 1) * (W + 1)] = (T)0;
@@ -1524,21 +1556,26 @@ static void with_flag(bool v, F&& f) {
   else f(std::integral_constant<bool, false>{});
 }
 
-template <int KM>
+template <int KM, int kGroups>
 static void sat_build_t(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W, hipStream_t s) {
-  const size_t shm = (size_t)kStrip * W * 4;
+  const size_t shm = (size_t)kStrip * kGroups * W * 4;
   if (is_int)
-    hipLaunchKernelGGL((k_sat_build<int, false, KM>), dim3(maps), dim3(256), shm, s, (const int*)x, (int*)sat,
-                       (float*)nullptr, H, W, 1, H, W);
+    hipLaunchKernelGGL((k_sat_build<int, false, KM, kGroups>), dim3(maps), dim3(256 * kGroups), shm, s,
+                       (const int*)x, (int*)sat, (float*)nullptr, H, W, 1, H, W);
   else
-    hipLaunchKernelGGL((k_sat_build<float, false, KM>), dim3(maps), dim3(256), shm, s, (const float*)x, (float*)sat,
-                       mean, H, W, 1, H, W);
+    hipLaunchKernelGGL((k_sat_build<float, false, KM, kGroups>), dim3(maps), dim3(256 * kGroups), shm, s,
+                       (const float*)x, (float*)sat, mean, H, W, 1, H, W);
 }
+
+// Fewer maps than 8 per CU leave one block per map short of filling the chip:
+// then maps up to 256 wide take blocks of 1024 threads over 64-row strips.
+constexpr int kSatFewMaps = 2048;
 
 hipError_t launch_sat_build(const void* x, bool is_int, void* sat, float* mean, int maps, int H, int W,
                             hipStream_t s) {
-  if (W <= 256) sat_build_t<4>(x, is_int, sat, mean, maps, H, W, s);
-  else sat_build_t<kSatMaxK>(x, is_int, sat, mean, maps, H, W, s);
+  if (W <= 256 && maps < kSatFewMaps) sat_build_t<4, 4>(x, is_int, sat, mean, maps, H, W, s);
+  else if (W <= 256) sat_build_t<4, 1>(x, is_int, sat, mean, maps, H, W, s);
+  else sat_build_t<kSatMaxK, 1>(x, is_int, sat, mean, maps, H, W, s);
   return last_error();
 }
 
@@ -1546,11 +1583,11 @@ hipError_t launch_sat_build_up(const float* x, float* sat, int maps, int H, int 
   const size_t shm = (size_t)kStrip * W * 4;
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   if (W <= 256)
-    hipLaunchKernelGGL((k_sat_build<float, true, 4>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H, W,
-                       stride, Ho, Wo);
-  else
-    hipLaunchKernelGGL((k_sat_build<float, true, kSatMaxK>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H,
+    hipLaunchKernelGGL((k_sat_build<float, true, 4, 1>), dim3(maps), dim3(256), shm, s, x, sat, (float*)nullptr, H,
                        W, stride, Ho, Wo);
+  else
+    hipLaunchKernelGGL((k_sat_build<float, true, kSatMaxK, 1>), dim3(maps), dim3(256), shm, s, x, sat,
+                       (float*)nullptr, H, W, stride, Ho, Wo);
   return last_error();
 }
 
