@@ -190,8 +190,31 @@ def cpu_baseline(wl, d, budget_s, inference=False, stride=1, split=None, piece_w
     if split is not None:
         what += f", boxes split {split}"
     return {"value": pb / t1 / 1e9, "unit": "Gpix·box/s", "cores": threads, "kind": "oracle",
+            "affinity_cores": len(os.sched_getaffinity(0)),
             "sample": f"{n} of {wl.N} images, all {wl.C} channels x {wl.B} boxes, one layer, "
                       f"{what}, fp64 NumPy, {t1:.1f} s"}
+
+
+def naive_eq1_baseline():
+    """Times the oracle's naive per-pixel loop of Eq. 1 (pure Python, one
+    core) on the whole tiny integer workload (one image, 8 channels x 4 boxes,
+    32x32 int32 maps, integer corners; about a second).  The loop's result is
+    checked against the oracle's forward before it is reported."""
+    import numpy as np
+    import oracle as O
+    from paper_1906_11367_amd import workloads as wlmod
+    wl = wlmod.WORKLOADS[1]
+    d = wlmod.make_inputs(wl)
+    x, bx = d["x"], d["boxes"]
+    t0 = time.perf_counter()
+    o = O.naive_box_forward_eq1(x, bx)
+    t1 = time.perf_counter() - t0
+    if not np.array_equal(o, O.box_forward(x, bx)):
+        raise RuntimeError("naive Eq. 1 loop disagrees with the oracle's forward")
+    pb = o.size
+    return {"value": pb / t1 / 1e9, "unit": "Gpix·box/s", "cores": 1, "kind": "oracle naive Eq. 1 loop",
+            "sample": f"{wl.key}: the whole workload, {wl.N} image, {wl.C} channels x {wl.B} boxes, "
+                      f"{wl.H}x{wl.W}, forward only, int64 pure Python, {t1:.1f} s"}
 
 
 def main():
@@ -200,6 +223,11 @@ def main():
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the layer's multi-GPU sharding is a design note only)", file=sys.stderr)
         return 2
+    # the CPU oracle's BLAS uses every core this process may run on, unless
+    # the environment already fixes the thread count
+    ncpu = str(len(os.sched_getaffinity(0)))
+    for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS"):
+        os.environ.setdefault(var, ncpu)
     import numpy as np
     import torch
 
@@ -290,9 +318,14 @@ def main():
     torch.cuda.synchronize()
     spin_cycles = int(probe * 100.0 / max(s0.elapsed_time(s1), 1e-3))
 
-    # timed region: plain steps
+    # timed region: plain steps.  A few untimed steps follow the spin before
+    # the first event: kernels run up to ~20 % longer for a few steps after
+    # it, and that transient stays outside the timing.
+    settle = 10
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     spin(spin_cycles)
+    for _ in range(settle):
+        step()
     e0.record(stream)
     for _ in range(args.steps):
         step()
@@ -304,8 +337,10 @@ def main():
     # beforehand, so the pass itself only records them)
     # at most 8 calls per layer and step, plus the step's start and clip
     timing["pool"] = [torch.cuda.Event(enable_timing=True) for _ in range((8 * wl.layers + 2) * args.steps)]
-    timing["on"] = True
     spin(spin_cycles)
+    for _ in range(settle):
+        step()
+    timing["on"] = True
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
@@ -378,6 +413,7 @@ def main():
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl, d, args.cpu_budget_s, args.inference, args.stride,
                                             args.split, piece_w)
+        line["cpu_baseline_naive_eq1"] = naive_eq1_baseline()
     print(json.dumps(line), flush=True)
     return 0
 

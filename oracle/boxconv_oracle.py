@@ -71,7 +71,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
-    "box_edges", "rounded_edges", "mirrored_boxes", "box_taps", "adjoint_taps", "overlap_matrix", "sat_exclusive",
+    "box_edges", "rounded_edges", "mirrored_boxes", "overlap_matrix", "sat_exclusive",
     "map_mean", "box_forward", "box_backward_input", "box_backward_params",
     "box_param_grad_from_edges", "bf16_round", "mix_forward",
     "mix_backward_data", "mix_backward_weight", "relu", "layer_forward",
@@ -115,55 +115,6 @@ def mirrored_boxes(boxes):
     m[..., 0] = -m[..., 0]
     m[..., 1] = -m[..., 1]
     return m
-
-
-def box_taps(boxes, mirror=False):
-    """The per-box precomputation of Section 3.1 (after Eq. 4): integer shifts
-    leave the corner fractions unchanged, so each box reduces to the floors of
-    its four edges and the bilinear weights of the two table columns (rows)
-    around each edge.
-
-    Returns (floors int64 [..., 4] = floor(a), floor(b), floor(c), floor(d);
-    wx fp32 [..., 4] for columns floor(a), floor(a)+1, floor(b), floor(b)+1;
-    wy fp32 [..., 4] likewise for rows).  Each weight is formed in fp64 from
-    the exact fraction and rounded once to fp32 (reading R5): the leading
-    edge of each axis enters with a minus sign (Eq. 2).
-    """
-    bx = mirrored_boxes(boxes) if mirror else np.asarray(boxes, dtype=np.float32)
-    a, b, c, d = box_edges(bx)
-    e = np.stack([a, b, c, d], axis=-1)
-    fl = np.floor(e)
-    fr = e - fl
-    w = np.stack([fr - 1.0, -fr, 1.0 - fr, fr], axis=-1)  # [..., edge, 4] candidates
-    wx = np.concatenate([w[..., 0, :2], w[..., 1, 2:]], axis=-1).astype(np.float32)
-    wy = np.concatenate([w[..., 2, :2], w[..., 3, 2:]], axis=-1).astype(np.float32)
-    return fl.astype(np.int64), wx, wy
-
-
-def adjoint_taps(boxes):
-    """Taps of the mirrored (adjoint) box in the form the backward pass uses
-    them: each edge e of the mirrored box is split as e = f + alpha with alpha
-    in (0, 1], i.e. f = ceil(e) - 1, instead of the floor.
-
-    Bilinear interpolation of the table is continuous, so the lookups equal
-    those of box_taps(mirror=True) (identical floors and weights wherever the
-    edge is not an integer).  At an integer edge the two taps straddle the
-    table column (row) just below the edge: in the adjoint, that is where the
-    right derivative of the original box's edge (reading R5) is read, since
-    moving an original edge up moves the mirrored edge down (a' = 1 - b,
-    b' = 1 - a, c' = 1 - d, d' = 1 - c).
-
-    Returns (floors int64 [..., 4], wx fp32 [..., 4], wy fp32 [..., 4]) laid
-    out as in box_taps.
-    """
-    a, b, c, d = box_edges(mirrored_boxes(boxes))
-    e = np.stack([a, b, c, d], axis=-1)
-    fl = np.ceil(e) - 1.0
-    fr = e - fl
-    w = np.stack([fr - 1.0, -fr, 1.0 - fr, fr], axis=-1)
-    wx = np.concatenate([w[..., 0, :2], w[..., 1, 2:]], axis=-1).astype(np.float32)
-    wy = np.concatenate([w[..., 2, :2], w[..., 3, 2:]], axis=-1).astype(np.float32)
-    return fl.astype(np.int64), wx, wy
 
 
 def overlap_matrix(n, lo, hi):

@@ -95,6 +95,46 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _need(t, shape, dtypes, what, name):
+    """Shape and dtype checks the C ABI cannot make (it sees only pointers):
+    a tensor of the wrong size or type would be read or written out of bounds
+    on the device.  shape entries of None match any extent."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise BoxConvError(f"{what}: {name} must be a tensor")
+    if isinstance(dtypes, torch.dtype):
+        dtypes = (dtypes,)
+    if t.dtype not in dtypes:
+        raise BoxConvError(f"{what}: {name} has dtype {t.dtype}, expected one of {tuple(dtypes)}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(e is not None and int(a) != int(e) for a, e in zip(t.shape, shape)):
+            raise BoxConvError(f"{what}: {name} has shape {tuple(t.shape)}, expected "
+                               f"{tuple('*' if e is None else e for e in shape)}")
+
+
+def _need_numel(t, n, dtypes, what, name):
+    if isinstance(dtypes, torch.dtype):
+        dtypes = (dtypes,)
+    if t.dtype not in dtypes:
+        raise BoxConvError(f"{what}: {name} has dtype {t.dtype}, expected one of {tuple(dtypes)}")
+    if t.numel() != n:
+        raise BoxConvError(f"{what}: {name} has {t.numel()} elements, expected {n}")
+
+
+_MAPS = (torch.int32, torch.float32)
+_F32 = torch.float32
+
+
+def _maps_and_boxes(x, boxes, what):
+    if not isinstance(x, torch.Tensor) or x.dim() != 4:
+        raise BoxConvError(f"{what}: x must be a 4-D [N, C, H, W] tensor")
+    _need(x, None, _MAPS, what, "x")
+    N, C, H, W = (int(v) for v in x.shape)
+    _need(boxes, (C, None, 4), _F32, what, "boxes")
+    return N, C, H, W, int(boxes.shape[1])
+
+
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -125,14 +165,21 @@ def mix_workspace_bytes(mode: int, N, M, K, P, compute_dt) -> int:
 
 def box_prep(boxes: torch.Tensor, table: torch.Tensor, flags: int = 0):
     """table: int32 tensor of 2*C*B*16 words (see boxconv.h)."""
+    _need(boxes, (None, None, 4), _F32, "box_prep", "boxes")
     C, B = boxes.shape[0], boxes.shape[1]
+    _need_numel(table, 2 * C * B * 16, torch.int32, "box_prep", "table")
     _check(load_library().box_prep(_ptr(boxes), C, B, flags, _ptr(table), _stream()), "box_prep")
     return table
 
 
 def sat_build(x: torch.Tensor, sat: torch.Tensor, mean: torch.Tensor | None = None):
     """x [N, C, H, W] int32/fp32 -> sat [N, C, H+1, W+1] (exclusive table)."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 4:
+        raise BoxConvError("sat_build: x must be a 4-D [N, C, H, W] tensor")
+    _need(x, None, _MAPS, "sat_build", "x")
     N, C, H, W = x.shape
+    _need(sat, (N, C, H + 1, W + 1), x.dtype, "sat_build", "sat")
+    _need(mean, (N, C), _F32, "sat_build", "mean")
     _check(load_library().sat_build(_ptr(x), dtype_code(x), _ptr(sat), _ptr(mean), N, C, H, W, _stream()),
            "sat_build")
     return sat
@@ -146,10 +193,9 @@ def box_conv_fwd(x: torch.Tensor, boxes: torch.Tensor, y: torch.Tensor, flags: i
                  ws: torch.Tensor | None = None, stride: int = 1):
     """x [N, C, H, W], boxes [C, B, 4] fp32 -> y [N, C*B, ceil(H/stride), ceil(W/stride)]
     (int32, fp32 or bf16); stride > 1 calls box_conv_fwd_strided."""
-    N, C, H, W = x.shape
-    B = boxes.shape[1]
-    if tuple(y.shape) != _strided_shape(N, C, H, W, B, stride):
-        raise BoxConvError(f"box_conv_fwd: y has shape {tuple(y.shape)}")
+    N, C, H, W, B = _maps_and_boxes(x, boxes, "box_conv_fwd")
+    _need(y, _strided_shape(N, C, H, W, B, stride),
+          torch.int32 if x.dtype == torch.int32 else (torch.float32, torch.bfloat16), "box_conv_fwd", "y")
     if ws is None:
         ws = _workspace(box_workspace_bytes(0, N, C, H, W, B, flags), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
@@ -171,10 +217,11 @@ def box_conv_fwd_strided(x, boxes, stride: int, y, flags: int = 0, ws=None):
 def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, grad_x: torch.Tensor | None,
                  grad_boxes: torch.Tensor | None, flags: int = 0, ws: torch.Tensor | None = None, stride: int = 1):
     """grad_y [N, C*B, ceil(H/stride), ceil(W/stride)]; stride > 1 calls box_conv_bwd_strided."""
-    N, C, H, W = x.shape
-    B = boxes.shape[1]
-    if tuple(grad_y.shape) != _strided_shape(N, C, H, W, B, stride):
-        raise BoxConvError(f"box_conv_bwd: grad_y has shape {tuple(grad_y.shape)}")
+    N, C, H, W, B = _maps_and_boxes(x, boxes, "box_conv_bwd")
+    _need(x, None, _F32, "box_conv_bwd", "x")
+    _need(grad_y, _strided_shape(N, C, H, W, B, stride), _F32, "box_conv_bwd", "grad_y")
+    _need(grad_x, (N, C, H, W), _F32, "box_conv_bwd", "grad_x")
+    _need(grad_boxes, (C, B, 4), _F32, "box_conv_bwd", "grad_boxes")
     if ws is None:
         ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
@@ -194,12 +241,12 @@ def box_conv_bwd_relu_bf16(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.T
                            ws: torch.Tensor | None = None, stride: int = 1):
     """As box_conv_bwd, with the input gradient written as bf16(x > 0 ? dL/dx : 0)
     (x: the rectified output of a bf16 mix before this layer)."""
-    N, C, H, W = x.shape
-    B = boxes.shape[1]
-    if tuple(grad_y.shape) != _strided_shape(N, C, H, W, B, stride):
-        raise BoxConvError(f"box_conv_bwd_relu_bf16: grad_y has shape {tuple(grad_y.shape)}")
-    if grad_x_bf16 is not None and (grad_x_bf16.dtype != torch.bfloat16 or tuple(grad_x_bf16.shape) != (N, C, H, W)):
-        raise BoxConvError("box_conv_bwd_relu_bf16: grad_x must be bf16 [N, C, H, W]")
+    what = "box_conv_bwd_relu_bf16"
+    N, C, H, W, B = _maps_and_boxes(x, boxes, what)
+    _need(x, None, _F32, what, "x")
+    _need(grad_y, _strided_shape(N, C, H, W, B, stride), _F32, what, "grad_y")
+    _need(grad_x_bf16, (N, C, H, W), torch.bfloat16, what, "grad_x")
+    _need(grad_boxes, (C, B, 4), _F32, what, "grad_boxes")
     if ws is None:
         ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
@@ -215,20 +262,25 @@ def box_conv_bwd_strided(x, boxes, grad_y, stride: int, grad_x, grad_boxes, flag
 
 def box_params_from_unit(u: torch.Tensor, max_w: float, max_h: float, boxes: torch.Tensor):
     """u [C, B, 4] unit corners -> boxes [C, B, 4] (cx, cy, rx, ry) in pixels."""
+    _need(u, (None, None, 4), _F32, "box_params_from_unit", "u")
     C, B = u.shape[0], u.shape[1]
+    _need(boxes, (C, B, 4), _F32, "box_params_from_unit", "boxes")
     _check(load_library().box_params_from_unit(_ptr(u), C, B, max_w, max_h, _ptr(boxes), _stream()),
            "box_params_from_unit")
     return boxes
 
 
 def box_params_unit_grad(grad_boxes: torch.Tensor, max_w: float, max_h: float, grad_u: torch.Tensor):
+    _need(grad_boxes, (None, None, 4), _F32, "box_params_unit_grad", "grad_boxes")
     C, B = grad_boxes.shape[0], grad_boxes.shape[1]
+    _need(grad_u, (C, B, 4), _F32, "box_params_unit_grad", "grad_u")
     _check(load_library().box_params_unit_grad(_ptr(grad_boxes), C, B, max_w, max_h, _ptr(grad_u), _stream()),
            "box_params_unit_grad")
     return grad_u
 
 
 def box_params_clip(u: torch.Tensor):
+    _need(u, (None, None, 4), _F32, "box_params_clip", "u")
     C, B = u.shape[0], u.shape[1]
     _check(load_library().box_params_clip(_ptr(u), C, B, _stream()), "box_params_clip")
     return u
@@ -257,10 +309,11 @@ def box_conv_split_fwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tens
     kernels even where the map's table fits in LDS."""
     m = _split_mode(mode)
     code = m | (BC_SPLIT_FORCE_HBM if force_hbm else 0)
-    N, C, H, W = x.shape
-    B = boxes.shape[1]
-    if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(y.shape) != (N, C * B, H, W):
-        raise BoxConvError("box_conv_split_fwd: piece_w or y has the wrong shape")
+    what = "box_conv_split_fwd"
+    N, C, H, W, B = _maps_and_boxes(x, boxes, what)
+    _need(x, None, _F32, what, "x")
+    _need(piece_w, (C, B, SPLIT_PIECES[m]), _F32, what, "piece_w")
+    _need(y, (N, C * B, H, W), (torch.float32, torch.bfloat16), what, "y")
     if ws is None:
         ws = _workspace(split_workspace_bytes(0, N, C, H, W, B, m, force_hbm), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
@@ -274,10 +327,14 @@ def box_conv_split_bwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tens
                        grad_w: torch.Tensor | None, ws: torch.Tensor | None = None, force_hbm: bool = False):
     m = _split_mode(mode)
     code = m | (BC_SPLIT_FORCE_HBM if force_hbm else 0)
-    N, C, H, W = x.shape
-    B = boxes.shape[1]
-    if tuple(piece_w.shape) != (C, B, SPLIT_PIECES[m]) or tuple(grad_y.shape) != (N, C * B, H, W):
-        raise BoxConvError("box_conv_split_bwd: piece_w or grad_y has the wrong shape")
+    what = "box_conv_split_bwd"
+    N, C, H, W, B = _maps_and_boxes(x, boxes, what)
+    _need(x, None, _F32, what, "x")
+    _need(piece_w, (C, B, SPLIT_PIECES[m]), _F32, what, "piece_w")
+    _need(grad_y, (N, C * B, H, W), _F32, what, "grad_y")
+    _need(grad_x, (N, C, H, W), _F32, what, "grad_x")
+    _need(grad_boxes, (C, B, 4), _F32, what, "grad_boxes")
+    _need(grad_w, (C, B, SPLIT_PIECES[m]), _F32, what, "grad_w")
     if ws is None:
         ws = _workspace(split_workspace_bytes(1, N, C, H, W, B, m, force_hbm), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
@@ -289,8 +346,8 @@ def box_conv_split_bwd(x: torch.Tensor, boxes: torch.Tensor, piece_w: torch.Tens
 
 def bc_cast_bf16(src: torch.Tensor, dst: torch.Tensor):
     """dst (bf16, same numel) = src (fp32) rounded to nearest even."""
-    if src.numel() != dst.numel():
-        raise BoxConvError("bc_cast_bf16: size mismatch")
+    _need_numel(src, src.numel(), _F32, "bc_cast_bf16", "src")
+    _need_numel(dst, src.numel(), torch.bfloat16, "bc_cast_bf16", "dst")
     _check(load_library().bc_cast_bf16(_ptr(src), _ptr(dst), src.numel(), _stream()), "bc_cast_bf16")
     return dst
 
@@ -309,6 +366,21 @@ def relu_grad_bf16(grad: torch.Tensor, out: torch.Tensor, dst: torch.Tensor):
 def pointwise_mix(mode: int, a: torch.Tensor, b: torch.Tensor, out: torch.Tensor, N: int, M: int, K: int,
                   P: int, compute_dt: int, relu: int = 0, aux: torch.Tensor | None = None,
                   accumulate: int = 0, ws: torch.Tensor | None = None):
+    """The 1x1 mix (include/boxconv.h): FWD out[N,M,P] = a[M,K] * b[N,K,P];
+    BWD_DATA out[N,K,P] = a[M,K]^T * b[N,M,P]; BWD_WEIGHT out[M,K] (+)=
+    sum_n a[N,M,P] * b[N,K,P]^T.  aux: the FWD output Z [N,M,P] (ReLU mask)."""
+    what = "pointwise_mix"
+    sizes = {BC_MIX_FWD: (M * K, N * K * P, N * M * P), BC_MIX_BWD_DATA: (M * K, N * M * P, N * K * P),
+             BC_MIX_BWD_WEIGHT: (N * M * P, N * K * P, M * K)}
+    if mode not in sizes:
+        raise BoxConvError(f"{what}: unknown mode {mode}")
+    na, nb, no = sizes[mode]
+    operand = (torch.int32, torch.float32, torch.bfloat16)
+    _need_numel(a, na, operand, what, "a")
+    _need_numel(b, nb, operand, what, "b")
+    _need_numel(out, no, (torch.int32, torch.float32), what, "out")
+    if aux is not None:
+        _need_numel(aux, N * M * P, _F32, what, "aux")
     if ws is None:
         ws = _workspace(mix_workspace_bytes(mode, N, M, K, P, compute_dt), a.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()

@@ -58,32 +58,46 @@ def layer_forward(x, boxes, w, relu):
     return {"x": x, "o": o, "D": D, "zpre": zpre, "ez": ez, "z": z}
 
 
-def layer_backward(fw, boxes, w, g, relu=False):
-    """Backward of that layer for an exact upstream gradient g (fp32 values,
-    so their bf16 codes are the same on both sides).  Ambiguous decisions:
-    the bf16 codes of O (they enter dW only: sum_p |bf16(g)| * D) and, with
-    ReLU, the mask where |zpre| is within its bound ez of zero (there the
-    masked gradient may be g or 0; the difference |g| is propagated through
-    the transposed mix and box operators with absolute values)."""
+def layer_backward(fw, boxes, w, g, relu=False, eg_in=None, mask_exact=False):
+    """Backward of that layer for an upstream gradient g.  The reference
+    values come from the oracle (mix_backward_weight / mix_backward_data on
+    the masked gradient, box_backward_input / box_backward_params); this
+    function adds only their deviation bounds.
+
+    Ambiguous decisions: the bf16 codes of O (they enter dW only:
+    sum_p |bf16(g)| * D); with ReLU, the mask where |zpre| is within its bound
+    ez of zero (there the masked gradient may be g or 0); and the bf16 codes
+    of the masked gradient itself where g carries an uncertainty eg_in (an
+    incoming gradient the GPU computed in fp32 from ambiguous operands; None:
+    g is exact, fp32 values whose codes agree on both sides).  mask_exact: the
+    ReLU mask is taken from an exact input (the layer above's input, which is
+    this layer's rectified output fed from the oracle), so it is unambiguous.
+    The uncertainty of the masked gradient is propagated through the
+    transposed mix and box operators with absolute values."""
     H, W = fw["o"].shape[-2:]
+    eg = np.zeros_like(g) if eg_in is None else np.asarray(eg_in, dtype=np.float64)
     if relu:
         on = fw["zpre"] > 0
-        amb = np.abs(fw["zpre"]) <= fw["ez"]
-        eg = np.where(amb, np.abs(g), 0.0)     # either choice of the mask is valid there
-        g = np.where(on, g, 0.0)
+        gm = np.where(on, g, 0.0)
+        if mask_exact:
+            eg = np.where(on, eg, 0.0)
+        else:
+            amb = np.abs(fw["zpre"]) <= fw["ez"]
+            # either choice of the mask is valid there
+            eg = np.where(amb, np.abs(g) + eg, np.where(on, eg, 0.0))
     else:
-        eg = np.zeros_like(g)
-    gb = O.bf16_round(g)
-    Dg = bf16_band(g, eg)
+        gm = g
+    gb = O.bf16_round(gm)
+    Dg = bf16_band(gm, eg)
     ob = O.bf16_round(fw["o"])
     wb = O.bf16_round(w)
     N, M = gb.shape[:2]
     K = ob.shape[1]
+    dw = O.mix_backward_weight(gm, fw["o"], compute="bf16")
+    do = O.mix_backward_data(w, gm, compute="bf16")
     g2, o2, D2, Dg2 = (a.reshape(a.shape[0], a.shape[1], -1) for a in (gb, ob, fw["D"], Dg))
-    dw = np.einsum("nmp,nkp->mk", g2, o2, optimize=True)
     edw = (np.einsum("nmp,nkp->mk", np.abs(g2) + Dg2, D2, optimize=True)
            + np.einsum("nmp,nkp->mk", Dg2, np.abs(o2), optimize=True))
-    do = np.einsum("mk,nmp->nkp", wb, g2, optimize=True).reshape(N, K, H, W)
     edo = np.einsum("mk,nmp->nkp", np.abs(wb), Dg2, optimize=True).reshape(N, K, H, W)
     dx = O.box_backward_input(do, boxes, H, W)
     edx = O.box_backward_input(edo, boxes, H, W)          # box weights are >= 0
@@ -91,7 +105,8 @@ def layer_backward(fw, boxes, w, g, relu=False):
     e = np.abs(O.box_param_grad_from_edges(np.abs(fw["x"]), edo, boxes))
     ea, eb, ec, ed = (e[..., k] for k in range(4))
     edth = np.stack([ea + eb, ec + ed, ea + eb, ec + ed], axis=-1)
-    return {"dw": dw, "edw": edw, "do": do, "edo": edo, "dx": dx, "edx": edx, "dth": dth, "edth": edth}
+    return {"dw": dw, "edw": edw, "do": do, "edo": edo, "dx": dx, "edx": edx, "dth": dth, "edth": edth,
+            "gm": gm, "eg": eg}
 
 
 def bounded_error(got, ref, bound):

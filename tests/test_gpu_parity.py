@@ -18,6 +18,7 @@ from paper_1906_11367_amd import workloads as wlmod
 from paper_1906_11367_amd.layer import LayerPlan, Stack
 
 import bf16_bounds as bb  # noqa: E402
+import tap_records as TR  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -57,21 +58,42 @@ def real_boxes(rng, C, B, cmax, rmin, rmax):
 # a1: per-box precomputation (integer decisions are bit-exact)
 # ---------------------------------------------------------------------------
 def test_box_prep_bit_exact():
+    """The records box_prep writes: their integer decisions (edge floors,
+    floor split forward, ceil - 1 split adjoint) and fp32 weights bit for bit
+    against the record layout (tests/tap_records.py); then the GPU's own
+    records, evaluated on exact tables, against the oracle's forward, input
+    gradient and box-parameter gradient."""
     rng = np.random.default_rng(100)
     C, B = 7, 5
     bx = real_boxes(rng, C, B, 40.0, 0.0, 60.0)
     bx[0, 0] = [0.0, 0.0, 0.5, 0.5]          # identity: integer edges
     bx[1, 1] = [0.25, -0.25, 1.75, 0.75]      # edges on quarter pixels
     bx[2, 2] = [3.0, -2.5, 2.5, 4.0]          # integer corners
+    bx[3, 3] = [0.5, -1.0, 1.0, 1.5]          # integer edges, one-sided derivatives
     table = torch.zeros(2 * C * B * 16, dtype=torch.int32, device="cuda")
     bc.box_prep(dev(bx), table)
     torch.cuda.synchronize()
-    t = table.cpu().numpy().reshape(2, C, B, 16)
-    for half, (fl, wx, wy) in enumerate([O.box_taps(bx), O.adjoint_taps(bx)]):
-        np.testing.assert_array_equal(t[half, ..., 0:4], fl)
-        np.testing.assert_array_equal(t[half, ..., 4:8].view(np.float32), wx)
-        np.testing.assert_array_equal(t[half, ..., 8:12].view(np.float32), wy)
-        np.testing.assert_array_equal(t[half, ..., 12:16], 0)
+    fwd, adj = TR.decode(table.cpu().numpy(), C, B)
+    for got, want in [(fwd, TR.box_records(bx)), (adj, TR.adjoint_records(bx))]:
+        for g, w in zip(got, want):
+            np.testing.assert_array_equal(g, w)
+    # the GPU's records on exact tables (maps large enough for every tap to
+    # land inside or at the clamped border for the smaller boxes)
+    H, W = 23, 19
+    bs = bx.copy()
+    bs[..., :2] = np.clip(bs[..., :2], -8, 8)
+    bs[..., 2:] = np.clip(bs[..., 2:], 0.0, 9)
+    bs[3, 3] = [0.5, -1.0, 1.0, 1.5]
+    table.zero_()
+    bc.box_prep(dev(bs), table)
+    torch.cuda.synchronize()
+    fwd, adj = TR.decode(table.cpu().numpy(), C, B)
+    x = rng.standard_normal((1, C, H, W))
+    g = rng.standard_normal((1, C * B, H, W))
+    check(TR.eval_forward(fwd, x), O.box_forward(x, bs), 2e-6, "GPU forward records on exact tables")
+    dI, dth = TR.eval_adjoint(adj, x, g)
+    check(dI, O.box_backward_input(g, bs, H, W), 2e-6, "GPU adjoint records: input gradient")
+    check(dth, O.box_backward_params(x, g, bs), 2e-6, "GPU adjoint records: box-parameter gradient")
 
 
 # ---------------------------------------------------------------------------
@@ -1041,10 +1063,12 @@ def test_layer_step_bf16_mix():
     check_bounded(host(z), fw["z"], fw["ez"], RTOL_BF16_MIX, "Z")
     dx, db, dw = plan.backward(xd, bd, wd, dev(d["grad"]))
     bw = bb.layer_backward(fw, d["boxes"], d["w"], d["grad"].astype(np.float64))
-    check_bounded(host(plan.do), bw["do"], bw["edo"], RTOL_BF16_MIX, "dO")
+    # without a ReLU, dO, dx and dboxes are fp32 results of the same bf16
+    # operands on both sides: no ambiguous decision, the fp32 bar
+    check_bounded(host(plan.do), bw["do"], bw["edo"], RTOL_F32, "dO")
     check_bounded(host(dw), bw["dw"], bw["edw"], RTOL_BF16_MIX, "dW")
-    check_bounded(host(dx), bw["dx"], bw["edx"], RTOL_BF16_MIX, "dx")
-    check_bounded(host(db), bw["dth"], bw["edth"], RTOL_BF16_MIX, "dboxes")
+    check_bounded(host(dx), bw["dx"], bw["edx"], RTOL_F32, "dx")
+    check_bounded(host(db), bw["dth"], bw["edth"], RTOL_F32, "dboxes")
 
 
 def test_stack_layers_relu_bf16_each_on_oracle_input():
@@ -1068,10 +1092,58 @@ def test_stack_layers_relu_bf16_each_on_oracle_input():
         dx, db, dw = plan.backward(xd, bd, wd, dev(g))
         bw = bb.layer_backward(fw, b, w, g.astype(np.float64), relu=True)
         check_bounded(host(dw), bw["dw"], bw["edw"], RTOL_BF16_MIX, f"dW[{li}]")
-        check_bounded(host(plan.do), bw["do"], bw["edo"], RTOL_BF16_MIX, f"dO[{li}]")
-        check_bounded(host(dx), bw["dx"], bw["edx"], RTOL_BF16_MIX, f"dx[{li}]")
-        check_bounded(host(db), bw["dth"], bw["edth"], RTOL_BF16_MIX, f"dboxes[{li}]")
+        check_bounded(host(plan.do), bw["do"], bw["edo"], RTOL_F32, f"dO[{li}]")
+        check_bounded(host(dx), bw["dx"], bw["edx"], RTOL_F32, f"dx[{li}]")
+        check_bounded(host(db), bw["dth"], bw["edth"], RTOL_F32, f"dboxes[{li}]")
         x = fw["z"]
+
+
+def test_stack_two_layers_chained_elementwise():
+    """Two stacked layers (bf16 mix + ReLU) through the chained backward the
+    stack runs: the top layer's box backward writes the bottom layer's masked
+    bf16 gradient operand (box_conv_bwd_relu_bf16) and the bottom layer's
+    GEMMs read it as given (grad_premasked).  Each layer's forward runs on the
+    oracle's input to that layer, so every gradient of both layers is checked
+    element by element: dW, dO, dboxes and the input gradients, within the
+    fp32 bar (1e-4; 1e-3 for dW, a bf16 mix result) beyond the bound of their
+    ambiguous bf16 codes and ReLU decisions."""
+    wl = wlmod.WORKLOADS[5].scaled(N=1, layers=2)
+    d = wlmod.make_inputs(wl)
+    (b0, w0), (b1, w1) = d["layers"]
+    say("stack c5: 2 layers, chained backward, N=1")
+    st = Stack(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, 2, "bf16", True)
+    p0, p1 = st.plans
+    assert p1.dx_relu_bf16 and p0.grad_premasked
+    x0 = d["x"].astype(np.float32)
+    fw0 = bb.layer_forward(x0.astype(np.float64), b0, w0, relu=True)
+    x1 = fw0["z"].astype(np.float32)                 # the oracle's input to layer 1
+    fw1 = bb.layer_forward(x1.astype(np.float64), b1, w1, relu=True)
+    params = [(dev(b0), dev(w0)), (dev(b1), dev(w1))]
+    inputs = [dev(x0), dev(x1)]
+    z0 = p0.forward(inputs[0], *params[0])
+    z1 = p1.forward(inputs[1], *params[1])
+    check_bounded(host(z0), fw0["z"], fw0["ez"], RTOL_BF16_MIX, "Z[0]")
+    check_bounded(host(z1), fw1["z"], fw1["ez"], RTOL_BF16_MIX, "Z[1]")
+    G = np.random.default_rng(110).standard_normal(fw1["z"].shape).astype(np.float32)
+    dx, grads = st.backward(inputs, params, dev(G))
+    torch.cuda.synchronize()
+    bw1 = bb.layer_backward(fw1, b1, w1, G.astype(np.float64), relu=True)
+    check_bounded(host(grads[1][1]), bw1["dw"], bw1["edw"], RTOL_BF16_MIX, "dW[1]")
+    check_bounded(host(p1.do), bw1["do"], bw1["edo"], RTOL_F32, "dO[1]")
+    check_bounded(host(grads[1][0]), bw1["dth"], bw1["edth"], RTOL_F32, "dboxes[1]")
+    # layer 1's input gradient, written masked and rounded: bf16(x1 > 0 ? dx1 : 0)
+    eg0 = bw1["edx"] + bb.scale_err(bw1["dx"], bb.E_F32)
+    on = x1 > 0
+    g0 = np.where(on, bw1["dx"], 0.0)
+    check_bounded(host(p1.dx), O.bf16_round(g0), bb.bf16_band(g0, np.where(on, eg0, 0.0)), RTOL_F32,
+                  "dx[1] (masked bf16)")
+    # layer 0 on that gradient: its mask comes from the exact x1, its bf16
+    # codes carry the uncertainty of layer 1's fp32 input gradient
+    bw0 = bb.layer_backward(fw0, b0, w0, bw1["dx"], relu=True, eg_in=eg0, mask_exact=True)
+    check_bounded(host(grads[0][1]), bw0["dw"], bw0["edw"], RTOL_BF16_MIX, "dW[0]")
+    check_bounded(host(p0.do), bw0["do"], bw0["edo"], RTOL_F32, "dO[0]")
+    check_bounded(host(grads[0][0]), bw0["dth"], bw0["edth"], RTOL_F32, "dboxes[0]")
+    check_bounded(host(dx), bw0["dx"], bw0["edx"], RTOL_F32, "dx[0]")
 
 
 RTOL_STACK_NORMWISE_PER_LAYER = 5e-3

@@ -56,6 +56,20 @@ def test_sat_matches_definition_loops(kind):
                     assert abs(s[m, u, v] - want) <= 1e-12 * (1 + abs(want))
 
 
+def test_map_mean_closed_forms():
+    """The per-map mean (the offset the large-map tables subtract): the
+    table's last entry over the pixel count (exact for integer maps), the
+    closed form of an arithmetic ramp, and a constant map."""
+    rng = np.random.default_rng(12)
+    x = rng.integers(-9, 10, size=(3, 2, 5, 7))
+    S = O.sat_exclusive(x)
+    np.testing.assert_array_equal(O.map_mean(x), S[..., 5, 7] / 35.0)
+    H, W = 6, 9
+    ramp = np.arange(H * W, dtype=np.float32).reshape(1, H, W)
+    assert O.map_mean(ramp)[0] == (H * W - 1) / 2
+    assert O.map_mean(np.full((2, 4, 4), 0.75, np.float32)).tolist() == [0.75, 0.75]
+
+
 # --------------------------------------------------------------------------
 # Forward box filter
 # --------------------------------------------------------------------------
@@ -122,101 +136,6 @@ def test_forward_equals_sat_four_corner_bilinear():
     got = O.box_forward(x, bx)
     want = _four_corner_bilinear(x, bx)
     assert np.max(np.abs(got - want)) <= 1e-11 * (1 + np.max(np.abs(want)))
-
-
-def test_box_taps_reproduce_forward_on_exact_table():
-    """The precomputed taps (floors + separable weights) evaluated on the
-    exact table with clamped indices give the oracle's forward result."""
-    rng = np.random.default_rng(20)
-    N, C, B, H, W = 1, 2, 3, 9, 8
-    x = rng.standard_normal((N, C, H, W))
-    bx = _real_boxes(rng, C, B, cmax=5.0, rmin=0.2, rmax=6.0)
-    fl, wx, wy = O.box_taps(bx)
-    S = O.sat_exclusive(x)
-    want = O.box_forward(x, bx)
-    for c in range(C):
-        for b in range(B):
-            fa, fb, fc, fd = fl[c, b]
-            ox = [fa, fa + 1, fb, fb + 1]
-            oy = [fc, fc + 1, fd, fd + 1]
-            for yy in range(H):
-                for xx in range(W):
-                    v = 0.0
-                    for r in range(4):
-                        for k in range(4):
-                            u = min(max(yy + oy[r], 0), H)
-                            t = min(max(xx + ox[k], 0), W)
-                            v += float(wy[c, b, r]) * float(wx[c, b, k]) * S[0, c, u, t]
-                    assert abs(v - want[0, c * B + b, yy, xx]) <= 1e-5 * (1 + abs(v))
-    # mirror = negated centre offset
-    flm, _, _ = O.box_taps(bx, mirror=True)
-    a, b_, c_, d = O.box_edges(O.mirrored_boxes(bx))
-    np.testing.assert_array_equal(flm[..., 0], np.floor(a))
-
-
-def test_adjoint_taps_match_mirror_taps_off_integer_edges():
-    """Away from integer edges the adjoint split is the floor split of the
-    mirrored box; on an integer edge the floor is one lower and the weights
-    put all of the edge on the upper tap."""
-    rng = np.random.default_rng(21)
-    bx = _real_boxes(rng, 3, 5, cmax=6.0, rmin=0.3, rmax=7.0)
-    fa, wxa, wya = O.adjoint_taps(bx)
-    fm, wxm, wym = O.box_taps(bx, mirror=True)
-    np.testing.assert_array_equal(fa, fm)
-    np.testing.assert_array_equal(wxa, wxm)
-    np.testing.assert_array_equal(wya, wym)
-    bi = np.array([[[1.5, -2.0, 1.0, 2.5]]], dtype=np.float32)   # all four edges integer
-    fa, wxa, wya = O.adjoint_taps(bi)
-    fm, _, _ = O.box_taps(bi, mirror=True)
-    np.testing.assert_array_equal(fa, fm - 1)
-    np.testing.assert_array_equal(wxa[0, 0], np.array([0, -1, 0, 1], np.float32))
-    np.testing.assert_array_equal(wya[0, 0], np.array([0, -1, 0, 1], np.float32))
-
-
-def _adjoint_param_grad(x, g, box):
-    """d<g, box(x)>/d(cx, cy, rx, ry) for one map through the adjoint:
-    <g, box(x)> = <x, D> with D the adjoint box sum of g read from g's
-    exclusive table at adjoint_taps; each edge derivative of D is a difference
-    of the two taps around that edge (small loops, independent of
-    box_backward_params)."""
-    H, W = x.shape
-    S = O.sat_exclusive(g[None, None])[0, 0]
-    fl, wx, wy = O.adjoint_taps(box[None, None])
-    fa, fb, fc, fd = fl[0, 0]
-    wx, wy = wx[0, 0].astype(np.float64), wy[0, 0].astype(np.float64)
-    ox, oy = [fa, fa + 1, fb, fb + 1], [fc, fc + 1, fd, fd + 1]
-    T = lambda u, v: S[min(max(u, 0), H), min(max(v, 0), W)]
-    ga = gb = gc = gd = 0.0
-    for i in range(H):
-        for j in range(W):
-            U = [sum(wx[k] * T(i + oy[r], j + ox[k]) for k in range(4)) for r in range(4)]
-            colA = sum(wy[r] * (T(i + oy[r], j + ox[1]) - T(i + oy[r], j + ox[0])) for r in range(4))
-            colB = sum(wy[r] * (T(i + oy[r], j + ox[3]) - T(i + oy[r], j + ox[2])) for r in range(4))
-            v = x[i, j]
-            ga -= v * colB          # a = 1 - b'
-            gb += v * colA          # b = 1 - a'
-            gc -= v * (U[3] - U[2])  # c = 1 - d'
-            gd += v * (U[1] - U[0])  # d = 1 - c'
-    return np.array([ga + gb, gc + gd, gb - ga, gd - gc])
-
-
-def test_adjoint_taps_carry_param_gradient():
-    """Through <g, box(x)> = <x, adjoint box(g)>, the table differences at
-    adjoint_taps reproduce the parameter gradient, including boxes whose
-    edges sit on pixel boundaries (where the one-sided derivative matters)."""
-    rng = np.random.default_rng(22)
-    H, W = 7, 6
-    boxes = [np.array([rng.uniform(-4, 4), rng.uniform(-4, 4), rng.uniform(0.3, 4), rng.uniform(0.3, 4)],
-                      np.float32) for _ in range(3)]
-    boxes += [np.array([0.5, -1.0, 1.0, 1.5], np.float32), np.array([-2.5, 2.0, 2.0, 0.5], np.float32),
-              np.array([3.0, 0.5, 1.5, 3.0], np.float32)]
-    for box in boxes:
-        x = rng.standard_normal((H, W))
-        g = rng.standard_normal((H, W))
-        want = O.box_backward_params(x[None, None], g[None, None], box[None, None])[0, 0]
-        got = _adjoint_param_grad(x, g, box)
-        # the tap weights are fp32 (reading R5): ~1e-7 relative per weight
-        assert np.all(np.abs(got - want) <= 1e-6 * (1.0 + np.abs(want))), (box, got, want)
 
 
 def test_forward_identity_box_exact():
@@ -833,10 +752,6 @@ def _mut_param_sign(x, grad_y, boxes, stride=1):
     return np.stack([ga + gb, gc + gd, ga - gb, gd - gc], axis=-1)
 
 
-def _mut_adjoint_floor_split(boxes):
-    return _OM.box_taps(boxes, mirror=True)
-
-
 def _mut_bf16_truncate(v):
     f = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
     u = (f.view(np.uint32) >> np.uint32(16)) << np.uint32(16)
@@ -925,7 +840,6 @@ _MUTATIONS = {
     "edge_selector_ceil": ("_edge_selector", _mut_edge_selector_ceil),
     "param_sign": ("box_backward_params", _mut_param_sign),
     "bf16_truncate": ("bf16_round", _mut_bf16_truncate),
-    "adjoint_floor_split": ("adjoint_taps", _mut_adjoint_floor_split),
     "bwd_input_no_transpose": ("box_backward_input", _mut_backward_input_no_transpose),
     "rounded_half_even": ("rounded_edges", _mut_rounded_half_even),
     "rounded_floor": ("rounded_edges", _mut_rounded_floor),
@@ -945,7 +859,7 @@ _PINS = [
     test_input_grad_adjoint_and_mirrored_box, test_input_grad_finite_difference,
     test_param_grad_finite_difference_exact, test_param_grad_edges_clipped_at_border,
     test_param_grad_constant_image_closed_form, test_bf16_round_matches_torch,
-    test_adjoint_taps_carry_param_gradient, test_rounded_edges_closed_form,
+    test_rounded_edges_closed_form,
     lambda: test_integer_corners_forward_equals_eq1_loops("int"), test_integer_corners_backward_is_adjoint,
     lambda: test_strided_forward_equals_eq1_loops(2), test_strided_input_grad_is_adjoint,
     test_strided_param_grad_finite_difference_exact, test_unit_params_identity_and_corners,
