@@ -349,6 +349,35 @@ bc_status bc_cast_bf16(const float* src, void* dst, size_t n, hipStream_t stream
  * ---------------------------------------------------------------------- */
 bc_status bc_relu_grad_bf16(const float* grad, const float* out, void* dst, size_t n, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * box_conv_bwd_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): box_conv_bwd with its workspace taken from a fixed device array
+ * the library owns, BC_NOALLOC_SCRATCH_BYTES bytes on each GPU it runs on,
+ * held until the process ends.  The call allocates nothing.
+ *
+ * Arguments, flags, results and errors are those of box_conv_bwd, without
+ * ws / ws_bytes.  A request whose workspace (bc_box_workspace_bytes(1, ...))
+ * exceeds BC_NOALLOC_SCRATCH_BYTES returns BC_ERR_WORKSPACE before anything
+ * runs: in practice the maps whose table fits in LDS (the pose-shaped layer:
+ * about 1.2 MB at N = 32, C = 256, B = 4, 64 x 48); maps that need their
+ * tables in HBM (256 x 256) do not fit.  bc_noalloc_scratch_bytes() returns
+ * the array's size.
+ *
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (the call writes every word it reads, so nothing stale is used):
+ * calls that overlap on one GPU -- on different streams, or from different
+ * host threads -- race on it and must be serialised by the caller.  The
+ * array's device address is looked up once per device, on the first call
+ * made with that device current.
+ * ---------------------------------------------------------------------- */
+#define BC_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+bc_status box_conv_bwd_noalloc(const float* x, const float* boxes, const float* grad_y,
+                               int N, int C, int H, int W, int B,
+                               float* grad_x, float* grad_boxes, unsigned flags,
+                               hipStream_t stream);
+size_t bc_noalloc_scratch_bytes(void);
+
 /* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd. */
 size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags);
 size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt);

@@ -51,6 +51,8 @@ SIGNATURES = {
     "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
     "bc_relu_grad_bf16": (_i, [_vp, _vp, _vp, _sz, _vp]),
     "box_conv_bwd_relu_bf16": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp, _sz, _vp]),
+    "box_conv_bwd_noalloc": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _u, _vp]),
+    "bc_noalloc_scratch_bytes": (_sz, []),
     "bc_status_string": (ctypes.c_char_p, [_i]),
     "bc_abi_version": (_i, []),
 }
@@ -254,6 +256,25 @@ def box_conv_bwd_relu_bf16(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.T
                                                  _ptr(grad_x_bf16), _ptr(grad_boxes), flags, _ptr(ws), nbytes,
                                                  _stream()), "box_conv_bwd_relu_bf16")
     return grad_x_bf16, grad_boxes
+
+
+def box_conv_bwd_noalloc(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, grad_x: torch.Tensor | None,
+                         grad_boxes: torch.Tensor | None, flags: int = 0):
+    """box_conv_bwd with the library's own fixed scratch array as workspace:
+    the call allocates nothing (bc_noalloc_scratch_bytes() is the limit)."""
+    what = "box_conv_bwd_noalloc"
+    N, C, H, W, B = _maps_and_boxes(x, boxes, what)
+    _need(x, None, _F32, what, "x")
+    _need(grad_y, (N, C * B, H, W), _F32, what, "grad_y")
+    _need(grad_x, (N, C, H, W), _F32, what, "grad_x")
+    _need(grad_boxes, (C, B, 4), _F32, what, "grad_boxes")
+    _check(load_library().box_conv_bwd_noalloc(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, _ptr(grad_x),
+                                               _ptr(grad_boxes), flags, _stream()), what)
+    return grad_x, grad_boxes
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(load_library().bc_noalloc_scratch_bytes())
 
 
 def box_conv_bwd_strided(x, boxes, grad_y, stride: int, grad_x, grad_boxes, flags: int = 0, ws=None):

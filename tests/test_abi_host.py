@@ -259,3 +259,15 @@ def test_workspace_queries():
     assert lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0) >= 4 * 128 * 8 * 257 * 257 * 4
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_FWD, 32, 256, 1024, 3072, bc.BC_BF16) == 0
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, 32, 256, 1024, 3072, bc.BC_BF16) > 0
+
+
+def test_noalloc_backward_rejects_oversized_request_before_any_launch():
+    """box_conv_bwd_noalloc compares the request's workspace with its fixed
+    array first: 256 x 256 maps (tables in HBM) are rejected on the host."""
+    lib = bc.load_library()
+    assert lib.bc_noalloc_scratch_bytes() == 16 << 20
+    need = lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0)
+    assert need > lib.bc_noalloc_scratch_bytes()
+    assert lib.box_conv_bwd_noalloc(FAKE, FAKE, FAKE, 4, 128, 256, 256, 8, FAKE, FAKE, 0, None) == 5
+    # invalid sizes are reported as such
+    assert lib.box_conv_bwd_noalloc(FAKE, FAKE, FAKE, 0, 128, 64, 48, 4, FAKE, FAKE, 0, None) == 2
