@@ -318,10 +318,13 @@ def main():
     torch.cuda.synchronize()
     spin_cycles = int(probe * 100.0 / max(s0.elapsed_time(s1), 1e-3))
 
-    # timed region: plain steps.  A few untimed steps follow the spin before
-    # the first event: kernels run up to ~20 % longer for a few steps after
-    # it, and that transient stays outside the timing.
-    settle = 10
+    # timed region: plain steps.  Untimed steps follow the spin before the
+    # first event: after any pause in the step stream (the spin included) the
+    # step time ramps down over ~40 steps (~25 ms; measured on the pose
+    # layer: ~730 us at the 5th step, 588 us from the 45th on), and the
+    # settle steps keep that ramp outside the timing, whatever --warmup and
+    # --steps are.
+    settle = 60
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     spin(spin_cycles)
     for _ in range(settle):

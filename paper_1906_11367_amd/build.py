@@ -20,7 +20,7 @@ OUT = os.path.join(PKG, "libboxconv.so")
 BUILD = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["bc_api.cpp", "bc_box.hip", "bc_mix.hip", "bc_noalloc.hip"]
+SOURCES = ["bc_api.cpp", "bc_box.hip", "bc_mix.hip", "bc_noalloc.hip", "bc_stream.hip"]
 
 
 def hipcc() -> str:

@@ -3,6 +3,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "../../include/boxconv.h"
 #include "bc_internal.hpp"
 
@@ -38,10 +40,29 @@ bool bwd_lds_fits(int H, int W) {
   return (size_t)(H + 1) * bc::lds_pitch(W) * 4 <= kLdsBudget && bc::box_bwd_lds_seg(H, W, bc::kBwdLdsItems) > 0;
 }
 
+// Which kernels evaluate a box call: the map's table built in LDS, tables in
+// HBM (built by sat_build, then gathered), or the streaming kernels (no
+// stored table).  BC_FLAG_FORCE_HBM always takes the HBM tables.
+enum class BoxPath { Lds, Hbm, Stream };
+#ifndef BC_STREAM_POLICY
+#define BC_STREAM_POLICY 1
+#endif
+// 0: never stream; 1: stream where the table does not fit LDS; 2: stream
+// wherever the streaming kernels apply.
+constexpr int kStreamPolicy = BC_STREAM_POLICY;
+BoxPath box_path(bool bwd, int H, int W, int B, unsigned flags, int stride) {
+  if (flags & BC_FLAG_FORCE_HBM) return BoxPath::Hbm;
+  const bool fits = bwd ? bwd_lds_fits(H, W) : fwd_lds_fits(H, W);
+  const bool can_stream = stride == 1 && bc::box_stream_supported(H, W, B);
+  if (can_stream && (kStreamPolicy == 2 || (kStreamPolicy == 1 && !fits))) return BoxPath::Stream;
+  return fits ? BoxPath::Lds : BoxPath::Hbm;
+}
+
 // Workspace layouts.  Every box entry point first writes the tap records of
 // all boxes (box_prep) at offset 0; the HBM paths add their tables after it.
 struct FwdWs { size_t taps, sat, means, total; };
-FwdWs fwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+FwdWs fwd_ws(int N, int C, int H, int W, int B, BoxPath path) {
+  const bool hbm = path == BoxPath::Hbm;
   FwdWs w{};
   w.taps = 0;
   w.sat = align_up(bc::tap_table_bytes(C, B));
@@ -55,11 +76,17 @@ FwdWs fwd_ws(int N, int C, int H, int W, int B, bool hbm) {
 }
 
 struct BwdWs { size_t taps, sat_g, partials, total; int P; };
-BwdWs bwd_ws(int N, int C, int H, int W, int B, bool hbm) {
+BwdWs bwd_ws(int N, int C, int H, int W, int B, BoxPath path) {
   BwdWs w{};
   w.taps = 0;
   const size_t after_taps = align_up(bc::tap_table_bytes(C, B));
-  if (!hbm) {
+  if (path == BoxPath::Stream) {   // one partial row per image
+    w.P = N;
+    w.partials = after_taps;
+    w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
+    return w;
+  }
+  if (path == BoxPath::Lds) {
     w.P = N * bc::box_bwd_lds_waves(H, W, bc::kBwdLdsItems);
     w.partials = after_taps;
     w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
@@ -114,13 +141,25 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean, int N, i
 
 size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags) {
   if (!dims_ok(N, C, H, W, B)) return 0;
+  // the workspace of the stride-1 call; a strided call never takes the
+  // streaming kernels, so it asks for the largest of the layouts
   if (op == 0) {
-    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
-    return fwd_ws(N, C, H, W, B, hbm).total;
+    const BoxPath path = box_path(false, H, W, B, flags, 1);
+    size_t n = fwd_ws(N, C, H, W, B, path).total;
+    if (path == BoxPath::Stream) {
+      const BoxPath alt = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W) ? BoxPath::Hbm : BoxPath::Lds;
+      n = std::max(n, fwd_ws(N, C, H, W, B, alt).total);
+    }
+    return n;
   }
   if (op == 1) {
-    const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W);
-    return bwd_ws(N, C, H, W, B, hbm).total;
+    const BoxPath path = box_path(true, H, W, B, flags, 1);
+    size_t n = bwd_ws(N, C, H, W, B, path).total;
+    if (path == BoxPath::Stream) {
+      const BoxPath alt = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W) ? BoxPath::Hbm : BoxPath::Lds;
+      n = std::max(n, bwd_ws(N, C, H, W, B, alt).total);
+    }
+    return n;
   }
   return 0;
 }
@@ -139,9 +178,10 @@ bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes,
   if (!aligned16(x) || !aligned16(boxes) || !aligned16(y)) return BC_ERR_ALIGN;
   const int out_kind = y_dt == BC_BF16 ? 2 : (is_int ? 0 : 1);
   const bool offset = (flags & BC_FLAG_MEAN_OFFSET) != 0;
-  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W);
+  const BoxPath path = box_path(false, H, W, B, flags, stride);
+  const bool hbm = path == BoxPath::Hbm;
   if (hbm && W > 1024) return BC_ERR_SHAPE;
-  const FwdWs L = fwd_ws(N, C, H, W, B, hbm);
+  const FwdWs L = fwd_ws(N, C, H, W, B, path);
   if (!ws) return BC_ERR_WORKSPACE;
   if (ws_bytes < L.total) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
@@ -149,6 +189,8 @@ bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes,
   const int* taps = reinterpret_cast<const int*>(base + L.taps);
   hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
+  if (path == BoxPath::Stream)
+    return hip_status(bc::launch_box_fwd_stream(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, rounded, stream));
   if (!hbm)
     return hip_status(
         bc::launch_box_fwd_lds(x, is_int, taps, y, out_kind, N, C, H, W, B, offset, rounded, stride, stream));
@@ -182,9 +224,10 @@ static bc_status box_bwd_impl(const float* x, const float* boxes, const float* g
   if (!grad_x && !grad_boxes) return BC_OK;
   // BC_FLAG_MEAN_OFFSET is accepted and has no effect here: the backward
   // tabulates only the upstream gradient, never x.
-  const bool hbm = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W);
+  const BoxPath path = box_path(true, H, W, B, flags, stride);
+  const bool hbm = path == BoxPath::Hbm;
   if (hbm && W > 1024) return BC_ERR_SHAPE;
-  const BwdWs L = bwd_ws(N, C, H, W, B, hbm);
+  const BwdWs L = bwd_ws(N, C, H, W, B, path);
   if (!ws) return BC_ERR_WORKSPACE;
   if (ws_bytes < L.total) return BC_ERR_WORKSPACE;
   if (!aligned16(ws)) return BC_ERR_ALIGN;
@@ -193,7 +236,9 @@ static bc_status box_bwd_impl(const float* x, const float* boxes, const float* g
   const int* taps = reinterpret_cast<const int*>(base + L.taps);
   hipError_t e = bc::launch_box_prep(boxes, C, B, rounded, base + L.taps, stream);
   if (e != hipSuccess) return BC_ERR_HIP;
-  if (!hbm) {
+  if (path == BoxPath::Stream) {
+    e = bc::launch_box_bwd_stream(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, relu_bf16, stream);
+  } else if (!hbm) {
     e = bc::launch_box_bwd_lds(x, taps, grad_y, grad_x, partials, N, C, H, W, B, rounded, relu_bf16, stride, stream);
   } else {
     float* sat_g = reinterpret_cast<float*>(base + L.sat_g);

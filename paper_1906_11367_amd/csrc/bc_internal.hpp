@@ -89,6 +89,14 @@ hipError_t launch_box_bwd_gather_split(const float* x, const float* sat_g, const
 hipError_t launch_split_grad_reduce(const float* partials, int Pn, int CB, int P, float* grad_boxes, float* grad_w,
                                     hipStream_t s);
 
+// Streaming box kernels (no stored table): maps up to 256 wide, B <= 16
+// (W <= 64) or B <= 8 (W <= 256).  Backward partials: [N][C*B][4] (P = N).
+bool box_stream_supported(int H, int W, int B);
+hipError_t launch_box_bwd_stream(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N,
+                                 int C, int H, int W, int B, bool rounded, bool relu_bf16, hipStream_t s);
+hipError_t launch_box_fwd_stream(const void* x, bool is_int, const int* taps, void* y, int out_kind, int N, int C,
+                                 int H, int W, int B, bool offset, bool rounded, hipStream_t s);
+
 // 1x1 mix GEMMs.
 hipError_t launch_mix(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out,
                       int out_dt, int N, int M, int K, int P, int compute_dt, int relu,

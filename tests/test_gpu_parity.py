@@ -156,6 +156,15 @@ def test_fwd_tiny_integer_workload_bit_exact(flags):
     (3, dict(N=2, C=8)),
     (2, dict(N=1, C=3, H=37, W=29, B=5)),   # ragged chunks and segments
     (3, dict(N=1, C=2, H=17, W=100, B=3)),
+    (2, dict(N=1, C=3, H=60, W=40, B=3)),
+    (2, dict(N=2, C=2, H=9, W=47, B=2)),
+    (2, dict(N=1, C=2, H=120, W=48, B=1)),
+    # maps whose table does not fit LDS, evaluated by the streaming kernels:
+    # tall and narrow (four boxes per wave), ragged widths, full 16-byte rows
+    (2, dict(N=1, C=2, H=500, W=47, B=3)),
+    (4, dict(N=1, C=2, H=300, W=128, B=3)),
+    (4, dict(N=1, C=1, H=200, W=200, B=5)),
+    (4, dict(N=1, C=2, H=130, W=256, B=8)),
 ])
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM, bc.BC_FLAG_MEAN_OFFSET])
 def test_fwd_f32(key, scale, flags):
@@ -265,7 +274,8 @@ def test_box_prep_rounded_bit_exact():
 
 
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
-@pytest.mark.parametrize("shape", [(2, 3, 32, 32), (1, 2, 37, 29)])
+@pytest.mark.parametrize("shape", [(2, 3, 32, 32), (1, 2, 37, 29),
+                                   (1, 2, 260, 200), (1, 2, 130, 256)])   # streamed int32 maps
 def test_fwd_integer_corners_int_bit_exact(flags, shape):
     say(f"fwd integer corners int32 {shape} flags={flags}")
     rng = np.random.default_rng(111)
@@ -714,6 +724,15 @@ def _bwd(x, bx, g, flags=0):
     (2, dict(N=1, C=3, H=37, W=29, B=5)),
     (3, dict(N=2, C=2, H=17, W=100, B=3)),
     (4, dict(N=1, C=1, B=3)),
+    # ragged rows and columns, a last column inside an item, 256-row maps
+    (2, dict(N=1, C=3, H=60, W=40, B=3)),
+    (2, dict(N=2, C=2, H=9, W=47, B=2)),
+    (2, dict(N=1, C=2, H=256, W=48, B=2)),
+    # maps the streaming backward takes (no table in LDS or HBM)
+    (2, dict(N=1, C=2, H=500, W=47, B=3)),
+    (4, dict(N=1, C=2, H=300, W=128, B=3)),
+    (4, dict(N=1, C=1, H=200, W=200, B=5)),
+    (4, dict(N=1, C=2, H=130, W=256, B=8)),
 ])
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM, bc.BC_FLAG_MEAN_OFFSET])
 def test_bwd(key, scale, flags):
