@@ -100,7 +100,24 @@ __device__ __forceinline__ float group_sum(float v) {
 // consecutive entries whose start is clamped to [-pad, W] then reads exactly
 // the clamped entries.
 template <int CPL> constexpr int stream_pad() { return CPL + 1; }
-template <int LG, int CPL> constexpr int stream_row_words() { return 2 * stream_pad<CPL>() + LG * CPL + 1; }
+// With an even CPL, lanes address a row CPL words apart, which puts lanes 32
+// / CPL apart on one LDS bank; one skip word every 32 words (index i at
+// i + i / 32) spreads them over all banks.  Odd CPL needs none.
+template <int CPL> constexpr bool stream_skew() { return CPL % 2 == 0; }
+template <int LG, int CPL> constexpr int stream_row_words() {
+  constexpr int n = 2 * stream_pad<CPL>() + LG * CPL + 1;
+  return stream_skew<CPL>() ? n + n / 32 + 1 : n;
+}
+// LDS index of row entry v (v in [-pad, LG * CPL + pad]).
+template <int CPL>
+__device__ __forceinline__ int stream_at(int v) {
+  const int i = v + stream_pad<CPL>();
+  return stream_skew<CPL>() ? i + (i >> 5) : i;
+}
+// LDS index of element j of a group's input-gradient slot (j in [0, LG*CPL)).
+template <int CPL>
+__device__ __forceinline__ int slot_at(int j) { return stream_skew<CPL>() ? j + (j >> 5) : j; }
+template <int LG, int CPL> constexpr int slot_words() { return stream_skew<CPL>() ? LG * CPL + LG * CPL / 32 : LG * CPL; }
 
 // Rows of a step are loaded kPrefetch steps ahead (a ring of registers), so
 // that a step's loads are in flight while the steps before it compute.
@@ -171,10 +188,11 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
   constexpr int RW = stream_row_words<LG, CPL>();
   constexpr int PF = kPrefetch;
   constexpr int LC = LG * CPL;            // columns a group covers
+  constexpr int SW = slot_words<LG, CPL>();
   extern __shared__ __align__(16) float smem[];
   float* SY = smem;                       // [NG][RW]: scan Y of each group's box
   float* SV = SY + NG * RW;               // [NG][RW]: suffix sums of the input row
-  float* DX = SV + NG * RW;               // [2][R][NG][LC]: adjoint sums, added over groups
+  float* DX = SV + NG * RW;               // [2][R][NG][SW]: adjoint sums, added over groups
   const int map = blockIdx.x, n = map / C, c = map - n * C;
   const int g = threadIdx.x / LG, p = threadIdx.x % LG;
   const int b = g;
@@ -185,19 +203,36 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
   const float* gbase = gy + (size_t)map * B * plane;
   const unsigned gmap = live ? 4u * (unsigned)(b * plane) : 0u;
   const LaneCols<CPL> cols(x0, W);
-  float* sy = SY + g * RW + PAD;          // sy[v] = scan Y (v), v in [-PAD, LC + PAD]
-  float* sv = SV + g * RW + PAD;
+  float* sy = SY + g * RW;                // sy[stream_at(v)] = scan Y (v), v in [-PAD, LC + PAD]
+  float* sv = SV + g * RW;
   // adjoint record of the box (each group its own; vector loads)
   const Taps<float> tp = load_taps(taps + (size_t)C * B * 16 + (size_t)(c * B + (live ? b : 0)) * 16, W, H);
   const int fa = tp.ox[0], fb = tp.ox[2], fc = tp.oy[0], fd = tp.oy[2];
   const float aa = -tp.wx[1], ab = tp.wx[3], bc_ = -tp.wy[1], bd = tp.wy[3];
-  const int ra0 = clampi(x0 + fa, -PAD, W), rb0 = clampi(x0 + fb, -PAD, W);   // tap runs in scan Y
-  const int va0 = clampi(x0 - fa, -PAD, W), vb0 = clampi(x0 - fb, -PAD, W);   // tap runs in the suffix sums
+  // LDS indices of the lane's tap runs (scan Y at the adjoint's x edges, the
+  // suffix sums at the mirrored taps) and of the entries it writes
+  int ia[CPL + 1], ib[CPL + 1], ja[CPL + 1], jb[CPL + 1], iw[CPL], jw[CPL];
+  {
+    const int ra0 = clampi(x0 + fa, -PAD, W), rb0 = clampi(x0 + fb, -PAD, W);
+    const int va0 = clampi(x0 - fa, -PAD, W), vb0 = clampi(x0 - fb, -PAD, W);
+#pragma unroll
+    for (int k = 0; k <= CPL; ++k) {
+      ia[k] = stream_at<CPL>(ra0 + k);
+      ib[k] = stream_at<CPL>(rb0 + k);
+      ja[k] = stream_at<CPL>(va0 + k);
+      jb[k] = stream_at<CPL>(vb0 + k);
+    }
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      iw[k] = stream_at<CPL>(x0 + k + 1);
+      jw[k] = stream_at<CPL>(x0 + k);
+    }
+  }
   // constant parts of the LDS rows: scan Y is 0 left of column 0, the input
   // row's suffix sums are 0 right of column W
   for (int t = p; t <= PAD; t += LG) {
-    sy[-PAD + t] = 0.f;
-    sv[LC + t] = 0.f;
+    sy[stream_at<CPL>(-PAD + t)] = 0.f;
+    sv[stream_at<CPL>(LC + t)] = 0.f;
   }
   // cursors: P(clamp(y + fc)) and P(clamp(y + fd)) at the lane's columns
   float pc[CPL], pd[CPL];
@@ -245,10 +280,10 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
     const float tot = s[CPL - 1];
     const float off = group_scan<LG, false>(tot) - tot;
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) sy[x0 + k + 1] = s[k] + off;
+    for (int k = 0; k < CPL; ++k) sy[iw[k]] = s[k] + off;
     if (p == LG - 1) {
 #pragma unroll
-      for (int t = 1; t <= PAD; ++t) sy[LC + t] = s[CPL - 1] + off;
+      for (int t = 1; t <= PAD; ++t) sy[stream_at<CPL>(LC + t)] = s[CPL - 1] + off;
     }
     // suffix sums of the input row (the same in every group)
     if constexpr (!kInt) {
@@ -258,19 +293,19 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
       const float vt = sfx[0];
       const float voff = group_scan<LG, true>(vt) - vt;
 #pragma unroll
-      for (int k = 0; k < CPL; ++k) sv[x0 + k] = sfx[k] + voff;
+      for (int k = 0; k < CPL; ++k) sv[jw[k]] = sfx[k] + voff;
       if (p == 0) {
 #pragma unroll
-        for (int t = 1; t <= PAD; ++t) sv[-t] = sfx[0] + voff;
+        for (int t = 1; t <= PAD; ++t) sv[stream_at<CPL>(-t)] = sfx[0] + voff;
       }
     }
     __builtin_amdgcn_wave_barrier();
     // the adjoint box sums of the lane's outputs and the edge terms
     float sa[CPL + 1], sb[CPL + 1];
 #pragma unroll
-    for (int k = 0; k <= CPL; ++k) { sa[k] = sy[ra0 + k]; sb[k] = sy[rb0 + k]; }
+    for (int k = 0; k <= CPL; ++k) { sa[k] = sy[ia[k]]; sb[k] = sy[ib[k]]; }
     const int bi = y / R, ri = y - bi * R;
-    float* dxs = DX + (((bi & 1) * R + ri) * NG + g) * LC;
+    float* dxs = DX + (((bi & 1) * R + ri) * NG + g) * SW;
 #pragma unroll
     for (int k = 0; k < CPL; ++k) {
       float d;
@@ -282,12 +317,12 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
         ca = fmaf(v[k], da, ca);
         cb = fmaf(v[k], db, cb);
       }
-      dxs[x0 + k] = live ? d : 0.f;
+      dxs[slot_at<CPL>(x0 + k)] = live ? d : 0.f;
     }
     if constexpr (!kInt) {
       float A[CPL + 1], Bv[CPL + 1];
 #pragma unroll
-      for (int k = 0; k <= CPL; ++k) { A[k] = sv[va0 + k]; Bv[k] = sv[vb0 + k]; }
+      for (int k = 0; k <= CPL; ++k) { A[k] = sv[ja[k]]; Bv[k] = sv[jb[k]]; }
 #pragma unroll
       for (int k = 0; k < CPL; ++k) {
         const float t = fmaf(-ab, Bv[k + 1] - Bv[k], fmaf(aa, A[k + 1] - A[k], Bv[k + 1] - A[k + 1]));
@@ -300,13 +335,13 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
     // the groups in a fixed order
     if (ri == R - 1 || y == H - 1) {
       __syncthreads();
-      const float* slots = DX + (bi & 1) * R * NG * LC;
+      const float* slots = DX + (bi & 1) * R * NG * SW;
       for (int r = 0; r <= ri; ++r) {
         const int yy = bi * R + r;
         for (int j = threadIdx.x; j < W; j += LG * NG) {
           float acc = 0.f;
 #pragma unroll
-          for (int h = 0; h < NG; ++h) acc += slots[(r * NG + h) * LC + j];
+          for (int h = 0; h < NG; ++h) acc += slots[(r * NG + h) * SW + slot_at<CPL>(j)];
           const size_t o = (size_t)map * plane + (size_t)yy * W + j;
           if constexpr (kRelu) {
             static_cast<uint16_t*>(gx)[o] = f32_to_bf16_rne(xs[(size_t)yy * W + j] > 0.f ? acc : 0.f);
@@ -375,7 +410,7 @@ __global__ __launch_bounds__(LG * NG) void k_box_fwd_stream(const T* __restrict_
   const size_t plane = (size_t)H * W;
   const T* xs = x + (size_t)map * plane;
   const LaneCols<CPL> cols(x0, W);
-  T* sy = SY + g * RW + PAD;
+  T* sy = SY + g * RW;                    // sy[stream_at(v)] = scan Y (v)
   float mu = 0.f;
   if constexpr (kOffset) {
     float sum = 0.f;
@@ -392,8 +427,18 @@ __global__ __launch_bounds__(LG * NG) void k_box_fwd_stream(const T* __restrict_
   const Taps<float> tp = load_taps(taps + (size_t)(c * B + (live ? b : 0)) * 16, W, H);
   const int fa = tp.ox[0], fb = tp.ox[2], fc = tp.oy[0], fd = tp.oy[2];
   const float aa = -tp.wx[1], ab = tp.wx[3], bc_ = -tp.wy[1], bd = tp.wy[3];
-  const int ra0 = clampi(x0 + fa, -PAD, W), rb0 = clampi(x0 + fb, -PAD, W);
-  for (int t = p; t <= PAD; t += LG) sy[-PAD + t] = (T)0;
+  int ia[CPL + 1], ib[CPL + 1], iw[CPL];
+  {
+    const int ra0 = clampi(x0 + fa, -PAD, W), rb0 = clampi(x0 + fb, -PAD, W);
+#pragma unroll
+    for (int k = 0; k <= CPL; ++k) {
+      ia[k] = stream_at<CPL>(ra0 + k);
+      ib[k] = stream_at<CPL>(rb0 + k);
+    }
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) iw[k] = stream_at<CPL>(x0 + k + 1);
+  }
+  for (int t = p; t <= PAD; t += LG) sy[stream_at<CPL>(-PAD + t)] = (T)0;
   T pc[CPL], pd[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) { pc[k] = (T)0; pd[k] = (T)0; }
@@ -451,15 +496,15 @@ __global__ __launch_bounds__(LG * NG) void k_box_fwd_stream(const T* __restrict_
     const T tot = s[CPL - 1];
     const T off = group_scan<LG, false>(tot) - tot;
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) sy[x0 + k + 1] = s[k] + off;
+    for (int k = 0; k < CPL; ++k) sy[iw[k]] = s[k] + off;
     if (p == LG - 1) {
 #pragma unroll
-      for (int t = 1; t <= PAD; ++t) sy[LC + t] = s[CPL - 1] + off;
+      for (int t = 1; t <= PAD; ++t) sy[stream_at<CPL>(LC + t)] = s[CPL - 1] + off;
     }
     __builtin_amdgcn_wave_barrier();
     T sa[CPL + 1], sb[CPL + 1];
 #pragma unroll
-    for (int k = 0; k <= CPL; ++k) { sa[k] = sy[ra0 + k]; sb[k] = sy[rb0 + k]; }
+    for (int k = 0; k <= CPL; ++k) { sa[k] = sy[ia[k]]; sb[k] = sy[ib[k]]; }
     float ey = 0.f;
     if constexpr (kOffset) {
       const int yc = yy + fc, yd = yy + fd;
@@ -545,7 +590,7 @@ static bool stream_geom(int H, int W, int B, StreamGeom& g) {
   g.ng = B <= 4 ? 4 : 8;
   // per-lane 32-bit byte offsets into a block's gradient maps
   if ((size_t)g.ng * H * W * 4 >= ((size_t)1 << 31)) return false;
-  const size_t slot_set = (size_t)g.ng * g.lg * g.cpl * 4;
+  const size_t slot_set = (size_t)g.ng * (g.lg * g.cpl + g.lg * g.cpl / 32) * 4;
   g.R = (int)std::max<size_t>(1, std::min<size_t>(8, (2u << 10) / slot_set));
   return true;
 }
@@ -563,7 +608,7 @@ template <int LG, int CPL, int NG>
 static void bwd_stream_t(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N, int C,
                          int H, int W, int B, bool rounded, bool relu_bf16, int R, hipStream_t s) {
   constexpr int RW = stream_row_words<LG, CPL>();
-  const size_t shm = ((size_t)2 * NG * RW + (size_t)2 * R * NG * LG * CPL) * sizeof(float);
+  const size_t shm = ((size_t)2 * NG * RW + (size_t)2 * R * NG * slot_words<LG, CPL>()) * sizeof(float);
   const dim3 grid(N * C), block(LG * NG);
   auto go = [&](auto ki, auto kr, auto kv) {
     hipLaunchKernelGGL((k_box_bwd_stream<LG, CPL, NG, decltype(ki)::value, decltype(kr)::value, decltype(kv)::value>),
