@@ -66,6 +66,10 @@ typedef enum {
   BC_MIX_BWD_WEIGHT = 2   /* out    = sum_n grad[n] * in[n]^T            */
 } bc_mix_mode;
 
+/* Arguments that select a dtype or a mix mode are plain ints holding one of
+   the enumerators above; any other value is rejected (BC_ERR_DTYPE,
+   BC_ERR_UNSUPPORTED, or a zero workspace size), never undefined. */
+
 /* Flags of box_conv_fwd / box_conv_bwd. */
 #define BC_FLAG_MEAN_OFFSET 1u   /* fp32 only: build the table of (map - mean of
                                     the map) and add mean * (clipped box area)
@@ -126,7 +130,7 @@ bc_status box_prep(const float* boxes, int C, int B, unsigned flags, void* table
  *          each map's mean there and tabulates (x - mean) instead of x.
  * Limits : 1 <= W <= 1024.
  * ---------------------------------------------------------------------- */
-bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
+bc_status sat_build(const void* x, int dt, void* sat, float* mean,
                     int N, int C, int H, int W, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -144,13 +148,18 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean,
  *          BC_FLAG_INTEGER_CORNERS (the box with rounded corners: the
  *          four-sample sum of Eq. 2, exact int32 for BC_I32 maps).
  * ws     : >= bc_box_workspace_bytes(0, ...) bytes: the tap records of
- *          box_prep (2*C*B*64 bytes), plus the maps' tables when a table does
- *          not fit in LDS ((H + 1) * ((W + 7) | 1) * 4 > 80 KiB) or
- *          BC_FLAG_FORCE_HBM is set.
+ *          box_prep (2*C*B*64 bytes), plus the maps' tables on the HBM path.
+ * Paths  : a map whose table fits in LDS ((H + 1) * ((W + 7) | 1) * 4 <=
+ *          80 KiB) has it built there, once per map and block; a larger map
+ *          up to 256 wide with B <= 8 is evaluated by the streaming kernels,
+ *          which keep each box's two table rows per y edge as running column
+ *          sums and scan one row per output row (no stored table, no extra
+ *          workspace); otherwise (or with BC_FLAG_FORCE_HBM) the tables are
+ *          built in HBM by sat_build and gathered (W <= 1024).
  * ---------------------------------------------------------------------- */
-bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
+bc_status box_conv_fwd(const void* x, int x_dt, const float* boxes,
                        int N, int C, int H, int W, int B,
-                       void* y, bc_dtype y_dt, unsigned flags,
+                       void* y, int y_dt, unsigned flags,
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -176,11 +185,13 @@ bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes,
  *              fixed-order (deterministic) reduction.
  * ws         : >= bc_box_workspace_bytes(1, ...) bytes: the tap records,
  *              the per-wave partial edge gradients, and with the HBM path
- *              the tables of all N*C*B gradient maps.  The HBM path is taken
- *              with BC_FLAG_FORCE_HBM, or when a map's table exceeds 80 KiB
- *              ((H + 1) * ((W + 7) | 1) * 4 bytes) or the map has more than
- *              1024 work items of 3 columns x 4 rows (one block per map in
- *              LDS otherwise); it needs W <= 1024 (BC_ERR_SHAPE otherwise).
+ *              the tables of all N*C*B gradient maps.  The table is built in
+ *              LDS when it takes at most 80 KiB ((H + 1) * ((W + 7) | 1) * 4
+ *              bytes) and the map has at most 1024 work items of 3 columns x
+ *              4 rows; otherwise maps up to 256 wide with B <= 8 take the
+ *              streaming kernels (no tables), and the rest (or any call with
+ *              BC_FLAG_FORCE_HBM) the HBM tables, which need W <= 1024
+ *              (BC_ERR_SHAPE otherwise).
  * ---------------------------------------------------------------------- */
 bc_status box_conv_bwd(const float* x, const float* boxes, const float* grad_y,
                        int N, int C, int H, int W, int B,
@@ -215,12 +226,13 @@ bc_status box_conv_bwd_relu_bf16(const float* x, const float* boxes, const float
  *            (the backward tabulates grad_y placed at every stride-th pixel,
  *            zeros elsewhere: the transpose of the sampling).
  * stride : 1 .. 1024 (BC_ERR_SHAPE otherwise); stride 1 is box_conv_fwd /
- *          box_conv_bwd.  Every other argument, flag and workspace size is
- *          as for those calls (the workspace query takes the input size).
+ *          box_conv_bwd.  Every other argument and flag is as for those
+ *          calls; the workspace is bc_box_workspace_bytes_strided(..., stride,
+ *          flags), which takes the input size.
  * ---------------------------------------------------------------------- */
-bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes,
+bc_status box_conv_fwd_strided(const void* x, int x_dt, const float* boxes,
                                int N, int C, int H, int W, int B, int stride,
-                               void* y, bc_dtype y_dt, unsigned flags,
+                               void* y, int y_dt, unsigned flags,
                                void* ws, size_t ws_bytes, hipStream_t stream);
 bc_status box_conv_bwd_strided(const float* x, const float* boxes, const float* grad_y,
                                int N, int C, int H, int W, int B, int stride,
@@ -292,7 +304,7 @@ bc_status box_params_clip(float* u, int C, int B, hipStream_t stream);
 #define BC_SPLIT_FORCE_HBM 0x100
 bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* piece_w,
                              int N, int C, int H, int W, int B, int mode,
-                             void* y, bc_dtype y_dt, void* ws, size_t ws_bytes, hipStream_t stream);
+                             void* y, int y_dt, void* ws, size_t ws_bytes, hipStream_t stream);
 bc_status box_conv_split_bwd(const float* x, const float* boxes, const float* piece_w,
                              const float* grad_y, int N, int C, int H, int W, int B, int mode,
                              float* grad_x, float* grad_boxes, float* grad_w,
@@ -319,9 +331,9 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
  * accumulate : BWD_WEIGHT only: 1 = out += result.
  * ws         : >= bc_mix_workspace_bytes(mode, ...) bytes.
  * ---------------------------------------------------------------------- */
-bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt,
-                        const void* b, bc_dtype b_dt, void* out, bc_dtype out_dt,
-                        int N, int M, int K, int P, bc_dtype compute_dt,
+bc_status pointwise_mix(int mode, const void* a, int a_dt,
+                        const void* b, int b_dt, void* out, int out_dt,
+                        int N, int M, int K, int P, int compute_dt,
                         int relu, const float* aux, int accumulate,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -378,12 +390,16 @@ bc_status box_conv_bwd_noalloc(const float* x, const float* boxes, const float* 
                                hipStream_t stream);
 size_t bc_noalloc_scratch_bytes(void);
 
-/* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd. */
+/* Workspace sizes in bytes.  op: 0 = box_conv_fwd, 1 = box_conv_bwd (and
+ * box_conv_bwd_relu_bf16); the _strided form for the strided entry points
+ * (stride 1 is the plain query).  0 for sizes the calls reject. */
 size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags);
-size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt);
+size_t bc_box_workspace_bytes_strided(int op, int N, int C, int H, int W, int B, int stride,
+                                      unsigned flags);
+size_t bc_mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt);
 
 /* Human-readable status; never NULL. */
-const char* bc_status_string(bc_status s);
+const char* bc_status_string(int status);
 
 /* ABI version of this library (incremented on incompatible changes). */
 int bc_abi_version(void);

@@ -47,6 +47,7 @@ SIGNATURES = {
     "box_conv_split_bwd": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _sz, _vp]),
     "bc_split_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
     "bc_box_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _u]),
+    "bc_box_workspace_bytes_strided": (_sz, [_i, _i, _i, _i, _i, _i, _i, _u]),
     "bc_mix_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "bc_cast_bf16": (_i, [_vp, _vp, _sz, _vp]),
     "bc_relu_grad_bf16": (_i, [_vp, _vp, _vp, _sz, _vp]),
@@ -157,8 +158,8 @@ def _workspace(nbytes: int, device) -> torch.Tensor | None:
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
-def box_workspace_bytes(op: int, N, C, H, W, B, flags=0) -> int:
-    return int(load_library().bc_box_workspace_bytes(op, N, C, H, W, B, flags))
+def box_workspace_bytes(op: int, N, C, H, W, B, flags=0, stride: int = 1) -> int:
+    return int(load_library().bc_box_workspace_bytes_strided(op, N, C, H, W, B, stride, flags))
 
 
 def mix_workspace_bytes(mode: int, N, M, K, P, compute_dt) -> int:
@@ -199,7 +200,7 @@ def box_conv_fwd(x: torch.Tensor, boxes: torch.Tensor, y: torch.Tensor, flags: i
     _need(y, _strided_shape(N, C, H, W, B, stride),
           torch.int32 if x.dtype == torch.int32 else (torch.float32, torch.bfloat16), "box_conv_fwd", "y")
     if ws is None:
-        ws = _workspace(box_workspace_bytes(0, N, C, H, W, B, flags), x.device)
+        ws = _workspace(box_workspace_bytes(0, N, C, H, W, B, flags, stride), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     lib = load_library()
     if stride == 1:
@@ -225,7 +226,7 @@ def box_conv_bwd(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.Tensor, gra
     _need(grad_x, (N, C, H, W), _F32, "box_conv_bwd", "grad_x")
     _need(grad_boxes, (C, B, 4), _F32, "box_conv_bwd", "grad_boxes")
     if ws is None:
-        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
+        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags, stride), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     lib = load_library()
     if stride == 1:
@@ -250,7 +251,7 @@ def box_conv_bwd_relu_bf16(x: torch.Tensor, boxes: torch.Tensor, grad_y: torch.T
     _need(grad_x_bf16, (N, C, H, W), torch.bfloat16, what, "grad_x")
     _need(grad_boxes, (C, B, 4), _F32, what, "grad_boxes")
     if ws is None:
-        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags), x.device)
+        ws = _workspace(box_workspace_bytes(1, N, C, H, W, B, flags, stride), x.device)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(load_library().box_conv_bwd_relu_bf16(_ptr(x), _ptr(boxes), _ptr(grad_y), N, C, H, W, B, stride,
                                                  _ptr(grad_x_bf16), _ptr(grad_boxes), flags, _ptr(ws), nbytes,

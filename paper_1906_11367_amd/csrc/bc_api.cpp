@@ -107,8 +107,8 @@ extern "C" {
 
 int bc_abi_version(void) { return 2; }
 
-const char* bc_status_string(bc_status s) {
-  switch (s) {
+const char* bc_status_string(int status) {
+  switch (status) {
     case BC_OK: return "ok";
     case BC_ERR_NULL: return "a required pointer is NULL";
     case BC_ERR_SHAPE: return "invalid or unsupported shape";
@@ -129,7 +129,7 @@ bc_status box_prep(const float* boxes, int C, int B, unsigned flags, void* table
   return hip_status(bc::launch_box_prep(boxes, C, B, (flags & BC_FLAG_INTEGER_CORNERS) != 0, table, stream));
 }
 
-bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean, int N, int C, int H, int W,
+bc_status sat_build(const void* x, int dt, void* sat, float* mean, int N, int C, int H, int W,
                     hipStream_t stream) {
   if (!x || !sat) return BC_ERR_NULL;
   if (!dims_ok(N, C, H, W, 1) || W > 1024) return BC_ERR_SHAPE;
@@ -139,33 +139,19 @@ bc_status sat_build(const void* x, bc_dtype dt, void* sat, float* mean, int N, i
   return hip_status(bc::launch_sat_build(x, dt == BC_I32, sat, mean, N * C, H, W, stream));
 }
 
-size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags) {
-  if (!dims_ok(N, C, H, W, B)) return 0;
-  // the workspace of the stride-1 call; a strided call never takes the
-  // streaming kernels, so it asks for the largest of the layouts
-  if (op == 0) {
-    const BoxPath path = box_path(false, H, W, B, flags, 1);
-    size_t n = fwd_ws(N, C, H, W, B, path).total;
-    if (path == BoxPath::Stream) {
-      const BoxPath alt = (flags & BC_FLAG_FORCE_HBM) || !fwd_lds_fits(H, W) ? BoxPath::Hbm : BoxPath::Lds;
-      n = std::max(n, fwd_ws(N, C, H, W, B, alt).total);
-    }
-    return n;
-  }
-  if (op == 1) {
-    const BoxPath path = box_path(true, H, W, B, flags, 1);
-    size_t n = bwd_ws(N, C, H, W, B, path).total;
-    if (path == BoxPath::Stream) {
-      const BoxPath alt = (flags & BC_FLAG_FORCE_HBM) || !bwd_lds_fits(H, W) ? BoxPath::Hbm : BoxPath::Lds;
-      n = std::max(n, bwd_ws(N, C, H, W, B, alt).total);
-    }
-    return n;
-  }
+size_t bc_box_workspace_bytes_strided(int op, int N, int C, int H, int W, int B, int stride, unsigned flags) {
+  if (!dims_ok(N, C, H, W, B) || stride < 1 || stride > kMaxStride) return 0;
+  if (op == 0) return fwd_ws(N, C, H, W, B, box_path(false, H, W, B, flags, stride)).total;
+  if (op == 1) return bwd_ws(N, C, H, W, B, box_path(true, H, W, B, flags, stride)).total;
   return 0;
 }
 
-bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
-                               int stride, void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes,
+size_t bc_box_workspace_bytes(int op, int N, int C, int H, int W, int B, unsigned flags) {
+  return bc_box_workspace_bytes_strided(op, N, C, H, W, B, 1, flags);
+}
+
+bc_status box_conv_fwd_strided(const void* x, int x_dt, const float* boxes, int N, int C, int H, int W, int B,
+                               int stride, void* y, int y_dt, unsigned flags, void* ws, size_t ws_bytes,
                                hipStream_t stream) {
   if (!x || !boxes || !y) return BC_ERR_NULL;
   if (!dims_ok(N, C, H, W, B) || stride < 1 || stride > kMaxStride) return BC_ERR_SHAPE;
@@ -201,8 +187,8 @@ bc_status box_conv_fwd_strided(const void* x, bc_dtype x_dt, const float* boxes,
                                               stride, stream));
 }
 
-bc_status box_conv_fwd(const void* x, bc_dtype x_dt, const float* boxes, int N, int C, int H, int W, int B,
-                       void* y, bc_dtype y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+bc_status box_conv_fwd(const void* x, int x_dt, const float* boxes, int N, int C, int H, int W, int B,
+                       void* y, int y_dt, unsigned flags, void* ws, size_t ws_bytes, hipStream_t stream) {
   return box_conv_fwd_strided(x, x_dt, boxes, N, C, H, W, B, 1, y, y_dt, flags, ws, ws_bytes, stream);
 }
 
@@ -327,7 +313,7 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
 }
 
 bc_status box_conv_split_fwd(const float* x, const float* boxes, const float* piece_w, int N, int C, int H, int W,
-                             int B, int mode, void* y, bc_dtype y_dt, void* ws, size_t ws_bytes,
+                             int B, int mode, void* y, int y_dt, void* ws, size_t ws_bytes,
                              hipStream_t stream) {
   if (!x || !boxes || !piece_w || !y) return BC_ERR_NULL;
   if (!split_dims_ok(N, C, H, W, B)) return BC_ERR_SHAPE;
@@ -428,20 +414,25 @@ bc_status bc_relu_grad_bf16(const float* grad, const float* out, void* dst, size
   return hip_status(bc::launch_relu_cast_bf16(grad, out, dst, n, stream));
 }
 
-size_t bc_mix_workspace_bytes(bc_mix_mode mode, int N, int M, int K, int P, bc_dtype compute_dt) {
-  if (N <= 0 || M <= 0 || K <= 0 || P <= 0) return 0;
+// The sizes pointwise_mix accepts (the workspace query answers 0 for others).
+static bool mix_dims_ok(int N, int M, int K, int P) {
+  if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || N > kMaxDim || M > kMaxDim || K > kMaxDim) return false;
+  return (long)K * P <= (1L << 30) && (long)M * P <= (1L << 30) && (long)M * K <= (1L << 30);
+}
+
+size_t bc_mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt) {
+  if (!mix_dims_ok(N, M, K, P)) return 0;
   return bc::mix_workspace_bytes((int)mode, N, M, K, P, (int)compute_dt);
 }
 
-bc_status pointwise_mix(bc_mix_mode mode, const void* a, bc_dtype a_dt, const void* b, bc_dtype b_dt, void* out,
-                        bc_dtype out_dt, int N, int M, int K, int P, bc_dtype compute_dt, int relu, const float* aux,
+bc_status pointwise_mix(int mode, const void* a, int a_dt, const void* b, int b_dt, void* out,
+                        int out_dt, int N, int M, int K, int P, int compute_dt, int relu, const float* aux,
                         int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!a || !b || !out) return BC_ERR_NULL;
   if (mode != BC_MIX_FWD && mode != BC_MIX_BWD_DATA && mode != BC_MIX_BWD_WEIGHT) return BC_ERR_UNSUPPORTED;
-  if (N <= 0 || M <= 0 || K <= 0 || P <= 0 || N > kMaxDim || M > kMaxDim || K > kMaxDim) return BC_ERR_SHAPE;
-  if ((long)K * P > (1L << 30) || (long)M * P > (1L << 30) || (long)M * K > (1L << 30)) return BC_ERR_SHAPE;
+  if (!mix_dims_ok(N, M, K, P)) return BC_ERR_SHAPE;
   if (compute_dt != BC_F32 && compute_dt != BC_BF16) return BC_ERR_DTYPE;
-  for (bc_dtype d : {a_dt, b_dt}) {
+  for (int d : {a_dt, b_dt}) {
     if (d != BC_I32 && d != BC_F32 && d != BC_BF16) return BC_ERR_DTYPE;
     if (d == BC_BF16 && compute_dt != BC_BF16) return BC_ERR_DTYPE;
     if (d == BC_I32 && compute_dt != BC_F32) return BC_ERR_DTYPE;

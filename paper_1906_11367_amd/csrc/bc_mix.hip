@@ -11,6 +11,8 @@
 // v_mfma_f32_32x32x16_bf16 (bf16 operands) or v_mfma_f32_32x32x2_f32.
 #include "bc_common.hpp"
 #include "bc_internal.hpp"
+
+#include <algorithm>
 #include <type_traits>
 
 namespace bc {
@@ -598,9 +600,9 @@ struct WeightSplit { int sp, chunk, S; };
 
 static WeightSplit weight_split(int N, int M, int K, int P, bool bf16) {
   const int BK = bf16 ? 64 : 32;
-  const int tiles = ((M + kBM - 1) / kBM) * ((K + kBN - 1) / kBN);
+  const long tiles = (long)((M + kBM - 1) / kBM) * ((K + kBN - 1) / kBN);
   const int max_sp = (P + BK - 1) / BK;
-  int sp = (512 + tiles * N - 1) / (tiles * N);
+  int sp = (int)std::min<long>(512, (512 + tiles * N - 1) / (tiles * N));
   if (sp < 1) sp = 1;
   if (sp > max_sp) sp = max_sp;
   int chunk = (P + sp - 1) / sp;

@@ -86,7 +86,7 @@ class LayerPlan:
             self.pieces = bc.SPLIT_PIECES[bc.SPLIT_MODES[self.split]]
             self.ws_fwd = _ws(bc.split_workspace_bytes(0, N, C, H, W, B, self.split), dev)
         else:
-            self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags), dev)
+            self.ws_fwd = _ws(bc.box_workspace_bytes(0, N, C, H, W, B, self.flags, self.stride), dev)
         if self.unit_size is not None:
             self.boxes_px = torch.empty((C, B, 4), dtype=torch.float32, device=dev)
         if self.M is not None:
@@ -99,7 +99,7 @@ class LayerPlan:
                 self.ws_bwd = _ws(bc.split_workspace_bytes(1, N, C, H, W, B, self.split), dev)
                 self.dpiece = torch.empty((C, B, self.pieces), dtype=torch.float32, device=dev)
             else:
-                self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags), dev)
+                self.ws_bwd = _ws(bc.box_workspace_bytes(1, N, C, H, W, B, self.flags, self.stride), dev)
             self.dx = torch.empty((N, C, H, W), dtype=torch.bfloat16 if self.dx_relu_bf16 else torch.float32,
                                   device=dev)
             self.dboxes = torch.empty((C, B, 4), dtype=torch.float32, device=dev)

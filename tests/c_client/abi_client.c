@@ -71,6 +71,41 @@ static int check(void) {
   EXPECT(box_params_clip(NULL, 1, 1, NULL) == BC_ERR_NULL);
   EXPECT(pointwise_mix((bc_mix_mode)9, fake, BC_F32, fake, BC_F32, fake, BC_F32, 1, 8, 8, 8, BC_F32, 0, NULL, 0,
                        NULL, 0, NULL) == BC_ERR_UNSUPPORTED);
+  /* sizes at and beyond the limits: the queries answer 0 and the calls
+     refuse, with no arithmetic overflow on the way */
+  EXPECT(bc_box_workspace_bytes(0, 1 << 16, 1 << 16, 1 << 16, 1 << 16, 1 << 16, 0) == 0);
+  EXPECT(bc_box_workspace_bytes(1, 1, 1, 1 << 15, 1 << 15, 1, 0) > 0);
+  EXPECT(bc_box_workspace_bytes(1, 2147483647, 1, 8, 8, 1, 0) == 0);
+  EXPECT(bc_box_workspace_bytes(0, -1, 1, 8, 8, 1, 0) == 0);
+  EXPECT(bc_box_workspace_bytes(2, 1, 1, 8, 8, 1, 0) == 0);
+  EXPECT(bc_mix_workspace_bytes(BC_MIX_BWD_WEIGHT, 1 << 16, 1 << 16, 1 << 16, 1 << 16, BC_BF16) >= 0);
+  EXPECT(box_conv_fwd(fake, BC_F32, fake, 2147483647, 2147483647, 8, 8, 1, fake, BC_F32, 0, fake, 1, NULL) ==
+         BC_ERR_SHAPE);
+  EXPECT(box_conv_bwd(fake, fake, fake, 1, 1, 1 << 16, 1 << 16, 1, fake, fake, 0, fake, 1, NULL) == BC_ERR_SHAPE);
+  EXPECT(pointwise_mix(BC_MIX_FWD, fake, BC_F32, fake, BC_F32, fake, BC_F32, 1, 1 << 16, 1 << 16, 1 << 20, BC_F32,
+                       0, NULL, 0, NULL, 0, NULL) == BC_ERR_SHAPE);
+  EXPECT(pointwise_mix(BC_MIX_FWD, fake, BC_I32, fake, BC_F32, fake, BC_F32, 1, 8, 8, 8, BC_F32, 0, NULL, 0, NULL,
+                       0, NULL) == BC_ERR_DTYPE);
+  EXPECT(box_prep(fake, 1 << 15, 1 << 15, 0, fake, NULL) == BC_ERR_SHAPE);
+  EXPECT(box_prep(fake, 4, 4, 1u << 9, fake, NULL) == BC_ERR_UNSUPPORTED);
+  EXPECT(sat_build(fake, BC_BF16, fake, NULL, 1, 1, 8, 8, NULL) == BC_ERR_DTYPE);
+  EXPECT(sat_build(fake, BC_I32, fake, fake, 1, 1, 8, 8, NULL) == BC_ERR_DTYPE);
+  EXPECT(box_params_from_unit(fake, 4, 4, 0.f, 8.f, fake, NULL) == BC_ERR_SHAPE);
+  EXPECT(box_params_unit_grad(fake, 4, 4, 8.f, 1e9f, fake, NULL) == BC_ERR_SHAPE);
+  EXPECT(bc_cast_bf16(fake, fake_mis, 8, NULL) == BC_ERR_ALIGN);
+  EXPECT(box_conv_split_bwd(fake, fake, fake, fake, 1, 1, 8, 8, 1, BC_SPLIT_2X, NULL, NULL, NULL, NULL, 0, NULL) ==
+         BC_OK);
+  EXPECT(box_conv_bwd_strided(fake, fake, fake, 1, 1, 8, 8, 1, 2000, fake, NULL, 0, NULL, 0, NULL) == BC_ERR_SHAPE);
+  /* 256 x 256 maps: the streaming backward needs no table workspace, but a
+     caller may still force the HBM tables */
+  EXPECT(bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, BC_FLAG_FORCE_HBM) >
+         bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0));
+  /* the allocation-free backward refuses a workspace beyond its array before
+     touching the device */
+  EXPECT(bc_noalloc_scratch_bytes() == BC_NOALLOC_SCRATCH_BYTES);
+  EXPECT(box_conv_bwd_noalloc(fake, fake, fake, 4, 128, 256, 256, 8, fake, fake, BC_FLAG_FORCE_HBM, NULL) ==
+         BC_ERR_WORKSPACE);
+  EXPECT(box_conv_bwd_noalloc(fake, fake, fake, 0, 1, 8, 8, 1, fake, fake, 0, NULL) == BC_ERR_SHAPE);
   return failures;
 }
 

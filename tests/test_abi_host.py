@@ -26,7 +26,7 @@ def declared_functions():
 def test_header_declares_the_four_entry_points():
     names = declared_functions()
     for n in ("sat_build", "box_conv_fwd", "box_conv_bwd", "pointwise_mix", "box_prep",
-              "bc_box_workspace_bytes", "bc_mix_workspace_bytes", "bc_status_string", "bc_abi_version",
+              "bc_box_workspace_bytes", "bc_box_workspace_bytes_strided", "bc_mix_workspace_bytes", "bc_status_string", "bc_abi_version",
               "box_conv_split_fwd", "box_conv_split_bwd", "bc_split_workspace_bytes"):
         assert n in names, n
 
@@ -252,11 +252,22 @@ def test_workspace_queries():
     taps = 2 * 256 * 4 * 64
     assert lib.bc_box_workspace_bytes(0, 32, 256, 64, 48, 4, 0) == taps
     assert lib.bc_box_workspace_bytes(1, 32, 256, 64, 48, 4, 0) >= taps + 32 * 256 * 4 * 16
-    # forced HBM path and 256x256 maps need tables in the workspace
-    big = lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, 0)
-    assert big >= 4 * 128 * 257 * 257 * 4
+    # 256x256 maps take the streaming kernels: tap records plus one row of
+    # edge-gradient partials per image, no tables
+    assert lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, 0) == 2 * 128 * 8 * 64
+    stream_bwd = lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0)
+    assert 2 * 128 * 8 * 64 < stream_bwd < 1 << 20
+    # the forced HBM path needs the tables in the workspace
+    assert lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, bc.BC_FLAG_FORCE_HBM) >= 4 * 128 * 257 * 257 * 4
     assert lib.bc_box_workspace_bytes(0, 2, 3, 8, 8, 4, bc.BC_FLAG_FORCE_HBM) >= 2 * 3 * 81 * 4
-    assert lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0) >= 4 * 128 * 8 * 257 * 257 * 4
+    assert lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, bc.BC_FLAG_FORCE_HBM) >= 4 * 128 * 8 * 257 * 257 * 4
+    # maps wider than the streaming kernels take (W > 256) need HBM tables
+    assert lib.bc_box_workspace_bytes(0, 1, 4, 128, 300, 4, 0) >= 4 * 129 * 301 * 4
+    # the strided query prices the path the strided call takes; stride 1 is the plain query
+    for op in (0, 1):
+        assert (lib.bc_box_workspace_bytes_strided(op, 4, 128, 256, 256, 8, 1, 0)
+                == lib.bc_box_workspace_bytes(op, 4, 128, 256, 256, 8, 0))
+    assert lib.bc_box_workspace_bytes_strided(0, 4, 128, 256, 256, 8, 0, 0) == 0
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_FWD, 32, 256, 1024, 3072, bc.BC_BF16) == 0
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, 32, 256, 1024, 3072, bc.BC_BF16) > 0
 
@@ -266,8 +277,9 @@ def test_noalloc_backward_rejects_oversized_request_before_any_launch():
     array first: 256 x 256 maps (tables in HBM) are rejected on the host."""
     lib = bc.load_library()
     assert lib.bc_noalloc_scratch_bytes() == 16 << 20
-    need = lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, 0)
+    F = bc.BC_FLAG_FORCE_HBM
+    need = lib.bc_box_workspace_bytes(1, 4, 128, 256, 256, 8, F)
     assert need > lib.bc_noalloc_scratch_bytes()
-    assert lib.box_conv_bwd_noalloc(FAKE, FAKE, FAKE, 4, 128, 256, 256, 8, FAKE, FAKE, 0, None) == 5
+    assert lib.box_conv_bwd_noalloc(FAKE, FAKE, FAKE, 4, 128, 256, 256, 8, FAKE, FAKE, F, None) == 5
     # invalid sizes are reported as such
     assert lib.box_conv_bwd_noalloc(FAKE, FAKE, FAKE, 0, 128, 64, 48, 4, FAKE, FAKE, 0, None) == 2

@@ -36,7 +36,9 @@ def _case(rng, N, C, H, W, B):
 def test_noalloc_backward_matches_allocating_backward():
     rng = np.random.default_rng(300)
     assert bc.noalloc_scratch_bytes() == 16 << 20
-    for shape in [(8, 64, 64, 48, 4), (2, 5, 37, 29, 3)]:
+    # maps whose table fits in LDS, then 200 x 256 maps (streaming kernels,
+    # no table in the workspace), then a small ragged case
+    for shape in [(8, 64, 64, 48, 4), (1, 8, 200, 256, 8), (2, 5, 37, 29, 3)]:
         N, C, H, W, B = shape
         say(f"noalloc backward {shape}")
         x, g, bx = _case(rng, *shape)
@@ -65,10 +67,10 @@ def test_noalloc_backward_matches_allocating_backward():
 
 
 def test_noalloc_backward_rejects_oversized_requests():
-    # 256 x 256 maps need their gradient tables in HBM: far beyond the array
+    # 256 x 256 maps with their gradient tables forced into HBM: far beyond the array
     N, C, H, W, B = 4, 128, 256, 256, 8
-    assert bc.box_workspace_bytes(1, N, C, H, W, B) > bc.noalloc_scratch_bytes()
+    assert bc.box_workspace_bytes(1, N, C, H, W, B, bc.BC_FLAG_FORCE_HBM) > bc.noalloc_scratch_bytes()
     x = torch.zeros((1, C, 8, 8), dtype=torch.float32, device="cuda")   # never read: rejected first
     st = bc.load_library().box_conv_bwd_noalloc(bc._ptr(x), bc._ptr(x), bc._ptr(x), N, C, H, W, B,
-                                                bc._ptr(x), None, 0, bc._stream())
+                                                bc._ptr(x), None, bc.BC_FLAG_FORCE_HBM, bc._stream())
     assert st == 5   # BC_ERR_WORKSPACE
