@@ -36,6 +36,18 @@
  *     errors return before anything is launched.  A failed launch returns
  *     BC_ERR_HIP.  Faults during execution surface at the caller's sync.
  *   - Outputs are overwritten (pointwise_mix with accumulate = 1 excepted).
+ *   - Non-finite values are not looked for; they spread as the integral image
+ *     spreads them.  A NaN or infinity at pixel (i, j) of a map makes every
+ *     table entry below and to the right of it non-finite.  Of that map's
+ *     outputs, every one whose box covers (i, j) is non-finite, every one whose
+ *     box ends above row i or left of column j is finite and exact, and the
+ *     ones in between (below and right of the pixel without covering it) may be
+ *     either; other maps are untouched.  With BC_FLAG_MEAN_OFFSET the map's
+ *     mean is non-finite too and so is every output of that map.  The
+ *     backward follows the same rule through the mirrored boxes; the edge
+ *     gradients of a box are non-finite when its input map or its gradient
+ *     map holds such a value.  Inputs outside the bf16 or fp32 range are not
+ *     clamped.
  */
 #ifndef BOXCONV_H
 #define BOXCONV_H

@@ -636,7 +636,7 @@ __global__ __launch_bounds__(256 * kGroups) void k_sat_build(const T* __restrict
             v[i][k] = run;
           }
         }
-        const T excl = wave_incl_scan(run, lane) - run;
+        const T excl = wave_excl_scan(run, lane);
         if (rr < rows) {
 #pragma unroll
           for (int k = 0; k < KM; ++k) {

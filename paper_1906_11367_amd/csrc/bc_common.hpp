@@ -333,4 +333,14 @@ __device__ __forceinline__ T wave_incl_scan(T v, int lane) {
   return v;
 }
 
+// Wave-level exclusive prefix sum: the inclusive sum of the lane before (0 in
+// lane 0), so a lane's value never enters its own prefix (a NaN or infinity in
+// it leaves the prefix exact).
+template <typename T>
+__device__ __forceinline__ T wave_excl_scan(T v, int lane) {
+  const T incl = wave_incl_scan(v, lane);
+  const T prev = __shfl_up(incl, 1, 64);
+  return lane ? prev : (T)0;
+}
+
 }  // namespace bc

@@ -83,6 +83,20 @@ __device__ __forceinline__ T group_scan(T v) {
   return v;
 }
 
+// Exclusive form of group_scan: the inclusive scan moved one lane along the
+// scan direction (lane 0 of the group, or its last lane when reversed, gets 0
+// from bound_ctrl).  Taking the neighbour's inclusive value, rather than
+// subtracting the lane's own value from its inclusive scan, keeps a lane's
+// earlier columns exact when a later column holds a NaN or an infinity, and
+// costs the same one instruction.
+template <int LG, bool kRev, typename T>
+__device__ __forceinline__ T group_excl(T v) {
+  const T incl = group_scan<LG, kRev>(v);
+  constexpr int ctrl = kRev ? (LG == 16 ? 0x101 : 0x130)    // row_shl:1 / wave_shl:1
+                            : (LG == 16 ? 0x111 : 0x138);   // row_shr:1 / wave_shr:1
+  return of_bits<T>(__builtin_amdgcn_update_dpp(0, bits_of(incl), ctrl, 0xF, 0xF, true));
+}
+
 // Sum over the lanes of a group, in every lane of the group.
 template <int LG>
 __device__ __forceinline__ float group_sum(float v) {
@@ -278,7 +292,7 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
       pd[k] += gd_[k];
     }
     const float tot = s[CPL - 1];
-    const float off = group_scan<LG, false>(tot) - tot;
+    const float off = group_excl<LG, false>(tot);
 #pragma unroll
     for (int k = 0; k < CPL; ++k) sy[iw[k]] = s[k] + off;
     if (p == LG - 1) {
@@ -291,7 +305,7 @@ __global__ __launch_bounds__(LG * NG) void k_box_bwd_stream(const float* __restr
 #pragma unroll
       for (int k = CPL - 1; k >= 0; --k) sfx[k] = k < CPL - 1 ? sfx[k + 1] + v[k] : v[k];
       const float vt = sfx[0];
-      const float voff = group_scan<LG, true>(vt) - vt;
+      const float voff = group_excl<LG, true>(vt);
 #pragma unroll
       for (int k = 0; k < CPL; ++k) sv[jw[k]] = sfx[k] + voff;
       if (p == 0) {
@@ -494,7 +508,7 @@ __global__ __launch_bounds__(LG * NG) void k_box_fwd_stream(const T* __restrict_
       pd[k] += gd_[k];
     }
     const T tot = s[CPL - 1];
-    const T off = group_scan<LG, false>(tot) - tot;
+    const T off = group_excl<LG, false>(tot);
 #pragma unroll
     for (int k = 0; k < CPL; ++k) sy[iw[k]] = s[k] + off;
     if (p == LG - 1) {

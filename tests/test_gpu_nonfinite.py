@@ -112,7 +112,9 @@ def _check_rest(got, want, touched, what):
 SHAPES = [
     ((2, 3, 40, 36, 4), 0),                        # table in LDS
     ((2, 3, 40, 36, 4), bc.BC_FLAG_FORCE_HBM),     # table in HBM
-    ((1, 3, 200, 256, 4), 0),                      # streaming kernels
+    ((1, 3, 200, 256, 4), bc.BC_FLAG_FORCE_HBM),   # table in HBM, several columns per lane
+    ((1, 3, 200, 256, 4), 0),                      # streaming kernels, whole-wave groups
+    ((1, 3, 500, 47, 3), 0),                       # streaming kernels, 16-lane groups
 ]
 
 
@@ -143,7 +145,7 @@ def test_backward_nonfinite_gradient(shape, flags):
     say(f"backward non-finite grad_y {shape} flags={flags}")
     x, bx, g = _inputs(*shape, seed=72)
     # one planted value in a gradient map of each channel
-    plants = _plants(H, W, [(0, 1), (N - 1, B + 2), (0, 2 * B + 3)])
+    plants = _plants(H, W, [(0, 1), (N - 1, B + 2 % B), (0, 2 * B + 3 % B)])
     gb_, gc = _plant(g, plants)
     gx = torch.empty((N, C, H, W), dtype=torch.float32, device="cuda")
     gbox = torch.empty((C, B, 4), dtype=torch.float32, device="cuda")
