@@ -2,14 +2,14 @@
 
     python -m paper_1906_11367_amd.profsum --stats DIR [--pmc NAME=DIR ...]
         [--copy-fetch DIR --copy-write DIR] [--kernel SUBSTR] [--json OUT]
-        [--warmup W --steps S]
+        [--warmup W --steps S [--settle T]]
 
 --stats   a rocprofv3 --kernel-trace --stats --output-format csv directory
---warmup, --steps
-          the traced bench.py run made W warmup steps and two timed passes of
-          S steps: each kernel's first W steps of dispatches are dropped and
-          its average is taken over the timed passes only (from the
-          per-dispatch trace), as bench.py times them.
+--warmup, --steps, --settle
+          the traced bench.py run made W warmup steps, then two passes of
+          `settle` untimed steps (bench.py: 60) followed by S timed steps:
+          each kernel's average is taken over the dispatches of the timed
+          steps only (from the per-dispatch trace), as bench.py times them.
 --pmc     counter directories (one rocprofv3 --pmc pass each)
 --copy-*  passes over a plain elementwise kernel that reads and writes a known
           number of bytes: FETCH_SIZE / WRITE_SIZE of the kernels above are
@@ -58,7 +58,7 @@ def counters(dir_):
     return {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in agg.items()}
 
 
-def stats(dir_, warmup=0, steps=0):
+def stats(dir_, warmup=0, steps=0, settle=0):
     if not steps:
         out = {}
         for r in _csv(dir_, "kernel_stats.csv"):
@@ -69,7 +69,7 @@ def stats(dir_, warmup=0, steps=0):
     per = collections.defaultdict(list)
     for r in _csv(dir_, "kernel_trace.csv"):
         per[short(r["Kernel_Name"])].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
-    total_steps = warmup + 2 * steps
+    total_steps = warmup + 2 * (settle + steps)
     out = {}
     for k, d in per.items():
         d.sort()
@@ -77,7 +77,9 @@ def stats(dir_, warmup=0, steps=0):
         if launches == 0 or len(d) % total_steps:     # not launched once per step: keep every dispatch
             kept = d
         else:
-            kept = d[warmup * launches:]
+            a1 = (warmup + settle) * launches
+            a2 = (warmup + 2 * settle + steps) * launches
+            kept = d[a1:a1 + steps * launches] + d[a2:a2 + steps * launches]
         durs = [(e - s) / 1e3 for s, e in kept]
         out[k] = {"calls": len(durs), "avg_us": sum(durs) / len(durs), "total_us": sum(durs)}
     tot = sum(v["total_us"] for v in out.values())
@@ -97,6 +99,7 @@ def main():
     ap.add_argument("--source-hash")
     ap.add_argument("--warmup", type=int, default=0)
     ap.add_argument("--steps", type=int, default=0)
+    ap.add_argument("--settle", type=int, default=60)
     ap.add_argument("--derived", action="store_true")
     a = ap.parse_args()
     fetch_f = write_f = None
@@ -113,7 +116,7 @@ def main():
         name, d = spec.split("=", 1)
         for k, v in counters(d).items():
             merged[k].update(v)
-    st = stats(a.stats, a.warmup, a.steps) if a.stats else {}
+    st = stats(a.stats, a.warmup, a.steps, a.settle) if a.stats else {}
     names = sorted(set(st) | set(merged), key=lambda n: -st.get(n, {}).get("total_us", 0))
     if fetch_f:
         print(f"calibration: FETCH_SIZE x {fetch_f:.4f}, WRITE_SIZE x {write_f:.4f} "
