@@ -341,7 +341,11 @@ size_t bc_split_workspace_bytes(int op, int N, int C, int H, int W, int B, int m
  *              gradient is multiplied by (aux > 0), aux = the forward output
  *              [N][M][P] fp32 (required then).
  * accumulate : BWD_WEIGHT only: 1 = out += result.
- * ws         : >= bc_mix_workspace_bytes(mode, ...) bytes.
+ * ws         : >= bc_mix_workspace_bytes(mode, ...) bytes (NULL when that is
+ *              0): BWD_WEIGHT's split-K partials; in BC_BF16, BWD_DATA's copy
+ *              of w^T in the MFMA operand order (2 * K * M bytes, rounded up
+ *              to 64 rows and 64 columns) when M <= 448 and K * P * 4 < 2^31,
+ *              the shapes its column-strip kernel takes.
  * ---------------------------------------------------------------------- */
 bc_status pointwise_mix(int mode, const void* a, int a_dt,
                         const void* b, int b_dt, void* out, int out_dt,

@@ -532,6 +532,201 @@ __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BM
   }
 }
 
+// ---------------------------------------------------------------------------
+// BWD_DATA in bf16, one block per column strip
+// ---------------------------------------------------------------------------
+// out[n] (K x P) = w^T (K x M) * grad[n] (M x P).  The reduction (the mix's
+// M output channels) is short and the output (K rows) is the widest tensor
+// of the layer, so the 128 x 128 tiles above spend most of their time on
+// exposed load latency: each tile has only M / 64 K-steps.  Here a block
+// owns kStripP columns of one image instead: it converts grad[n][:, strip]
+// to bf16 once, into LDS in B-operand order (rows p, reduction m contiguous),
+// and each wave then produces 64 output rows at a time with no further
+// barrier, reading its A operand (w transposed, written in MFMA operand
+// order by k_wt_frags) from L2 a group of m-steps ahead, and storing each
+// finished 64 x 64 tile while the next one's MFMAs run.  The MFMA sequence
+// of every output element is the one k_mix_gemm issues (m ascending in
+// steps of 16), so both kernels give the same bits.
+constexpr int kStripP = 64;     // output columns per block
+constexpr int kWtGroup = 4;     // m-steps of 16 loaded together (one group ahead)
+
+// Fragment count of w^T: K rounded up to 64 rows (two 32-row A fragments per
+// wave tile), M to kWtGroup m-steps of 16.
+__host__ __device__ __forceinline__ int wt_ksteps(int K) { return ((K + 63) / 64) * 2; }
+__host__ __device__ __forceinline__ int wt_msteps(int M) { return ((M + 16 * kWtGroup - 1) / (16 * kWtGroup)) * kWtGroup; }
+
+// w [M][K] -> A fragments of w^T: fragment (kb, ms) is 64 lanes x 8 bf16,
+// lane l holding w[16 ms + 8 (l / 32) + e][32 kb + l % 32], e = 0..7 (zero
+// outside w), stored at frags[(kb * msteps + ms) * 64 + l].
+template <int ADT>
+__global__ void k_wt_frags(const void* __restrict__ w, int M, int K, int msteps, size_t total,
+                           uint4* __restrict__ frags) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int lane = (int)(i & 63);
+  const size_t f = i >> 6;
+  const int ms = (int)(f % msteps), kb = (int)(f / msteps);
+  const int k = kb * 32 + (lane & 31), m0 = ms * 16 + 8 * (lane >> 5);
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int m = m0 + e;
+    const bool in = m < M && k < K;
+    const size_t idx = in ? (size_t)m * K + k : 0;
+    if constexpr (ADT == 2) h[e] = in ? (uint32_t)reinterpret_cast<const uint16_t*>(w)[idx] : 0u;
+    else h[e] = in ? (pack2_bf16(reinterpret_cast<const float*>(w)[idx], 0.f) & 0xffffu) : 0u;
+  }
+  frags[i] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+}
+
+template <int BDT, bool BMASK>
+__global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_mix_bwd_data_strip(const uint4* __restrict__ frags,
+                                                                    const void* __restrict__ g,
+                                                                    const float* __restrict__ aux,
+                                                                    float* __restrict__ out, int M, int K, int P,
+                                                                    int msteps, int nstrips) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  uint16_t* Bs = reinterpret_cast<uint16_t*>(smem_raw);
+  const int pitch = msteps * 16 + 8;   // bf16 elements; rows 16-byte aligned, 4 banks apart
+  const int strip = blockIdx.x % nstrips, n = blockIdx.x / nstrips;
+  const int p0 = strip * kStripP;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const size_t plane = (size_t)M * P;
+
+  // grad[n][m][p0 + j] -> Bs[j * pitch + m]: units of 8 m x 4 p, transposed
+  // in registers so each LDS write is 16 contiguous bytes of one row.
+  {
+    const bool vec = (P & 3) == 0;
+    const char* gb = reinterpret_cast<const char*>(g) + (size_t)n * plane * StoreBytes<BDT>::v;
+    const float* mb = BMASK ? aux + (size_t)n * plane : nullptr;
+    const int units = (msteps * 16 / 8) * (kStripP / 4);
+    for (int u = tid; u < units; u += kMixThreads) {
+      const int pg = u % (kStripP / 4), mg = u / (kStripP / 4);
+      const int pp = p0 + pg * 4, m0 = mg * 8;
+      uint32_t v[8][4];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int m = m0 + e;
+        const int avail = m < M ? max(0, min(4, P - pp)) : 0;
+        const size_t idx = avail > 0 ? (size_t)m * P + pp : 0;
+        uint32_t raw[4], mk[4] = {0u, 0u, 0u, 0u};
+        ld_run<BDT, 4>(gb, idx, vec && avail == 4, avail, raw);
+        if constexpr (BMASK) ld_run<1, 4>(reinterpret_cast<const char*>(mb), idx, vec && avail == 4, avail, mk);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (BDT == 2 && !BMASK) v[e][i] = raw[i] & 0xffffu;
+          else v[e][i] = i < avail ? (pack2_bf16(operand_f32<BDT, BMASK>(raw[i], mk[i]), 0.f) & 0xffffu) : 0u;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4 q = make_uint4(v[0][i] | (v[1][i] << 16), v[2][i] | (v[3][i] << 16), v[4][i] | (v[5][i] << 16),
+                                   v[6][i] | (v[7][i] << 16));
+        *reinterpret_cast<uint4*>(Bs + (pg * 4 + i) * pitch + m0) = q;
+      }
+    }
+  }
+  __syncthreads();
+
+  // wave tiles: rows [64 (wave + 4 t), + 64) for t = 0, 1, ...; all 64 columns
+  const int ntile = (K + 63) / 64;
+  const int mytiles = ntile > wave ? (ntile - wave + 3) / 4 : 0;
+  const int ngroups = msteps / kWtGroup;
+  const int total = mytiles * ngroups;
+  // Fragment loads and output stores go through buffer descriptors: one
+  // per-lane offset plus a wave-uniform offset each, so the 8 loads of a
+  // group and the 64 stores of a tile keep no per-element addresses in
+  // registers.
+  const __amdgpu_buffer_rsrc_t fr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(frags), (short)0,
+                                                                      (int)((size_t)wt_ksteps(K) * msteps * 1024), kBufWord3);
+  const __amdgpu_buffer_rsrc_t orr = __builtin_amdgcn_make_buffer_rsrc(out + (size_t)n * K * P, (short)0,
+                                                                       (int)((size_t)K * P * 4), kBufWord3);
+  auto load_group = [&](int t, uint4 (&a)[kWtGroup][2]) {
+    const int kb = 2 * (wave + 4 * (t / ngroups));
+    const int ms0 = (t % ngroups) * kWtGroup;
+#pragma unroll
+    for (int s = 0; s < kWtGroup; ++s)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) a[s][x] = buf_ld16(fr, (uint32_t)lane * 16, (uint32_t)(((kb + x) * msteps + ms0 + s) * 1024));
+  };
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.f;
+  const uint16_t* brow = Bs + (lane & 31) * pitch + 8 * (lane >> 5);
+  float* obase = out + (size_t)n * K * P;
+  // the MFMAs of group t (m-steps of one tile), then the tile's store when
+  // it is the tile's last group
+  auto step = [&](int t, const uint4 (&a)[kWtGroup][2]) {
+    const int ms0 = (t % ngroups) * kWtGroup;
+#pragma unroll
+    for (int s = 0; s < kWtGroup; ++s) {
+      bf16x8_t bf[2];
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+        bf[y] = *reinterpret_cast<const bf16x8_t*>(brow + y * 32 * pitch + (ms0 + s) * 16);
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, a[s][x]);
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf[y], acc[x][y], 0, 0, 0);
+      }
+    }
+    if (t % ngroups != ngroups - 1) return;
+    const int i0 = 64 * (wave + 4 * (t / ngroups));
+    const int ib = i0 + 4 * (lane >> 5), jb = p0 + (lane & 31);
+    if (i0 + 64 <= K && p0 + kStripP <= P) {
+      const uint32_t vo = (uint32_t)(ib * P + jb) * 4;
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[x][y][r]), orr, (int)vo,
+                                                  ((x * 32 + 8 * (r >> 2) + (r & 3)) * P + y * 32) * 4, 2);
+    } else {
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = ib + x * 32 + 8 * (r >> 2) + (r & 3), j = jb + y * 32;
+            if (i < K && j < P) __builtin_nontemporal_store(acc[x][y][r], obase + (size_t)i * P + j);
+          }
+    }
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.f;
+  };
+  // groups alternate between two register sets, each loaded one group ahead
+  uint4 a0[kWtGroup][2], a1[kWtGroup][2];
+  if (total > 0) load_group(0, a0);
+  for (int t = 0; t < total; t += 2) {
+    if (t + 1 < total) load_group(t + 1, a1);
+    step(t, a0);
+    if (t + 1 >= total) break;
+    if (t + 2 < total) load_group(t + 2, a0);
+    step(t + 1, a1);
+  }
+}
+
+// LDS bytes of the strip kernel's B operand, or 0 where it does not apply.
+static size_t strip_lds_bytes(int M) {
+  const size_t b = (size_t)kStripP * (wt_msteps(M) * 16 + 8) * 2;
+  return b <= (64u << 10) ? b : 0;
+}
+
+static size_t wt_frag_bytes(int M, int K) { return (size_t)wt_ksteps(K) * wt_msteps(M) * 64 * 16; }
+
 // dst[i] = bf16(src[i]), round to nearest even, 8 elements per thread.
 __global__ void k_cast_bf16(const float* __restrict__ src, uint16_t* __restrict__ dst, size_t n) {
   const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
@@ -612,6 +807,8 @@ static WeightSplit weight_split(int N, int M, int K, int P, bool bf16) {
 }
 
 size_t mix_workspace_bytes(int mode, int N, int M, int K, int P, int compute_dt) {
+  if (mode == 1)
+    return (compute_dt == 2 && strip_lds_bytes(M) > 0 && (size_t)K * P * 4 < ((size_t)1 << 31)) ? wt_frag_bytes(M, K) : 0;
   if (mode != 2) return 0;
   const WeightSplit ws = weight_split(N, M, K, P, compute_dt == 2);
   return ws.S > 1 ? (size_t)ws.S * M * K * sizeof(float) : 0;
@@ -666,6 +863,27 @@ static hipError_t launch_mix_t(int mode, const void* a, int a_dt, const void* b,
         gemm_launch<BF16, decltype(ad)::value, true, false, decltype(bd)::value, false, false>(
             a, b, nullptr, out, M, P, K, K, P, P, 0, (long)K * P, (long)M * P, N, 0, 0, ok_fwd, relu, s);
       });
+    });
+    return hipGetLastError();
+  }
+  if (mode == 1 && BF16 && strip_lds_bytes(M) > 0 && out_dt == 1 && (size_t)K * P * 4 < ((size_t)1 << 31)) {
+    // strip kernel: w^T in fragment order in the workspace, then one block
+    // per (image, kStripP columns)
+    const int ms = wt_msteps(M);
+    const size_t nfr = (size_t)wt_ksteps(K) * ms * 64;
+    with_dt<true>(a_dt, [&](auto ad) {
+      hipLaunchKernelGGL(k_wt_frags<decltype(ad)::value>, dim3((unsigned)((nfr + 255) / 256)), dim3(256), 0, s, a, M,
+                         K, ms, nfr, (uint4*)ws);
+    });
+    const int nstrips = (P + kStripP - 1) / kStripP;
+    const size_t shm = strip_lds_bytes(M);
+    with_dt<true>(b_dt, [&](auto bd) {
+      if (relu)
+        hipLaunchKernelGGL((k_mix_bwd_data_strip<decltype(bd)::value, true>), dim3(N * nstrips), dim3(kMixThreads),
+                           shm, s, (const uint4*)ws, b, aux, (float*)out, M, K, P, ms, nstrips);
+      else
+        hipLaunchKernelGGL((k_mix_bwd_data_strip<decltype(bd)::value, false>), dim3(N * nstrips), dim3(kMixThreads),
+                           shm, s, (const uint4*)ws, b, aux, (float*)out, M, K, P, ms, nstrips);
     });
     return hipGetLastError();
   }

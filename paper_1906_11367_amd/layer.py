@@ -110,6 +110,8 @@ class LayerPlan:
                 self.dw = torch.empty((self.M, K), dtype=torch.float32, device=dev)
                 self.ws_mixw = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, N, self.M, K, P,
                                                           self.compute), dev)
+                self.ws_mixd = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_DATA, N, self.M, K, P,
+                                                          self.compute), dev)
                 # the masked incoming gradient in bf16 (ReLU after a bf16 mix)
                 self.dz_bf16 = (torch.empty((N, self.M, Ho, Wo), dtype=torch.bfloat16, device=dev)
                                 if self.relu and self.compute == bc.BC_BF16 and not self.grad_premasked else None)
@@ -187,7 +189,7 @@ class LayerPlan:
             if self.w_c is not None:
                 w = self.w_c
             bc.pointwise_mix(bc.BC_MIX_BWD_DATA, w, grad_out, self.do, self.N, self.M, self.K, self.P,
-                             self.compute, relu=relu, aux=aux)
+                             self.compute, relu=relu, aux=aux, ws=self.ws_mixd)
             tap("mix_bwd_data")
             do = self.do
             dw = self.dw

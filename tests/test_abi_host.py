@@ -270,6 +270,17 @@ def test_workspace_queries():
     assert lib.bc_box_workspace_bytes_strided(0, 4, 128, 256, 256, 8, 0, 0) == 0
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_FWD, 32, 256, 1024, 3072, bc.BC_BF16) == 0
     assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_WEIGHT, 32, 256, 1024, 3072, bc.BC_BF16) > 0
+    # bf16 BWD_DATA keeps w^T in MFMA operand order: K x M bf16, both sides
+    # rounded up to 64; fp32 compute and wide M take the tiled GEMM (none)
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_DATA, 32, 256, 1024, 3072, bc.BC_BF16) == 1024 * 256 * 2
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_DATA, 2, 100, 70, 50, bc.BC_BF16) == 128 * 128 * 2
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_DATA, 32, 256, 1024, 3072, bc.BC_F32) == 0
+    assert lib.bc_mix_workspace_bytes(bc.BC_MIX_BWD_DATA, 2, 512, 64, 64, bc.BC_BF16) == 0
+    # a missing or short workspace is refused before any launch
+    assert lib.pointwise_mix(bc.BC_MIX_BWD_DATA, FAKE, bc.BC_BF16, FAKE, bc.BC_F32, FAKE, bc.BC_F32, 32, 256,
+                             1024, 3072, bc.BC_BF16, 0, None, 0, None, 0, None) == 5
+    assert lib.pointwise_mix(bc.BC_MIX_BWD_DATA, FAKE, bc.BC_BF16, FAKE, bc.BC_F32, FAKE, bc.BC_F32, 32, 256,
+                             1024, 3072, bc.BC_BF16, 0, None, 0, FAKE, 1024, None) == 5
 
 
 def test_noalloc_backward_rejects_oversized_request_before_any_launch():
