@@ -882,7 +882,13 @@ def test_bwd_deterministic():
 # ---------------------------------------------------------------------------
 # a4 / a5 / a6: 1x1 mix
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("dims", [(2, 64, 512, 3072), (1, 40, 72, 1000), (3, 8, 32, 1024), (2, 130, 260, 129)])
+# bf16 with bf16 storage takes the column-strip kernels where they apply
+# (FWD: M <= 256, K % 128 == 0, P % 4 == 0; BWD_DATA: M <= 448): the pose
+# shape at one image, rows ragged across waves, a ragged last strip, an odd
+# number of reduction chunks, a single chunk
+@pytest.mark.parametrize("dims", [(2, 64, 512, 3072), (1, 40, 72, 1000), (3, 8, 32, 1024), (2, 130, 260, 129),
+                                  (1, 256, 1024, 3072), (2, 100, 256, 1000), (2, 200, 384, 132),
+                                  (1, 16, 128, 64)])
 @pytest.mark.parametrize("compute,storage", [("f32", torch.float32), ("bf16", torch.float32),
                                              ("bf16", torch.bfloat16)])
 @pytest.mark.parametrize("relu", [0, 1])
