@@ -276,7 +276,8 @@ def main():
     if grad is not None and s_ > 1:
         grad = grad[..., ::s_, ::s_].contiguous()
     for plan in st.plans:
-        plan.overlap = not args.serial
+        if args.serial:
+            plan.overlap = False
     stream = torch.cuda.current_stream()
     timing = {"on": False, "events": [], "pool": []}
 
@@ -404,7 +405,7 @@ def main():
                    "mix": None if wl.mix_out is None else f"{wl.C * wl.B}->{wl.mix_out} {wl.mix_dtype}",
                    "layers": wl.layers, "relu": wl.relu, "mean_offset": bool(flags & bc.BC_FLAG_MEAN_OFFSET),
                    "integer_corners": bool(args.inference), "backward": backward,
-                   "overlap_weight_grad": backward and not args.serial, "stride": args.stride,
+                   "overlap_weight_grad": backward and any(p.overlap for p in st.plans), "stride": args.stride,
                    "unit_params": bool(args.unit_params), "split": args.split,
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,

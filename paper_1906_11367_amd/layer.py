@@ -47,7 +47,12 @@ class LayerPlan:
     flags: int = 0
     with_backward: bool = True
     device: str = "cuda"
-    overlap: bool = True       # weight gradient on a second stream during the backward
+    # weight gradient on a second stream during the backward; None: where it
+    # pays -- with an fp32 incoming gradient (pose layer step 0.603 -> 0.550
+    # ms), not with the masked bf16 one of a ReLU after a bf16 mix, where the
+    # GEMMs contend with the box backward for more than they gain (six stacked
+    # layers 3.465 -> 3.515 ms with it)
+    overlap: bool | None = None
     stride: int = 1            # box filter stride: outputs ceil(H/stride) x ceil(W/stride)
     # (max_w, max_h): the boxes are given as unit corners u in [-1, 1] relative
     # to that maximum box size (converted in the forward; the backward returns
@@ -60,6 +65,8 @@ class LayerPlan:
     grad_premasked: bool = False
 
     def __post_init__(self):
+        if self.overlap is None:
+            self.overlap = not (self.relu and self.mix_dtype == "bf16")
         dev = torch.device(self.device)
         N, C, H, W, B = self.N, self.C, self.H, self.W, self.B
         Ho, Wo = (H + self.stride - 1) // self.stride, (W + self.stride - 1) // self.stride
