@@ -142,12 +142,22 @@ def test_stack6_full_size_image0():
     dx, grads = st.backward(inputs, params, dev(d["grad"]))
     torch.cuda.synchronize()
     cache = O.stack_forward(d["x"][:1], d["layers"], compute="bf16", apply_relu=True)
-    dxr, _ = O.stack_backward(cache, d["layers"], d["grad"][:1], compute="bf16", apply_relu=True)
+    dxr, gr = O.stack_backward(cache, d["layers"], d["grad"][:1], compute="bf16", apply_relu=True)
     # end-to-end sanity bar, scaled with depth: ReLU decisions that the two
     # sides may legitimately take differently compound through the layers
     # (the elementwise parity of every layer is tested on oracle inputs)
     bar = 5e-3 * wl.layers
-    for name, got, ref in [("Z_last[0]", out[:1], cache[-1][2]), ("dx[0]", dx[:1], dxr)]:
+    pairs = [("Z_last[0]", out[:1], cache[-1][2]), ("dx[0]", dx[:1], dxr)]
+    # every layer's weight and box gradients of image 0: the same stack at one
+    # image (its gradients sum over that image only)
+    say(f"{wl.key} full size, image 0 alone")
+    st1 = Stack(1, wl.C, wl.H, wl.W, wl.B, wl.mix_out, wl.layers, "bf16", True)
+    inputs1, _ = st1.forward(dev(d["x"][:1]), params)
+    _, grads1 = st1.backward(inputs1, params, dev(d["grad"][:1]))
+    torch.cuda.synchronize()
+    for li in range(wl.layers):
+        pairs += [(f"dboxes[{li}]", grads1[li][0], gr[li][0]), (f"dW[{li}]", grads1[li][1], gr[li][1])]
+    for name, got, ref in pairs:
         pw, nw = O.rel_errors(host(got), ref)
         say(f"  {name}: normwise {nw:.3e}  pointwise {pw:.3e}  (bar {bar})")
         assert nw <= bar
