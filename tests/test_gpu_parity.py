@@ -184,10 +184,16 @@ def test_fwd_large_maps_hbm_table(flags):
     check(got, O.box_forward(d["x"], d["boxes"]), RTOL_F32, "O")
 
 
-def test_fwd_bf16_output_is_rounded_fp32():
-    wl = wlmod.WORKLOADS[3].scaled(N=1, C=4)
+# the pose shape (table in LDS), and maps the streaming kernels take; each
+# also with the tables in HBM
+@pytest.mark.parametrize("key,scale", [(3, dict(N=1, C=4)), (4, dict(N=1, C=2, H=300, W=128, B=3)),
+                                       (2, dict(N=1, C=2, H=500, W=47, B=3))])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
+def test_fwd_bf16_output_is_rounded_fp32(key, scale, flags):
+    wl = wlmod.WORKLOADS[key].scaled(**scale)
     d = wlmod.make_inputs(wl)
-    got = _fwd(d["x"], d["boxes"], torch.bfloat16)
+    say(f"fwd bf16 out {wl.key} {scale} flags={flags}")
+    got = _fwd(d["x"], d["boxes"], torch.bfloat16, flags)
     ref = O.box_forward(d["x"], d["boxes"])
     # the kernel rounds its fp32 value; that value is within the fp32 error
     # bound of the oracle's, so its bf16 code is one of the codes reachable
