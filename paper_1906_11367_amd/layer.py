@@ -48,10 +48,11 @@ class LayerPlan:
     with_backward: bool = True
     device: str = "cuda"
     # weight gradient on a second stream during the backward; None: where it
-    # pays -- with an fp32 incoming gradient (pose layer step 0.603 -> 0.550
-    # ms), not with the masked bf16 one of a ReLU after a bf16 mix, where the
-    # GEMMs contend with the box backward for more than they gain (six stacked
-    # layers 3.465 -> 3.515 ms with it)
+    # was measured to pay -- a bf16 mix without ReLU (pose layer step 0.603 ->
+    # 0.550 ms).  Elsewhere the GEMMs contend with the backward's other calls
+    # for more than they gain: the masked bf16 gradient of stacked ReLU layers
+    # (six layers 3.465 -> 3.515 ms with it), the compute-bound fp32 mix of
+    # the 256x256 layer (2.567 -> 2.666 ms).
     overlap: bool | None = None
     stride: int = 1            # box filter stride: outputs ceil(H/stride) x ceil(W/stride)
     # (max_w, max_h): the boxes are given as unit corners u in [-1, 1] relative
@@ -66,7 +67,7 @@ class LayerPlan:
 
     def __post_init__(self):
         if self.overlap is None:
-            self.overlap = not (self.relu and self.mix_dtype == "bf16")
+            self.overlap = self.mix_dtype == "bf16" and not self.relu
         dev = torch.device(self.device)
         N, C, H, W, B = self.N, self.C, self.H, self.W, self.B
         Ho, Wo = (H + self.stride - 1) // self.stride, (W + self.stride - 1) // self.stride

@@ -57,7 +57,7 @@ class Workload:
         return dataclasses.replace(self, **kw)
 
 
-# The five workloads.  Sizes and distributions follow the layer configurations
+# The workloads.  Sizes and distributions follow the layer configurations
 # the benchmark reports; unstated details are fixed here: the tiny integer case
 # uses a 31-wide window [-15, 15] centred on the pixel and boxes that overlap
 # it by at least one pixel; real-valued centre offsets are uniform in
@@ -83,6 +83,12 @@ WORKLOADS = {
                 x_kind="absnormal", box_kind="real", centre_max=16.0,
                 half_min=0.5, half_max=32.0, mix_out=256, mix_dtype="bf16",
                 backward=True, layers=6, relu=True),
+    # the 256x256 maps and boxes of c4 (same seed: the same x and boxes)
+    # followed by a 1x1 mix 1024 -> 128 in fp32, reported on its own line
+    6: Workload("c4_hires_mix128_f32", 4, N=4, C=128, H=256, W=256, B=8,
+                x_kind="normal+0.5", box_kind="real", centre_max=16.0,
+                half_min=32.0, half_max=127.0, mix_out=128, mix_dtype="f32",
+                backward=True, mean_offset=True),
 }
 
 

@@ -1046,7 +1046,8 @@ def check_bounded(got, ref, bound, rtol, what):
     assert excess <= rtol, f"{what}: error beyond the ambiguity bound {excess} > {rtol}"
 
 
-@pytest.mark.parametrize("key,scale", [(1, {}), (2, dict(N=2, C=8)), (4, dict(N=1, C=2, B=2))])
+@pytest.mark.parametrize("key,scale", [(1, {}), (2, dict(N=2, C=8)), (4, dict(N=1, C=2, B=2)),
+                                       (6, dict(N=1, C=4, B=2, mix_out=16))])
 def test_layer_step_exact_decisions(key, scale):
     """Workloads without bf16 rounding or ReLU decisions: plain tolerances."""
     wl = wlmod.WORKLOADS[key].scaled(**scale)
