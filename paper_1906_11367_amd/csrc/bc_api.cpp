@@ -87,7 +87,7 @@ BwdWs bwd_ws(int N, int C, int H, int W, int B, BoxPath path) {
     return w;
   }
   if (path == BoxPath::Lds) {
-    w.P = N * bc::box_bwd_lds_waves(H, W, bc::kBwdLdsItems);
+    w.P = N * bc::box_bwd_lds_waves_maps(H, W, (long)N * C);
     w.partials = after_taps;
     w.total = w.partials + align_up((size_t)w.P * C * B * 4 * 4);
     return w;

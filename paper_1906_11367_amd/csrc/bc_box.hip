@@ -904,11 +904,14 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // (stride s > 1): grad_y is [maps][Ho][Wo] and is tabulated zero-upsampled,
 // which makes every gradient that of the strided layer.  kRelu: gx is bf16,
 // store_item_relu_bf16 (not with kInt, which does not read x).
+// Four waves per SIMD: the 8-row items would take 144 VGPRs (three waves);
+// bounded to 128 they spill 14 VGPRs to scratch and still run faster (pose
+// layer backward 172.5 -> 162.5 us, results bit-identical); the 4-row items
+// fit 128 without spilling.
 template <int SEG, bool kInt, bool kUp, int kMaxT, bool kRelu>
-__global__ __launch_bounds__(kMaxT) void k_box_bwd_lds(const float* __restrict__ x, const int* __restrict__ taps,
-                                                     const float* __restrict__ gy, void* __restrict__ gx,
-                                                     float* __restrict__ partials, int C, int H, int W, int B,
-                                                     int s, int Ho, int Wo) {
+__global__ __launch_bounds__(kMaxT) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_box_bwd_lds(
+    const float* __restrict__ x, const int* __restrict__ taps, const float* __restrict__ gy, void* __restrict__ gx,
+    float* __restrict__ partials, int C, int H, int W, int B, int s, int Ho, int Wo) {
   static_assert(!(kInt && kRelu), "the ReLU mask needs x");
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
@@ -1712,10 +1715,28 @@ int box_bwd_lds_waves(int H, int W, int max_items) {
   return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
 }
 
+// A call whose maps give fewer than kBwdFillWaves waves with 8-row items
+// takes 4-row items instead (twice the waves, each with fewer registers):
+// 8 x 64 maps of 64x48 with 8 boxes, 51.5 -> 46.4 us; with 32 x 256 maps the
+// 8-row items stay faster (163 against 209 us).
+constexpr long kBwdFillWaves = 2048;  // 8 waves on each of 256 CUs
+int box_bwd_lds_seg_maps(int H, int W, long maps) {
+  const int seg = box_bwd_lds_seg(H, W, kBwdLdsItems);
+  if (seg == 8 && maps * ((n_chunks(W) * n_segs(H, 8) + 63) / 64) < kBwdFillWaves &&
+      n_chunks(W) * n_segs(H, 4) <= 256)
+    return 4;
+  return seg;
+}
+
+int box_bwd_lds_waves_maps(int H, int W, long maps) {
+  const int seg = box_bwd_lds_seg_maps(H, W, maps);
+  return seg == 0 ? 0 : (n_chunks(W) * n_segs(H, seg) + 63) / 64;
+}
+
 hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N,
                               int C, int H, int W, int B, bool rounded, bool relu_bf16, int stride, hipStream_t s) {
   if (rounded && relu_bf16) return hipErrorInvalidValue;
-  const int seg = box_bwd_lds_seg(H, W, kBwdLdsItems);
+  const int seg = box_bwd_lds_seg_maps(H, W, (long)N * C);
   if (seg == 8) bwd_lds_t<8, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, relu_bf16, stride, s);
   else if (seg == 4 && n_chunks(W) * n_segs(H, 4) <= 256)
     bwd_lds_t<4, 256>(x, taps, gy, gx, partials, N, C, H, W, B, rounded, relu_bf16, stride, s);

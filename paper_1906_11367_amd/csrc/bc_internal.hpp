@@ -52,6 +52,10 @@ hipError_t launch_box_bwd_lds(const float* x, const int* taps, const float* gy, 
 constexpr int kBwdLdsItems = 1024;
 int box_bwd_lds_seg(int H, int W, int max_items);
 int box_bwd_lds_waves(int H, int W, int max_items);
+// The plain and strided LDS backward (launch_box_bwd_lds) over `maps` = N*C
+// maps: its segment length and waves per map (P = N * waves).
+int box_bwd_lds_seg_maps(int H, int W, long maps);
+int box_bwd_lds_waves_maps(int H, int W, long maps);
 // HBM path: tables of every gradient map in sat_g (built by sat_build, or
 // sat_build_up for stride > 1);
 // P = N * box_bwd_gather_blocks() * 4.
