@@ -392,6 +392,28 @@ def main():
                 "per_launch": ("algo_bytes=%d" % dc["algo_bytes"]) if dc["bound"] == "hbm"
                 else ("algo_flops=%d" % dc["algo_flops"])}
 
+    # HBM bandwidth a plain streaming kernel reaches on this GPU (the spec peak
+    # beside it): an fp32 elementwise multiply, 256 MiB read and 256 MiB
+    # written per launch, timed over 20 launches after 5
+    src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.mul(src, 2.0, out=dst)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(20):
+        torch.mul(src, 2.0, out=dst)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * src.numel() * 4 / (c0.elapsed_time(c1) / 20 * 1e-3) / 1e9
+    del src, dst
+    if roofline["bound"] == "hbm":
+        roofline["frac_of_measured_copy"] = round(roofline["achieved"] / copy_gbs, 4)
+    for ent in calls.values():
+        gbs = ent["achieved"] if ent["bound"] == "hbm" else ent.get("hbm_gbs")
+        if gbs is not None:
+            ent["hbm_frac_of_measured_copy"] = round(gbs / copy_gbs, 4)
+
     pix_box = wl.N * wl.C * wl.B * st.plans[0].Ho * st.plans[0].Wo * wl.layers
     value = pix_box / (ms * 1e-3) / 1e9
     box_ms = sum(calls[k]["avg_us"] * calls[k]["launches"] for k in calls if k.startswith("box")) / 1e3
@@ -410,6 +432,7 @@ def main():
                    "parallelism": "single GPU"},
         "box_only_gpixbox_s": round(pix_box / (box_ms * 1e-3) / 1e9, 3) if box_ms > 0 else None,
         "roofline": roofline,
+        "hbm_measured_copy_gbs": round(copy_gbs, 1),
         "calls": calls,
         "source_hash": src_hash,
     }
