@@ -904,10 +904,10 @@ __device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict_
 // (stride s > 1): grad_y is [maps][Ho][Wo] and is tabulated zero-upsampled,
 // which makes every gradient that of the strided layer.  kRelu: gx is bf16,
 // store_item_relu_bf16 (not with kInt, which does not read x).
-// Four waves per SIMD: the 8-row items would take 144 VGPRs (three waves);
-// bounded to 128 they spill 14 VGPRs to scratch and still run faster (pose
-// layer backward 172.5 -> 162.5 us, results bit-identical); the 4-row items
-// fit 128 without spilling.
+// Four waves per SIMD: bounded to 128 VGPRs (from 144, three waves) the
+// 8-row items fit without spilling once the final stores recompute their
+// addresses (below); pose-layer backward 172.5 -> 151.5 us, results
+// bit-identical.  The 4-row items take 92.
 template <int SEG, bool kInt, bool kUp, int kMaxT, bool kRelu>
 __global__ __launch_bounds__(kMaxT) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_box_bwd_lds(
     const float* __restrict__ x, const int* __restrict__ taps, const float* __restrict__ gy, void* __restrict__ gx,
@@ -959,8 +959,14 @@ __global__ __launch_bounds__(kMaxT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
     store_wave_partial(g4, partials + (((size_t)n * nw + wave) * C * B + (size_t)c * B + b) * 4);
   }
   if (active && gx != nullptr) {
-    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * plane, H, W, x0, y0, acc, rmask);
-    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * plane, H, W, x0, y0, acc);
+    // The stores recompute their row addresses here: an opaque copy of the
+    // item's origin keeps the compiler from holding the 64-bit row offsets of
+    // load_item live across the box loop (seven register pairs, spilled at
+    // four waves per SIMD).
+    int sx = x0, sy = y0;
+    asm volatile("" : "+v"(sx), "+v"(sy));
+    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * plane, H, W, sx, sy, acc, rmask);
+    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * plane, H, W, sx, sy, acc);
   }
 }
 
