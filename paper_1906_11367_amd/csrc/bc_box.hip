@@ -829,9 +829,17 @@ __device__ __forceinline__ void load_item(const float* __restrict__ xs, int H, i
     }
 }
 
+// The item's origin passes through an opaque copy (an empty asm with the
+// coordinates as operands): the stores then recompute their row addresses
+// instead of the compiler holding load_item's 64-bit row offsets live across
+// a whole kernel (seven register pairs in the 8-row backward, which spilled
+// them at four waves per SIMD).
+__device__ __forceinline__ void opaque_origin(int& x0, int& y0) { asm volatile("" : "+v"(x0), "+v"(y0)); }
+
 template <int SEG>
 __device__ __forceinline__ void store_item(float* __restrict__ out, int H, int W, int x0, int y0,
                                            const float (&acc)[SEG][kQ]) {
+  opaque_origin(x0, y0);
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int yy = y0 + s;
@@ -872,6 +880,7 @@ __device__ __forceinline__ uint16_t bf16_rne_bits(float f) {
 template <int SEG>
 __device__ __forceinline__ void store_item_relu_bf16(uint16_t* __restrict__ out, int H, int W, int x0, int y0,
                                                      const float (&acc)[SEG][kQ], uint32_t mask) {
+  opaque_origin(x0, y0);
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int yy = y0 + s;
@@ -959,14 +968,8 @@ __global__ __launch_bounds__(kMaxT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
     store_wave_partial(g4, partials + (((size_t)n * nw + wave) * C * B + (size_t)c * B + b) * 4);
   }
   if (active && gx != nullptr) {
-    // The stores recompute their row addresses here: an opaque copy of the
-    // item's origin keeps the compiler from holding the 64-bit row offsets of
-    // load_item live across the box loop (seven register pairs, spilled at
-    // four waves per SIMD).
-    int sx = x0, sy = y0;
-    asm volatile("" : "+v"(sx), "+v"(sy));
-    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * plane, H, W, sx, sy, acc, rmask);
-    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * plane, H, W, sx, sy, acc);
+    if constexpr (kRelu) store_item_relu_bf16<SEG>(static_cast<uint16_t*>(gx) + (size_t)map * plane, H, W, x0, y0, acc, rmask);
+    else store_item<SEG>(static_cast<float*>(gx) + (size_t)map * plane, H, W, x0, y0, acc);
   }
 }
 
