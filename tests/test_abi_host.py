@@ -252,6 +252,12 @@ def test_workspace_queries():
     taps = 2 * 256 * 4 * 64
     assert lib.bc_box_workspace_bytes(0, 32, 256, 64, 48, 4, 0) == taps
     assert lib.bc_box_workspace_bytes(1, 32, 256, 64, 48, 4, 0) >= taps + 32 * 256 * 4 * 16
+    # the LDS backward's partials: one row per wave and image.  A call with
+    # enough maps for 2048 waves of 8-row items takes them (two waves per
+    # 64x48 map); fewer maps take 4-row items (four waves per map)
+    a256 = lambda v: (v + 255) // 256 * 256
+    for N, waves in ((32, 2), (4, 2), (3, 4), (1, 4)):
+        assert lib.bc_box_workspace_bytes(1, N, 256, 64, 48, 4, 0) == a256(taps) + a256(N * waves * 256 * 4 * 16)
     # 256x256 maps take the streaming kernels: tap records plus one row of
     # edge-gradient partials per image, no tables
     assert lib.bc_box_workspace_bytes(0, 4, 128, 256, 256, 8, 0) == 2 * 128 * 8 * 64

@@ -752,6 +752,40 @@ def test_bwd(key, scale, flags):
     check(gb, O.box_backward_params(d["x"], g, d["boxes"]), RTOL_F32, "dboxes")
 
 
+@pytest.mark.parametrize("stride", [1, 2])
+def test_bwd_eight_row_items(stride):
+    """The LDS backward with 8-row items (two waves per 64x48 map), which it
+    takes once a call has enough maps to fill the GPU with them (here 4 x 256
+    maps, as in the pose layer): dx and the box gradient against the oracle,
+    and the masked bf16 variant bit for bit against bc_relu_grad_bf16 of it.
+    Smaller calls take 4-row items (the other backward tests)."""
+    wl = wlmod.WORKLOADS[3].scaled(N=4, C=256)
+    N, C, H, W, B = wl.N, wl.C, wl.H, wl.W, wl.B
+    # 8-row items: 128 per map, two waves, so N * 2 partial rows per box
+    taps = 2 * C * B * 16 * 4
+    a256 = lambda v: (v + 255) // 256 * 256
+    assert bc.box_workspace_bytes(1, N, C, H, W, B, 0, stride) == a256(taps) + a256(N * 2 * C * B * 16)
+    d = wlmod.make_inputs(wl)
+    x = np.maximum(d["x"], 0)          # a rectified map: the ReLU mask has zeros
+    Ho, Wo = O.strided_size(H, stride), O.strided_size(W, stride)
+    g = np.random.default_rng(116 + stride).standard_normal((N, C * B, Ho, Wo)).astype(np.float32)
+    say(f"bwd 8-row items {N}x{C} stride={stride}")
+    xd, bd, gd = dev(x), dev(d["boxes"]), dev(g)
+    gx = torch.empty((N, C, H, W), dtype=torch.float32, device="cuda")
+    gb = torch.empty((C, B, 4), dtype=torch.float32, device="cuda")
+    bc.box_conv_bwd(xd, bd, gd, gx, gb, 0, stride=stride)
+    check(host(gx), O.box_backward_input(g, d["boxes"], H, W, stride=stride), RTOL_F32, "dx")
+    check(host(gb), O.box_backward_params(x, g, d["boxes"], stride=stride), RTOL_F32, "dboxes")
+    want = torch.empty((N, C, H, W), dtype=torch.bfloat16, device="cuda")
+    bc.relu_grad_bf16(gx, xd, want)
+    got = torch.empty_like(want)
+    gb2 = torch.empty_like(gb)
+    bc.box_conv_bwd_relu_bf16(xd, bd, gd, got, gb2, 0, stride=stride)
+    torch.cuda.synchronize()
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+    assert torch.equal(gb2, gb)
+
+
 @pytest.mark.parametrize("flags", [0, bc.BC_FLAG_FORCE_HBM])
 def test_bwd_integer_edges(flags):
     """Boxes whose edges all sit on pixel boundaries: the parameter gradient
