@@ -9,7 +9,8 @@ pose-estimation feature maps, already resident in HBM when timing starts.
 
 Prints ONE JSON line.  `value` is filtered-map elements (pixel*box, summed over
 layers) per second of the whole step, in Gpix*box/s, timed on steps run as the
-layer runs them (the weight gradient overlapped on a second stream).
+layer runs them (every call in order on one stream; with --overlap the weight
+gradient runs on a second stream).
 `roofline` reports the dominant library call, timed with HIP events in a
 second pass where every call runs in order on one stream (`serial_ms_per_step`
 is that pass's step); `cpu_baseline` times the CPU oracle on a bounded sample
@@ -57,8 +58,11 @@ def parse():
                    help="kernel splitting: every box cut into 2 (along x or y) or 4 pieces with their own "
                         "weights (fp32 maps, stride 1; the table-offset flag is not used)")
     p.add_argument("--serial", action="store_true",
-                   help="run every call in order on one stream in the timed pass too (no overlapped "
-                        "weight gradient): the configuration the per-kernel profiles are taken in")
+                   help="run every call in order on one stream in the timed pass (the layer's default; "
+                        "overrides --overlap): the configuration the per-kernel profiles are taken in")
+    p.add_argument("--overlap", action="store_true",
+                   help="run each layer's weight gradient on a second stream beside its other backward "
+                        "calls")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain elementwise kernel that reads 256 MiB and writes 256 MiB, 5 "
                         "times (reference for the FETCH_SIZE / WRITE_SIZE counters), and exit")
@@ -84,8 +88,9 @@ def call_cost(label, wl, o_bytes, stride=1):
                    peak; also the operand bytes it must move (fwd: read O,
                    write Z; bwd_data: read dZ, write dO; bwd_weight: read dZ
                    and O), reported against the HBM peak; dZ is 2 bytes per
-                   element after relu_grad (ReLU after a bf16 mix), else 4
+                   element for a bf16 mix (cast or masked once), else 4
     relu_grad    : read dZ and Z (fp32), write the masked dZ (bf16)
+    grad_cast    : read dZ (fp32), write it in bf16
     """
     if label.startswith("box_params"):        # read and write [C][B][4] fp32
         return {"bound": "hbm", "bytes": 2 * wl.C * wl.B * 16}
@@ -103,7 +108,9 @@ def call_cost(label, wl, o_bytes, stride=1):
     z = 4 * nz
     if label == "relu_grad":
         return {"bound": "hbm", "bytes": 10 * nz}
-    dz = 2 * nz if (wl.relu and wl.mix_dtype == "bf16") else z
+    if label == "grad_cast":
+        return {"bound": "hbm", "bytes": 6 * nz}
+    dz = 2 * nz if wl.mix_dtype == "bf16" else z
     mix_bytes = {"mix_fwd": o_bytes * pb + z, "mix_bwd_data": dz + 4 * pb, "mix_bwd_weight": dz + o_bytes * pb}
     return {"bound": "mfma", "flops": flops, "bytes": mix_bytes.get(label)}
 
@@ -276,8 +283,7 @@ def main():
     if grad is not None and s_ > 1:
         grad = grad[..., ::s_, ::s_].contiguous()
     for plan in st.plans:
-        if args.serial:
-            plan.overlap = False
+        plan.overlap = args.overlap and not args.serial
     stream = torch.cuda.current_stream()
     timing = {"on": False, "events": [], "pool": []}
 
@@ -288,9 +294,8 @@ def main():
             timing["events"].append((label, e))
 
     def step():
-        # The plain pass runs the layer as a user would (the weight gradient
-        # overlapped on a second stream); the per-call pass records an event
-        # after every call, in order on one stream.
+        # The plain pass runs the layer as a user would; the per-call pass
+        # records an event after every call, in order on one stream.
         t = tap if timing["on"] else None
         if t:
             t("start")

@@ -5,21 +5,22 @@ Forward:  O = box_conv_fwd(x)            (bf16 copy when the mix runs in bf16)
 Backward: dW = pointwise_mix(BWD_WEIGHT, dZ, O)
           dO = pointwise_mix(BWD_DATA, w, dZ)
           dx, dboxes = box_conv_bwd(x, dO)
-With a ReLU after a bf16 mix, dZ is first masked and rounded once
-(bc_relu_grad_bf16): both GEMMs then read those bf16 operands unmasked, the
-same operand bits the masked GEMMs would form from the fp32 gradient, so the
-results are bitwise the same (six stacked pose layers: 4.47 -> 3.71 ms per
-step).  Without the ReLU a plain cast of dZ gains nothing on the step (the
-cast costs what the GEMMs save), so the GEMMs round dZ on load.  In a stack
-the masked operand of layer l comes straight from the box backward of layer
-l + 1 (box_conv_bwd_relu_bf16: its input is layer l's rectified output, so
-x > 0 is the mask), with no fp32 gradient written or read back.
+With a bf16 mix, dZ is first rounded to bf16 once (bc_cast_bf16), or masked
+and rounded with a ReLU (bc_relu_grad_bf16): both GEMMs then read those bf16
+operands, the same operand bits they would form from the fp32 gradient
+themselves, so the results are bitwise the same (pose layer 0.574 -> 0.556 ms
+per step; six stacked layers 4.47 -> 3.71 ms).  In a stack the masked
+operand of layer l comes straight from the box backward of layer l + 1
+(box_conv_bwd_relu_bf16: its input is layer l's rectified output, so x > 0
+is the mask), with no fp32 gradient written or read back.
 With kernel splitting (`split` = "2x", "2y" or "4") the box filter is
 box_conv_split_fwd / box_conv_split_bwd: the boxes argument is then the pair
 (boxes, piece weights) and the backward returns the pair of their gradients.
-The weight gradient depends on neither of the other two backward calls; it
-runs on a second stream (default priority) alongside them, and the caller's
-stream waits for it before the backward returns.
+The weight gradient depends on neither of the other two backward calls; a
+plan built with `overlap` runs it on a second stream (default priority)
+alongside them, and the caller's stream waits for it before the backward
+returns.  By default every call runs in order on the caller's stream, which
+was measured faster on every workload here.
 All buffers and workspaces are allocated once per plan (torch is used for
 device memory and streams only); every arithmetic step runs in libboxconv's
 kernels.
@@ -47,13 +48,12 @@ class LayerPlan:
     flags: int = 0
     with_backward: bool = True
     device: str = "cuda"
-    # weight gradient on a second stream during the backward; None: where it
-    # was measured to pay -- a bf16 mix without ReLU (pose layer step 0.603 ->
-    # 0.550 ms).  Elsewhere the GEMMs contend with the backward's other calls
-    # for more than they gain: the masked bf16 gradient of stacked ReLU layers
-    # (six layers 3.465 -> 3.515 ms with it), the compute-bound fp32 mix of
-    # the 256x256 layer (2.567 -> 2.666 ms).
-    overlap: bool | None = None
+    # weight gradient on a second stream during the backward (default off).
+    # With the incoming gradient in bf16 (below) the two backward GEMMs run
+    # faster in order than side by side (pose layer 0.556 against 0.587 ms),
+    # and so do the stacked ReLU layers (3.465 against 3.515 ms) and the
+    # compute-bound fp32 mix of the 256x256 layer (2.525 against 2.666 ms).
+    overlap: bool = False
     stride: int = 1            # box filter stride: outputs ceil(H/stride) x ceil(W/stride)
     # (max_w, max_h): the boxes are given as unit corners u in [-1, 1] relative
     # to that maximum box size (converted in the forward; the backward returns
@@ -66,8 +66,6 @@ class LayerPlan:
     grad_premasked: bool = False
 
     def __post_init__(self):
-        if self.overlap is None:
-            self.overlap = self.mix_dtype == "bf16" and not self.relu
         dev = torch.device(self.device)
         N, C, H, W, B = self.N, self.C, self.H, self.W, self.B
         Ho, Wo = (H + self.stride - 1) // self.stride, (W + self.stride - 1) // self.stride
@@ -120,9 +118,13 @@ class LayerPlan:
                                                           self.compute), dev)
                 self.ws_mixd = _ws(bc.mix_workspace_bytes(bc.BC_MIX_BWD_DATA, N, self.M, K, P,
                                                           self.compute), dev)
-                # the masked incoming gradient in bf16 (ReLU after a bf16 mix)
+                # the incoming gradient in bf16, once, for both backward GEMMs of a
+                # bf16 mix (masked by the ReLU if there is one): the GEMMs round it
+                # to the same bits themselves, but read as bf16 it costs half the
+                # bytes and arrives from cache (pose layer: BWD_DATA 145 -> 100 us,
+                # BWD_WEIGHT 110 -> 97 us, for a 28 us cast; step 0.574 -> 0.556 ms)
                 self.dz_bf16 = (torch.empty((N, self.M, Ho, Wo), dtype=torch.bfloat16, device=dev)
-                                if self.relu and self.compute == bc.BC_BF16 and not self.grad_premasked else None)
+                                if self.compute == bc.BC_BF16 and not self.grad_premasked else None)
                 self.side = torch.cuda.Stream(device=dev)   # default priority
                 self.ev_in = torch.cuda.Event()
                 self.ev_dw = torch.cuda.Event()
@@ -178,10 +180,13 @@ class LayerPlan:
                 if grad_out.dtype != torch.bfloat16:
                     raise ValueError("grad_out must be the masked bf16 operand")
                 aux, relu = None, 0
-            elif self.dz_bf16 is not None:
+            elif self.dz_bf16 is not None and self.relu:
                 grad_out = bc.relu_grad_bf16(grad_out, self.z, self.dz_bf16)
                 tap("relu_grad")
                 aux, relu = None, 0
+            elif self.dz_bf16 is not None:
+                grad_out = bc.bc_cast_bf16(grad_out, self.dz_bf16)
+                tap("grad_cast")
             main = torch.cuda.current_stream()
             if overlap:
                 self.ev_in.record(main)         # O, Z and dZ are ready on the caller's stream

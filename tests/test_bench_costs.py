@@ -27,8 +27,10 @@ def test_pose_layer_call_costs():
     c = bench.call_cost("mix_fwd", wl, 2)
     assert c["bound"] == "mfma" and c["flops"] == 2 * 32 * 256 * 1024 * 64 * 48
     assert c["bytes"] == 2 * pb + 4 * nz                                  # O read, Z written
-    assert bench.call_cost("mix_bwd_data", wl, 2)["bytes"] == 4 * nz + 4 * pb
-    assert bench.call_cost("mix_bwd_weight", wl, 2)["bytes"] == 4 * nz + 2 * pb
+    # the layer casts dZ to bf16 once for both backward GEMMs of a bf16 mix
+    assert bench.call_cost("grad_cast", wl, 2)["bytes"] == 6 * nz          # fp32 read, bf16 written
+    assert bench.call_cost("mix_bwd_data", wl, 2)["bytes"] == 2 * nz + 4 * pb
+    assert bench.call_cost("mix_bwd_weight", wl, 2)["bytes"] == 2 * nz + 2 * pb
 
 
 def test_stacked_relu_call_costs():

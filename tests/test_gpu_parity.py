@@ -627,9 +627,8 @@ def test_split_unit_weights_equal_the_box_layer():
 
 @pytest.mark.parametrize("relu", [False, True])
 def test_layer_split_fp32(relu):
-    """The whole layer with boxes split in four (fp32 mix, overlapped weight
-    gradient): outputs and every gradient against the oracle's split box
-    filter composed with its mix."""
+    """The whole layer with boxes split in four (fp32 mix): outputs and every
+    gradient against the oracle's split box filter composed with its mix."""
     wl = wlmod.WORKLOADS[2].scaled(N=2, C=8)
     d = wlmod.make_inputs(wl)
     pw = wlmod.make_piece_weights(wl, 4)
@@ -1135,6 +1134,28 @@ def test_layer_step_bf16_mix():
     check_bounded(host(dw), bw["dw"], bw["edw"], RTOL_BF16_MIX, "dW")
     check_bounded(host(dx), bw["dx"], bw["edx"], RTOL_F32, "dx")
     check_bounded(host(db), bw["dth"], bw["edth"], RTOL_F32, "dboxes")
+
+
+@pytest.mark.parametrize("relu", [False, True])
+def test_layer_overlap_matches_in_order(relu):
+    """A layer built with the weight gradient on a second stream gives the
+    same bits as the in-order layer (the same kernels on the same operands;
+    the caller's stream waits for the side stream before the backward
+    returns), for the bf16 mix with the cast and with the masked gradient."""
+    wl = wlmod.WORKLOADS[3].scaled(N=2, C=32)
+    d = wlmod.make_inputs(wl)
+    xd, bd, wd, gd = dev(d["x"]), dev(d["boxes"]), dev(d["w"]), dev(d["grad"])
+    say(f"layer overlap relu={relu}")
+    outs = []
+    for overlap in (False, True):
+        plan = LayerPlan(wl.N, wl.C, wl.H, wl.W, wl.B, wl.mix_out, torch.float32, "bf16", relu, 0, True,
+                         overlap=overlap)
+        z = plan.forward(xd, bd, wd)
+        dx, db, dw = plan.backward(xd, bd, wd, gd)
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in (z, dx, db, dw)])
+    for a_, b_, what in zip(outs[0], outs[1], ("Z", "dx", "dboxes", "dW")):
+        assert torch.equal(a_, b_), what
 
 
 def test_stack_layers_relu_bf16_each_on_oracle_input():
