@@ -788,6 +788,25 @@ __global__ void k_mix_reduce(const float* __restrict__ part, int S, size_t n, fl
   out[i] = s;
 }
 
+// The same sum, four consecutive outputs per thread (n a multiple of 4), the
+// partials' loads unrolled so that several are in flight; each output's
+// additions keep their order, so the bits are those of k_mix_reduce.
+__global__ void k_mix_reduce4(const float4* __restrict__ part, int S, size_t n4, float4* __restrict__ out,
+                              int accumulate) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 s = accumulate ? out[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+  for (int k = 0; k < S; ++k) {
+    const float4 p = part[(size_t)k * n4 + i];
+    s.x += p.x;
+    s.y += p.y;
+    s.z += p.z;
+    s.w += p.w;
+  }
+  out[i] = s;
+}
+
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
@@ -923,8 +942,14 @@ static hipError_t launch_mix_t(int mode, const void* a, int a_dt, const void* b,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || direct) return e;
   const size_t n = (size_t)M * K;
-  hipLaunchKernelGGL(k_mix_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const float*)ws, sp.S, n,
-                     (float*)out, accumulate);
+  if ((n & 3) == 0 && ((uintptr_t)out & 15) == 0) {
+    const size_t n4 = n / 4;
+    hipLaunchKernelGGL(k_mix_reduce4, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, (const float4*)ws, sp.S,
+                       n4, (float4*)out, accumulate);
+  } else {
+    hipLaunchKernelGGL(k_mix_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const float*)ws, sp.S, n,
+                       (float*)out, accumulate);
+  }
   return hipGetLastError();
 }
 
