@@ -927,7 +927,9 @@ def test_bwd_deterministic():
 # number of reduction chunks, a single chunk
 @pytest.mark.parametrize("dims", [(2, 64, 512, 3072), (1, 40, 72, 1000), (3, 8, 32, 1024), (2, 130, 260, 129),
                                   (1, 256, 1024, 3072), (2, 100, 256, 1000), (2, 200, 384, 132),
-                                  (1, 16, 128, 64)])
+                                  (1, 16, 128, 64),
+                                  # M * K odd: the split-K sum one output per thread
+                                  (2, 7, 9, 200)])
 @pytest.mark.parametrize("compute,storage", [("f32", torch.float32), ("bf16", torch.float32),
                                              ("bf16", torch.bfloat16)])
 @pytest.mark.parametrize("relu", [0, 1])
