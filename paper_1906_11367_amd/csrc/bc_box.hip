@@ -893,14 +893,40 @@ __device__ __forceinline__ void store_item_relu_bf16(uint16_t* __restrict__ out,
   }
 }
 
-// The wave's sums of the four edge gradients, written by lane 0 to pp[0..3].
-__device__ __forceinline__ void store_wave_partial(float* g4, float* __restrict__ pp) {
-#pragma unroll
-  for (int k = 0; k < 4; ++k) g4[k] = wave_sum_dpp(g4[k]);
-  if ((threadIdx.x & 63) == 0) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) pp[k] = g4[k];
-  }
+// Lane move (data-parallel primitive `ctrl`), 0 where the source lane is
+// disabled.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xF, 0xF, false));
+}
+
+// The wave's sums of the four edge gradients, written to pp[0..3] (lanes 0..3
+// store one each).  A transposed reduction: the pair step (lane ^ 1) leaves
+// even lanes summing values 0 and 1 and odd lanes values 2 and 3, the quad
+// step (lane ^ 2) one value per lane, index 2 * (lane & 1) + ((lane >> 1) &
+// 1); rotations by 4 and 8 lanes inside each 16-lane row, then the row
+// swaps (lane ^ 16, lane ^ 32), finish the sum in every lane.  17 vector
+// operations for the four sums instead of four separate reductions (four
+// lane moves and four lane reads each).  Every lane of the wave must be
+// active; the order of the additions is fixed, so the sums are
+// deterministic.
+__device__ __forceinline__ void store_wave_partial(const float* g4, float* __restrict__ pp) {
+  const int lane = threadIdx.x & 63;
+  const bool odd = lane & 1, hi = lane & 2;
+  float k0 = odd ? g4[2] : g4[0], k1 = odd ? g4[3] : g4[1];
+  const float s0 = odd ? g4[0] : g4[2], s1 = odd ? g4[1] : g4[3];
+  k0 += dpp_move<0xB1>(s0);  // quad_perm 1,0,3,2: lane ^ 1
+  k1 += dpp_move<0xB1>(s1);
+  float t = hi ? k1 : k0;
+  const float u = hi ? k0 : k1;
+  t += dpp_move<0x4E>(u);    // quad_perm 2,3,0,1: lane ^ 2
+  t += dpp_move<0x124>(t);   // row_ror:4
+  t += dpp_move<0x128>(t);   // row_ror:8
+  auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+  t = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);  // rows 0+1 and 2+3
+  auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(t), __float_as_uint(t), false, false);
+  t = __uint_as_float(r32[0]) + __uint_as_float(r32[1]);  // halves
+  if (lane < 4) pp[2 * (lane & 1) + (lane >> 1)] = t;
 }
 
 // Backward, table in LDS: one block per map (n, c); items (row segment,

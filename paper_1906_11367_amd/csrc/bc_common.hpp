@@ -304,17 +304,6 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
-// Wave64 sum, wave-uniform result: row sums, then the four rows' values read
-// from lanes 0, 16, 32, 48 (added in a fixed order).
-__device__ __forceinline__ float wave_sum_dpp(float v) {
-  v = row16_sum(v);
-  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-  return (r0 + r1) + (r2 + r3);
-}
-
 // Wave-level sum (wave64), result valid in every lane.
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
