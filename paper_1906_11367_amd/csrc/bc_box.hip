@@ -943,11 +943,16 @@ __device__ __forceinline__ void store_wave_partial(const float* g4, float* __res
 // 8-row items fit without spilling once the final stores recompute their
 // addresses (below); pose-layer backward 172.5 -> 151.5 us, results
 // bit-identical.  The 4-row items take 92.
-template <int SEG, bool kInt, bool kUp, int kMaxT, bool kRelu>
+// kW > 0: the map width as a compile-time constant (W is then ignored), so
+// the table pitch is one too and every row offset of the scans, the walk and
+// the item loads and stores is an immediate of its LDS or global access
+// instead of a per-element address add; the results are the same bits.
+template <int SEG, bool kInt, bool kUp, int kMaxT, bool kRelu, int kW = 0>
 __global__ __launch_bounds__(kMaxT) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_box_bwd_lds(
     const float* __restrict__ x, const int* __restrict__ taps, const float* __restrict__ gy, void* __restrict__ gx,
-    float* __restrict__ partials, int C, int H, int W, int B, int s, int Ho, int Wo) {
+    float* __restrict__ partials, int C, int H, int W_arg, int B, int s, int Ho, int Wo) {
   static_assert(!(kInt && kRelu), "the ReLU mask needs x");
+  const int W = kW > 0 ? kW : W_arg;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -1718,6 +1723,8 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
   return last_error();
 }
 
+constexpr int kPoseW = 48;
+
 template <int SEG, int kMaxT>
 static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N, int C,
                       int H, int W, int B, bool rounded, bool relu_bf16, int stride, hipStream_t s) {
@@ -1726,8 +1733,14 @@ static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   auto go = [&](auto ki, auto ku, auto kr) {
-    hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT, decltype(kr)::value>),
-                       dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
+    // the pose network's 48-column maps (a 192-pixel-wide input at stride
+    // 4) take the instance with the width compiled in
+    if (SEG == 8 && !decltype(ku)::value && W == kPoseW)
+      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, false, kMaxT, decltype(kr)::value, kPoseW>),
+                         dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
+    else
+      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT, decltype(kr)::value>),
+                         dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
   };
   with_flag(stride > 1, [&](auto ku) {
     if (rounded) go(std::true_type{}, ku, std::false_type{});
