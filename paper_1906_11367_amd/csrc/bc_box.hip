@@ -708,10 +708,13 @@ __device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __r
 
 // Forward, table in LDS: one block per (map, group of bpg boxes).  The block
 // builds the map's table once and evaluates every box of its group.
-template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
+// kW > 0: the map width compiled in (W is then ignored), as in the LDS
+// backward.
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt, int kW = 0>
 __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const int* __restrict__ taps,
-                                                     OutT* __restrict__ y, int C, int H, int W, int B, int bpg,
+                                                     OutT* __restrict__ y, int C, int H, int W_arg, int B, int bpg,
                                                      int per_box_p) {
+  const int W = kW > 0 ? kW : W_arg;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* S = reinterpret_cast<T*>(smem_raw);
   __shared__ float red[16];
@@ -1634,6 +1637,11 @@ static FwdGeom fwd_geom(int N, int C, int H, int W, int B, int seg) {
   return fwd_geom_items(N, C, B, n_chunks(W) * n_segs(H, seg));
 }
 
+// The pose network's maps are 48 columns wide (a 192-pixel-wide input at
+// stride 4): the LDS forward and backward take instances with that width
+// compiled in.
+constexpr int kPoseW = 48;
+
 template <typename T, typename OutT, bool kOffset>
 static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int H, int W, int B, bool rounded,
                       int stride, hipStream_t s) {
@@ -1642,8 +1650,12 @@ static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int
   if (stride == 1) {
     const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
     with_flag(rounded, [&](auto ki) {
-      hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
-                         dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+      if (std::is_same<T, float>::value && W == kPoseW)
+        hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value, kPoseW>), dim3(N * C * g.ngrp),
+                           dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
+      else
+        hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, SEG, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
+                           dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, g.bpg, g.per_box_p);
     });
     return;
   }
@@ -1723,8 +1735,6 @@ hipError_t launch_box_fwd_gather(const void* sat, bool is_int, const float* mean
   return last_error();
 }
 
-constexpr int kPoseW = 48;
-
 template <int SEG, int kMaxT>
 static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx, float* partials, int N, int C,
                       int H, int W, int B, bool rounded, bool relu_bf16, int stride, hipStream_t s) {
@@ -1733,8 +1743,6 @@ static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   auto go = [&](auto ki, auto ku, auto kr) {
-    // the pose network's 48-column maps (a 192-pixel-wide input at stride
-    // 4) take the instance with the width compiled in
     if (SEG == 8 && !decltype(ku)::value && W == kPoseW)
       hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, false, kMaxT, decltype(kr)::value, kPoseW>),
                          dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
