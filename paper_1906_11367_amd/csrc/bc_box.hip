@@ -1404,11 +1404,13 @@ __device__ __forceinline__ void split_box_grads(const float* __restrict__ f, con
 // one item of 3 columns x SEG rows per thread, input values in registers), one
 // walk over each box's mirrored corners.  Each wave writes its split_box_grads
 // sums to partials[(n * nw + wave) * C*B + c*B + b][8].
-template <int SEG, int NXC, int NYC, int kMaxT>
+// kW > 0: the map width compiled in, as in k_box_bwd_lds.
+template <int SEG, int NXC, int NYC, int kMaxT, int kW = 0>
 __global__ __launch_bounds__(kMaxT) void k_box_bwd_lds_split(const float* __restrict__ x, const int* __restrict__ rec,
                                                            const float* __restrict__ gy, float* __restrict__ gx,
-                                                           float* __restrict__ partials, int C, int H, int W,
+                                                           float* __restrict__ partials, int C, int H, int W_arg,
                                                            int B) {
+  const int W = kW > 0 ? kW : W_arg;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int pitch = lds_pitch_dev(W);
   float* SG = reinterpret_cast<float*>(smem_raw);
@@ -1743,8 +1745,8 @@ static void bwd_lds_t(const float* x, const int* taps, const float* gy, void* gx
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   auto go = [&](auto ki, auto ku, auto kr) {
-    if (SEG == 8 && !decltype(ku)::value && W == kPoseW)
-      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, false, kMaxT, decltype(kr)::value, kPoseW>),
+    if (SEG == 8 && W == kPoseW)
+      hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT, decltype(kr)::value, kPoseW>),
                          dim3(N * C), dim3(threads), shm, s, x, taps, gy, gx, partials, C, H, W, B, stride, Ho, Wo);
     else
       hipLaunchKernelGGL((k_box_bwd_lds<SEG, decltype(ki)::value, decltype(ku)::value, kMaxT, decltype(kr)::value>),
@@ -1871,8 +1873,12 @@ static void bwd_split_t(const float* x, const int* rec, const float* gy, float* 
                         int H, int W, int B, hipStream_t s) {
   const int threads = ((n_chunks(W) * n_segs(H, SEG) + 63) / 64) * 64;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(float);
-  hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC, kMaxT>), dim3(N * C), dim3(threads), shm, s, x, rec, gy,
-                     gx, partials, C, H, W, B);
+  if (SEG == 8 && W == kPoseW)
+    hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC, kMaxT, kPoseW>), dim3(N * C), dim3(threads), shm, s, x,
+                       rec, gy, gx, partials, C, H, W, B);
+  else
+    hipLaunchKernelGGL((k_box_bwd_lds_split<SEG, NXC, NYC, kMaxT>), dim3(N * C), dim3(threads), shm, s, x, rec, gy,
+                       gx, partials, C, H, W, B);
 }
 
 template <int SEG, int kMaxT>

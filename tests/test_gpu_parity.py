@@ -326,6 +326,7 @@ def test_fwd_integer_corners_bf16_output():
 
 @pytest.mark.parametrize("key,scale", [
     (3, dict(N=3, C=4)),
+    (3, dict(N=4, C=256)),                      # enough maps for 8-row items
     (2, dict(N=1, C=3, H=37, W=29, B=5)),
     (3, dict(N=2, C=2, H=17, W=100, B=3)),
     (3, dict(N=1, C=2, H=96, W=97, B=3)),       # 792 items: one block of 832 threads
