@@ -777,10 +777,11 @@ __device__ __forceinline__ void fwd_boxes_strided(const LdsTable<T>& tab, const 
   }
 }
 
-template <typename T, typename OutT, bool kOffset, bool kInt>
+template <typename T, typename OutT, bool kOffset, bool kInt, int kW = 0>
 __global__ __launch_bounds__(256) void k_box_fwd_lds_strided(const T* __restrict__ x, const int* __restrict__ taps,
-                                                             OutT* __restrict__ y, int C, int H, int W, int B, int s,
+                                                             OutT* __restrict__ y, int C, int H, int W_arg, int B, int s,
                                                              int Ho, int Wo, int bpg, int per_box_p) {
+  const int W = kW > 0 ? kW : W_arg;  // kW > 0: the map width compiled in
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* S = reinterpret_cast<T*>(smem_raw);
   __shared__ float red[16];
@@ -1664,9 +1665,14 @@ static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int
   const int Ho = (H + stride - 1) / stride, Wo = (W + stride - 1) / stride;
   const FwdGeom g = fwd_geom_items(N, C, B, Wo * ((Ho + kSegS - 1) / kSegS));
   with_flag(rounded, [&](auto ki) {
-    hipLaunchKernelGGL((k_box_fwd_lds_strided<T, OutT, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
-                       dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, stride, Ho, Wo, g.bpg,
-                       g.per_box_p);
+    if (std::is_same<T, float>::value && W == kPoseW)
+      hipLaunchKernelGGL((k_box_fwd_lds_strided<T, OutT, kOffset, decltype(ki)::value, kPoseW>), dim3(N * C * g.ngrp),
+                         dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, stride, Ho, Wo, g.bpg,
+                         g.per_box_p);
+    else
+      hipLaunchKernelGGL((k_box_fwd_lds_strided<T, OutT, kOffset, decltype(ki)::value>), dim3(N * C * g.ngrp),
+                         dim3(g.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W, B, stride, Ho, Wo, g.bpg,
+                         g.per_box_p);
   });
 }
 
