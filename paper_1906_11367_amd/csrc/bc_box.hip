@@ -226,6 +226,33 @@ __device__ void build_table_lds_up(const float* __restrict__ src, float* S, int 
 // Walks with compile-time segment length (registers indexed statically)
 // ---------------------------------------------------------------------------
 
+// The columns of a Q-column item (Q a multiple of kQ) as Q / kQ groups of
+// kQ, each with its own clamped run start: the LDS table's padding (kPad = 3
+// columns a side) covers runs of kQ + 1 words only, so a wider item reads
+// its runs group by group.
+template <int Q, typename Src>
+struct ColGroups {
+  static_assert(Q % kQ == 0, "items are whole groups of kQ columns");
+  static constexpr int NG = Q / kQ;
+  typename Src::Cols c[NG];
+  __device__ __forceinline__ ColGroups(const Src& S, int ba, int bb) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) c[g] = S.cols(ba + g * kQ, bb + g * kQ);
+  }
+  // x-interpolated row (table_row) for all Q columns
+  template <typename T>
+  __device__ __forceinline__ void row(const Src& S, int coord, const Taps<T>& tp, T* U) const {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) table_row(S, coord, c[g], tp, U + g * kQ);
+  }
+  // the kQ-word runs at both x edges, for all Q columns
+  template <typename T>
+  __device__ __forceinline__ void runs(const Src& S, int coord, T* sa, T* sb) const {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) S.template runs<kQ>(coord, c[g], sa + g * kQ, sb + g * kQ);
+  }
+};
+
 // Forward walk: emit.put<kFull>(s, o) for s in [0, SEG) with y0 + s < y1.
 // kFull: the item is known to be whole (y1 = y0 + SEG, x0 + kQ <= W), so no
 // step or column is guarded and the unrolled window needs no register copies.
@@ -234,45 +261,44 @@ __device__ void build_table_lds_up(const float* __restrict__ src, float* S, int 
 // mu * (clipped box area) is added back: the clipped area is the same tap
 // combination applied to the clamped coordinates (the table of a constant
 // image is mu * u * v).
-template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
+template <int SEG, typename T, bool kOffset, bool kFull, int Q = kQ, typename Src, typename Emit>
 __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H, int W, int x0,
                                          int y0, int y1, float mu, Emit& emit) {
   const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
-  const typename Src::Cols cl = S.cols(ba, bb);
+  const ColGroups<Q, Src> cl(S, ba, bb);
   const int st = S.row_step();
   const int rc = S.row_coord(y0 + tp.oy[0]), rd = S.row_coord(y0 + tp.oy[2]);
-  T uc[kQ], ud[kQ];
-  table_row(S, rc, cl, tp, uc);
-  table_row(S, rd, cl, tp, ud);
-  float ex[kQ];
+  T uc[Q], ud[Q];
+  cl.row(S, rc, tp, uc);
+  cl.row(S, rd, tp, ud);
+  float ex[Q];
   if (kOffset) {
 #pragma unroll
-    for (int q = 0; q < kQ; ++q)
-      ex[q] = (float)tp.wx[0] * (float)clampi(ba + q, 0, W) + (float)tp.wx[1] * (float)clampi(ba + q + 1, 0, W) +
-              (float)tp.wx[2] * (float)clampi(bb + q, 0, W) + (float)tp.wx[3] * (float)clampi(bb + q + 1, 0, W);
+    for (int q = 0; q < Q; ++q)
+      ex[q] = wsum4((float)tp.wx[0], (float)clampi(ba + q, 0, W), (float)tp.wx[1], (float)clampi(ba + q + 1, 0, W),
+                    (float)tp.wx[2], (float)clampi(bb + q, 0, W), (float)tp.wx[3], (float)clampi(bb + q + 1, 0, W));
   }
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
     if (kFull || y < y1) {
-      T uc1[kQ], ud1[kQ];
-      table_row(S, rc + (s + 1) * st, cl, tp, uc1);
-      table_row(S, rd + (s + 1) * st, cl, tp, ud1);
-      T o[kQ];
+      T uc1[Q], ud1[Q];
+      cl.row(S, rc + (s + 1) * st, tp, uc1);
+      cl.row(S, rd + (s + 1) * st, tp, ud1);
+      T o[Q];
 #pragma unroll
-      for (int q = 0; q < kQ; ++q)
-        o[q] = tp.wy[0] * uc[q] + tp.wy[1] * uc1[q] + tp.wy[2] * ud[q] + tp.wy[3] * ud1[q];
+      for (int q = 0; q < Q; ++q)
+        o[q] = wsum4(tp.wy[0], uc[q], tp.wy[1], uc1[q], tp.wy[2], ud[q], tp.wy[3], ud1[q]);
       if (kOffset) {
-        const float ey = (float)tp.wy[0] * (float)clampi(y + tp.oy[0], 0, H) +
-                         (float)tp.wy[1] * (float)clampi(y + tp.oy[1], 0, H) +
-                         (float)tp.wy[2] * (float)clampi(y + tp.oy[2], 0, H) +
-                         (float)tp.wy[3] * (float)clampi(y + tp.oy[3], 0, H);
+        const float ey = wsum4((float)tp.wy[0], (float)clampi(y + tp.oy[0], 0, H), (float)tp.wy[1],
+                               (float)clampi(y + tp.oy[1], 0, H), (float)tp.wy[2], (float)clampi(y + tp.oy[2], 0, H),
+                               (float)tp.wy[3], (float)clampi(y + tp.oy[3], 0, H));
 #pragma unroll
-        for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
+        for (int q = 0; q < Q; ++q) o[q] = add_offset(o[q], mu, ex[q] * ey);
       }
       emit.template put<kFull>(s, o);
 #pragma unroll
-      for (int q = 0; q < kQ; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
+      for (int q = 0; q < Q; ++q) { uc[q] = uc1[q]; ud[q] = ud1[q]; }
     }
   }
 }
@@ -284,32 +310,32 @@ __device__ __forceinline__ void box_walk(const Src& S, const Taps<T>& tp, int H,
 // S(y+c, x+a)).  emit.put<kFull>(s, o) for s in [0, SEG) with y0 + s < y1.
 // With kOffset the table holds the map minus mu, and mu * (clipped area) is
 // added back.
-template <int SEG, typename T, bool kOffset, bool kFull, typename Src, typename Emit>
+template <int SEG, typename T, bool kOffset, bool kFull, int Q = kQ, typename Src, typename Emit>
 __device__ __forceinline__ void box_walk_int(const Src& S, const Taps<T>& tp, int H, int W, int x0, int y0,
                                              int y1, float mu, Emit& emit) {
   const int ba = x0 + tp.ox[0], bb = x0 + tp.ox[2];
-  const typename Src::Cols cl = S.cols(ba, bb);
+  const ColGroups<Q, Src> cl(S, ba, bb);
   const int st = S.row_step();
   const int rc = S.row_coord(y0 + tp.oy[0]), rd = S.row_coord(y0 + tp.oy[2]);
-  float ex[kQ];
+  float ex[Q];
   if (kOffset) {
 #pragma unroll
-    for (int q = 0; q < kQ; ++q) ex[q] = (float)(clampi(bb + q, 0, W) - clampi(ba + q, 0, W));
+    for (int q = 0; q < Q; ++q) ex[q] = (float)(clampi(bb + q, 0, W) - clampi(ba + q, 0, W));
   }
 #pragma unroll
   for (int s = 0; s < SEG; ++s) {
     const int y = y0 + s;
     if (kFull || y < y1) {
-      T ca[kQ], cb[kQ], da[kQ], db[kQ];
-      S.template runs<kQ>(rc + s * st, cl, ca, cb);
-      S.template runs<kQ>(rd + s * st, cl, da, db);
-      T o[kQ];
+      T ca[Q], cb[Q], da[Q], db[Q];
+      cl.runs(S, rc + s * st, ca, cb);
+      cl.runs(S, rd + s * st, da, db);
+      T o[Q];
 #pragma unroll
-      for (int q = 0; q < kQ; ++q) o[q] = (db[q] - da[q]) - (cb[q] - ca[q]);
+      for (int q = 0; q < Q; ++q) o[q] = (db[q] - da[q]) - (cb[q] - ca[q]);
       if (kOffset) {
         const float ey = (float)(clampi(y + tp.oy[2], 0, H) - clampi(y + tp.oy[0], 0, H));
 #pragma unroll
-        for (int q = 0; q < kQ; ++q) o[q] = o[q] + (T)(mu * (ex[q] * ey));
+        for (int q = 0; q < Q; ++q) o[q] = add_offset(o[q], mu, ex[q] * ey);
       }
       emit.template put<kFull>(s, o);
     }
@@ -332,8 +358,8 @@ __device__ __forceinline__ void box_walk_strided(const Src& S, const Taps<T>& tp
   float ex = 0.f;
   if (kOffset) {
     ex = kInt ? (float)(clampi(bb, 0, W) - clampi(ba, 0, W))
-              : (float)tp.wx[0] * (float)clampi(ba, 0, W) + (float)tp.wx[1] * (float)clampi(ba + 1, 0, W) +
-                    (float)tp.wx[2] * (float)clampi(bb, 0, W) + (float)tp.wx[3] * (float)clampi(bb + 1, 0, W);
+              : wsum4((float)tp.wx[0], (float)clampi(ba, 0, W), (float)tp.wx[1], (float)clampi(ba + 1, 0, W),
+                      (float)tp.wx[2], (float)clampi(bb, 0, W), (float)tp.wx[3], (float)clampi(bb + 1, 0, W));
   }
 #pragma unroll
   for (int k = 0; k < SEGS; ++k) {
@@ -354,17 +380,17 @@ __device__ __forceinline__ void box_walk_strided(const Src& S, const Taps<T>& tp
         for (int r = 0; r < 4; ++r) {
           T sa[2], sb[2];
           S.template runs<2>(rows[r], cl, sa, sb);
-          u[r] = tp.wx[0] * sa[0] + tp.wx[1] * sa[1] + tp.wx[2] * sb[0] + tp.wx[3] * sb[1];
+          u[r] = wsum4(tp.wx[0], sa[0], tp.wx[1], sa[1], tp.wx[2], sb[0], tp.wx[3], sb[1]);
         }
-        o = tp.wy[0] * u[0] + tp.wy[1] * u[1] + tp.wy[2] * u[2] + tp.wy[3] * u[3];
+        o = wsum4(tp.wy[0], u[0], tp.wy[1], u[1], tp.wy[2], u[2], tp.wy[3], u[3]);
       }
       if (kOffset) {
         const float ey = kInt ? (float)(clampi(y + tp.oy[2], 0, H) - clampi(y + tp.oy[0], 0, H))
-                              : (float)tp.wy[0] * (float)clampi(y + tp.oy[0], 0, H) +
-                                    (float)tp.wy[1] * (float)clampi(y + tp.oy[1], 0, H) +
-                                    (float)tp.wy[2] * (float)clampi(y + tp.oy[2], 0, H) +
-                                    (float)tp.wy[3] * (float)clampi(y + tp.oy[3], 0, H);
-        o = o + (T)(mu * (ex * ey));
+                              : wsum4((float)tp.wy[0], (float)clampi(y + tp.oy[0], 0, H), (float)tp.wy[1],
+                                      (float)clampi(y + tp.oy[1], 0, H), (float)tp.wy[2],
+                                      (float)clampi(y + tp.oy[2], 0, H), (float)tp.wy[3],
+                                      (float)clampi(y + tp.oy[3], 0, H));
+        o = add_offset(o, mu, ex * ey);
       }
       emit.put(k, o);
     }
@@ -381,11 +407,11 @@ struct StoreCol {
 };
 
 // Forward walk of one item: integer-corner or interpolated.
-template <int SEG, typename T, bool kOffset, bool kFull, bool kInt, typename Src, typename Emit>
+template <int SEG, typename T, bool kOffset, bool kFull, bool kInt, int Q = kQ, typename Src, typename Emit>
 __device__ __forceinline__ void walk_fwd(const Src& S, const Taps<T>& tp, int H, int W, int x0, int y0, int y1,
                                          float mu, Emit& emit) {
-  if constexpr (kInt) box_walk_int<SEG, T, kOffset, kFull>(S, tp, H, W, x0, y0, y1, mu, emit);
-  else box_walk<SEG, T, kOffset, kFull>(S, tp, H, W, x0, y0, y1, mu, emit);
+  if constexpr (kInt) box_walk_int<SEG, T, kOffset, kFull, Q>(S, tp, H, W, x0, y0, y1, mu, emit);
+  else box_walk<SEG, T, kOffset, kFull, Q>(S, tp, H, W, x0, y0, y1, mu, emit);
 }
 
 // Emitter that adds an item's outputs to its register accumulator (the
@@ -470,19 +496,34 @@ __device__ __forceinline__ void adjoint_walk(const Src& S, const Taps<float>& tp
   }
 }
 
-// Emitter of forward outputs: the kQ outputs of row y0 + s at plane offset
+// Emitter of forward outputs: the Q outputs of row y0 + s at plane offset
 // off0 + s * W (elements; off0 = y0 * W + x0).
 // kNT: non-temporal stores (the HBM-table forwards with outputs larger than
-// the last-level cache, see kStreamOutBytes).
-template <typename OutT, typename T, bool kNT = false>
+// the last-level cache, see kStreamOutBytes).  kPack (bf16 outputs, Q even,
+// every row offset and x0 even and the output 4-byte aligned): a whole row
+// of the item goes out as Q / 2 packed words in one store.
+template <typename OutT, typename T, bool kNT = false, int Q = kQ, bool kPack = false>
 struct StoreRows {
   OutT* out;
   int W, x0, off0;
   template <bool kFull>
   __device__ __forceinline__ void put(int s, const T* o) {
+    if constexpr (kPack && kFull) {
+      static_assert(std::is_same<OutT, uint16_t>::value && std::is_same<T, float>::value && Q % 2 == 0 && !kNT,
+                    "packed rows are bf16 pairs");
+      // one v_cvt_pk_bf16_f32 per pair (the rounding of convert_out); the
+      // row's word offset s * W / 2 folds into the store's immediate
+      typedef float f32x2 __attribute__((ext_vector_type(2)));
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      uint32_t* w = reinterpret_cast<uint32_t*>(out + off0) + s * (W >> 1);
+#pragma unroll
+      for (int k = 0; k < Q / 2; ++k)
+        w[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){o[2 * k], o[2 * k + 1]}, bf16x2));
+      return;
+    }
     OutT* row = out + (unsigned)(off0 + s * W);
 #pragma unroll
-    for (int q = 0; q < kQ; ++q)
+    for (int q = 0; q < Q; ++q)
       if (kFull || x0 + q < W) {
         if constexpr (kNT) __builtin_nontemporal_store(convert_out<OutT, T>(o[q]), row + q);
         else row[q] = convert_out<OutT, T>(o[q]);
@@ -686,11 +727,11 @@ template <> __device__ __forceinline__ Taps<int> typed_taps<int>(const Taps<floa
 // adjacent lanes write adjacent columns; each box's items are padded to a
 // multiple of 64 (per_box_p) so that a wave works on one box and reads its
 // taps through scalar loads.
-template <typename T, typename OutT, int SEG, bool kOffset, bool kInt>
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt, int Q = kQ, bool kPack = false>
 __device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __restrict__ taps,
                                           OutT* __restrict__ y, int map, int c, int b0, int nb, int H, int W,
                                           int B, int per_box_p, float mu) {
-  const int nch = (W + kQ - 1) / kQ, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
+  const int nch = (W + Q - 1) / Q, nseg = (H + SEG - 1) / SEG, per_box = nch * nseg;
   for (int it = threadIdx.x; it < nb * per_box_p; it += blockDim.x) {
     const int bl = __builtin_amdgcn_readfirstlane(it / per_box_p);
     const int r = it - bl * per_box_p;
@@ -699,18 +740,18 @@ __device__ __forceinline__ void fwd_boxes(const LdsTable<T>& tab, const int* __r
     const int b = b0 + bl;
     const Taps<T> tp = typed_taps<T>(load_taps(taps + (size_t)(c * B + b) * 16, W, H));
     OutT* out = y + ((size_t)map * B + b) * H * W;
-    const int x0 = ch * kQ, y0 = seg * SEG, y1 = min(y0 + SEG, H);
-    StoreRows<OutT, T> em{out, W, x0, y0 * W + x0};
-    if (y0 + SEG <= H && x0 + kQ <= W) walk_fwd<SEG, T, kOffset, true, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
-    else walk_fwd<SEG, T, kOffset, false, kInt>(tab, tp, H, W, x0, y0, y1, mu, em);
+    const int x0 = ch * Q, y0 = seg * SEG, y1 = min(y0 + SEG, H);
+    StoreRows<OutT, T, false, Q, kPack> em{out, W, x0, y0 * W + x0};
+    if (y0 + SEG <= H && x0 + Q <= W) walk_fwd<SEG, T, kOffset, true, kInt, Q>(tab, tp, H, W, x0, y0, y1, mu, em);
+    else walk_fwd<SEG, T, kOffset, false, kInt, Q>(tab, tp, H, W, x0, y0, y1, mu, em);
   }
 }
 
 // Forward, table in LDS: one block per (map, group of bpg boxes).  The block
 // builds the map's table once and evaluates every box of its group.
 // kW > 0: the map width compiled in (W is then ignored), as in the LDS
-// backward.
-template <typename T, typename OutT, int SEG, bool kOffset, bool kInt, int kW = 0>
+// backward.  Q: columns per item; kPack: packed bf16 row stores (StoreRows).
+template <typename T, typename OutT, int SEG, bool kOffset, bool kInt, int kW = 0, int Q = kQ, bool kPack = false>
 __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, const int* __restrict__ taps,
                                                      OutT* __restrict__ y, int C, int H, int W_arg, int B, int bpg,
                                                      int per_box_p) {
@@ -726,8 +767,8 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
   if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
   build_table_lds(src, S, H, W, pitch, mu, kOffset);
   const int b0 = grp * bpg;
-  fwd_boxes<T, OutT, SEG, kOffset, kInt>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0, min(bpg, B - b0), H,
-                                   W, B, per_box_p, mu);
+  fwd_boxes<T, OutT, SEG, kOffset, kInt, Q, kPack>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0,
+                                                   min(bpg, B - b0), H, W, B, per_box_p, mu);
 }
 
 // Forward, table in HBM: one block per (map, box, block of 256 items), mapped
@@ -1651,6 +1692,21 @@ static void fwd_lds_t(const void* x, const int* taps, void* y, int N, int C, int
   constexpr int SEG = 16;
   const size_t shm = (size_t)(H + 1) * lds_pitch(W) * sizeof(T);
   if (stride == 1) {
+    // bf16 output of 48-column maps, 4-byte aligned: items of 6 columns x 8
+    // rows (still 64 per box on 64-row maps), each row stored as 3 packed
+    // words
+    if constexpr (std::is_same<T, float>::value && std::is_same<OutT, uint16_t>::value) {
+      if (W == kPoseW && ((uintptr_t)y & 3) == 0) {  // the ABI also requires 16-byte aligned tensors
+        constexpr int kSeg6 = 8, kQ6 = 6;
+        const FwdGeom g6 = fwd_geom_items(N, C, B, ((W + kQ6 - 1) / kQ6) * n_segs(H, kSeg6));
+        with_flag(rounded, [&](auto ki) {
+          hipLaunchKernelGGL((k_box_fwd_lds<T, OutT, kSeg6, kOffset, decltype(ki)::value, kPoseW, kQ6, true>),
+                             dim3(N * C * g6.ngrp), dim3(g6.threads), shm, s, (const T*)x, taps, (OutT*)y, C, H, W,
+                             B, g6.bpg, g6.per_box_p);
+        });
+        return;
+      }
+    }
     const FwdGeom g = fwd_geom(N, C, H, W, B, SEG);
     with_flag(rounded, [&](auto ki) {
       if (std::is_same<T, float>::value && W == kPoseW)

@@ -11,6 +11,7 @@
 // {fc, fc+1, fd, fd+1} with separable signed weights; the 16 tap weights of
 // the paper are the products wy[r] * wx[k].
 #pragma once
+#include <type_traits>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -237,6 +238,24 @@ struct GlobalTable {
   }
 };
 
+// w0*a + w1*b + w2*c + w3*d in a fixed rounding sequence (one product, then
+// three fused multiply-adds in term order), so that every kernel instance
+// evaluating the same sum gets the same bits whatever the compiler would
+// contract; exact for integers.
+template <typename T>
+__device__ __forceinline__ T wsum4(T w0, T a, T w1, T b, T w2, T c, T w3, T d) {
+  if constexpr (std::is_same<T, float>::value) return fmaf(w3, d, fmaf(w2, c, fmaf(w1, b, w0 * a)));
+  else return w0 * a + w1 * b + w2 * c + w3 * d;
+}
+
+// o + mu * e, the mean offset's contribution added back (fused for floats,
+// for the same reason as wsum4).
+template <typename T>
+__device__ __forceinline__ T add_offset(T o, float mu, float e) {
+  if constexpr (std::is_same<T, float>::value) return fmaf(mu, e, o);
+  else return o + (T)(mu * e);
+}
+
 // The x-interpolated table row for kQ consecutive outputs x0 + q: for q in
 // [0, kQ),  U[q] = sum_k wx[k] * S(v, clamp(x0 + q + ox[k])).
 template <typename T, typename Src>
@@ -246,7 +265,7 @@ __device__ __forceinline__ void table_row(const Src& S, int coord, const typenam
   S.runs(coord, c, sa, sb);
 #pragma unroll
   for (int q = 0; q < kQ; ++q)
-    U[q] = tp.wx[0] * sa[q] + tp.wx[1] * sa[q + 1] + tp.wx[2] * sb[q] + tp.wx[3] * sb[q + 1];
+    U[q] = wsum4(tp.wx[0], sa[q], tp.wx[1], sa[q + 1], tp.wx[2], sb[q], tp.wx[3], sb[q + 1]);
 }
 
 // Same row for adjoint taps, also returning the column differences at the

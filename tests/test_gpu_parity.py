@@ -314,6 +314,28 @@ def test_fwd_integer_corners_large_maps(flags):
     check(got, O.box_forward(d["x"], d["boxes"], integer_corners=True), RTOL_F32, "O")
 
 
+@pytest.mark.parametrize("H", [64, 37])
+@pytest.mark.parametrize("flags", [0, bc.BC_FLAG_MEAN_OFFSET, bc.BC_FLAG_INTEGER_CORNERS])
+def test_fwd_bf16_rows_are_rounded_fp32_outputs(H, flags):
+    """48-column maps with a bf16 output take 6-column items whose rows go out
+    as packed words (a ragged last segment, when H is not a multiple of 8,
+    takes per-element stores); the fp32 output takes 3-column items.  Every
+    bf16 value is the round-to-nearest-even bf16 of the same call's fp32
+    output, bit for bit."""
+    wl = wlmod.WORKLOADS[3].scaled(N=2, C=4, H=H)
+    d = wlmod.make_inputs(wl)
+    N, C, B, W = wl.N, wl.C, wl.B, wl.W
+    say(f"fwd bf16 rows 48 wide H={H} flags={flags}")
+    xd, bd = dev(d["x"]), dev(d["boxes"])
+    y32 = torch.empty((N, C * B, H, W), dtype=torch.float32, device="cuda")
+    bc.box_conv_fwd(xd, bd, y32, flags)
+    want = y32.to(torch.bfloat16)
+    y16 = torch.empty_like(want)
+    bc.box_conv_fwd(xd, bd, y16, flags)
+    torch.cuda.synchronize()
+    assert torch.equal(y16.view(torch.int16), want.view(torch.int16))
+
+
 def test_fwd_integer_corners_bf16_output():
     wl = wlmod.WORKLOADS[3].scaled(N=1, C=4)
     d = wlmod.make_inputs(wl)
