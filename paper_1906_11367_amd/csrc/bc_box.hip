@@ -140,7 +140,7 @@ __device__ __forceinline__ typename Vec4<T>::type load_stream4(const typename Ve
 // not stored, so no lane branches around a load).  Then a column pass (lanes
 // own columns) and the row pass, each reading kScan elements ahead before it
 // writes.  With `sub`, mu is subtracted from the tabulated values.
-template <typename T>
+template <typename T, bool kSkip = false>
 __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, int pitch, float mu, bool sub) {
   using V = typename Vec4<T>::type;
   constexpr int kBatch = 8;
@@ -159,11 +159,16 @@ __device__ void build_table_lds(const T* __restrict__ src, T* S, int H, int W, i
     const int step = di * pitch + 4 * dj, wrap = pitch - W;
     const V* s4 = reinterpret_cast<const V*>(src);
     for (int base = 0; base < n4; base += nt * kBatch) {
+      // kSkip: slots past the map for every thread of the block (the tail
+      // of the last batch) issue nothing, a block-uniform test (the
+      // backward keeps the unconditional form, which fits its registers)
       V q[kBatch];
 #pragma unroll
-      for (int b = 0; b < kBatch; ++b) q[b] = load_stream4<T>(s4 + min(base + b * nt + tid, n4 - 1));
+      for (int b = 0; b < kBatch; ++b)
+        if (!kSkip || base + b * nt < n4) q[b] = load_stream4<T>(s4 + min(base + b * nt + tid, n4 - 1));
 #pragma unroll
       for (int b = 0; b < kBatch; ++b) {
+        if (kSkip && base + b * nt >= n4) break;
         if (tid < n4 - base - b * nt) {
           const T w4[4] = {(T)q[b].x, (T)q[b].y, (T)q[b].z, (T)q[b].w};
 #pragma unroll
@@ -765,7 +770,7 @@ __global__ __launch_bounds__(256) void k_box_fwd_lds(const T* __restrict__ x, co
   const T* src = x + (size_t)map * H * W;
   float mu = 0.f;
   if (kOffset) mu = block_mean(reinterpret_cast<const float*>(src), H * W, red);
-  build_table_lds(src, S, H, W, pitch, mu, kOffset);
+  build_table_lds<T, true>(src, S, H, W, pitch, mu, kOffset);
   const int b0 = grp * bpg;
   fwd_boxes<T, OutT, SEG, kOffset, kInt, Q, kPack>(LdsTable<T>{S, pitch, W, H}, taps, y, map, map % C, b0,
                                                    min(bpg, B - b0), H, W, B, per_box_p, mu);
