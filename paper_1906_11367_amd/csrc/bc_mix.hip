@@ -127,7 +127,9 @@ __device__ __forceinline__ float operand_f32(uint32_t b, uint32_t m) {
 // then both hit distinct banks.
 template <int PITCH>
 __device__ __forceinline__ int bf16_tile_off(int r, int l) {
-  return r * PITCH + ((((l >> 3) ^ (r >> 4)) & 7) << 3) + (l & 7);
+  constexpr int kChunks = (PITCH - 8) / 8;  // 16-byte chunks per row: 8 (64 deep) or 16 (128 deep)
+  static_assert((kChunks & (kChunks - 1)) == 0, "a power of two");
+  return r * PITCH + ((((l >> 3) ^ (r >> 4)) & (kChunks - 1)) << 3) + (l & 7);
 }
 
 // One GEMM operand X(r, l): rows r in [0, rows), reduction index l in
@@ -145,9 +147,9 @@ __device__ __forceinline__ int bf16_tile_off(int r, int l) {
 //           4 x UL block is transposed in registers so every LDS write is
 //           16 contiguous bytes of one row.
 // bf16 storage without a mask is kept packed and never converted.
-template <bool BF16, int DT, bool KC, bool MASK>
+template <bool BF16, int DT, bool KC, bool MASK, int kDeep = 0>
 struct Stager {
-  static constexpr int BK = BF16 ? 64 : 32;
+  static constexpr int BK = kDeep > 0 ? kDeep : (BF16 ? 64 : 32);
   static constexpr int PITCH = BF16 ? BK + 8 : BK + 1;  // elements; bf16 rows are 16-byte aligned
   static constexpr int UL = BF16 ? 8 : 4;               // l per unit
   static constexpr int NU = KC ? (kBM * BK / UL) / kMixThreads : 1;
@@ -412,8 +414,11 @@ __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BM
     const void* __restrict__ a, const void* __restrict__ b, const float* __restrict__ aux, void* __restrict__ out,
     int rows, int cols, int depth, long lda, long ldb, long ldc, long a_bs, long b_bs, long c_bs,
     int mt, int nt, int zt, int nsplit_p, int pchunk, int out_kind, int relu) {
-  using SA = Stager<BF16, ADT, AKC, AMASK>;
-  using SB = Stager<BF16, BDT, BKC, BMASK>;
+  // bf16 storage on both operands, both contiguous along the reduction
+  // (BWD_WEIGHT): 128-deep K-steps, each operand row read as 256-byte runs
+  constexpr int kDeep = (BF16 && AKC && BKC && !AMASK && !BMASK && ADT == 2 && BDT == 2) ? 128 : 0;
+  using SA = Stager<BF16, ADT, AKC, AMASK, kDeep>;
+  using SB = Stager<BF16, BDT, BKC, BMASK, kDeep>;
   constexpr int BK = SA::BK, PITCH = SA::PITCH;
   using E = typename SA::E;
   __shared__ __align__(16) E As[kBM * PITCH];
@@ -449,6 +454,10 @@ __attribute__((amdgpu_waves_per_eu(mix_waves<BF16, ADT, AKC, AMASK, BDT, BKC, BM
   sb.init_offsets();
   sa.vec_ok = sa.vec_ok && sa.buf_ok();
   sb.vec_ok = sb.vec_ok && sb.buf_ok();
+  // loads stop at this block's reduction range (a split chunk need not be a
+  // whole number of K-steps; the descriptors keep the operand's extent)
+  sa.depth = l_end;
+  sb.depth = l_end;
 
   const int i0 = tm * kBM, j0 = tn * kBN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
