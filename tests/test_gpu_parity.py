@@ -986,6 +986,13 @@ def test_mix(dims, compute, storage, relu):
     # accumulate adds onto the existing contents
     bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, dev(gz), od, dw, N, M, K, P, cd, relu=relu, aux=aux, accumulate=1)
     check(host(dw), 2 * dwr, rtol, "dW accumulated")
+    if storage == torch.bfloat16 and not relu:
+        # dZ in bf16 storage too (both operands bf16: the 128-deep K-steps,
+        # with split chunks that end inside a K-step for the small P); the
+        # oracle rounds the same operands to bf16, so the reference is dwr
+        dw2 = torch.empty_like(dw)
+        bc.pointwise_mix(bc.BC_MIX_BWD_WEIGHT, dev(gz).to(storage), od, dw2, N, M, K, P, cd)
+        check(host(dw2), dwr, rtol, "dW (bf16 dZ)")
 
 
 def test_cast_bf16_bit_exact():
